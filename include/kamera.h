@@ -1,0 +1,253 @@
+/*
+ * kamera.h -- C ABI of the Kamera chunk-reuse operator for AMD Instinct MI355X
+ * (gfx950).
+ *
+ * Kamera (arxiv 2606.23581) stores each cached chunk position-free -- the
+ * pre-RoPE keys and the values of every layer and KV head, or an MLA latent
+ * plus its decoupled rope key -- together with a rank-m "conditioning patch"
+ * per layer and head (Eq. eq:operator, Sec. 1; Sec. 3).  Reusing the chunk at
+ * a new position needs no forward pass: the keys are re-rotated to the target
+ * position and the patch is added back (App. A, serve step).  This library
+ * performs that serve step on the GPU:
+ *
+ *   kamera_rehydrate     K' = R(pos) (K + U_k W_k),  V' = V + U_v W_v,
+ *                        into a dense buffer or straight into a paged KV pool;
+ *   kamera_shift         K' = R(delta) K, in place, for keys that are already
+ *                        rotated (R(delta) R(p) = R(p + delta), Sec. 1 and 3:
+ *                        reorder, sliding-window survivors, Sec. 5);
+ *   kamera_scatter_paged a bit copy of dense token rows into the pool slots a
+ *                        page table names (the clean-view overwrite, App. E).
+ *
+ * Conventions shared by every entry point
+ *   - Every tensor pointer is a DEVICE pointer owned by the caller.  The
+ *     library never allocates, frees or synchronises; a call enqueues one
+ *     kernel on `stream` (a hipStream_t; NULL = the default stream) and
+ *     returns.  Results are visible to later work on that stream.
+ *   - KV rows are bf16.  Strides are in ELEMENTS (bf16) unless named _bytes;
+ *     the innermost (column) stride is always 1.  Row starts must be 16-byte
+ *     aligned: base pointers 16-byte aligned and every stride a multiple of 8.
+ *   - Per-chunk integers (positions, deltas, row bases, token counts, page
+ *     tables) are int32 arrays in device memory.
+ *   - Return value: KAMERA_OK (0) or a negative kamera_status.  Argument
+ *     errors are detected on the host BEFORE any HIP call, so a failed call
+ *     has no side effect; kamera_last_error() then describes the problem.
+ *   - Calls are thread-safe; the error text is per thread.
+ *   - Contents of device arrays (page-table entries, positions) cannot be
+ *     checked on the host.  Page numbers outside [0, n_pool_pages) are
+ *     skipped by the kernels and flagged in the optional `status` word
+ *     (bit KAMERA_STATUS_BAD_PAGE), never written out of bounds.  A page
+ *     table must be injective for the result to be defined;
+ *     kamera_check_page_table() verifies a host copy.
+ */
+#ifndef KAMERA_H
+#define KAMERA_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define KAMERA_ABI_VERSION 1
+
+/* Largest patch rank m accepted (>= the 128-wide head, so a full-rank patch
+ * that reproduces any Delta K exactly can be applied). */
+#define KAMERA_MAX_RANK 128
+/* Rotated band width limit and row width limit, in elements. */
+#define KAMERA_MAX_ROPE_DIM 128
+#define KAMERA_MAX_HEAD_DIM 4096
+
+typedef enum {
+  KAMERA_OK = 0,
+  KAMERA_ERR_NULL = -1,        /* a required pointer is NULL                    */
+  KAMERA_ERR_SHAPE = -2,       /* inconsistent sizes, bands or sections         */
+  KAMERA_ERR_ALIGN = -3,       /* pointer or stride breaks 16-byte row alignment */
+  KAMERA_ERR_RANGE = -4,       /* a size or rank beyond the supported maximum    */
+  KAMERA_ERR_ALIAS = -5,       /* an output overlaps an input it must not        */
+  KAMERA_ERR_UNSUPPORTED = -6, /* a valid request this build does not implement  */
+  KAMERA_ERR_HIP = -7          /* the HIP runtime refused the launch             */
+} kamera_status;
+
+/* bits of the optional device status word */
+#define KAMERA_STATUS_BAD_PAGE 1u
+
+typedef enum {
+  KAMERA_PAIR_NEOX = 0,        /* pair j = columns (j, j + rope_dim/2)          */
+  KAMERA_PAIR_INTERLEAVED = 1  /* pair j = columns (2j, 2j + 1)                 */
+} kamera_pairing;
+
+typedef enum {
+  KAMERA_SECTIONS_BLOCKED = 0,     /* pairs [0,s0) use t, [s0,s0+s1) h, rest w  */
+  KAMERA_SECTIONS_INTERLEAVED = 1  /* pairs cycle t,h,w, skipping a coordinate
+                                      whose section count is used up            */
+} kamera_section_order;
+
+typedef enum {
+  KAMERA_POS_LINEAR = 0,   /* token i at p0 + i on every coordinate;
+                              chunk_pos[c*3 + 0] = p0                         */
+  KAMERA_POS_GRID3 = 1,    /* token i at (t0, h0 + i / grid_w, w0 + i % grid_w);
+                              chunk_pos[c*3 + 0..2] = (t0, h0, w0)            */
+  KAMERA_POS_EXPLICIT = 2  /* token i of chunk c at explicit_pos[c*explicit_
+                              chunk_stride + i*3 + (0,1,2)]                   */
+} kamera_pos_mode;
+
+typedef enum {
+  KAMERA_PATCH_PRE_ROPE = 0,  /* K' = R(pos)(K + U W): the patch lives in the
+                                 stored, position-free frame (Sec. 3)         */
+  KAMERA_PATCH_POST_ROPE = 1  /* K' = R(pos) K + U W: the literal form of
+                                 Eq. eq:operator                              */
+} kamera_patch_frame;
+
+/* RoPE variant (Sec. 3 content | RoPE split; Fig. fig:unify for M-RoPE).
+ * Pair j has frequency theta^(-2j/rope_dim) and rotates by angle
+ * coord(j) * frequency, x' = x cos - y sin, y' = x sin + y cos. */
+typedef struct {
+  double theta;            /* rotary base, > 1                                */
+  int32_t rope_offset;     /* first rotated column (0 for GQA/MHA, 512 MLA)  */
+  int32_t rope_dim;        /* rotated width: even, <= KAMERA_MAX_ROPE_DIM    */
+  int32_t pairing;         /* kamera_pairing                                 */
+  int32_t n_sections;      /* 1: 1-D RoPE (coordinate t); 3: (t, h, w)       */
+  int32_t sections[3];     /* pair counts of t, h, w; sum = rope_dim / 2     */
+  int32_t section_order;   /* kamera_section_order                           */
+} kamera_rope;
+
+/* One stream of rows the call rebuilds: the keys (rotate = 1) or the values
+ * (rotate = 0).  Element (c, l, i, h, col) of the input sits at
+ *   in + c*in_stride[0] + l*in_stride[1] + i*in_stride[2] + h*in_stride[3] + col.
+ * The patch factors of (c, l, h): U is n x m (token i, rank k) at
+ *   U + c*u_stride[0] + l*u_stride[1] + h*u_stride[2] + i*u_stride[3] + k,
+ * W is m x patch_dim at
+ *   W + c*w_stride[0] + l*w_stride[1] + h*w_stride[2] + k*w_stride[3] + col',
+ * col' = col - patch_offset.  A stride of 0 shares a factor (e.g. one basis
+ * per layer for every chunk).  m = 0 disables the patch (U, W may be NULL). */
+typedef struct {
+  const void* in;
+  int64_t in_stride[4];
+  void* out;               /* dense or pool base, see kamera_rehydrate_args  */
+  int64_t out_stride[4];
+  const void* U;
+  int64_t u_stride[4];
+  const void* W;
+  int64_t w_stride[4];
+  int32_t m;               /* patch rank, 0 .. KAMERA_MAX_RANK               */
+  int32_t rotate;          /* 1: rotate the rope band (keys); 0: values      */
+  int32_t patch_offset;    /* patched columns [patch_offset,                 */
+  int32_t patch_dim;       /*                  patch_offset + patch_dim)     */
+} kamera_plane;
+
+/* kamera_rehydrate -- Eq. eq:operator with the patch in the stored frame;
+ * the serve step of App. A for every (chunk, layer, KV head) at once.
+ *
+ * Output destination of token i of chunk c, layer l, head h:
+ *   dense (paged = 0): out + c*out_stride[0] + l*out_stride[1]
+ *                          + (row_base[c] + i)*out_stride[2] + h*out_stride[3]
+ *                      (row_base NULL = 0 for every chunk)
+ *   paged (paged = 1): slot = page_table[c*pt_stride + i/page_size]*page_size
+ *                             + i % page_size,
+ *                      out + l*out_stride[1] + slot*out_stride[2]
+ *                          + h*out_stride[3]   (out_stride[0] unused)
+ * Outputs must not overlap inputs (not checked for strided views beyond
+ * the base pointers). */
+typedef struct {
+  int32_t n_chunks;
+  int32_t n_layers;
+  int32_t n_heads;             /* KV heads (1 for an MLA latent row)          */
+  int32_t head_dim;            /* row width in elements, multiple of 32       */
+  int32_t n_tokens;            /* tokens per chunk (the maximum if ragged)     */
+  const int32_t* chunk_tokens; /* device [n_chunks] (<= n_tokens) or NULL      */
+  int32_t patch_frame;         /* kamera_patch_frame                           */
+  kamera_rope rope;
+  int32_t pos_mode;            /* kamera_pos_mode                              */
+  const int32_t* chunk_pos;    /* device [n_chunks][3] (LINEAR, GRID3)         */
+  int32_t grid_w;              /* GRID3 tokens per grid row, > 0               */
+  const int32_t* explicit_pos; /* device (EXPLICIT)                            */
+  int64_t explicit_chunk_stride;
+  int32_t n_planes;            /* 1 (keys only, e.g. MLA) or 2 (keys, values)  */
+  kamera_plane plane[2];
+  int32_t paged;
+  const int32_t* row_base;     /* dense: device [n_chunks] or NULL             */
+  const int32_t* page_table;   /* paged: device [n_chunks][pt_stride]          */
+  int32_t pt_stride;
+  int32_t page_size;
+  int32_t n_pool_pages;
+  uint32_t* status;            /* optional device word, bits OR-ed in          */
+} kamera_rehydrate_args;
+
+/* kamera_shift -- K' = R(delta_c) K in place on the rope band of every token
+ * of every listed chunk (Sec. 1, Sec. 3; survivors of a window slide, Sec. 5).
+ * Columns outside the band and the values are never touched.
+ * delta: device [n_chunks][3] int32, the move of (t, h, w); 1-D RoPE reads
+ * delta[c*3 + 0].  Token i of chunk c is row
+ *   dense: k + c*k_stride[0] + l*k_stride[1] + (row_base[c] + i)*k_stride[2]
+ *            + h*k_stride[3]          (row_base NULL = 0)
+ *   paged: k + l*k_stride[1] + slot*k_stride[2] + h*k_stride[3],
+ *          slot as in kamera_rehydrate. */
+typedef struct {
+  int32_t n_chunks;
+  int32_t n_layers;
+  int32_t n_heads;
+  int32_t head_dim;
+  int32_t n_tokens;
+  const int32_t* chunk_tokens;
+  kamera_rope rope;
+  const int32_t* delta;
+  void* k;
+  int64_t k_stride[4];
+  int32_t paged;
+  const int32_t* row_base;
+  const int32_t* page_table;
+  int32_t pt_stride;
+  int32_t page_size;
+  int32_t n_pool_pages;
+  uint32_t* status;
+} kamera_shift_args;
+
+/* kamera_scatter_paged -- bit-exact copy of dense token rows into a paged
+ * pool (the copy half of the conditioning switch, App. E; the pool is the
+ * paged KV store the serve step writes into, Sec. 6).  Token i of chunk c,
+ * layer l: row_bytes bytes from
+ *   src + c*src_stride_bytes[0] + l*src_stride_bytes[1] + i*src_stride_bytes[2]
+ * to pool + l*pool_stride_bytes[0] + slot*pool_stride_bytes[1], slot as in
+ * kamera_rehydrate.  row_bytes and all strides: multiples of 16. */
+typedef struct {
+  int32_t n_chunks;
+  int32_t n_layers;
+  int32_t n_tokens;
+  const int32_t* chunk_tokens;
+  int64_t row_bytes;
+  const void* src;
+  int64_t src_stride_bytes[3];
+  void* pool;
+  int64_t pool_stride_bytes[2];
+  const int32_t* page_table;
+  int32_t pt_stride;
+  int32_t page_size;
+  int32_t n_pool_pages;
+  uint32_t* status;
+} kamera_scatter_args;
+
+int kamera_rehydrate(const kamera_rehydrate_args* args, void* stream);
+int kamera_shift(const kamera_shift_args* args, void* stream);
+int kamera_scatter_paged(const kamera_scatter_args* args, void* stream);
+
+/* Host-side check of a page table copy (host memory, n_chunks x pt_stride,
+ * the first ceil(tokens/page_size) entries of each row are used): every used
+ * entry in [0, n_pool_pages) and no page used twice.  Returns KAMERA_OK or
+ * KAMERA_ERR_RANGE (out of range) / KAMERA_ERR_ALIAS (duplicate). */
+int kamera_check_page_table(const int32_t* host_page_table, int32_t n_chunks,
+                            int32_t pt_stride, int32_t n_tokens,
+                            int32_t page_size, int32_t n_pool_pages);
+
+/* Text of the last error on the calling thread ("" after a successful call);
+ * valid until the next call on that thread. */
+const char* kamera_last_error(void);
+int kamera_abi_version(void);
+/* sizeof of the argument structs: 0 rehydrate, 1 shift, 2 scatter, 3 plane,
+ * 4 rope; -1 otherwise.  Lets a foreign-function binding check its layout. */
+int64_t kamera_struct_size(int32_t which);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KAMERA_H */

@@ -1,0 +1,491 @@
+// Host side of the Kamera C ABI: argument validation (no HIP call happens
+// before every check has passed), translation into kernel parameters, launch.
+// The operator itself is defined in include/kamera.h.
+
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+#include <vector>
+
+#include "kamera.h"
+#include "kamera_launch.h"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+int fail(int code, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return code;
+}
+
+int ok() {
+  g_err[0] = '\0';
+  return KAMERA_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+constexpr double kTwoPi = 6.283185307179586476925286766559;
+
+// ---------------------------------------------------------------------------
+// RoPE descriptor
+// ---------------------------------------------------------------------------
+
+int check_rope(const kamera_rope& r, int32_t head_dim, const char* who) {
+  if (!(r.theta > 0.0) || !isfinite(r.theta))
+    return fail(KAMERA_ERR_SHAPE, "%s: rope.theta must be a finite positive number (got %g)", who, r.theta);
+  if (r.rope_dim <= 0 || (r.rope_dim & 1))
+    return fail(KAMERA_ERR_SHAPE, "%s: rope.rope_dim must be positive and even (got %d)", who, r.rope_dim);
+  if (r.rope_dim > KAMERA_MAX_ROPE_DIM)
+    return fail(KAMERA_ERR_RANGE, "%s: rope.rope_dim %d exceeds %d", who, r.rope_dim, KAMERA_MAX_ROPE_DIM);
+  if (r.rope_offset < 0 || (int64_t)r.rope_offset + r.rope_dim > head_dim)
+    return fail(KAMERA_ERR_SHAPE, "%s: rope band [%d, %d) lies outside the %d-column row", who,
+                r.rope_offset, r.rope_offset + r.rope_dim, head_dim);
+  if (r.pairing != KAMERA_PAIR_NEOX && r.pairing != KAMERA_PAIR_INTERLEAVED)
+    return fail(KAMERA_ERR_SHAPE, "%s: unknown rope.pairing %d", who, r.pairing);
+  if (r.n_sections != 1 && r.n_sections != 3)
+    return fail(KAMERA_ERR_SHAPE, "%s: rope.n_sections must be 1 or 3 (got %d)", who, r.n_sections);
+  if (r.n_sections == 3) {
+    if (r.sections[0] < 0 || r.sections[1] < 0 || r.sections[2] < 0 ||
+        r.sections[0] + r.sections[1] + r.sections[2] != r.rope_dim / 2)
+      return fail(KAMERA_ERR_SHAPE, "%s: sections %d/%d/%d must be >= 0 and sum to rope_dim/2 = %d", who,
+                  r.sections[0], r.sections[1], r.sections[2], r.rope_dim / 2);
+    if (r.section_order != KAMERA_SECTIONS_BLOCKED && r.section_order != KAMERA_SECTIONS_INTERLEAVED)
+      return fail(KAMERA_ERR_SHAPE, "%s: unknown rope.section_order %d", who, r.section_order);
+  }
+  return KAMERA_OK;
+}
+
+// Frequencies in revolutions per position step, and the (t, h, w) coordinate
+// of each pair.
+void fill_rope(const kamera_rope& r, kamera::RopeParams& o) {
+  memset(&o, 0, sizeof(o));
+  const int half = r.rope_dim / 2;
+  for (int j = 0; j < half; ++j) o.rev_freq[j] = pow(r.theta, -2.0 * j / (double)r.rope_dim) / kTwoPi;
+  if (r.n_sections == 3) {
+    if (r.section_order == KAMERA_SECTIONS_BLOCKED) {
+      for (int j = 0; j < half; ++j)
+        o.coord[j] = (int8_t)(j < r.sections[0] ? 0 : (j < r.sections[0] + r.sections[1] ? 1 : 2));
+    } else {
+      int left[3] = {r.sections[0], r.sections[1], r.sections[2]};
+      int j = 0;
+      while (j < half) {
+        for (int s = 0; s < 3 && j < half; ++s)
+          if (left[s] > 0) {
+            o.coord[j++] = (int8_t)s;
+            --left[s];
+          }
+      }
+    }
+  }
+  o.rope_offset = r.rope_offset;
+  o.rope_dim = r.rope_dim;
+  o.pairing = r.pairing;
+}
+
+// ---------------------------------------------------------------------------
+// placement (dense rows or paged slots)
+// ---------------------------------------------------------------------------
+
+int check_paging(int32_t paged, const int32_t* page_table, int32_t pt_stride, int32_t page_size,
+                 int32_t n_pool_pages, int32_t n_tokens, const char* who) {
+  if (paged != 0 && paged != 1) return fail(KAMERA_ERR_SHAPE, "%s: paged must be 0 or 1", who);
+  if (!paged) return KAMERA_OK;
+  if (page_table == nullptr) return fail(KAMERA_ERR_NULL, "%s: paged output needs a page_table", who);
+  if (page_size <= 0) return fail(KAMERA_ERR_SHAPE, "%s: page_size must be positive (got %d)", who, page_size);
+  if (n_pool_pages <= 0) return fail(KAMERA_ERR_SHAPE, "%s: n_pool_pages must be positive", who);
+  if (pt_stride < ceil_div(n_tokens, page_size))
+    return fail(KAMERA_ERR_SHAPE, "%s: pt_stride %d < %lld pages needed for %d tokens", who, pt_stride,
+                (long long)ceil_div(n_tokens, page_size), n_tokens);
+  return KAMERA_OK;
+}
+
+void fill_place(kamera::Placement& pl, int32_t n_tokens, const int32_t* chunk_tokens, int32_t paged,
+                const int32_t* row_base, const int32_t* page_table, int32_t pt_stride, int32_t page_size,
+                int32_t n_pool_pages, uint32_t* status) {
+  memset(&pl, 0, sizeof(pl));
+  pl.n_tokens = n_tokens;
+  pl.paged = paged;
+  pl.chunk_tokens = chunk_tokens;
+  pl.row_base = paged ? nullptr : row_base;
+  pl.page_table = paged ? page_table : nullptr;
+  pl.pt_stride = pt_stride;
+  pl.page_size = paged ? page_size : 1;
+  pl.n_pool_pages = n_pool_pages;
+  pl.status = status;
+}
+
+bool strides_ok(const int64_t* s, int n) {
+  for (int k = 0; k < n; ++k)
+    if (s[k] % 8 != 0) return false;
+  return true;
+}
+
+// byte range [lo, hi) spanned by a 4-D strided bf16 view with the given extents
+void extent(const void* base, const int64_t* s, const int64_t* ext, int64_t row_elems, uintptr_t& lo,
+            uintptr_t& hi) {
+  int64_t a = 0, b = 0;
+  for (int k = 0; k < 4; ++k) {
+    if (ext[k] <= 0) continue;
+    const int64_t d = (ext[k] - 1) * s[k];
+    if (d < 0) a += d; else b += d;
+  }
+  lo = reinterpret_cast<uintptr_t>(base) + a * 2;
+  hi = reinterpret_cast<uintptr_t>(base) + (b + row_elems) * 2;
+}
+
+bool overlap(uintptr_t a0, uintptr_t a1, uintptr_t b0, uintptr_t b1) { return a0 < b1 && b0 < a1; }
+
+int pick_grid(int64_t n_tasks, int32_t& per_xcd, const char* who) {
+  const int64_t px = ceil_div(n_tasks, 8);
+  // the dispatch packet counts work-items in 32 bits
+  if (px * 8 * kamera::kThreads > 0xFFFFFFFFLL)
+    return fail(KAMERA_ERR_RANGE, "%s: %lld workgroup tasks exceed one launch", who, (long long)n_tasks);
+  per_xcd = (int32_t)px;
+  return KAMERA_OK;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// kamera_rehydrate
+// ---------------------------------------------------------------------------
+
+extern "C" int kamera_rehydrate(const kamera_rehydrate_args* a, void* stream) {
+  const char* who = "kamera_rehydrate";
+  if (a == nullptr) return fail(KAMERA_ERR_NULL, "%s: args is NULL", who);
+  if (a->n_chunks < 0 || a->n_layers < 0 || a->n_heads < 0 || a->n_tokens < 0)
+    return fail(KAMERA_ERR_SHAPE, "%s: negative n_chunks/n_layers/n_heads/n_tokens", who);
+  if (a->head_dim <= 0 || a->head_dim % 32 != 0)
+    return fail(KAMERA_ERR_UNSUPPORTED, "%s: head_dim must be a positive multiple of 32 (got %d)", who, a->head_dim);
+  if (a->head_dim > KAMERA_MAX_HEAD_DIM)
+    return fail(KAMERA_ERR_RANGE, "%s: head_dim %d exceeds %d", who, a->head_dim, KAMERA_MAX_HEAD_DIM);
+  if (a->n_planes != 1 && a->n_planes != 2)
+    return fail(KAMERA_ERR_SHAPE, "%s: n_planes must be 1 or 2 (got %d)", who, a->n_planes);
+  if (a->patch_frame != KAMERA_PATCH_PRE_ROPE && a->patch_frame != KAMERA_PATCH_POST_ROPE)
+    return fail(KAMERA_ERR_SHAPE, "%s: unknown patch_frame %d", who, a->patch_frame);
+  bool any_rot = false;
+  for (int p = 0; p < a->n_planes; ++p) any_rot = any_rot || a->plane[p].rotate;
+  if (any_rot) {
+    int rc = check_rope(a->rope, a->head_dim, who);
+    if (rc) return rc;
+    const kamera_rope& r = a->rope;
+    if (r.rope_offset % 32 != 0 || r.rope_dim % 32 != 0)
+      return fail(KAMERA_ERR_UNSUPPORTED, "%s: the rope band must start and end on a multiple of 32 columns", who);
+    if (r.pairing == KAMERA_PAIR_NEOX && r.rope_dim % 64 != 0)
+      return fail(KAMERA_ERR_UNSUPPORTED, "%s: NeoX pairing needs rope_dim %% 64 == 0 (got %d)", who, r.rope_dim);
+    if (a->pos_mode != KAMERA_POS_LINEAR && a->pos_mode != KAMERA_POS_GRID3 && a->pos_mode != KAMERA_POS_EXPLICIT)
+      return fail(KAMERA_ERR_SHAPE, "%s: unknown pos_mode %d", who, a->pos_mode);
+    if (a->pos_mode == KAMERA_POS_GRID3 && a->grid_w <= 0)
+      return fail(KAMERA_ERR_SHAPE, "%s: GRID3 positions need grid_w > 0", who);
+    if (a->pos_mode == KAMERA_POS_EXPLICIT && a->explicit_chunk_stride < 0)
+      return fail(KAMERA_ERR_SHAPE, "%s: explicit_chunk_stride must be >= 0", who);
+  }
+  for (int p = 0; p < a->n_planes; ++p) {
+    const kamera_plane& q = a->plane[p];
+    if (q.m < 0 || q.m > KAMERA_MAX_RANK)
+      return fail(KAMERA_ERR_RANGE, "%s: plane %d rank m = %d outside [0, %d]", who, p, q.m, KAMERA_MAX_RANK);
+    if (q.rotate != 0 && q.rotate != 1) return fail(KAMERA_ERR_SHAPE, "%s: plane %d rotate must be 0 or 1", who, p);
+    if (q.m > 0) {
+      if (q.patch_offset < 0 || q.patch_dim <= 0 || (int64_t)q.patch_offset + q.patch_dim > a->head_dim)
+        return fail(KAMERA_ERR_SHAPE, "%s: plane %d patch columns [%d, %d) outside the %d-column row", who, p,
+                    q.patch_offset, q.patch_offset + q.patch_dim, a->head_dim);
+      if (q.patch_offset % 8 != 0 || q.patch_dim % 8 != 0)
+        return fail(KAMERA_ERR_UNSUPPORTED, "%s: plane %d patch columns must start/end on multiples of 8", who, p);
+    }
+  }
+  int rc = check_paging(a->paged, a->page_table, a->pt_stride, a->page_size, a->n_pool_pages, a->n_tokens, who);
+  if (rc) return rc;
+
+  const int64_t work = (int64_t)a->n_chunks * a->n_layers * a->n_heads * a->n_tokens;
+  if (work == 0) return ok();  // empty call: nothing to read or write
+
+  if (any_rot && a->pos_mode != KAMERA_POS_EXPLICIT && a->chunk_pos == nullptr)
+    return fail(KAMERA_ERR_NULL, "%s: chunk_pos is NULL", who);
+  if (any_rot && a->pos_mode == KAMERA_POS_EXPLICIT && a->explicit_pos == nullptr)
+    return fail(KAMERA_ERR_NULL, "%s: explicit_pos is NULL", who);
+  for (int p = 0; p < a->n_planes; ++p) {
+    const kamera_plane& q = a->plane[p];
+    if (q.in == nullptr || q.out == nullptr) return fail(KAMERA_ERR_NULL, "%s: plane %d in/out is NULL", who, p);
+    if (q.m > 0 && (q.U == nullptr || q.W == nullptr))
+      return fail(KAMERA_ERR_NULL, "%s: plane %d has m = %d but U or W is NULL", who, p, q.m);
+    if (!aligned16(q.in) || !aligned16(q.out) || !strides_ok(q.in_stride, 4) || !strides_ok(q.out_stride, 4))
+      return fail(KAMERA_ERR_ALIGN, "%s: plane %d in/out rows must be 16-byte aligned (base %% 16, strides %% 8)",
+                  who, p);
+  }
+  // inputs must not be overwritten while other workgroups still read them
+  for (int p = 0; p < a->n_planes; ++p) {
+    const kamera_plane& q = a->plane[p];
+    const int64_t ein[4] = {a->n_chunks, a->n_layers, a->n_tokens, a->n_heads};
+    uintptr_t ilo, ihi;
+    extent(q.in, q.in_stride, ein, a->head_dim, ilo, ihi);
+    for (int o = 0; o < a->n_planes; ++o) {
+      const kamera_plane& r = a->plane[o];
+      uintptr_t olo, ohi;
+      if (a->paged) {
+        const int64_t eo[4] = {1, a->n_layers, (int64_t)a->n_pool_pages * a->page_size, a->n_heads};
+        extent(r.out, r.out_stride, eo, a->head_dim, olo, ohi);
+      } else {
+        extent(r.out, r.out_stride, ein, a->head_dim, olo, ohi);
+      }
+      if (overlap(ilo, ihi, olo, ohi))
+        return fail(KAMERA_ERR_ALIAS, "%s: output of plane %d overlaps the input of plane %d", who, o, p);
+    }
+  }
+
+  kamera::RehydrateParams P;
+  memset(&P, 0, sizeof(P));
+  if (any_rot) fill_rope(a->rope, P.rope);
+  fill_place(P.place, a->n_tokens, a->chunk_tokens, a->paged, a->row_base, a->page_table, a->pt_stride,
+             a->page_size, a->n_pool_pages, a->status);
+  P.chunk_pos = a->chunk_pos;
+  P.explicit_pos = a->explicit_pos;
+  P.explicit_cs = a->explicit_chunk_stride;
+  P.pos_mode = a->pos_mode;
+  P.grid_w = a->grid_w > 0 ? a->grid_w : 1;
+  P.patch_post_rope = a->patch_frame == KAMERA_PATCH_POST_ROPE;
+  P.n_planes = a->n_planes;
+  P.n_chunks = a->n_chunks;
+  P.n_layers = a->n_layers;
+  P.n_heads = a->n_heads;
+
+  int64_t units = 0;
+  for (int p = 0; p < a->n_planes; ++p) {
+    const kamera_plane& q = a->plane[p];
+    kamera::PlaneParams& o = P.plane[p];
+    o.in = static_cast<const uint16_t*>(q.in);
+    o.out = static_cast<uint16_t*>(q.out);
+    o.U = static_cast<const uint16_t*>(q.U);
+    o.W = static_cast<const uint16_t*>(q.W);
+    memcpy(o.in_s, q.in_stride, sizeof(o.in_s));
+    memcpy(o.out_s, q.out_stride, sizeof(o.out_s));
+    memcpy(o.u_s, q.u_stride, sizeof(o.u_s));
+    memcpy(o.w_s, q.w_stride, sizeof(o.w_s));
+    o.m = q.m;
+    o.m_steps = (q.m + 31) / 32;
+    o.patch_lo = q.m > 0 ? q.patch_offset : 0;
+    o.patch_hi = q.m > 0 ? q.patch_offset + q.patch_dim : 0;
+    o.u_vec = q.m % 8 == 0 && aligned16(q.U) && strides_ok(q.u_stride, 4);
+    o.w_vec = aligned16(q.W) && strides_ok(q.w_stride, 4);
+    // column blocks: the rotated band as one block, the rest in <= 128-column pieces
+    std::vector<std::pair<int, int>> segs;  // [col0, col1)
+    const int D = a->head_dim;
+    if (q.rotate) {
+      const int r0 = a->rope.rope_offset, r1 = r0 + a->rope.rope_dim;
+      if (r0 > 0) segs.push_back({0, r0});
+      segs.push_back({r0, r1});
+      if (r1 < D) segs.push_back({r1, D});
+    } else {
+      segs.push_back({0, D});
+    }
+    int nb = 0;
+    for (auto& sg : segs) {
+      const bool band = q.rotate && sg.first == a->rope.rope_offset;
+      for (int c0 = sg.first; c0 < sg.second; c0 += 128) {
+        const int w = band ? sg.second - sg.first : std::min(128, sg.second - c0);
+        if (nb >= kamera::kMaxBlocks) return fail(KAMERA_ERR_RANGE, "%s: too many column blocks", who);
+        kamera::ColBlock& b = o.blk[nb++];
+        b.col0 = (int16_t)(c0 / 8);
+        b.nq = (int8_t)(w / 32);
+        int flags = 0;
+        if (band) flags |= kamera::kBlkRotate;
+        if (q.m > 0 && c0 < o.patch_hi && c0 + w > o.patch_lo) flags |= kamera::kBlkPatch;
+        b.flags = (int8_t)flags;
+        if (band) break;
+      }
+    }
+    o.n_blocks = nb;
+    units += (int64_t)a->n_chunks * a->n_layers * a->n_heads * nb;
+  }
+  // token block: as large as possible while keeping >= 16 workgroups per CU
+  int tb = 1024;
+  while (tb > 64 && units * ceil_div(a->n_tokens, tb) < 4096) tb /= 2;
+  tb = (int)std::min<int64_t>(tb, ceil_div(a->n_tokens, 64) * 64);
+  P.token_block = tb;
+  P.n_tblk = (int32_t)ceil_div(a->n_tokens, tb);
+  int64_t base = 0;
+  for (int p = 0; p < a->n_planes; ++p) {
+    P.plane[p].task_base = (int32_t)base;
+    base += (int64_t)a->n_chunks * a->n_layers * a->n_heads * P.n_tblk * P.plane[p].n_blocks;
+  }
+  if (base >= (int64_t)1 << 31) return fail(KAMERA_ERR_RANGE, "%s: %lld tasks exceed one launch", who, (long long)base);
+  P.n_tasks = base;
+  rc = pick_grid(P.n_tasks, P.per_xcd, who);
+  if (rc) return rc;
+
+  const hipError_t e = kamera::launch_rehydrate(P, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(KAMERA_ERR_HIP, "%s: launch failed: %s", who, hipGetErrorString(e));
+  return ok();
+}
+
+// ---------------------------------------------------------------------------
+// kamera_shift
+// ---------------------------------------------------------------------------
+
+extern "C" int kamera_shift(const kamera_shift_args* a, void* stream) {
+  const char* who = "kamera_shift";
+  if (a == nullptr) return fail(KAMERA_ERR_NULL, "%s: args is NULL", who);
+  if (a->n_chunks < 0 || a->n_layers < 0 || a->n_heads < 0 || a->n_tokens < 0)
+    return fail(KAMERA_ERR_SHAPE, "%s: negative n_chunks/n_layers/n_heads/n_tokens", who);
+  if (a->head_dim <= 0 || a->head_dim % 8 != 0)
+    return fail(KAMERA_ERR_UNSUPPORTED, "%s: head_dim must be a positive multiple of 8 (got %d)", who, a->head_dim);
+  if (a->head_dim > KAMERA_MAX_HEAD_DIM)
+    return fail(KAMERA_ERR_RANGE, "%s: head_dim %d exceeds %d", who, a->head_dim, KAMERA_MAX_HEAD_DIM);
+  int rc = check_rope(a->rope, a->head_dim, who);
+  if (rc) return rc;
+  const kamera_rope& r = a->rope;
+  if (r.rope_offset % 8 != 0)
+    return fail(KAMERA_ERR_UNSUPPORTED, "%s: rope_offset must be a multiple of 8", who);
+  if (r.pairing == KAMERA_PAIR_NEOX && r.rope_dim % 16 != 0)
+    return fail(KAMERA_ERR_UNSUPPORTED, "%s: NeoX pairing needs rope_dim %% 16 == 0", who);
+  if (r.pairing == KAMERA_PAIR_INTERLEAVED && r.rope_dim % 8 != 0)
+    return fail(KAMERA_ERR_UNSUPPORTED, "%s: interleaved pairing needs rope_dim %% 8 == 0", who);
+  rc = check_paging(a->paged, a->page_table, a->pt_stride, a->page_size, a->n_pool_pages, a->n_tokens, who);
+  if (rc) return rc;
+  const int64_t work = (int64_t)a->n_chunks * a->n_layers * a->n_heads * a->n_tokens;
+  if (work == 0) return ok();
+  if (a->k == nullptr) return fail(KAMERA_ERR_NULL, "%s: k is NULL", who);
+  if (a->delta == nullptr) return fail(KAMERA_ERR_NULL, "%s: delta is NULL", who);
+  if (!aligned16(a->k) || !strides_ok(a->k_stride, 4))
+    return fail(KAMERA_ERR_ALIGN, "%s: k rows must be 16-byte aligned (base %% 16, strides %% 8)", who);
+
+  kamera::ShiftParams P;
+  memset(&P, 0, sizeof(P));
+  fill_rope(r, P.rope);
+  fill_place(P.place, a->n_tokens, a->chunk_tokens, a->paged, a->row_base, a->page_table, a->pt_stride,
+             a->page_size, a->n_pool_pages, a->status);
+  P.delta = a->delta;
+  P.k = static_cast<uint16_t*>(a->k);
+  memcpy(P.k_s, a->k_stride, sizeof(P.k_s));
+  P.n_chunks = a->n_chunks;
+  P.n_layers = a->n_layers;
+  P.n_heads = a->n_heads;
+  P.vec_per_row = r.pairing == KAMERA_PAIR_NEOX ? r.rope_dim / 16 : r.rope_dim / 8;
+  // about 2048 rows per task, at least 2048 tasks when the call is large enough
+  int tb = 16;
+  while (tb < 1024 && (int64_t)tb * a->n_heads < 2048) tb *= 2;
+  while (tb > 16 && (int64_t)a->n_chunks * a->n_layers * ceil_div(a->n_tokens, tb) < 2048) tb /= 2;
+  P.token_block = tb;
+  P.n_tblk = (int32_t)ceil_div(a->n_tokens, tb);
+  P.n_tasks = (int64_t)a->n_chunks * a->n_layers * P.n_tblk;
+  rc = pick_grid(P.n_tasks, P.per_xcd, who);
+  if (rc) return rc;
+  const hipError_t e = kamera::launch_shift(P, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(KAMERA_ERR_HIP, "%s: launch failed: %s", who, hipGetErrorString(e));
+  return ok();
+}
+
+// ---------------------------------------------------------------------------
+// kamera_scatter_paged
+// ---------------------------------------------------------------------------
+
+extern "C" int kamera_scatter_paged(const kamera_scatter_args* a, void* stream) {
+  const char* who = "kamera_scatter_paged";
+  if (a == nullptr) return fail(KAMERA_ERR_NULL, "%s: args is NULL", who);
+  if (a->n_chunks < 0 || a->n_layers < 0 || a->n_tokens < 0)
+    return fail(KAMERA_ERR_SHAPE, "%s: negative n_chunks/n_layers/n_tokens", who);
+  if (a->row_bytes <= 0 || a->row_bytes % 16 != 0)
+    return fail(KAMERA_ERR_ALIGN, "%s: row_bytes must be a positive multiple of 16", who);
+  int rc = check_paging(1, a->page_table, a->pt_stride, a->page_size, a->n_pool_pages, a->n_tokens, who);
+  if (rc) return rc;
+  const int64_t work = (int64_t)a->n_chunks * a->n_layers * a->n_tokens;
+  if (work == 0) return ok();
+  if (a->src == nullptr || a->pool == nullptr) return fail(KAMERA_ERR_NULL, "%s: src or pool is NULL", who);
+  for (int k = 0; k < 3; ++k)
+    if (a->src_stride_bytes[k] % 16 != 0) return fail(KAMERA_ERR_ALIGN, "%s: src strides must be multiples of 16", who);
+  for (int k = 0; k < 2; ++k)
+    if (a->pool_stride_bytes[k] % 16 != 0) return fail(KAMERA_ERR_ALIGN, "%s: pool strides must be multiples of 16", who);
+  if (!aligned16(a->src) || !aligned16(a->pool)) return fail(KAMERA_ERR_ALIGN, "%s: src/pool must be 16-byte aligned", who);
+  {
+    // the source rows and the pool must be different memory
+    int64_t a0 = 0, b0 = 0;
+    const int64_t ext[3] = {a->n_chunks, a->n_layers, a->n_tokens};
+    for (int k = 0; k < 3; ++k) {
+      const int64_t d = (ext[k] - 1) * a->src_stride_bytes[k];
+      if (d < 0) a0 += d; else b0 += d;
+    }
+    const uintptr_t slo = reinterpret_cast<uintptr_t>(a->src) + a0, shi = reinterpret_cast<uintptr_t>(a->src) + b0 + a->row_bytes;
+    int64_t a1 = 0, b1 = 0;
+    const int64_t pext[2] = {a->n_layers, (int64_t)a->n_pool_pages * a->page_size};
+    for (int k = 0; k < 2; ++k) {
+      const int64_t d = (pext[k] - 1) * a->pool_stride_bytes[k];
+      if (d < 0) a1 += d; else b1 += d;
+    }
+    const uintptr_t plo = reinterpret_cast<uintptr_t>(a->pool) + a1, phi = reinterpret_cast<uintptr_t>(a->pool) + b1 + a->row_bytes;
+    if (overlap(slo, shi, plo, phi)) return fail(KAMERA_ERR_ALIAS, "%s: src overlaps the pool", who);
+  }
+
+  kamera::ScatterParams P;
+  memset(&P, 0, sizeof(P));
+  fill_place(P.place, a->n_tokens, a->chunk_tokens, 1, nullptr, a->page_table, a->pt_stride, a->page_size,
+             a->n_pool_pages, a->status);
+  P.src = static_cast<const uint8_t*>(a->src);
+  P.pool = static_cast<uint8_t*>(a->pool);
+  memcpy(P.src_s, a->src_stride_bytes, sizeof(P.src_s));
+  memcpy(P.pool_s, a->pool_stride_bytes, sizeof(P.pool_s));
+  P.row_vecs = a->row_bytes / 16;
+  P.n_chunks = a->n_chunks;
+  P.n_layers = a->n_layers;
+  // about 16K 16-byte vectors (256 KiB) per task
+  int tb = 16;
+  while (tb < 1024 && (int64_t)tb * P.row_vecs < 16384) tb *= 2;
+  while (tb > 16 && (int64_t)a->n_chunks * a->n_layers * ceil_div(a->n_tokens, tb) < 2048) tb /= 2;
+  P.token_block = tb;
+  P.n_tblk = (int32_t)ceil_div(a->n_tokens, tb);
+  P.n_tasks = (int64_t)a->n_chunks * a->n_layers * P.n_tblk;
+  rc = pick_grid(P.n_tasks, P.per_xcd, who);
+  if (rc) return rc;
+  const hipError_t e = kamera::launch_scatter(P, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(KAMERA_ERR_HIP, "%s: launch failed: %s", who, hipGetErrorString(e));
+  return ok();
+}
+
+// ---------------------------------------------------------------------------
+// small exports
+// ---------------------------------------------------------------------------
+
+extern "C" int kamera_check_page_table(const int32_t* pt, int32_t n_chunks, int32_t pt_stride, int32_t n_tokens,
+                                       int32_t page_size, int32_t n_pool_pages) {
+  const char* who = "kamera_check_page_table";
+  if (n_chunks < 0 || n_tokens < 0) return fail(KAMERA_ERR_SHAPE, "%s: negative sizes", who);
+  if (n_chunks == 0 || n_tokens == 0) return ok();
+  if (pt == nullptr) return fail(KAMERA_ERR_NULL, "%s: page table is NULL", who);
+  if (page_size <= 0 || n_pool_pages <= 0) return fail(KAMERA_ERR_SHAPE, "%s: page_size and n_pool_pages must be > 0", who);
+  const int64_t used = ceil_div(n_tokens, page_size);
+  if (pt_stride < used) return fail(KAMERA_ERR_SHAPE, "%s: pt_stride %d < %lld pages per chunk", who, pt_stride, (long long)used);
+  std::vector<uint8_t> seen((size_t)n_pool_pages, 0);
+  for (int64_t c = 0; c < n_chunks; ++c)
+    for (int64_t k = 0; k < used; ++k) {
+      const int32_t pg = pt[c * pt_stride + k];
+      if (pg < 0 || pg >= n_pool_pages)
+        return fail(KAMERA_ERR_RANGE, "%s: chunk %lld page %lld = %d outside [0, %d)", who, (long long)c,
+                    (long long)k, pg, n_pool_pages);
+      if (seen[(size_t)pg]) return fail(KAMERA_ERR_ALIAS, "%s: pool page %d is used twice", who, pg);
+      seen[(size_t)pg] = 1;
+    }
+  return ok();
+}
+
+extern "C" const char* kamera_last_error(void) { return g_err; }
+
+extern "C" int kamera_abi_version(void) { return KAMERA_ABI_VERSION; }
+
+extern "C" int64_t kamera_struct_size(int32_t which) {
+  switch (which) {
+    case 0: return (int64_t)sizeof(kamera_rehydrate_args);
+    case 1: return (int64_t)sizeof(kamera_shift_args);
+    case 2: return (int64_t)sizeof(kamera_scatter_args);
+    case 3: return (int64_t)sizeof(kamera_plane);
+    case 4: return (int64_t)sizeof(kamera_rope);
+    default: return -1;
+  }
+}

@@ -1,0 +1,120 @@
+// Launch parameters passed by value to the gfx950 kernels (kernel arguments),
+// built and validated by the host layer in kamera_abi.cpp.
+#pragma once
+
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+namespace kamera {
+
+constexpr int kThreads = 256;        // 4 wave64 per workgroup
+constexpr int kTileTokens = 16;      // tokens per wave tile (MFMA N dimension)
+constexpr int kMaxBlocks = 36;       // column blocks per row (head_dim <= 4096)
+constexpr int kMaxPairs = 64;        // rotated pairs (rope_dim <= 128)
+
+enum BlockFlags : int { kBlkPatch = 1, kBlkRotate = 2 };
+
+// One rotated band: per-pair frequency in revolutions per position unit,
+// theta^(-2j/rope_dim) / (2 pi), in fp64, and the coordinate (t, h, w) it uses.
+struct RopeParams {
+  double rev_freq[kMaxPairs];
+  int8_t coord[kMaxPairs];
+  int32_t rope_offset;
+  int32_t rope_dim;
+  int32_t pairing;                   // 0 NeoX, 1 interleaved
+  int32_t pad_;
+};
+
+struct ColBlock {
+  int16_t col0;                      // first column / 8  (column = 8 * col0)
+  int8_t nq;                         // width = 32 * nq columns (1..4)
+  int8_t flags;                      // kBlkPatch | kBlkRotate
+};
+
+struct PlaneParams {
+  const uint16_t* in;
+  uint16_t* out;
+  const uint16_t* U;
+  const uint16_t* W;
+  int64_t in_s[4];
+  int64_t out_s[4];
+  int64_t u_s[4];
+  int64_t w_s[4];
+  int32_t m;
+  int32_t m_steps;                   // ceil(m / 32): K-steps of the 16x16x32 MFMA
+  int32_t patch_lo;
+  int32_t patch_hi;
+  int32_t u_vec;                     // 16-byte U loads are legal
+  int32_t w_vec;                     // 16-byte W loads are legal
+  int32_t n_blocks;
+  int32_t task_base;                 // first task index of this plane
+  ColBlock blk[kMaxBlocks];
+};
+
+struct Placement {                   // where token i of chunk c lands / sits
+  int32_t n_tokens;
+  int32_t paged;
+  const int32_t* chunk_tokens;
+  const int32_t* row_base;
+  const int32_t* page_table;
+  int32_t pt_stride;
+  int32_t page_size;
+  int32_t n_pool_pages;
+  int32_t pad_;
+  uint32_t* status;
+};
+
+struct RehydrateParams {
+  RopeParams rope;
+  PlaneParams plane[2];
+  Placement place;
+  const int32_t* chunk_pos;
+  const int32_t* explicit_pos;
+  int64_t explicit_cs;
+  int32_t pos_mode;
+  int32_t grid_w;
+  int32_t patch_post_rope;
+  int32_t n_planes;
+  int32_t n_chunks, n_layers, n_heads;
+  int32_t token_block;               // tokens per workgroup task (multiple of 64)
+  int32_t n_tblk;                    // token blocks per chunk
+  int32_t per_xcd;                   // tasks per XCD slice of the grid
+  int64_t n_tasks;
+};
+
+struct ShiftParams {
+  RopeParams rope;
+  Placement place;
+  const int32_t* delta;
+  uint16_t* k;
+  int64_t k_s[4];
+  int32_t n_chunks, n_layers, n_heads;
+  int32_t vec_per_row;               // 16-byte vectors of the band per row
+  int32_t token_block;
+  int32_t n_tblk;
+  int32_t per_xcd;
+  int32_t pad_;
+  int64_t n_tasks;
+};
+
+struct ScatterParams {
+  Placement place;
+  const uint8_t* src;
+  uint8_t* pool;
+  int64_t src_s[3];
+  int64_t pool_s[2];
+  int64_t row_vecs;                  // 16-byte vectors per row
+  int32_t n_chunks, n_layers;
+  int32_t token_block;
+  int32_t n_tblk;
+  int32_t per_xcd;
+  int32_t pad_;
+  int64_t n_tasks;
+};
+
+hipError_t launch_rehydrate(const RehydrateParams& p, hipStream_t s);
+hipError_t launch_shift(const ShiftParams& p, hipStream_t s);
+hipError_t launch_scatter(const ScatterParams& p, hipStream_t s);
+
+}  // namespace kamera

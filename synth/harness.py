@@ -1,0 +1,152 @@
+"""Device set-up of the operator workloads in ``synth.WORKLOADS``.
+
+Builds the seeded device tensors of a workload and a prepared library call
+that performs one pass of it (the unit the benchmark times and the full-size
+parity tests check).  It draws inputs and lays them out; every number the
+operator produces comes from the HIP library.
+"""
+
+from __future__ import annotations
+
+import dataclasses
+from typing import Callable, Dict, List, Optional
+
+import numpy as np
+
+from . import WORKLOADS, Workload, chunk_meta, randn_bf16_device, window_survivor_slots
+
+
+@dataclasses.dataclass
+class Prepared:
+    workload: Workload
+    tensors: Dict[str, object]          # device tensors by name
+    meta: object                        # synth.ChunkMeta
+    step: Callable[[], None]            # one pass of the hot path (one launch)
+    bytes_per_step: int                 # algorithmic bytes (K/V in + U, W + K/V out)
+    chunks_per_step: int
+    extra: Dict[str, object] = dataclasses.field(default_factory=dict)
+
+
+def algorithmic_bytes(w: Workload) -> int:
+    """K/V rows read + patch factors read + K/V rows written, bf16.
+
+    rehydrate, per (chunk, layer, head): 2 planes x (n*D read + n*D written)
+    plus, per patched plane, U (n*m) and W (m*patch_dim).  The page table and
+    positions are excluded.  shift: the rope band of every survivor row read
+    and written.
+    """
+    units = w.n_chunks * w.n_layers * w.n_heads
+    n, D = w.n_tokens, w.head_dim
+    if w.kind == "shift":
+        return units * n * w.rope_dim * 2 * 2
+    planes = 2 if w.has_v else 1
+    b = planes * 2 * n * D * 2
+    for m in ((w.m_k, w.m_v) if w.has_v else (w.m_k,)):
+        if m > 0:
+            b += (n * m + m * w.patch_dim) * 2
+    return units * b
+
+
+def _rope_spec(w: Workload):
+    import paper_2606_23581_amd as km
+
+    return km.RopeSpec(theta=w.theta, rope_dim=w.rope_dim, pairing=w.pairing,
+                       rope_offset=w.rope_offset, sections=w.sections,
+                       section_order=w.section_order)
+
+
+def prepare(name: str, device="cuda", seed: Optional[int] = None) -> Prepared:
+    import torch
+
+    import paper_2606_23581_amd as km
+
+    w = WORKLOADS[name]
+    meta = chunk_meta(w, seed)
+    gen = torch.Generator(device=device)
+    gen.manual_seed(w.seed if seed is None else seed)
+    C, L, H, n, D = w.n_chunks, w.n_layers, w.n_heads, w.n_tokens, w.head_dim
+    rope = _rope_spec(w)
+    T: Dict[str, object] = {}
+
+    if w.kind == "shift":
+        # ring window of S chunk slots [L, S*n, H, D], already rotated keys
+        S = w.window_slots
+        T["window"] = randn_bf16_device((L, S * n, H, D), 1.0, gen, device, slab_dim=0)
+        T["delta"] = torch.from_numpy(meta.delta).to(device)
+        state = {"slide": 0}
+        T["row_base"] = torch.zeros(C, dtype=torch.int32, device=device)
+
+        def set_slide(k):
+            slots = window_survivor_slots(w, k)
+            T["row_base"].copy_(torch.from_numpy((slots * n).astype(np.int32)))
+            state["slide"] = k
+
+        set_slide(0)
+        call = km.prepare_shift(T["window"], T["delta"], rope=rope, n_chunks=C, n_tokens=n,
+                                row_base=T["row_base"])
+
+        def step():
+            call.launch()
+
+        p = Prepared(w, T, meta, step, algorithmic_bytes(w), C)
+        p.extra["set_slide"] = set_slide
+        p.extra["call"] = call
+        return p
+
+    T["k_in"] = randn_bf16_device((C, L, n, H, D), 1.0, gen, device)
+    if w.has_v:
+        T["v_in"] = randn_bf16_device((C, L, n, H, D), 1.0, gen, device)
+    if w.m_k > 0:
+        T["u_k"] = randn_bf16_device((C, L, H, n, w.m_k), w.u_std, gen, device)
+        T["w_k"] = randn_bf16_device((C, L, H, w.m_k, w.patch_dim), w.w_std, gen, device)
+    if w.has_v and w.m_v > 0:
+        T["u_v"] = randn_bf16_device((C, L, H, n, w.m_v), w.u_std, gen, device)
+        T["w_v"] = randn_bf16_device((C, L, H, w.m_v, w.patch_dim), w.w_std, gen, device)
+    T["chunk_pos"] = torch.from_numpy(meta.pos).to(device)
+    kw = dict(rope=rope, chunk_pos=T["chunk_pos"], u_k=T.get("u_k"), w_k=T.get("w_k"),
+              k_patch=(w.patch_offset, w.patch_dim),
+              pos_mode=km.POS_GRID3 if w.pos_mode == "grid3" else km.POS_LINEAR, grid_w=w.grid_w)
+    if w.paged:
+        slots = w.n_pool_pages * w.page_size
+        T["k_pool"] = torch.zeros((L, slots, H, D), dtype=torch.bfloat16, device=device)
+        T["page_table"] = torch.from_numpy(meta.page_table).to(device)
+        kw.update(page_table=T["page_table"], page_size=w.page_size, n_pool_pages=w.n_pool_pages)
+        k_out = T["k_pool"]
+        if w.has_v:
+            T["v_pool"] = torch.zeros((L, slots, H, D), dtype=torch.bfloat16, device=device)
+            v_out = T["v_pool"]
+    else:
+        rows = int(meta.row_base.max()) + n
+        T["k_out_rows"] = torch.zeros((L, rows, H, D), dtype=torch.bfloat16, device=device)
+        k_out = T["k_out_rows"].unsqueeze(0).expand(C, L, rows, H, D)
+        T["row_base"] = torch.from_numpy(meta.row_base).to(device)
+        kw["row_base"] = T["row_base"]
+        if w.has_v:
+            T["v_out_rows"] = torch.zeros((L, rows, H, D), dtype=torch.bfloat16, device=device)
+            v_out = T["v_out_rows"].unsqueeze(0).expand(C, L, rows, H, D)
+    if w.has_v:
+        kw.update(v_in=T["v_in"], v_out=v_out, u_v=T.get("u_v"), w_v=T.get("w_v"),
+                  v_patch=(w.patch_offset, w.patch_dim))
+    call = km.prepare_rehydrate(T["k_in"], k_out, **kw)
+
+    def step():
+        call.launch()
+
+    p = Prepared(w, T, meta, step, algorithmic_bytes(w), C)
+    p.extra["call"] = call
+    return p
+
+
+def sample_units(w: Workload, k: int, seed: int = 0) -> List[tuple]:
+    """k distinct (chunk, layer, head) units, always including the first and last."""
+    rng = np.random.default_rng(seed)
+    total = w.n_chunks * w.n_layers * w.n_heads
+    idx = set([0, total - 1])
+    while len(idx) < min(k, total):
+        idx.add(int(rng.integers(0, total)))
+    out = []
+    for u in sorted(idx):
+        c, rem = divmod(u, w.n_layers * w.n_heads)
+        l, h = divmod(rem, w.n_heads)
+        out.append((c, l, h))
+    return out

@@ -1,0 +1,342 @@
+"""The C-ABI library on the host: it loads, exports every declared symbol, and
+rejects bad arguments before any HIP call (no GPU needed for any of this)."""
+
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+import paper_2606_23581_amd as km
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "kamera.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(km.LIB_PATH), reason="libkamera.so not built")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[a-z_0-9]+\s*\*?\s*(kamera_[a-z_0-9]+)\s*\(", text, re.M)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for want in ("kamera_rehydrate", "kamera_shift", "kamera_scatter_paged", "kamera_last_error",
+                 "kamera_abi_version", "kamera_check_page_table", "kamera_struct_size"):
+        assert want in names
+
+
+def test_library_exports_every_declared_symbol():
+    out = subprocess.run(["nm", "-D", "--defined-only", km.LIB_PATH], capture_output=True, text=True,
+                         check=True).stdout
+    exported = set(re.findall(r"\bT\s+(kamera_[a-z_0-9]+)$", out, re.M))
+    for name in declared_functions():
+        assert name in exported, name
+    L = km.lib()
+    for name in declared_functions():
+        assert hasattr(L, name)
+
+
+def test_version_and_struct_layout():
+    L = km.lib()
+    assert L.kamera_abi_version() == 1
+    assert L.kamera_struct_size(0) == ctypes.sizeof(km.CRehydrateArgs)
+    assert L.kamera_struct_size(1) == ctypes.sizeof(km.CShiftArgs)
+    assert L.kamera_struct_size(2) == ctypes.sizeof(km.CScatterArgs)
+    assert L.kamera_struct_size(3) == ctypes.sizeof(km.CPlane)
+    assert L.kamera_struct_size(4) == ctypes.sizeof(km.CRope)
+    assert L.kamera_struct_size(99) == -1
+
+
+# ---------------------------------------------------------------------------
+# validation: fake, never dereferenced device addresses
+# ---------------------------------------------------------------------------
+
+FAKE = 0x7F0000000000      # 16-byte aligned, never touched: every case fails before a launch
+
+
+def rehydrate_args(**over):
+    a = km.CRehydrateArgs()
+    a.n_chunks, a.n_layers, a.n_heads, a.head_dim, a.n_tokens = 2, 3, 4, 128, 64
+    a.rope = km.RopeSpec(theta=1e6, rope_dim=128).to_c()
+    a.pos_mode = km.POS_LINEAR
+    a.chunk_pos = FAKE + 0x100000000
+    a.n_planes = 2
+    big = 1 << 32
+    for p in range(2):
+        pl = a.plane[p]
+        pl.in_ = FAKE + (p + 1) * big * 4
+        pl.out = FAKE + (p + 3) * big * 4
+        strides = [3 * 64 * 4 * 128, 64 * 4 * 128, 4 * 128, 128]
+        for k in range(4):
+            pl.in_stride[k] = strides[k]
+            pl.out_stride[k] = strides[k]
+        pl.U = FAKE + (p + 5) * big * 4
+        pl.W = FAKE + (p + 7) * big * 4
+        us = [3 * 4 * 64 * 16, 4 * 64 * 16, 64 * 16, 16]
+        ws = [3 * 4 * 16 * 128, 4 * 16 * 128, 16 * 128, 128]
+        for k in range(4):
+            pl.u_stride[k] = us[k]
+            pl.w_stride[k] = ws[k]
+        pl.m = 16
+        pl.rotate = 1 if p == 0 else 0
+        pl.patch_offset, pl.patch_dim = 0, 128
+    for k, v in over.items():
+        setattr(a, k, v)
+    return a
+
+
+def call_rehydrate(a):
+    return km.lib().kamera_rehydrate(ctypes.byref(a), None)
+
+
+def test_empty_call_is_a_noop():
+    a = rehydrate_args()
+    a.n_tokens = 0
+    assert call_rehydrate(a) == km.OK
+    assert km.last_error() == ""
+
+
+@pytest.mark.parametrize("case,code", [
+    ("null_args", km.ERR_NULL),
+    ("negative", km.ERR_SHAPE),
+    ("head_dim_not_32", km.ERR_UNSUPPORTED),
+    ("head_dim_huge", km.ERR_RANGE),
+    ("n_planes_3", km.ERR_SHAPE),
+    ("rope_odd", km.ERR_SHAPE),
+    ("rope_outside_row", km.ERR_SHAPE),
+    ("rope_too_wide", km.ERR_RANGE),
+    ("sections_sum", km.ERR_SHAPE),
+    ("theta_negative", km.ERR_SHAPE),
+    ("neox_32", km.ERR_UNSUPPORTED),
+    ("band_unaligned", km.ERR_UNSUPPORTED),
+    ("rank_too_big", km.ERR_RANGE),
+    ("rank_negative", km.ERR_RANGE),
+    ("patch_outside", km.ERR_SHAPE),
+    ("patch_unaligned", km.ERR_UNSUPPORTED),
+    ("u_null", km.ERR_NULL),
+    ("in_null", km.ERR_NULL),
+    ("pos_null", km.ERR_NULL),
+    ("misaligned_base", km.ERR_ALIGN),
+    ("misaligned_stride", km.ERR_ALIGN),
+    ("alias", km.ERR_ALIAS),
+    ("paged_no_table", km.ERR_NULL),
+    ("paged_short_table", km.ERR_SHAPE),
+    ("paged_page_size", km.ERR_SHAPE),
+    ("grid_w_zero", km.ERR_SHAPE),
+    ("bad_pos_mode", km.ERR_SHAPE),
+    ("bad_frame", km.ERR_SHAPE),
+])
+def test_rehydrate_rejects(case, code):
+    L = km.lib()
+    if case == "null_args":
+        assert L.kamera_rehydrate(None, None) == code
+        assert "NULL" in km.last_error()
+        return
+    a = rehydrate_args()
+    if case == "negative":
+        a.n_layers = -1
+    elif case == "head_dim_not_32":
+        a.head_dim = 120
+    elif case == "head_dim_huge":
+        a.head_dim = 8192
+    elif case == "n_planes_3":
+        a.n_planes = 3
+    elif case == "rope_odd":
+        a.rope.rope_dim = 127
+    elif case == "rope_outside_row":
+        a.rope.rope_offset = 64
+    elif case == "rope_too_wide":
+        a.head_dim = 256
+        a.rope.rope_dim = 256
+    elif case == "sections_sum":
+        a.rope.n_sections = 3
+        a.rope.sections[0], a.rope.sections[1], a.rope.sections[2] = 16, 24, 23
+    elif case == "theta_negative":
+        a.rope.theta = -1.0
+    elif case == "neox_32":
+        a.rope.rope_dim = 32
+    elif case == "band_unaligned":
+        a.rope.rope_offset = 16
+        a.rope.rope_dim = 64
+        a.rope.pairing = km.PAIR_INTERLEAVED
+    elif case == "rank_too_big":
+        a.plane[0].m = 129
+    elif case == "rank_negative":
+        a.plane[1].m = -2
+    elif case == "patch_outside":
+        a.plane[0].patch_offset = 64
+    elif case == "patch_unaligned":
+        a.plane[0].patch_dim = 100
+    elif case == "u_null":
+        a.plane[1].U = None
+    elif case == "in_null":
+        a.plane[0].in_ = None
+    elif case == "pos_null":
+        a.chunk_pos = None
+    elif case == "misaligned_base":
+        a.plane[0].out = a.plane[0].out + 2
+    elif case == "misaligned_stride":
+        a.plane[1].in_stride[2] = 4 * 128 + 4
+    elif case == "alias":
+        a.plane[1].out = a.plane[0].in_ + 4096
+    elif case == "paged_no_table":
+        a.paged = 1
+        a.page_size, a.n_pool_pages, a.pt_stride = 16, 64, 4
+    elif case == "paged_short_table":
+        a.paged = 1
+        a.page_table = FAKE + (9 << 36)
+        a.page_size, a.n_pool_pages, a.pt_stride = 16, 64, 3
+    elif case == "paged_page_size":
+        a.paged = 1
+        a.page_table = FAKE + (9 << 36)
+        a.page_size, a.n_pool_pages, a.pt_stride = 0, 64, 4
+    elif case == "grid_w_zero":
+        a.pos_mode = km.POS_GRID3
+        a.grid_w = 0
+    elif case == "bad_pos_mode":
+        a.pos_mode = 7
+    elif case == "bad_frame":
+        a.patch_frame = 5
+    assert call_rehydrate(a) == code, km.last_error()
+    assert km.last_error().startswith("kamera_rehydrate")
+
+
+def test_error_text_is_per_thread():
+    import threading
+
+    a = rehydrate_args()
+    a.head_dim = 120
+    assert call_rehydrate(a) == km.ERR_UNSUPPORTED
+    seen = {}
+
+    def other():
+        seen["text"] = km.last_error()
+
+    th = threading.Thread(target=other)
+    th.start()
+    th.join()
+    assert seen["text"] == ""
+    assert "head_dim" in km.last_error()
+
+
+def shift_args():
+    a = km.CShiftArgs()
+    a.n_chunks, a.n_layers, a.n_heads, a.head_dim, a.n_tokens = 3, 2, 4, 128, 32
+    a.rope = km.RopeSpec(theta=1e4, rope_dim=128, pairing="interleaved").to_c()
+    a.delta = FAKE
+    a.k = FAKE + (1 << 36)
+    for k, s in enumerate([2 * 32 * 4 * 128, 32 * 4 * 128, 4 * 128, 128]):
+        a.k_stride[k] = s
+    return a
+
+
+@pytest.mark.parametrize("case,code", [
+    ("k_null", km.ERR_NULL), ("delta_null", km.ERR_NULL), ("rope_dim_12_neox", km.ERR_UNSUPPORTED),
+    ("offset_4", km.ERR_UNSUPPORTED), ("misaligned", km.ERR_ALIGN), ("band_outside", km.ERR_SHAPE),
+    ("paged_no_table", km.ERR_NULL),
+])
+def test_shift_rejects(case, code):
+    a = shift_args()
+    if case == "k_null":
+        a.k = None
+    elif case == "delta_null":
+        a.delta = None
+    elif case == "rope_dim_12_neox":
+        a.rope.pairing = km.PAIR_NEOX
+        a.rope.rope_dim = 24
+    elif case == "offset_4":
+        a.rope.rope_offset = 4
+        a.rope.rope_dim = 64
+    elif case == "misaligned":
+        a.k_stride[3] = 132
+    elif case == "band_outside":
+        a.rope.rope_offset = 8
+    elif case == "paged_no_table":
+        a.paged = 1
+        a.page_size, a.pt_stride, a.n_pool_pages = 16, 2, 8
+    assert km.lib().kamera_shift(ctypes.byref(a), None) == code, km.last_error()
+
+
+def test_shift_empty_ok():
+    a = shift_args()
+    a.n_chunks = 0
+    a.k = None
+    assert km.lib().kamera_shift(ctypes.byref(a), None) == km.OK
+
+
+def scatter_args():
+    a = km.CScatterArgs()
+    a.n_chunks, a.n_layers, a.n_tokens = 2, 3, 40
+    a.row_bytes = 2048
+    a.src = FAKE
+    a.src_stride_bytes[0], a.src_stride_bytes[1], a.src_stride_bytes[2] = 3 * 40 * 2048, 40 * 2048, 2048
+    a.pool = FAKE + (1 << 36)
+    a.pool_stride_bytes[0], a.pool_stride_bytes[1] = 64 * 16 * 2048, 2048
+    a.page_table = FAKE + (2 << 36)
+    a.pt_stride, a.page_size, a.n_pool_pages = 3, 16, 64
+    return a
+
+
+@pytest.mark.parametrize("case,code", [
+    ("row_bytes", km.ERR_ALIGN), ("src_null", km.ERR_NULL), ("table_null", km.ERR_NULL),
+    ("short_table", km.ERR_SHAPE), ("stride", km.ERR_ALIGN), ("alias", km.ERR_ALIAS),
+])
+def test_scatter_rejects(case, code):
+    a = scatter_args()
+    if case == "row_bytes":
+        a.row_bytes = 2040
+    elif case == "src_null":
+        a.src = None
+    elif case == "table_null":
+        a.page_table = None
+    elif case == "short_table":
+        a.pt_stride = 2
+    elif case == "stride":
+        a.src_stride_bytes[2] = 2056
+    elif case == "alias":
+        a.pool = a.src + 4096
+    assert km.lib().kamera_scatter_paged(ctypes.byref(a), None) == code, km.last_error()
+
+
+def test_check_page_table():
+    pt = np.arange(12, dtype=np.int32).reshape(3, 4)
+    km.check_page_table(pt, n_tokens=64, page_size=16, n_pool_pages=12)
+    bad = pt.copy()
+    bad[2, 1] = 3
+    with pytest.raises(km.KameraError) as e:
+        km.check_page_table(bad, n_tokens=64, page_size=16, n_pool_pages=12)
+    assert e.value.code == km.ERR_ALIAS
+    bad = pt.copy()
+    bad[1, 0] = 12
+    with pytest.raises(km.KameraError) as e:
+        km.check_page_table(bad, n_tokens=64, page_size=16, n_pool_pages=12)
+    assert e.value.code == km.ERR_RANGE
+    # only the pages the tokens use are checked: 40 tokens need 3 of the 4
+    tail = pt.copy()
+    tail[:, 3] = -1
+    km.check_page_table(tail, n_tokens=40, page_size=16, n_pool_pages=12)
+
+
+def test_product_path_has_no_fallback(monkeypatch):
+    """Without the library every entry point raises; nothing runs on the CPU."""
+    monkeypatch.setattr(km, "_LIB", None)
+    monkeypatch.setattr(km, "LIB_PATH", km.LIB_PATH + ".missing")
+    with pytest.raises(km.KameraUnavailable):
+        km.lib()
+    with pytest.raises(km.KameraUnavailable):
+        km.check_page_table(np.zeros((1, 1), np.int32), 16, 16, 1)
+
+
+def test_product_package_does_not_import_the_oracle():
+    pkg = os.path.join(ROOT, "paper_2606_23581_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".hip", ".cpp", ".h")):
+                text = open(os.path.join(dirpath, f)).read()
+                assert "oracle" not in text.replace("oracles", ""), f

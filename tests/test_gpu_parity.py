@@ -1,0 +1,268 @@
+"""HIP library vs the fp64 reference on small seeded cases (several 16-token
+tiles, ragged tails, every RoPE variant, ranks 0..128, dense and paged)."""
+
+from __future__ import annotations
+
+import zlib
+
+import numpy as np
+import pytest
+
+import oracle as ref
+import synth
+from tests.gpu_util import (SENTINEL, RehydrateCase, assert_close, bits, dev, dev_i32, oracle_rope,
+                            require_gpu, run_rehydrate)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def device():
+    return require_gpu()
+
+
+REHYDRATE_CASES = {
+    "gqa_neox_m16": RehydrateCase(),
+    "gqa_neox_m0": RehydrateCase(m_k=0, m_v=0, seed=1),
+    "gqa_neox_m8": RehydrateCase(m_k=8, m_v=8, n=37, seed=2),
+    "gqa_neox_m32_m64": RehydrateCase(m_k=32, m_v=64, seed=3),
+    "gqa_full_rank_128": RehydrateCase(m_k=128, m_v=128, n=48, C=1, L=1, H=2, seed=4),
+    "gqa_odd_rank_5_33": RehydrateCase(m_k=5, m_v=33, n=50, seed=5),
+    "gqa_interleaved": RehydrateCase(pairing="interleaved", theta=1e4, seed=6),
+    "gqa_large_positions": RehydrateCase(p0_range=(1 << 20, (1 << 20) + 5000), seed=7),
+    "gqa_negative_positions": RehydrateCase(p0_range=(-70000, -1000), seed=8),
+    "gqa_one_token": RehydrateCase(n=1, seed=9),
+    "gqa_ragged": RehydrateCase(ragged=True, n=90, C=4, seed=10),
+    "gqa_post_rope_frame": RehydrateCase(post_rope=True, seed=11),
+    "gqa_shared_basis": RehydrateCase(shared_w=True, C=3, seed=12),
+    "gqa_partial_rotary": RehydrateCase(rope_dim=64, rope_offset=64, pairing="neox", patch=(32, 64), seed=13),
+    "gqa_d256": RehydrateCase(D=256, rope_dim=128, rope_offset=128, patch=(0, 256), n=40, seed=14),
+    "mla_interleaved": RehydrateCase(D=576, H=1, rope_dim=64, rope_offset=512, pairing="interleaved",
+                                     theta=1e4, patch=(0, 512), m_k=32, has_v=False, n=77, seed=15),
+    "mla_neox": RehydrateCase(D=576, H=1, rope_dim=64, rope_offset=512, pairing="neox", theta=1e4,
+                              patch=(0, 512), m_k=32, has_v=False, n=50, seed=16),
+    "mrope_blocked_grid_paged": RehydrateCase(sections=(16, 24, 24), pos_mode="grid3", grid_w=32,
+                                              paged=True, m_k=64, m_v=64, n=96, p0_range=(1, 4097),
+                                              seed=17),
+    "mrope_interleaved_grid7_paged": RehydrateCase(sections=(24, 20, 20), section_order="interleaved",
+                                                   pos_mode="grid3", grid_w=7, paged=True, page_size=5,
+                                                   n=61, seed=18),
+    "explicit_positions": RehydrateCase(sections=(16, 24, 24), pos_mode="explicit", n=45, seed=19),
+    "paged_page_size_1": RehydrateCase(paged=True, page_size=1, n=20, seed=20),
+}
+
+
+@pytest.mark.parametrize("name", sorted(REHYDRATE_CASES))
+def test_rehydrate_matches_oracle(device, name):
+    print(f"[case] rehydrate {name}", flush=True)
+    run_rehydrate(REHYDRATE_CASES[name], device)
+
+
+def test_rehydrate_identity_is_bit_exact(device):
+    """Position 0 with no patch reproduces the stored bits at the page slots."""
+    import paper_2606_23581_amd as km
+    import torch
+
+    print("[case] rehydrate identity", flush=True)
+    rng = np.random.default_rng(30)
+    C, L, n, H, D, P = 3, 2, 45, 2, 128, 16
+    K = synth.randn_bf16_numpy((C, L, n, H, D), 1.0, rng)
+    pages = (n + P - 1) // P
+    pt = rng.permutation(C * pages + 2)[: C * pages].reshape(C, pages).astype(np.int32)
+    slots = (C * pages + 2) * P
+    for pairing in ("neox", "interleaved"):
+        pool = dev(np.full((L, slots, H, D), SENTINEL, np.uint16), device)
+        # every token at position 0 (explicit positions; a linear p0 = 0 puts token i at i)
+        km.rehydrate(dev(K, device), pool, rope=km.RopeSpec(theta=1e4, rope_dim=128, pairing=pairing),
+                     pos_mode=km.POS_EXPLICIT, explicit_pos=dev_i32(np.zeros((C, n, 3)), device),
+                     page_table=dev_i32(pt, device), page_size=P, n_pool_pages=C * pages + 2)
+        torch.cuda.synchronize()
+        out = bits(pool)
+        for c in range(C):
+            for i in range(n):
+                s = ref.paged_slot(pt[c], i, P)
+                assert np.array_equal(out[:, s], K[c, :, i]), (pairing, c, i)
+
+
+def test_rehydrate_empty_call_writes_nothing(device):
+    import paper_2606_23581_amd as km
+    import torch
+
+    print("[case] rehydrate empty", flush=True)
+    K = dev(np.zeros((2, 1, 0, 2, 128), np.uint16), device)
+    out = dev(np.full((2, 1, 4, 2, 128), SENTINEL, np.uint16), device)
+    km.rehydrate(K, out, rope=km.RopeSpec(theta=1e4, rope_dim=128), chunk_pos=dev_i32(np.zeros((2, 3)), device))
+    torch.cuda.synchronize()
+    assert np.all(bits(out) == SENTINEL)
+
+
+def test_rehydrate_bad_page_is_flagged_not_written(device):
+    """A page number outside the pool is skipped by the kernel and flagged."""
+    import paper_2606_23581_amd as km
+    import torch
+
+    print("[case] rehydrate bad page", flush=True)
+    rng = np.random.default_rng(31)
+    C, L, n, H, D, P = 1, 1, 32, 2, 128, 16
+    K = synth.randn_bf16_numpy((C, L, n, H, D), 1.0, rng)
+    pt = np.array([[1, 7]], dtype=np.int32)       # page 7 is outside a 3-page pool
+    pool = dev(np.full((L, 3 * P, H, D), SENTINEL, np.uint16), device)
+    status = dev_i32(np.zeros(1), device)
+    km.rehydrate(dev(K, device), pool, rope=km.RopeSpec(theta=1e4, rope_dim=128),
+                 pos_mode=km.POS_EXPLICIT, explicit_pos=dev_i32(np.zeros((C, n, 3)), device),
+                 page_table=dev_i32(pt, device), page_size=P, n_pool_pages=3, status=status)
+    torch.cuda.synchronize()
+    assert int(status.cpu()[0]) & km.STATUS_BAD_PAGE
+    out = bits(pool)
+    assert np.array_equal(out[0, P:2 * P], K[0, 0, :P])     # page 1 written (position 0: identity)
+    assert np.all(out[0, :P] == SENTINEL) and np.all(out[0, 2 * P:] == SENTINEL)
+
+
+# ---------------------------------------------------------------------------
+# shift
+# ---------------------------------------------------------------------------
+
+SHIFT_CASES = {
+    "interleaved_5d": dict(pairing="interleaved", theta=1e4, rope_dim=128, D=128, layout="5d"),
+    "neox_rowbase": dict(pairing="neox", theta=1e6, rope_dim=128, D=128, layout="rowbase"),
+    "neox_partial_band": dict(pairing="neox", theta=1e6, rope_dim=64, rope_offset=64, D=128, layout="5d"),
+    "mla_band": dict(pairing="interleaved", theta=1e4, rope_dim=64, rope_offset=512, D=576, H=1, layout="5d"),
+    "mrope_sections_paged": dict(pairing="neox", theta=1e6, rope_dim=128, D=128, sections=(16, 24, 24),
+                                 layout="paged"),
+    "interleaved_rd48_ragged": dict(pairing="interleaved", theta=1e4, rope_dim=48, rope_offset=16, D=64,
+                                    layout="5d", ragged=True),
+}
+
+
+@pytest.mark.parametrize("name", sorted(SHIFT_CASES))
+def test_shift_matches_oracle(device, name):
+    import paper_2606_23581_amd as km
+    import torch
+
+    print(f"[case] shift {name}", flush=True)
+    cfg = dict(SHIFT_CASES[name])
+    rng = np.random.default_rng(zlib.crc32(name.encode()))
+    C, L, n = 3, 2, 70
+    H = cfg.get("H", 3)
+    D = cfg["D"]
+    rs = km.RopeSpec(theta=cfg["theta"], rope_dim=cfg["rope_dim"], pairing=cfg["pairing"],
+                     rope_offset=cfg.get("rope_offset", 0), sections=cfg.get("sections"))
+    orope = oracle_rope(rs)
+    delta = rng.integers(-9000, 9000, size=(C, 3)).astype(np.int32)
+    if cfg.get("sections") is None:
+        delta[:, 1:] = delta[:, :1]
+    n_c = rng.integers(0, n + 1, size=C).astype(np.int32) if cfg.get("ragged") else np.full(C, n, np.int32)
+    status = dev_i32(np.zeros(1), device)
+    layout = cfg["layout"]
+    if layout == "5d":
+        Kb = synth.randn_bf16_numpy((C, L, n, H, D), 1.0, rng)
+        kt = dev(Kb, device)
+        km.shift(kt, dev_i32(delta, device), rope=rs, status=status,
+                 chunk_tokens=dev_i32(n_c, device) if cfg.get("ragged") else None)
+        torch.cuda.synchronize()
+        out = bits(kt)
+        for c in range(C):
+            for l in range(L):
+                for h in range(H):
+                    nc = int(n_c[c])
+                    want = ref.shift_k(ref.bf16_to_f64(Kb[c, l, :nc, h]), orope, delta[c])
+                    assert_close(out[c, l, :nc, h], want, f"c{c} l{l} h{h}")
+                    assert np.array_equal(out[c, l, nc:, h], Kb[c, l, nc:, h])
+        band = slice(rs.rope_offset, rs.rope_offset + rs.rope_dim)
+        outside = np.ones(D, bool)
+        outside[band] = False
+        assert np.array_equal(out[..., outside], Kb[..., outside]), "columns outside the band changed"
+    else:
+        rows = C * n + 11
+        Wb = synth.randn_bf16_numpy((L, rows, H, D), 1.0, rng)
+        wt = dev(Wb, device)
+        if layout == "rowbase":
+            rb = (rng.permutation(C) * n + 5).astype(np.int32)
+            km.shift(wt, dev_i32(delta, device), rope=rs, n_chunks=C, n_tokens=n,
+                     row_base=dev_i32(rb, device), status=status)
+            dst = [rb[c] + np.arange(n) for c in range(C)]
+        else:
+            P = 16
+            pages = (n + P - 1) // P
+            npp = rows // P
+            pt = rng.permutation(npp)[: C * pages].reshape(C, pages).astype(np.int32)
+            km.shift(wt, dev_i32(delta, device), rope=rs, n_chunks=C, n_tokens=n,
+                     page_table=dev_i32(pt, device), page_size=P, n_pool_pages=npp, status=status)
+            dst = [np.array([ref.paged_slot(pt[c], i, P) for i in range(n)]) for c in range(C)]
+        torch.cuda.synchronize()
+        out = bits(wt)
+        touched = np.zeros((rows,), bool)
+        for c in range(C):
+            touched[dst[c]] = True
+            for l in range(L):
+                for h in range(H):
+                    want = ref.shift_k(ref.bf16_to_f64(Wb[l, dst[c], h]), orope, delta[c])
+                    assert_close(out[l, dst[c], h], want, f"c{c} l{l} h{h}")
+        assert np.array_equal(out[:, ~touched], Wb[:, ~touched]), "rows of other chunks changed"
+    assert int(status.cpu()[0]) == 0
+
+
+def test_shift_round_trip(device):
+    """Shift by delta then -delta returns the keys within two bf16 roundings."""
+    import paper_2606_23581_amd as km
+    import torch
+
+    print("[case] shift round trip", flush=True)
+    rng = np.random.default_rng(40)
+    Kb = synth.randn_bf16_numpy((2, 2, 64, 4, 128), 1.0, rng)
+    kt = dev(Kb, device)
+    rs = km.RopeSpec(theta=1e4, rope_dim=128, pairing="interleaved")
+    d = np.array([[-512] * 3, [3000] * 3], dtype=np.int32)
+    km.shift(kt, dev_i32(d, device), rope=rs)
+    km.shift(kt, dev_i32(-d, device), rope=rs)
+    torch.cuda.synchronize()
+    got = ref.bf16_to_f64(bits(kt))
+    want = ref.bf16_to_f64(Kb)
+    assert np.max(np.abs(got - want) / np.maximum(1, np.abs(want))) <= 2 * TOL
+
+
+# ---------------------------------------------------------------------------
+# scatter
+# ---------------------------------------------------------------------------
+
+def test_scatter_is_bit_exact(device):
+    import paper_2606_23581_amd as km
+    import torch
+
+    print("[case] scatter", flush=True)
+    rng = np.random.default_rng(50)
+    C, L, n, H, D, P = 4, 3, 53, 2, 128, 16
+    src = rng.integers(0, 1 << 16, size=(C, L, n, H, D)).astype(np.uint16)
+    pages = (n + P - 1) // P
+    npp = C * pages + 7
+    pt = rng.permutation(npp)[: C * pages].reshape(C, pages).astype(np.int32)
+    n_c = np.array([n, 0, 17, 40], dtype=np.int32)
+    pool = dev(np.full((L, npp * P, H, D), SENTINEL, np.uint16), device)
+    status = dev_i32(np.zeros(1), device)
+    km.scatter_paged(dev(src, device), pool, dev_i32(pt, device), page_size=P, n_pool_pages=npp,
+                     chunk_tokens=dev_i32(n_c, device), status=status)
+    torch.cuda.synchronize()
+    out = bits(pool)
+    want = np.full((L, npp * P, H, D), SENTINEL, np.uint16)
+    for c in range(C):
+        for l in range(L):
+            want[l] = ref.scatter_paged(src[c, l, : n_c[c]], pt[c], P, want[l])
+    assert np.array_equal(out, want)
+    assert int(status.cpu()[0]) == 0
+
+
+def test_scatter_bad_page_is_flagged(device):
+    import paper_2606_23581_amd as km
+    import torch
+
+    print("[case] scatter bad page", flush=True)
+    src = np.arange(2 * 16 * 8, dtype=np.uint16).reshape(1, 1, 32, 8)
+    pool = dev(np.full((1, 32, 8), SENTINEL, np.uint16), device)
+    status = dev_i32(np.zeros(1), device)
+    km.scatter_paged(dev(src, device), pool, dev_i32([[1, -3]], device), page_size=16, n_pool_pages=2,
+                     status=status)
+    torch.cuda.synchronize()
+    out = bits(pool)
+    assert int(status.cpu()[0]) & km.STATUS_BAD_PAGE
+    assert np.array_equal(out[0, 16:], src[0, 0, :16])
+    assert np.all(out[0, :16] == SENTINEL)
