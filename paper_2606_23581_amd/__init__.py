@@ -200,7 +200,7 @@ def _stream(stream) -> Optional[int]:
 
 def _strides(t, n: int) -> Sequence[int]:
     """The first n strides (elements) of a tensor whose last stride must be 1."""
-    if t.stride(-1) != 1 and t.shape[-1] > 1:
+    if t.numel() > 0 and t.stride(-1) != 1 and t.shape[-1] > 1:
         raise ValueError("the innermost dimension must be contiguous")
     return [int(s) for s in t.stride()[:n]]
 

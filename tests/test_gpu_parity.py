@@ -10,7 +10,7 @@ import pytest
 
 import oracle as ref
 import synth
-from tests.gpu_util import (SENTINEL, RehydrateCase, assert_close, bits, dev, dev_i32, oracle_rope,
+from tests.gpu_util import (SENTINEL, TOL, RehydrateCase, assert_close, bits, dev, dev_i32, oracle_rope,
                             require_gpu, run_rehydrate)
 
 pytestmark = pytest.mark.gpu
@@ -173,7 +173,9 @@ def test_shift_matches_oracle(device, name):
         outside[band] = False
         assert np.array_equal(out[..., outside], Kb[..., outside]), "columns outside the band changed"
     else:
-        rows = C * n + 11
+        P = 16
+        pages = (n + P - 1) // P
+        rows = C * n + 11 if layout == "rowbase" else (C * pages + 2) * P
         Wb = synth.randn_bf16_numpy((L, rows, H, D), 1.0, rng)
         wt = dev(Wb, device)
         if layout == "rowbase":
@@ -182,8 +184,6 @@ def test_shift_matches_oracle(device, name):
                      row_base=dev_i32(rb, device), status=status)
             dst = [rb[c] + np.arange(n) for c in range(C)]
         else:
-            P = 16
-            pages = (n + P - 1) // P
             npp = rows // P
             pt = rng.permutation(npp)[: C * pages].reshape(C, pages).astype(np.int32)
             km.shift(wt, dev_i32(delta, device), rope=rs, n_chunks=C, n_tokens=n,

@@ -1,0 +1,153 @@
+"""The five operator workloads at full size, in the launch configuration the
+benchmark times, checked on sampled (chunk, layer, head) units against the
+fp64 reference (every token and column of a sampled unit)."""
+
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+import oracle as ref
+import synth
+from synth import harness
+from tests.gpu_util import assert_close, bits, dev_i32, oracle_rope, require_gpu
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def device():
+    return require_gpu()
+
+
+def _free():
+    import gc
+
+    import torch
+
+    gc.collect()
+    torch.cuda.empty_cache()
+
+
+def _positions(w, meta, c):
+    if w.pos_mode == "grid3":
+        return ref.positions_grid3(meta.pos[c], w.grid_w, w.n_tokens)
+    return ref.positions_linear(int(meta.pos[c, 0]), w.n_tokens)
+
+
+def _check_rehydrate_units(p, units):
+    w, T, meta = p.workload, p.tensors, p.meta
+    orope = oracle_rope(harness._rope_spec(w))
+    n = w.n_tokens
+    for (c, l, h) in units:
+        p3 = _positions(w, meta, c)
+        if w.paged:
+            dst = np.array([ref.paged_slot(meta.page_table[c], i, w.page_size) for i in range(n)])
+            ko = bits(T["k_pool"][l, dst, h])
+        else:
+            dst = int(meta.row_base[c]) + np.arange(n)
+            ko = bits(T["k_out_rows"][l, dst[0]:dst[-1] + 1, h])
+        K = ref.bf16_to_f64(bits(T["k_in"][c, l, :, h]))
+        U = ref.bf16_to_f64(bits(T["u_k"][c, l, h])) if w.m_k else None
+        W = ref.bf16_to_f64(bits(T["w_k"][c, l, h])) if w.m_k else None
+        assert_close(ko, ref.rehydrate_k(K, U, W, orope, p3, w.patch_offset), f"{w.name} K c{c} l{l} h{h}")
+        if w.has_v:
+            vo = bits(T["v_pool"][l, dst, h]) if w.paged else bits(T["v_out_rows"][l, dst[0]:dst[-1] + 1, h])
+            V = ref.bf16_to_f64(bits(T["v_in"][c, l, :, h]))
+            U = ref.bf16_to_f64(bits(T["u_v"][c, l, h])) if w.m_v else None
+            W = ref.bf16_to_f64(bits(T["w_v"][c, l, h])) if w.m_v else None
+            assert_close(vo, ref.rehydrate_v(V, U, W, w.patch_offset), f"{w.name} V c{c} l{l} h{h}")
+
+
+@pytest.mark.parametrize("name", ["gqa1l_256tok_m8", "gqa28l_8x1024_m16_reorder", "mla27l_4x2048_m32",
+                                  "gqa80l_64x1024_m64_mrope_paged"])
+def test_workload_rehydrate(device, name):
+    import torch
+
+    print(f"[case] workload {name}", flush=True)
+    p = harness.prepare(name, device)
+    p.step()
+    torch.cuda.synchronize()
+    units = harness.sample_units(p.workload, 12 if p.workload.units() > 12 else p.workload.units(), seed=1)
+    _check_rehydrate_units(p, units)
+    if p.workload.paged:
+        # the page table of this workload is a permutation: every slot is written exactly once,
+        # and a second pass writes identical bits (no slot is hit by two tokens)
+        meta = p.meta
+        assert len(np.unique(meta.page_table)) == meta.page_table.size
+        before = bits(p.tensors["k_pool"][0, :4096])
+        p.step()
+        torch.cuda.synchronize()
+        assert np.array_equal(before, bits(p.tensors["k_pool"][0, :4096]))
+    del p
+    _free()
+
+
+def test_workload_one_layer_then_shift(device):
+    """The one-layer chunk is rehydrated at 1000 and then shifted by -256:
+    keys land at 744 + i, values are untouched by the shift."""
+    import paper_2606_23581_amd as km
+    import torch
+
+    print("[case] workload gqa1l shift", flush=True)
+    p = harness.prepare("gqa1l_256tok_m8", device)
+    p.step()
+    torch.cuda.synchronize()
+    w, T = p.workload, p.tensors
+    k_before = bits(T["k_out_rows"])
+    v_before = bits(T["v_out_rows"])
+    rs = harness._rope_spec(w)
+    km.shift(T["k_out_rows"], dev_i32(p.meta.delta, device), rope=rs, n_chunks=1, n_tokens=w.n_tokens,
+             row_base=T["row_base"])
+    torch.cuda.synchronize()
+    k_after = bits(T["k_out_rows"])
+    assert np.array_equal(v_before, bits(T["v_out_rows"]))
+    orope = oracle_rope(rs)
+    for h in range(w.n_heads):
+        want = ref.shift_k(ref.bf16_to_f64(k_before[0, :, h]), orope, p.meta.delta[0])
+        assert_close(k_after[0, :, h], want, f"shift h{h}")
+        # and against rehydrating straight at 744 + i (two bf16 roundings apart)
+        K = ref.bf16_to_f64(bits(T["k_in"][0, 0, :, h]))
+        U = ref.bf16_to_f64(bits(T["u_k"][0, 0, h]))
+        W = ref.bf16_to_f64(bits(T["w_k"][0, 0, h]))
+        direct = ref.rehydrate_k(K, U, W, orope, ref.positions_linear(744, w.n_tokens))
+        got = ref.bf16_to_f64(k_after[0, :, h])
+        assert np.max(np.abs(got - direct) / np.maximum(1, np.abs(direct))) <= 2 * 2.0 ** -7
+    del p
+    _free()
+
+
+def test_workload_window_slides(device):
+    """Sliding window: 8 slides of 15 survivor chunks moved by -512 in place;
+    each slide checked on sampled units; the evicted slot is never touched."""
+    import torch
+
+    print("[case] workload mha32l window", flush=True)
+    p = harness.prepare("mha32l_window16x512_shift", device)
+    w, T = p.workload, p.tensors
+    orope = oracle_rope(harness._rope_spec(w))
+    n = w.n_tokens
+    rng = np.random.default_rng(5)
+    gen = torch.Generator(device=device)
+    gen.manual_seed(77)
+    for k in range(w.slides):
+        p.extra["set_slide"](k)
+        slots = synth.window_survivor_slots(w, k)
+        evict = k % w.window_slots
+        picks = [(int(rng.integers(0, w.n_chunks)), int(rng.integers(0, w.n_layers)),
+                  int(rng.integers(0, w.n_heads))) for _ in range(3)]
+        picks.append((w.n_chunks - 1, w.n_layers - 1, w.n_heads - 1))
+        before = {u: bits(T["window"][u[1], slots[u[0]] * n:(slots[u[0]] + 1) * n, u[2]]) for u in picks}
+        ev_before = bits(T["window"][0, evict * n:(evict + 1) * n, 0])
+        p.step()
+        torch.cuda.synchronize()
+        for u, b in before.items():
+            got = bits(T["window"][u[1], slots[u[0]] * n:(slots[u[0]] + 1) * n, u[2]])
+            assert_close(got, ref.shift_k(ref.bf16_to_f64(b), orope, (w.delta,) * 3), f"slide {k} unit {u}")
+        assert np.array_equal(ev_before, bits(T["window"][0, evict * n:(evict + 1) * n, 0]))
+        # admit a fresh chunk into the evicted slot (not part of the operator)
+        fresh = synth.randn_bf16_device((w.n_layers, n, w.n_heads, w.head_dim), 1.0, gen, device)
+        T["window"][:, evict * n:(evict + 1) * n].copy_(fresh)
+        del fresh
+    del p
+    _free()
