@@ -89,6 +89,15 @@ __device__ __forceinline__ int64_t page_slot(const Placement& pl, int c, int i) 
   return (int64_t)page * pl.page_size + i % pl.page_size;
 }
 
+// The launch parameters are read in place from the kernel-argument segment.
+// Taking the address of a by-value kernel parameter (its arrays are indexed
+// with run-time values) would make the compiler copy the whole struct into
+// scratch memory first.
+template <typename T>
+__device__ __forceinline__ const T& kernel_params() {
+  return *static_cast<const T*>((const void*)__builtin_amdgcn_kernarg_segment_ptr());
+}
+
 // XCD-aware task index: workgroups are dealt round-robin to the 8 XCDs, so
 // workgroup w runs on XCD w % 8.  Give each XCD a contiguous range of tasks so
 // neighbouring tasks (same chunk/layer/head, same W factor) share its L2.
@@ -105,8 +114,10 @@ struct TileCtx {
   const PlaneParams* Q;
   int c, l, h, n_c;
   int col0;           // first column of the block
-  int flags;
   int ldw;            // LDS row stride of W^T in elements
+  bool patched;       // block intersects the patch columns and m > 0
+  int64_t in_base;    // element offset of (c, l, token 0, h, col0) in the input
+  int64_t u_base;     // element offset of (c, l, h, token 0) in U
 };
 
 // position of token i of chunk c on each coordinate, as exact doubles
@@ -115,7 +126,7 @@ __device__ __forceinline__ void token_position(const RehydrateParams& P, int c, 
   if (P.pos_mode == 0) {                       // linear: p0 + i
     const double p = (double)P.chunk_pos[3 * c] + (double)i;
     pt = ph = pw = p;
-  } else if (P.pos_mode == 1) {                // 32x32-style grid of patches
+  } else if (P.pos_mode == 1) {                // grid of patches, row-major
     pt = (double)P.chunk_pos[3 * c];
     ph = (double)P.chunk_pos[3 * c + 1] + (double)(i / P.grid_w);
     pw = (double)P.chunk_pos[3 * c + 2] + (double)(i % P.grid_w);
@@ -127,30 +138,28 @@ __device__ __forceinline__ void token_position(const RehydrateParams& P, int c, 
   }
 }
 
-template <int NQ>
-__device__ __forceinline__ void rotate_tile(f32x4 (&acc)[2 * NQ], int g, int pairing,
-                                            const double* s_freq, const int* s_coord,
-                                            double pt, double ph, double pw) {
-  if (pairing == 0) {
-    if constexpr (NQ % 2 == 0) {
+// ROT: 1 = NeoX pairs (chunk q <-> q + NQ/2), 2 = interleaved (adjacent elements)
+template <int NQ, int ROT>
+__device__ __forceinline__ void rotate_tile(f32x4 (&acc)[2 * NQ], int g, const double* s_freq,
+                                            const int* s_coord, double pt, double ph, double pw) {
+  if constexpr (ROT == 1 && NQ % 2 == 0) {
 #pragma unroll
-      for (int q = 0; q < NQ / 2; ++q) {
+    for (int q = 0; q < NQ / 2; ++q) {
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const int j = 8 * g + 32 * q + e;
-          const int sc = s_coord[j];
-          const double pos = sc == 0 ? pt : (sc == 1 ? ph : pw);
-          float sn, cs;
-          sincos_rev(pos, s_freq[j], sn, cs);
-          const int ax = 2 * q + (e >> 2), ay = 2 * (q + NQ / 2) + (e >> 2), k = e & 3;
-          const float x = acc[ax][k];
-          const float y = acc[ay][k];
-          acc[ax][k] = x * cs - y * sn;
-          acc[ay][k] = x * sn + y * cs;
-        }
+      for (int e = 0; e < 8; ++e) {
+        const int j = 8 * g + 32 * q + e;
+        const int sc = s_coord[j];
+        const double pos = sc == 0 ? pt : (sc == 1 ? ph : pw);
+        float sn, cs;
+        sincos_rev(pos, s_freq[j], sn, cs);
+        const int ax = 2 * q + (e >> 2), ay = 2 * (q + NQ / 2) + (e >> 2), k = e & 3;
+        const float x = acc[ax][k];
+        const float y = acc[ay][k];
+        acc[ax][k] = x * cs - y * sn;
+        acc[ay][k] = x * sn + y * cs;
       }
     }
-  } else {
+  } else if constexpr (ROT == 2) {
 #pragma unroll
     for (int q = 0; q < NQ; ++q) {
 #pragma unroll
@@ -170,118 +179,230 @@ __device__ __forceinline__ void rotate_tile(f32x4 (&acc)[2 * NQ], int g, int pai
   }
 }
 
+// ---------------------------------------------------------------------------
+// Tile I/O.  Global memory is accessed row-contiguously: one load or store
+// instruction of a wave covers 64 consecutive 16-byte chunks, i.e. whole
+// token rows (4 rows of a 128-column block).  The MFMA layout above wants 4
+// lanes per row instead, so each wave passes its tile through a private LDS
+// buffer (padded rows keep both access orders free of bank conflicts).  The
+// direct path (MFMA layout straight from global memory) remains for blocks of
+// 96 columns and for U rows that are not 16-byte aligned.
+// ---------------------------------------------------------------------------
+
+constexpr int kRowPad = 16;                          // LDS row padding, bytes
+
 template <int NQ>
-__device__ void rehydrate_tile(const RehydrateParams& P, const TileCtx& T, int i0,
-                               const uint16_t* __restrict__ Wt, const double* s_freq,
-                               const int* s_coord) {
+struct Staged {
+  static constexpr bool value = NQ == 1 || NQ == 2 || NQ == 4;
+};
+
+// LDS bytes of one wave's staging buffer: a 16 x 128-column bf16 tile, or the
+// tile's U rows (16 x up to 128 ranks); the phases of a tile use it in turn.
+__host__ __device__ constexpr int tile_lds_bytes() { return kTileTokens * (64 * 4 + kRowPad); }
+
+template <int NQ, int MS>
+struct TileRegs {
+  u32x4 k[NQ];                  // K (or V) chunks, in load order
+  u32x4 u[MS > 0 ? MS : 1];     // U chunks, in load order (staged) or B-operand order (direct)
+};
+
+// Issue the global loads of one tile.
+template <int NQ, int MS>
+__device__ __forceinline__ void tile_load(const TileCtx& T, int i0, TileRegs<NQ, MS>& R) {
+  const PlaneParams& Q = *T.Q;
+  const int lane = threadIdx.x & 63;
+  if constexpr (Staged<NQ>::value) {
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      const int cidx = 64 * q + lane;                // chunk of the tile, row-major
+      const int row = cidx / (4 * NQ), c16 = cidx % (4 * NQ);
+      const int i = i0 + row;
+      R.k[q] = i < T.n_c ? ld16(Q.in + T.in_base + (int64_t)i * Q.in_s[2] + 8 * c16) : u32x4{0, 0, 0, 0};
+    }
+  } else {
+    const int g = lane >> 4, i = i0 + (lane & 15);
+    const uint16_t* src = Q.in + T.in_base + (int64_t)i * Q.in_s[2];
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) R.k[q] = i < T.n_c ? ld16(src + 8 * (g + 4 * q)) : u32x4{0, 0, 0, 0};
+  }
+  if constexpr (MS > 0) {
+    if (!T.patched) return;
+    if (Q.u_vec && Staged<NQ>::value) {
+      // 16 rows x 4*m_steps chunks (rank padded to 32); chunks past m stay zero
+      const int cpr = Q.m >> 3, cpad = 4 * Q.m_steps;
+#pragma unroll
+      for (int s = 0; s < MS; ++s) {
+        const int cidx = 64 * s + lane;
+        u32x4 v = u32x4{0, 0, 0, 0};
+        if (cidx < kTileTokens * cpad) {
+          const int row = cidx / cpad, c = cidx % cpad;
+          const int i = i0 + row;
+          if (c < cpr && i < T.n_c) v = ld16(Q.U + T.u_base + (int64_t)i * Q.u_s[3] + 8 * c);
+        }
+        R.u[s] = v;
+      }
+    } else {
+      const int g = lane >> 4, i = i0 + (lane & 15);
+      const uint16_t* urow = Q.U + T.u_base + (int64_t)i * Q.u_s[3];
+#pragma unroll
+      for (int s = 0; s < MS; ++s) {
+        u32x4 v = u32x4{0, 0, 0, 0};
+        const int k0 = 32 * s + 8 * g;
+        if (s < Q.m_steps && i < T.n_c) {
+          if (Q.u_vec) {
+            if (k0 < Q.m) v = ld16(urow + k0);
+          } else {
+            uint32_t w4[4] = {0, 0, 0, 0};
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+              const uint32_t b = (k0 + e < Q.m) ? urow[k0 + e] : 0u;
+              w4[e >> 1] |= (e & 1) ? (b << 16) : b;
+            }
+            v = u32x4{w4[0], w4[1], w4[2], w4[3]};
+          }
+        }
+        R.u[s] = v;
+      }
+    }
+  }
+}
+
+template <int NQ, int MS, int ROT>
+__device__ __forceinline__ void tile_compute(const RehydrateParams& P, const TileCtx& T, int i0,
+                                             const TileRegs<NQ, MS>& R, const uint16_t* __restrict__ Wt,
+                                             uint8_t* tile_lds, const double* s_freq,
+                                             const int* s_coord) {
   const PlaneParams& Q = *T.Q;
   const int lane = threadIdx.x & 63;
   const int g = lane >> 4;
   const int t = lane & 15;
-  const int i = i0 + t;
-  const bool valid = i < T.n_c;
+  constexpr int kRowB = 64 * NQ + kRowPad;          // LDS row stride of the tile buffer
+  const bool u_staged = MS > 0 && T.patched && Q.u_vec && Staged<NQ>::value;
+  const int u_rowb = 64 * Q.m_steps + kRowPad;
 
-  // ---- load the K (or V) tile straight into accumulator order ----
-  u32x4 raw[NQ];
-  const uint16_t* src = Q.in + (int64_t)T.c * Q.in_s[0] + (int64_t)T.l * Q.in_s[1] +
-                        (int64_t)i * Q.in_s[2] + (int64_t)T.h * Q.in_s[3] + T.col0;
+  // ---- K chunks in MFMA order: lane (g, t) takes chunks g + 4q of row t ----
+  u32x4 kc[NQ];
+  if constexpr (Staged<NQ>::value) {
 #pragma unroll
-  for (int q = 0; q < NQ; ++q) raw[q] = valid ? ld16(src + 8 * (g + 4 * q)) : u32x4{0, 0, 0, 0};
-
-  const bool patched = (T.flags & kBlkPatch) && Q.m > 0;
-  // ---- patch coefficients of this token (B operand) ----
-  bf16x8 ub[4];
-  if (patched) {
-    const uint16_t* urow = Q.U + (int64_t)T.c * Q.u_s[0] + (int64_t)T.l * Q.u_s[1] +
-                           (int64_t)T.h * Q.u_s[2] + (int64_t)i * Q.u_s[3];
+    for (int q = 0; q < NQ; ++q) {
+      const int cidx = 64 * q + lane;
+      *reinterpret_cast<u32x4*>(tile_lds + (cidx / (4 * NQ)) * kRowB + 16 * (cidx % (4 * NQ))) = R.k[q];
+    }
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      u32x4 v = u32x4{0, 0, 0, 0};
-      if (s < Q.m_steps) {
-        const int k0 = 32 * s + 8 * g;
-        if (Q.u_vec) {
-          if (valid && k0 < Q.m) v = ld16(urow + k0);
-        } else if (valid) {
-          uint32_t w4[4] = {0, 0, 0, 0};
+    for (int q = 0; q < NQ; ++q) kc[q] = *reinterpret_cast<const u32x4*>(tile_lds + t * kRowB + 16 * (g + 4 * q));
+  } else {
 #pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const uint32_t b = (k0 + e < Q.m) ? urow[k0 + e] : 0u;
-            w4[e >> 1] |= (e & 1) ? (b << 16) : b;
-          }
-          v = u32x4{w4[0], w4[1], w4[2], w4[3]};
-        }
+    for (int q = 0; q < NQ; ++q) kc[q] = R.k[q];
+  }
+  // the K chunks are in registers now: the buffer takes the U rows
+  uint8_t* u_lds = tile_lds;
+  if constexpr (MS > 0) {
+    if (u_staged) {
+      const int cpad = 4 * Q.m_steps;
+#pragma unroll
+      for (int s = 0; s < MS; ++s) {
+        const int cidx = 64 * s + lane;
+        if (cidx < kTileTokens * cpad)
+          *reinterpret_cast<u32x4*>(u_lds + (cidx / cpad) * u_rowb + 16 * (cidx % cpad)) = R.u[s];
       }
-      ub[s] = __builtin_bit_cast(bf16x8, v);
     }
   }
 
   f32x4 acc[2 * NQ];
 #pragma unroll
   for (int q = 0; q < NQ; ++q) {
-    acc[2 * q][0] = bf_lo(raw[q].x);
-    acc[2 * q][1] = bf_hi(raw[q].x);
-    acc[2 * q][2] = bf_lo(raw[q].y);
-    acc[2 * q][3] = bf_hi(raw[q].y);
-    acc[2 * q + 1][0] = bf_lo(raw[q].z);
-    acc[2 * q + 1][1] = bf_hi(raw[q].z);
-    acc[2 * q + 1][2] = bf_lo(raw[q].w);
-    acc[2 * q + 1][3] = bf_hi(raw[q].w);
+    acc[2 * q][0] = bf_lo(kc[q].x);
+    acc[2 * q][1] = bf_hi(kc[q].x);
+    acc[2 * q][2] = bf_lo(kc[q].y);
+    acc[2 * q][3] = bf_hi(kc[q].y);
+    acc[2 * q + 1][0] = bf_lo(kc[q].z);
+    acc[2 * q + 1][1] = bf_hi(kc[q].z);
+    acc[2 * q + 1][2] = bf_lo(kc[q].w);
+    acc[2 * q + 1][3] = bf_hi(kc[q].w);
   }
 
-  const bool rotated = (T.flags & kBlkRotate) != 0;
+  const int i = i0 + t;
+  const bool valid = i < T.n_c;
   double pt = 0.0, ph = 0.0, pw = 0.0;
-  if (rotated) token_position(P, T.c, i < T.n_c ? i : T.n_c - 1, pt, ph, pw);
+  if constexpr (ROT != 0) {
+    token_position(P, T.c, valid ? i : T.n_c - 1, pt, ph, pw);
+    if (P.patch_post_rope) rotate_tile<NQ, ROT>(acc, g, s_freq, s_coord, pt, ph, pw);
+  }
 
-  if (rotated && P.patch_post_rope)
-    rotate_tile<NQ>(acc, g, P.rope.pairing, s_freq, s_coord, pt, ph, pw);
-
-  if (patched) {
-    // A operand row r = t: block column 8*(r/4) + 32*(mt/2) + 4*(mt%2) + r%4
-    const int rbase = 8 * (t >> 2) + (t & 3);
+  if constexpr (MS > 0) {
+    if (T.patched) {
+      // A operand row r = t: block column 8*(r/4) + 32*(mt/2) + 4*(mt%2) + r%4
+      const int rbase = 8 * (t >> 2) + (t & 3);
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      if (s < Q.m_steps) {
+      for (int s = 0; s < MS; ++s) {
+        if (s < Q.m_steps) {
+          const u32x4 ub = u_staged ? *reinterpret_cast<const u32x4*>(u_lds + t * u_rowb + 2 * (32 * s + 8 * g))
+                                    : R.u[s];
+          const bf16x8 b = __builtin_bit_cast(bf16x8, ub);
 #pragma unroll
-        for (int mt = 0; mt < 2 * NQ; ++mt) {
-          const int prow = rbase + 32 * (mt >> 1) + 4 * (mt & 1);
-          const bf16x8 a = *reinterpret_cast<const bf16x8*>(Wt + prow * T.ldw + 32 * s + 8 * g);
-          acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, ub[s], acc[mt], 0, 0, 0);
+          for (int mt = 0; mt < 2 * NQ; ++mt) {
+            const int prow = rbase + 32 * (mt >> 1) + 4 * (mt & 1);
+            const bf16x8 a = *reinterpret_cast<const bf16x8*>(Wt + prow * T.ldw + 32 * s + 8 * g);
+            acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc[mt], 0, 0, 0);
+          }
         }
       }
     }
   }
 
-  if (rotated && !P.patch_post_rope)
-    rotate_tile<NQ>(acc, g, P.rope.pairing, s_freq, s_coord, pt, ph, pw);
-
-  // ---- round to bf16 and store ----
-  if (!valid) return;
-  int64_t dst;
-  if (P.place.paged) {
-    const int64_t slot = page_slot(P.place, T.c, i);
-    if (slot < 0) return;
-    dst = (int64_t)T.l * Q.out_s[1] + slot * Q.out_s[2] + (int64_t)T.h * Q.out_s[3];
-  } else {
-    const int rb = P.place.row_base ? P.place.row_base[T.c] : 0;
-    dst = (int64_t)T.c * Q.out_s[0] + (int64_t)T.l * Q.out_s[1] + (int64_t)(rb + i) * Q.out_s[2] +
-          (int64_t)T.h * Q.out_s[3];
+  if constexpr (ROT != 0) {
+    if (!P.patch_post_rope) rotate_tile<NQ, ROT>(acc, g, s_freq, s_coord, pt, ph, pw);
   }
-  uint16_t* drow = Q.out + dst + T.col0;
+
+  // ---- round to bf16 (nearest even) ----
+  u32x4 o[NQ];
 #pragma unroll
   for (int q = 0; q < NQ; ++q) {
-    u32x4 o;
-    o.x = pack_bf16x2(acc[2 * q][0], acc[2 * q][1]);
-    o.y = pack_bf16x2(acc[2 * q][2], acc[2 * q][3]);
-    o.z = pack_bf16x2(acc[2 * q + 1][0], acc[2 * q + 1][1]);
-    o.w = pack_bf16x2(acc[2 * q + 1][2], acc[2 * q + 1][3]);
-    st16(drow + 8 * (g + 4 * q), o);
+    o[q].x = pack_bf16x2(acc[2 * q][0], acc[2 * q][1]);
+    o[q].y = pack_bf16x2(acc[2 * q][2], acc[2 * q][3]);
+    o[q].z = pack_bf16x2(acc[2 * q + 1][0], acc[2 * q + 1][1]);
+    o[q].w = pack_bf16x2(acc[2 * q + 1][2], acc[2 * q + 1][3]);
+  }
+
+  // ---- store ----
+  auto row_dst = [&](int ii, int64_t& dst) -> bool {
+    if (ii >= T.n_c) return false;
+    if (P.place.paged) {
+      const int64_t slot = page_slot(P.place, T.c, ii);
+      if (slot < 0) return false;
+      dst = (int64_t)T.l * Q.out_s[1] + slot * Q.out_s[2] + (int64_t)T.h * Q.out_s[3] + T.col0;
+    } else {
+      const int rb = P.place.row_base ? P.place.row_base[T.c] : 0;
+      dst = (int64_t)T.c * Q.out_s[0] + (int64_t)T.l * Q.out_s[1] + (int64_t)(rb + ii) * Q.out_s[2] +
+            (int64_t)T.h * Q.out_s[3] + T.col0;
+    }
+    return true;
+  };
+  if constexpr (Staged<NQ>::value) {
+    // back through LDS (same buffer: its K and U contents are consumed)
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) *reinterpret_cast<u32x4*>(tile_lds + t * kRowB + 16 * (g + 4 * q)) = o[q];
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      const int cidx = 64 * q + lane;
+      const int row = cidx / (4 * NQ), c16 = cidx % (4 * NQ);
+      const u32x4 v = *reinterpret_cast<const u32x4*>(tile_lds + row * kRowB + 16 * c16);
+      int64_t dst;
+      if (row_dst(i0 + row, dst)) st16(Q.out + dst + 8 * c16, v);
+    }
+  } else {
+    int64_t dst;
+    if (row_dst(i, dst)) {
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) st16(Q.out + dst + 8 * (g + 4 * q), o[q]);
+    }
   }
 }
 
 // Stage W^T of one column block into LDS: Wt[col][k], col in [0, 32*NQ),
 // k in [0, 32*m_steps); columns outside the patch range and k >= m are zero.
 template <int NQ>
-__device__ void stage_w(const RehydrateParams& P, const TileCtx& T, uint16_t* Wt) {
+__device__ __forceinline__ void stage_w(const TileCtx& T, uint16_t* Wt) {
   const PlaneParams& Q = *T.Q;
   const int m_pad = 32 * Q.m_steps;
   const int n_items = m_pad * (4 * NQ);
@@ -311,13 +432,16 @@ __device__ void stage_w(const RehydrateParams& P, const TileCtx& T, uint16_t* Wt
   }
 }
 
-template <int NQ>
-__device__ void rehydrate_block(const RehydrateParams& P, TileCtx& T, int t_begin, int t_end,
-                                uint16_t* Wt, double* s_freq, int* s_coord) {
-  const PlaneParams& Q = *T.Q;
-  const bool patched = (T.flags & kBlkPatch) && Q.m > 0;
-  if (patched) stage_w<NQ>(P, T, Wt);
-  if (T.flags & kBlkRotate) {
+template <int NQ, int MS, int ROT>
+__device__ __forceinline__ void rehydrate_block(const RehydrateParams& P, const TileCtx& T, int t_begin, int t_end,
+                                                uint8_t* lds, double* s_freq, int* s_coord) {
+  uint16_t* Wt = reinterpret_cast<uint16_t*>(lds);
+  const int wave = threadIdx.x >> 6;
+  uint8_t* tile_lds = lds + 128 * (32 * MS + 8) * 2 + wave * tile_lds_bytes();
+  if constexpr (MS > 0) {
+    if (T.patched) stage_w<NQ>(T, Wt);
+  }
+  if constexpr (ROT != 0) {
     const int half = P.rope.rope_dim / 2;
     for (int j = threadIdx.x; j < half; j += kThreads) {
       s_freq[j] = P.rope.rev_freq[j];
@@ -325,14 +449,19 @@ __device__ void rehydrate_block(const RehydrateParams& P, TileCtx& T, int t_begi
     }
   }
   __syncthreads();
-  const int wave = threadIdx.x >> 6;
+  constexpr int kWaves = kThreads / 64;
   const int n_tiles = (t_end - t_begin + kTileTokens - 1) / kTileTokens;
-  for (int tile = wave; tile < n_tiles; tile += kThreads / 64)
-    rehydrate_tile<NQ>(P, T, t_begin + tile * kTileTokens, Wt, s_freq, s_coord);
+  for (int tile = wave; tile < n_tiles; tile += kWaves) {
+    TileRegs<NQ, MS> R;
+    tile_load<NQ, MS>(T, t_begin + tile * kTileTokens, R);
+    tile_compute<NQ, MS, ROT>(P, T, t_begin + tile * kTileTokens, R, Wt, tile_lds, s_freq, s_coord);
+  }
 }
 
-__global__ __launch_bounds__(kThreads) void rehydrate_kernel(const RehydrateParams P) {
-  extern __shared__ __align__(16) uint16_t lds_w[];
+template <int MS>
+__global__ __launch_bounds__(kThreads, MS == 4 ? 3 : 4) void rehydrate_kernel(const RehydrateParams /*by value, read in place*/) {
+  const RehydrateParams& P = kernel_params<RehydrateParams>();
+  extern __shared__ __align__(16) uint8_t lds_dyn[];
   __shared__ double s_freq[kMaxPairs];
   __shared__ int s_coord[kMaxPairs];
 
@@ -357,22 +486,39 @@ __global__ __launch_bounds__(kThreads) void rehydrate_kernel(const RehydratePara
   const int t_end = min(t_begin + P.token_block, T.n_c);
   const ColBlock B = Q.blk[b];
   T.col0 = 8 * (int)B.col0;
-  T.flags = B.flags;
   T.ldw = 32 * Q.m_steps + 8;
-  switch (B.nq) {
-    case 1: rehydrate_block<1>(P, T, t_begin, t_end, lds_w, s_freq, s_coord); break;
-    case 2: rehydrate_block<2>(P, T, t_begin, t_end, lds_w, s_freq, s_coord); break;
-    case 3: rehydrate_block<3>(P, T, t_begin, t_end, lds_w, s_freq, s_coord); break;
-    default: rehydrate_block<4>(P, T, t_begin, t_end, lds_w, s_freq, s_coord); break;
+  T.patched = (B.flags & kBlkPatch) && Q.m > 0;
+  T.in_base = (int64_t)T.c * Q.in_s[0] + (int64_t)T.l * Q.in_s[1] + (int64_t)T.h * Q.in_s[3] + T.col0;
+  T.u_base = (int64_t)T.c * Q.u_s[0] + (int64_t)T.l * Q.u_s[1] + (int64_t)T.h * Q.u_s[2];
+  const int rot = (B.flags & kBlkRotate) ? (P.rope.pairing == 0 ? 1 : 2) : 0;
+  switch (B.nq * 3 + rot) {
+    case 1 * 3 + 0: rehydrate_block<1, MS, 0>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
+    case 1 * 3 + 2: rehydrate_block<1, MS, 2>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
+    case 2 * 3 + 0: rehydrate_block<2, MS, 0>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
+    case 2 * 3 + 1: rehydrate_block<2, MS, 1>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
+    case 2 * 3 + 2: rehydrate_block<2, MS, 2>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
+    case 3 * 3 + 0: rehydrate_block<3, MS, 0>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
+    case 3 * 3 + 2: rehydrate_block<3, MS, 2>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
+    case 4 * 3 + 0: rehydrate_block<4, MS, 0>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
+    case 4 * 3 + 1: rehydrate_block<4, MS, 1>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
+    case 4 * 3 + 2: rehydrate_block<4, MS, 2>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
+    default: break;                              // rejected on the host (NeoX needs an even NQ)
   }
 }
 
 hipError_t launch_rehydrate(const RehydrateParams& p, hipStream_t s) {
   int max_steps = 0;
   for (int k = 0; k < p.n_planes; ++k) max_steps = max_steps > p.plane[k].m_steps ? max_steps : p.plane[k].m_steps;
-  const size_t lds = max_steps > 0 ? (size_t)128 * (32 * max_steps + 8) * sizeof(uint16_t) : 16;
-  const int64_t grid = (int64_t)p.per_xcd * 8;
-  hipLaunchKernelGGL(rehydrate_kernel, dim3((uint32_t)grid), dim3(kThreads), lds, s, p);
+  const int ms = max_steps == 0 ? 0 : (max_steps <= 2 ? max_steps : 4);   // template rank steps
+  const size_t lds = (size_t)128 * (32 * ms + 8) * sizeof(uint16_t) +
+                     (size_t)(kThreads / 64) * tile_lds_bytes();
+  const dim3 grid((uint32_t)((int64_t)p.per_xcd * 8)), block(kThreads);
+  switch (max_steps) {
+    case 0: hipLaunchKernelGGL(rehydrate_kernel<0>, grid, block, lds, s, p); break;
+    case 1: hipLaunchKernelGGL(rehydrate_kernel<1>, grid, block, lds, s, p); break;
+    case 2: hipLaunchKernelGGL(rehydrate_kernel<2>, grid, block, lds, s, p); break;
+    default: hipLaunchKernelGGL(rehydrate_kernel<4>, grid, block, lds, s, p); break;
+  }
   return hipGetLastError();
 }
 
@@ -382,7 +528,8 @@ hipError_t launch_rehydrate(const RehydrateParams& p, hipStream_t s) {
 
 constexpr int kShiftUnroll = 4;
 
-__global__ __launch_bounds__(kThreads) void shift_kernel(const ShiftParams P) {
+__global__ __launch_bounds__(kThreads) void shift_kernel(const ShiftParams /*by value, read in place*/) {
+  const ShiftParams& P = kernel_params<ShiftParams>();
   const int64_t task = xcd_task(P.per_xcd);
   if (task >= P.n_tasks) return;
   const int tb = (int)(task % P.n_tblk);
@@ -491,7 +638,8 @@ hipError_t launch_shift(const ShiftParams& p, hipStream_t s) {
 
 constexpr int kScatterUnroll = 4;
 
-__global__ __launch_bounds__(kThreads) void scatter_kernel(const ScatterParams P) {
+__global__ __launch_bounds__(kThreads) void scatter_kernel(const ScatterParams /*by value, read in place*/) {
+  const ScatterParams& P = kernel_params<ScatterParams>();
   const int64_t task = xcd_task(P.per_xcd);
   if (task >= P.n_tasks) return;
   const int tb = (int)(task % P.n_tblk);

@@ -55,7 +55,18 @@ def _rope_spec(w: Workload):
                        section_order=w.section_order)
 
 
-def prepare(name: str, device="cuda", seed: Optional[int] = None) -> Prepared:
+def _kv_rows(shape, gen, device, unit_major: bool):
+    """K/V of one workload, [C, L, n, H, D] as the operator sees it.  With
+    ``unit_major`` the memory is [C, L, H, n, D]: every (chunk, layer, head)
+    unit is one contiguous run of rows."""
+    C, L, n, H, D = shape
+    if unit_major:
+        return randn_bf16_device((C, L, H, n, D), 1.0, gen, device).permute(0, 1, 3, 2, 4)
+    return randn_bf16_device(shape, 1.0, gen, device)
+
+
+def prepare(name: str, device="cuda", seed: Optional[int] = None, unit_major: bool = True,
+            pool_head_major: bool = False) -> Prepared:
     import torch
 
     import paper_2606_23581_amd as km
@@ -93,9 +104,9 @@ def prepare(name: str, device="cuda", seed: Optional[int] = None) -> Prepared:
         p.extra["call"] = call
         return p
 
-    T["k_in"] = randn_bf16_device((C, L, n, H, D), 1.0, gen, device)
+    T["k_in"] = _kv_rows((C, L, n, H, D), gen, device, unit_major)
     if w.has_v:
-        T["v_in"] = randn_bf16_device((C, L, n, H, D), 1.0, gen, device)
+        T["v_in"] = _kv_rows((C, L, n, H, D), gen, device, unit_major)
     if w.m_k > 0:
         T["u_k"] = randn_bf16_device((C, L, H, n, w.m_k), w.u_std, gen, device)
         T["w_k"] = randn_bf16_device((C, L, H, w.m_k, w.patch_dim), w.w_std, gen, device)
@@ -108,12 +119,18 @@ def prepare(name: str, device="cuda", seed: Optional[int] = None) -> Prepared:
               pos_mode=km.POS_GRID3 if w.pos_mode == "grid3" else km.POS_LINEAR, grid_w=w.grid_w)
     if w.paged:
         slots = w.n_pool_pages * w.page_size
-        T["k_pool"] = torch.zeros((L, slots, H, D), dtype=torch.bfloat16, device=device)
+        if pool_head_major:   # [L, H, slots, D] memory, [L, slots, H, D] view
+            T["k_pool"] = torch.zeros((L, H, slots, D), dtype=torch.bfloat16, device=device).transpose(1, 2)
+        else:
+            T["k_pool"] = torch.zeros((L, slots, H, D), dtype=torch.bfloat16, device=device)
         T["page_table"] = torch.from_numpy(meta.page_table).to(device)
         kw.update(page_table=T["page_table"], page_size=w.page_size, n_pool_pages=w.n_pool_pages)
         k_out = T["k_pool"]
         if w.has_v:
-            T["v_pool"] = torch.zeros((L, slots, H, D), dtype=torch.bfloat16, device=device)
+            if pool_head_major:
+                T["v_pool"] = torch.zeros((L, H, slots, D), dtype=torch.bfloat16, device=device).transpose(1, 2)
+            else:
+                T["v_pool"] = torch.zeros((L, slots, H, D), dtype=torch.bfloat16, device=device)
             v_out = T["v_pool"]
     else:
         rows = int(meta.row_base.max()) + n
