@@ -312,13 +312,16 @@ extern "C" int kamera_rehydrate(const kamera_rehydrate_args* a, void* stream) {
   tb = (int)std::min<int64_t>(tb, ceil_div(a->n_tokens, 64) * 64);
   P.token_block = tb;
   P.n_tblk = (int32_t)ceil_div(a->n_tokens, tb);
-  int64_t base = 0;
+  int32_t nb_all = 0;
   for (int p = 0; p < a->n_planes; ++p) {
-    P.plane[p].task_base = (int32_t)base;
-    base += (int64_t)a->n_chunks * a->n_layers * a->n_heads * P.n_tblk * P.plane[p].n_blocks;
+    P.plane[p].block_base = nb_all;
+    nb_all += P.plane[p].n_blocks;
   }
-  if (base >= (int64_t)1 << 31) return fail(KAMERA_ERR_RANGE, "%s: %lld tasks exceed one launch", who, (long long)base);
-  P.n_tasks = base;
+  P.blocks_per_group = nb_all;
+  const int64_t n_tasks = (int64_t)a->n_chunks * a->n_layers * a->n_heads * P.n_tblk * nb_all;
+  if (n_tasks >= (int64_t)1 << 31)
+    return fail(KAMERA_ERR_RANGE, "%s: %lld tasks exceed one launch", who, (long long)n_tasks);
+  P.n_tasks = n_tasks;
   rc = pick_grid(P.n_tasks, P.per_xcd, who);
   if (rc) return rc;
 
@@ -370,9 +373,9 @@ extern "C" int kamera_shift(const kamera_shift_args* a, void* stream) {
   P.n_layers = a->n_layers;
   P.n_heads = a->n_heads;
   P.vec_per_row = r.pairing == KAMERA_PAIR_NEOX ? r.rope_dim / 16 : r.rope_dim / 8;
-  // about 2048 rows per task, at least 2048 tasks when the call is large enough
+  // about 512 rows per task, at least 2048 tasks when the call is large enough
   int tb = 16;
-  while (tb < 1024 && (int64_t)tb * a->n_heads < 2048) tb *= 2;
+  while (tb < 1024 && (int64_t)tb * a->n_heads < 512) tb *= 2;
   while (tb > 16 && (int64_t)a->n_chunks * a->n_layers * ceil_div(a->n_tokens, tb) < 2048) tb /= 2;
   P.token_block = tb;
   P.n_tblk = (int32_t)ceil_div(a->n_tokens, tb);

@@ -467,11 +467,13 @@ __global__ __launch_bounds__(kThreads, MS == 4 ? 3 : 4) void rehydrate_kernel(co
 
   const int64_t task = xcd_task(P.per_xcd);
   if (task >= P.n_tasks) return;
-  const int pl = (P.n_planes == 2 && task >= P.plane[1].task_base) ? 1 : 0;
+  // tasks of one (chunk, layer, head, token block) are adjacent: the key
+  // blocks (rotation, VALU-heavier) run next to the value blocks (pure streams)
+  int64_t rem = task / P.blocks_per_group;
+  const int r = (int)(task % P.blocks_per_group);
+  const int pl = (P.n_planes == 2 && r >= P.plane[1].block_base) ? 1 : 0;
   const PlaneParams& Q = P.plane[pl];
-  int64_t rem = task - Q.task_base;
-  const int b = (int)(rem % Q.n_blocks);
-  rem /= Q.n_blocks;
+  const int b = r - Q.block_base;
   const int tb = (int)(rem % P.n_tblk);
   rem /= P.n_tblk;
   TileCtx T;

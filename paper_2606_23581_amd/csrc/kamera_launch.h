@@ -48,7 +48,7 @@ struct PlaneParams {
   int32_t u_vec;                     // 16-byte U loads are legal
   int32_t w_vec;                     // 16-byte W loads are legal
   int32_t n_blocks;
-  int32_t task_base;                 // first task index of this plane
+  int32_t block_base;                // index of this plane's first block within a task group
   ColBlock blk[kMaxBlocks];
 };
 
@@ -80,6 +80,8 @@ struct RehydrateParams {
   int32_t token_block;               // tokens per workgroup task (multiple of 64)
   int32_t n_tblk;                    // token blocks per chunk
   int32_t per_xcd;                   // tasks per XCD slice of the grid
+  int32_t blocks_per_group;          // column blocks of all planes for one (chunk, layer, head, token block)
+  int32_t pad2_;
   int64_t n_tasks;
 };
 
