@@ -401,33 +401,47 @@ __device__ __forceinline__ void tile_compute(const RehydrateParams& P, const Til
 
 // Stage W^T of one column block into LDS: Wt[col][k], col in [0, 32*NQ),
 // k in [0, 32*m_steps); columns outside the patch range and k >= m are zero.
+// A thread takes 4 ranks x 8 columns: four 16-byte row loads, transposed in
+// registers into eight 8-byte LDS writes (4 consecutive ranks of one column).
 template <int NQ>
 __device__ __forceinline__ void stage_w(const TileCtx& T, uint16_t* Wt) {
   const PlaneParams& Q = *T.Q;
   const int m_pad = 32 * Q.m_steps;
-  const int n_items = m_pad * (4 * NQ);
+  const int k4s = m_pad / 4;
+  const int n_items = k4s * (4 * NQ);
   const uint16_t* wbase = Q.W + (int64_t)T.c * Q.w_s[0] + (int64_t)T.l * Q.w_s[1] +
                           (int64_t)T.h * Q.w_s[2];
   for (int item = threadIdx.x; item < n_items; item += kThreads) {
-    const int k = item % m_pad;
-    const int cc = item / m_pad;
-    const int colb = 8 * cc;                        // block column of the 8-chunk
-    const int wcol = T.col0 + colb - Q.patch_lo;    // W column
-    uint32_t w4[4] = {0, 0, 0, 0};
-    if (k < Q.m && T.col0 + colb >= Q.patch_lo && T.col0 + colb + 8 <= Q.patch_hi) {
-      const uint16_t* p = wbase + (int64_t)k * Q.w_s[3] + wcol;
-      if (Q.w_vec) {
-        const u32x4 v = *reinterpret_cast<const u32x4*>(p);
-        w4[0] = v.x; w4[1] = v.y; w4[2] = v.z; w4[3] = v.w;
-      } else {
+    const int k0 = 4 * (item % k4s);
+    const int colb = 8 * (item / k4s);               // block column of the 8-chunk
+    const int wcol = T.col0 + colb - Q.patch_lo;     // W column
+    const bool in_patch = T.col0 + colb >= Q.patch_lo && T.col0 + colb + 8 <= Q.patch_hi;
+    uint32_t w[4][4];                                 // [rank][column pair]
 #pragma unroll
-        for (int e = 0; e < 8; ++e) w4[e >> 1] |= (e & 1) ? ((uint32_t)p[e] << 16) : (uint32_t)p[e];
+    for (int r = 0; r < 4; ++r) {
+      w[r][0] = w[r][1] = w[r][2] = w[r][3] = 0u;
+      const int k = k0 + r;
+      if (in_patch && k < Q.m) {
+        const uint16_t* p = wbase + (int64_t)k * Q.w_s[3] + wcol;
+        if (Q.w_vec) {
+          const u32x4 v = *reinterpret_cast<const u32x4*>(p);
+          w[r][0] = v.x; w[r][1] = v.y; w[r][2] = v.z; w[r][3] = v.w;
+        } else {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) w[r][e >> 1] |= (e & 1) ? ((uint32_t)p[e] << 16) : (uint32_t)p[e];
+        }
       }
     }
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      const uint32_t wv = w4[e >> 1];
-      Wt[(colb + e) * T.ldw + k] = (uint16_t)((e & 1) ? (wv >> 16) : (wv & 0xffffu));
+      // column e of the chunk, ranks k0..k0+3
+      const int sh = (e & 1) ? 16 : 0;
+      const uint32_t r0 = (w[0][e >> 1] >> sh) & 0xffffu, r1 = (w[1][e >> 1] >> sh) & 0xffffu;
+      const uint32_t r2 = (w[2][e >> 1] >> sh) & 0xffffu, r3 = (w[3][e >> 1] >> sh) & 0xffffu;
+      uint2 v;
+      v.x = r0 | (r1 << 16);
+      v.y = r2 | (r3 << 16);
+      *reinterpret_cast<uint2*>(Wt + (colb + e) * T.ldw + k0) = v;
     }
   }
 }
