@@ -19,6 +19,7 @@ from .kamera_ref import (  # noqa: F401
     positions_linear,
     rehydrate_k,
     rehydrate_v,
+    relocate_k,
     rope_angles,
     rotate,
     round_bf16,

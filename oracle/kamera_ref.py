@@ -255,6 +255,26 @@ def shift_k(K: np.ndarray, rope: Rope, delta3: Sequence[int]) -> np.ndarray:
     return rotate(np.asarray(K, np.float64), rope, rope_angles(rope, d))
 
 
+def relocate_k(K: np.ndarray, U, W, rope: Rope, pos3_target: np.ndarray, delta3: Sequence[int],
+               patch_offset: int = 0, patch_after_rope: bool = False) -> np.ndarray:
+    """Move already-rotated keys by delta and add a patch (survivor removal patch).
+
+    Survivors of a window slide keep their conditioned keys, stored rotated at
+    their old positions; they move by delta (Sec. 5), and where the evicted
+    chunk's influence must be removed a low-rank removal patch is added (Sec. 5,
+    Table ``tab:evict``).  K' = R(delta) K + R(pos) U W with pos the target
+    position (the patch kept in the position-free frame, as for rehydrate), or
+    K' = R(delta) K + U W when the patch lives in the rotated frame.
+    """
+    moved = shift_k(K, rope, delta3)
+    if U is None or W is None or np.asarray(U).shape[1] == 0:
+        return moved
+    patch = add_patch(np.zeros_like(moved), U, W, patch_offset)
+    if not patch_after_rope:
+        patch = rotate(patch, rope, rope_angles(rope, pos3_target))
+    return moved + patch
+
+
 def paged_slot(page_table_row: np.ndarray, i: int, page_size: int) -> int:
     """Physical pool slot of a chunk's token i: page_table[i // P] * P + i % P."""
     return int(page_table_row[i // page_size]) * page_size + i % page_size

@@ -405,4 +405,42 @@ def pin_paged_slot_and_scatter(ref):
             assert np.all(out[s] == 0xDEAD)
 
 
+def pin_relocate(ref):
+    """Survivor relocation with a removal patch: a key rehydrated at p (no
+    patch) and then moved by delta with the patch equals rehydrating it at
+    p + delta with the patch, because R(delta) R(p) = R(p + delta) and the
+    patch lives in the position-free frame; with no patch it is a plain shift;
+    in the rotated frame the patch is added unrotated."""
+    rng = _rng(27)
+    for rope in (ref.Rope(theta=1e6, rope_dim=64, pairing="neox"),
+                 ref.Rope(theta=1e4, rope_dim=32, pairing="interleaved", rope_offset=32),
+                 ref.Rope(theta=1e6, rope_dim=64, pairing="neox", sections=(8, 12, 12))):
+        D = rope.rope_offset + rope.rope_dim
+        K0 = rng.standard_normal((6, D))
+        U = rng.standard_normal((6, 3))
+        W = rng.standard_normal((3, D))
+        old = np.array([[50, 3, 4], [51, 3, 5], [52, 4, 0], [53, 4, 1], [54, 4, 2], [55, 5, 0]])
+        d3 = np.array([-512, 7, -2]) if rope.sections else np.array([-512, -512, -512])
+        stored = ref.rehydrate_k(K0, None, None, rope, old)
+        got = ref.relocate_k(stored, U, W, rope, old + d3[None, :], d3)
+        want = ref.rehydrate_k(K0, U, W, rope, old + d3[None, :])
+        assert np.max(np.abs(got - want)) < 1e-11
+        assert np.max(np.abs(ref.relocate_k(stored, None, None, rope, old + d3, d3) -
+                             ref.shift_k(stored, rope, d3))) < 1e-13
+        post = ref.relocate_k(stored, U, W, rope, old + d3, d3, patch_after_rope=True)
+        assert np.max(np.abs(post - (ref.shift_k(stored, rope, d3) + U @ W))) < 1e-11
+    # brute force, one NeoX pair per token
+    K = rng.standard_normal((3, 2))
+    U = rng.standard_normal((3, 1))
+    W = rng.standard_normal((1, 2))
+    rope = ref.Rope(theta=10.0, rope_dim=2)
+    tgt = np.array([[5, 5, 5], [9, 9, 9], [-4, -4, -4]])
+    got = ref.relocate_k(K, U, W, rope, tgt, (3, 3, 3))
+    for i in range(3):
+        zk = complex(K[i, 0], K[i, 1]) * cmath.exp(1j * 3.0)
+        zp = complex(U[i, 0] * W[0, 0], U[i, 0] * W[0, 1]) * cmath.exp(1j * float(tgt[i, 0]))
+        z = zk + zp
+        assert abs(got[i, 0] - z.real) < 1e-12 and abs(got[i, 1] - z.imag) < 1e-12
+
+
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

@@ -98,6 +98,15 @@ def _slot_wrong(page_table_row, i, page_size):
     return int(page_table_row[i // page_size]) * page_size + i // page_size
 
 
+def _relocate_patch_at_old_position(K, U, W, rope, pos3_target, delta3, patch_offset=0, patch_after_rope=False):
+    moved = ref.shift_k(K, rope, delta3)
+    if U is None or W is None or np.asarray(U).shape[1] == 0:
+        return moved
+    patch = ref.add_patch(np.zeros_like(moved), U, W, patch_offset)
+    old = np.asarray(pos3_target) - np.asarray(delta3)[None, :]
+    return moved + ref.rotate(patch, rope, ref.rope_angles(rope, old))
+
+
 def _shift_negated(K, rope, delta3):
     return _orig["shift_k"](K, rope, [-int(v) for v in delta3])
 
@@ -117,6 +126,7 @@ MUTANTS = {
     "bf16 truncation": ("round_bf16", _round_truncate),
     "page slot offset i // P": ("paged_slot", _slot_wrong),
     "shift direction negated": ("shift_k", _shift_negated),
+    "removal patch rotated to the old position": ("relocate_k", _relocate_patch_at_old_position),
 }
 
 
