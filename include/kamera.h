@@ -119,7 +119,18 @@ typedef struct {
  * W is m x patch_dim at
  *   W + c*w_stride[0] + l*w_stride[1] + h*w_stride[2] + k*w_stride[3] + col',
  * col' = col - patch_offset.  A stride of 0 shares a factor (e.g. one basis
- * per layer for every chunk).  m = 0 disables the patch (U, W may be NULL). */
+ * per layer for every chunk).  m = 0 disables the patch (U, W may be NULL).
+ *
+ * A plane covers the columns [col_begin, col_end) of the row (both 0: the
+ * whole row; otherwise multiples of 32).  Two planes over the same rows with
+ * disjoint column ranges give one row two patches of different rank, e.g. the
+ * MLA latent (rank m) and the small extra patch on its rope key band that
+ * Sec. 3 adds to close the latent-only residual.
+ *
+ * layer_rank (optional device int32 [n_layers]) lowers the rank per layer:
+ * layer l uses the first min(layer_rank[l], m) ranks, 0 = no patch at that
+ * layer -- the deep-half patch that stores factors for the deepest layers
+ * only (Sec. 1 contributions, Table menu). */
 typedef struct {
   const void* in;
   int64_t in_stride[4];
@@ -133,6 +144,9 @@ typedef struct {
   int32_t rotate;          /* 1: rotate the rope band (keys); 0: values      */
   int32_t patch_offset;    /* patched columns [patch_offset,                 */
   int32_t patch_dim;       /*                  patch_offset + patch_dim)     */
+  int32_t col_begin;       /* columns this plane covers (0, 0: all)          */
+  int32_t col_end;
+  const int32_t* layer_rank;
 } kamera_plane;
 
 /* kamera_rehydrate -- Eq. eq:operator with the patch in the stored frame;
@@ -146,8 +160,17 @@ typedef struct {
  *                             + i % page_size,
  *                      out + l*out_stride[1] + slot*out_stride[2]
  *                          + h*out_stride[3]   (out_stride[0] unused)
- * Outputs must not overlap inputs (not checked for strided views beyond
- * the base pointers). */
+ * Outputs must not overlap inputs (checked on the extents the host-visible
+ * sizes imply).
+ *
+ * Relocation (delta != NULL, device int32 [n_chunks][3]): the input keys are
+ * already rotated, at target - delta (survivors of a window slide, Sec. 5),
+ * and the rotated planes compute
+ *   K' = R(delta) K + R(target) U W      (KAMERA_PATCH_PRE_ROPE), or
+ *   K' = R(delta) K + U W                (KAMERA_PATCH_POST_ROPE),
+ * i.e. the move of kamera_shift fused with a (removal) patch (Sec. 5, Table
+ * evict); target positions come from pos_mode as usual.  Unrotated planes
+ * (values, latents) are unaffected by delta. */
 typedef struct {
   int32_t n_chunks;
   int32_t n_layers;
@@ -171,6 +194,7 @@ typedef struct {
   int32_t page_size;
   int32_t n_pool_pages;
   uint32_t* status;            /* optional device word, bits OR-ed in          */
+  const int32_t* delta;        /* optional: relocation of rotated keys         */
 } kamera_rehydrate_args;
 
 /* kamera_shift -- K' = R(delta_c) K in place on the rope band of every token

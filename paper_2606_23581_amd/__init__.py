@@ -76,7 +76,8 @@ class CRope(ctypes.Structure):
 class CPlane(ctypes.Structure):
     _fields_ = [("in_", _vp), ("in_stride", _i64 * 4), ("out", _vp), ("out_stride", _i64 * 4),
                 ("U", _vp), ("u_stride", _i64 * 4), ("W", _vp), ("w_stride", _i64 * 4),
-                ("m", _i32), ("rotate", _i32), ("patch_offset", _i32), ("patch_dim", _i32)]
+                ("m", _i32), ("rotate", _i32), ("patch_offset", _i32), ("patch_dim", _i32),
+                ("col_begin", _i32), ("col_end", _i32), ("layer_rank", _vp)]
 
 
 class CRehydrateArgs(ctypes.Structure):
@@ -85,7 +86,7 @@ class CRehydrateArgs(ctypes.Structure):
                 ("pos_mode", _i32), ("chunk_pos", _vp), ("grid_w", _i32), ("explicit_pos", _vp),
                 ("explicit_chunk_stride", _i64), ("n_planes", _i32), ("plane", CPlane * 2),
                 ("paged", _i32), ("row_base", _vp), ("page_table", _vp), ("pt_stride", _i32),
-                ("page_size", _i32), ("n_pool_pages", _i32), ("status", _vp)]
+                ("page_size", _i32), ("n_pool_pages", _i32), ("status", _vp), ("delta", _vp)]
 
 
 class CShiftArgs(ctypes.Structure):
@@ -221,7 +222,8 @@ def _i32_dev(t, name):
     return t
 
 
-def _fill_plane(pl: CPlane, x_in, x_out, U, W, rotate: bool, patch: Tuple[int, int], paged: bool):
+def _fill_plane(pl: CPlane, x_in, x_out, U, W, rotate: bool, patch: Tuple[int, int], paged: bool,
+                cols: Tuple[int, int] = (0, 0), layer_rank=None):
     pl.in_ = _ptr(x_in)
     for k, s in enumerate(_strides(x_in, 4)):
         pl.in_stride[k] = s
@@ -244,6 +246,8 @@ def _fill_plane(pl: CPlane, x_in, x_out, U, W, rotate: bool, patch: Tuple[int, i
         pl.patch_offset, pl.patch_dim = int(patch[0]), int(patch[1])
     else:
         pl.m = 0
+    pl.col_begin, pl.col_end = int(cols[0]), int(cols[1])
+    pl.layer_rank = _ptr(layer_rank)
 
 
 # ---------------------------------------------------------------------------
@@ -276,7 +280,9 @@ def prepare_rehydrate(k_in, k_out, *, rope: RopeSpec, chunk_pos=None, v_in=None,
                       v_patch: Tuple[int, int] = None, pos_mode: int = POS_LINEAR, grid_w: int = 0,
                       explicit_pos=None, chunk_tokens=None, row_base=None, page_table=None,
                       page_size: int = 16, n_pool_pages: int = 0,
-                      patch_frame: int = PATCH_PRE_ROPE, status=None) -> Prepared:
+                      patch_frame: int = PATCH_PRE_ROPE, status=None, delta=None,
+                      u_pe=None, w_pe=None, k_layer_rank=None, v_layer_rank=None,
+                      pe_layer_rank=None) -> Prepared:
     """Rebuild cached chunks at their target positions (``kamera_rehydrate``).
 
     k_in, v_in: [C, L, n, H, D] bf16 (any strides, last dim contiguous).
@@ -284,6 +290,13 @@ def prepare_rehydrate(k_in, k_out, *, rope: RopeSpec, chunk_pos=None, v_in=None,
     [L, slots, H, D].  u_*: [C, L, H, n, m]; w_*: [C, L, H, m, patch_dim]
     (expand() views with stride 0 share a factor).  chunk_pos: int32 [C, 3]
     device tensor (p0 or the grid origin).  Keys rotate; values do not.
+
+    delta: int32 [C, 3] device tensor -> relocation: the keys are already
+    rotated (at target - delta) and become R(delta) K + R(target) U W.
+    u_pe, w_pe: a second, separate patch on the rope band (MLA k_pe band):
+    the row splits into two planes, [0, rope_offset) patched by u_k/w_k and the
+    band patched by u_pe/w_pe ([C, L, H, n, m_pe], [C, L, H, m_pe, rope_dim]).
+    *_layer_rank: int32 [L] device tensors lowering the rank per layer.
     """
     L = lib()
     _bf16(k_in, "k_in"), _bf16(k_out, "k_out"), _bf16(v_in, "v_in"), _bf16(v_out, "v_out")
@@ -304,10 +317,22 @@ def prepare_rehydrate(k_in, k_out, *, rope: RopeSpec, chunk_pos=None, v_in=None,
     a.explicit_pos = _ptr(explicit_pos)
     a.explicit_chunk_stride = int(explicit_pos.stride(0)) if explicit_pos is not None else 0
     paged = page_table is not None
-    _fill_plane(a.plane[0], k_in, k_out, u_k, w_k, True, k_patch or (0, D), paged)
-    a.n_planes = 1
+    if u_pe is not None:
+        if v_in is not None:
+            raise ValueError("a separate rope-band patch splits the key row into two planes; "
+                             "values need a call of their own")
+        _bf16(u_pe, "u_pe"), _bf16(w_pe, "w_pe")
+        ro = int(rope.rope_offset)
+        _fill_plane(a.plane[0], k_in, k_out, u_k, w_k, False, k_patch or (0, ro), paged, (0, ro),
+                    k_layer_rank)
+        _fill_plane(a.plane[1], k_in, k_out, u_pe, w_pe, True, (ro, int(rope.rope_dim)), paged, (ro, D),
+                    pe_layer_rank)
+        a.n_planes = 2
+    else:
+        _fill_plane(a.plane[0], k_in, k_out, u_k, w_k, True, k_patch or (0, D), paged, (0, 0), k_layer_rank)
+        a.n_planes = 1
     if v_in is not None:
-        _fill_plane(a.plane[1], v_in, v_out, u_v, w_v, False, v_patch or (0, D), paged)
+        _fill_plane(a.plane[1], v_in, v_out, u_v, w_v, False, v_patch or (0, D), paged, (0, 0), v_layer_rank)
         a.n_planes = 2
     a.paged = 1 if paged else 0
     a.row_base = _ptr(row_base)
@@ -317,8 +342,10 @@ def prepare_rehydrate(k_in, k_out, *, rope: RopeSpec, chunk_pos=None, v_in=None,
         a.page_size = int(page_size)
         a.n_pool_pages = int(n_pool_pages)
     a.status = _ptr(status)
+    _i32_dev(delta, "delta")
+    a.delta = _ptr(delta)
     keep = (k_in, k_out, v_in, v_out, u_k, w_k, u_v, w_v, chunk_pos, explicit_pos, chunk_tokens,
-            row_base, page_table, status)
+            row_base, page_table, status, delta, u_pe, w_pe, k_layer_rank, v_layer_rank, pe_layer_rank)
     return Prepared(L.kamera_rehydrate, a, keep)
 
 

@@ -192,6 +192,18 @@ extern "C" int kamera_rehydrate(const kamera_rehydrate_args* a, void* stream) {
   }
   for (int p = 0; p < a->n_planes; ++p) {
     const kamera_plane& q = a->plane[p];
+    int cb = q.col_begin, ce = q.col_end;
+    if (cb == 0 && ce == 0) ce = a->head_dim;
+    if (cb < 0 || ce > a->head_dim || cb >= ce)
+      return fail(KAMERA_ERR_SHAPE, "%s: plane %d columns [%d, %d) outside the %d-column row", who, p, cb, ce,
+                  a->head_dim);
+    if (cb % 32 != 0 || ce % 32 != 0)
+      return fail(KAMERA_ERR_UNSUPPORTED, "%s: plane %d column range must start/end on multiples of 32", who, p);
+    if (q.rotate && (a->rope.rope_offset < cb || a->rope.rope_offset + a->rope.rope_dim > ce))
+      return fail(KAMERA_ERR_SHAPE, "%s: plane %d rotates but its columns [%d, %d) do not hold the rope band",
+                  who, p, cb, ce);
+    if (q.m > 0 && (q.patch_offset < cb || (int64_t)q.patch_offset + q.patch_dim > ce))
+      return fail(KAMERA_ERR_SHAPE, "%s: plane %d patch columns lie outside its column range", who, p);
     if (q.m < 0 || q.m > KAMERA_MAX_RANK)
       return fail(KAMERA_ERR_RANGE, "%s: plane %d rank m = %d outside [0, %d]", who, p, q.m, KAMERA_MAX_RANK);
     if (q.rotate != 0 && q.rotate != 1) return fail(KAMERA_ERR_SHAPE, "%s: plane %d rotate must be 0 or 1", who, p);
@@ -249,6 +261,7 @@ extern "C" int kamera_rehydrate(const kamera_rehydrate_args* a, void* stream) {
              a->page_size, a->n_pool_pages, a->status);
   P.chunk_pos = a->chunk_pos;
   P.explicit_pos = a->explicit_pos;
+  P.delta = any_rot ? a->delta : nullptr;
   P.explicit_cs = a->explicit_chunk_stride;
   P.pos_mode = a->pos_mode;
   P.grid_w = a->grid_w > 0 ? a->grid_w : 1;
@@ -272,20 +285,21 @@ extern "C" int kamera_rehydrate(const kamera_rehydrate_args* a, void* stream) {
     memcpy(o.w_s, q.w_stride, sizeof(o.w_s));
     o.m = q.m;
     o.m_steps = (q.m + 31) / 32;
+    o.layer_rank = q.layer_rank;
     o.patch_lo = q.m > 0 ? q.patch_offset : 0;
     o.patch_hi = q.m > 0 ? q.patch_offset + q.patch_dim : 0;
     o.u_vec = q.m % 8 == 0 && aligned16(q.U) && strides_ok(q.u_stride, 4);
     o.w_vec = aligned16(q.W) && strides_ok(q.w_stride, 4);
     // column blocks: the rotated band as one block, the rest in <= 128-column pieces
     std::vector<std::pair<int, int>> segs;  // [col0, col1)
-    const int D = a->head_dim;
+    const int cb = q.col_begin, ce = (q.col_begin == 0 && q.col_end == 0) ? a->head_dim : q.col_end;
     if (q.rotate) {
       const int r0 = a->rope.rope_offset, r1 = r0 + a->rope.rope_dim;
-      if (r0 > 0) segs.push_back({0, r0});
+      if (r0 > cb) segs.push_back({cb, r0});
       segs.push_back({r0, r1});
-      if (r1 < D) segs.push_back({r1, D});
+      if (r1 < ce) segs.push_back({r1, ce});
     } else {
-      segs.push_back({0, D});
+      segs.push_back({cb, ce});
     }
     int nb = 0;
     for (auto& sg : segs) {

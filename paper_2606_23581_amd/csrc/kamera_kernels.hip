@@ -116,6 +116,9 @@ struct TileCtx {
   int col0;           // first column of the block
   int ldw;            // LDS row stride of W^T in elements
   bool patched;       // block intersects the patch columns and m > 0
+  bool u_vec;         // 16-byte U loads are legal at this layer's rank
+  int m;              // rank at this layer (layer_rank may lower the plane's m)
+  int m_steps;        // ceil(m / 32)
   int64_t in_base;    // element offset of (c, l, token 0, h, col0) in the input
   int64_t u_base;     // element offset of (c, l, h, token 0) in U
 };
@@ -227,9 +230,9 @@ __device__ __forceinline__ void tile_load(const TileCtx& T, int i0, TileRegs<NQ,
   }
   if constexpr (MS > 0) {
     if (!T.patched) return;
-    if (Q.u_vec && Staged<NQ>::value) {
+    if (T.u_vec && Staged<NQ>::value) {
       // 16 rows x 4*m_steps chunks (rank padded to 32); chunks past m stay zero
-      const int cpr = Q.m >> 3, cpad = 4 * Q.m_steps;
+      const int cpr = T.m >> 3, cpad = 4 * T.m_steps;
 #pragma unroll
       for (int s = 0; s < MS; ++s) {
         const int cidx = 64 * s + lane;
@@ -248,14 +251,14 @@ __device__ __forceinline__ void tile_load(const TileCtx& T, int i0, TileRegs<NQ,
       for (int s = 0; s < MS; ++s) {
         u32x4 v = u32x4{0, 0, 0, 0};
         const int k0 = 32 * s + 8 * g;
-        if (s < Q.m_steps && i < T.n_c) {
-          if (Q.u_vec) {
-            if (k0 < Q.m) v = ld16(urow + k0);
+        if (s < T.m_steps && i < T.n_c) {
+          if (T.u_vec) {
+            if (k0 < T.m) v = ld16(urow + k0);
           } else {
             uint32_t w4[4] = {0, 0, 0, 0};
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
-              const uint32_t b = (k0 + e < Q.m) ? urow[k0 + e] : 0u;
+              const uint32_t b = (k0 + e < T.m) ? urow[k0 + e] : 0u;
               w4[e >> 1] |= (e & 1) ? (b << 16) : b;
             }
             v = u32x4{w4[0], w4[1], w4[2], w4[3]};
@@ -267,7 +270,7 @@ __device__ __forceinline__ void tile_load(const TileCtx& T, int i0, TileRegs<NQ,
   }
 }
 
-template <int NQ, int MS, int ROT>
+template <int NQ, int MS, int ROT, bool RELOC>
 __device__ __forceinline__ void tile_compute(const RehydrateParams& P, const TileCtx& T, int i0,
                                              const TileRegs<NQ, MS>& R, const uint16_t* __restrict__ Wt,
                                              uint8_t* tile_lds, const double* s_freq,
@@ -277,7 +280,7 @@ __device__ __forceinline__ void tile_compute(const RehydrateParams& P, const Til
   const int g = lane >> 4;
   const int t = lane & 15;
   constexpr int kRowB = 64 * NQ + kRowPad;          // LDS row stride of the tile buffer
-  const bool u_staged = MS > 0 && T.patched && Q.u_vec && Staged<NQ>::value;
+  const bool u_staged = MS > 0 && T.patched && T.u_vec && Staged<NQ>::value;
   const int u_rowb = 64 * Q.m_steps + kRowPad;
 
   // ---- K chunks in MFMA order: lane (g, t) takes chunks g + 4q of row t ----
@@ -298,7 +301,7 @@ __device__ __forceinline__ void tile_compute(const RehydrateParams& P, const Til
   uint8_t* u_lds = tile_lds;
   if constexpr (MS > 0) {
     if (u_staged) {
-      const int cpad = 4 * Q.m_steps;
+      const int cpad = 4 * T.m_steps;
 #pragma unroll
       for (int s = 0; s < MS; ++s) {
         const int cidx = 64 * s + lane;
@@ -326,7 +329,21 @@ __device__ __forceinline__ void tile_compute(const RehydrateParams& P, const Til
   double pt = 0.0, ph = 0.0, pw = 0.0;
   if constexpr (ROT != 0) {
     token_position(P, T.c, valid ? i : T.n_c - 1, pt, ph, pw);
-    if (P.patch_post_rope) rotate_tile<NQ, ROT>(acc, g, s_freq, s_coord, pt, ph, pw);
+    // Rotation applied before the patch:
+    //   post-rope frame:            R(p) K          (+ U W after)
+    //   relocation, post-rope:      R(delta) K      (+ U W after)
+    //   relocation, pre-rope:       R(-(p - delta)) K, the stored frame
+    //                               (+ U W, then R(p) below)
+    if constexpr (RELOC) {
+      const double dt = (double)P.delta[3 * T.c], dh = (double)P.delta[3 * T.c + 1],
+                   dw = (double)P.delta[3 * T.c + 2];
+      if (P.patch_post_rope)
+        rotate_tile<NQ, ROT>(acc, g, s_freq, s_coord, dt, dh, dw);
+      else
+        rotate_tile<NQ, ROT>(acc, g, s_freq, s_coord, dt - pt, dh - ph, dw - pw);
+    } else if (P.patch_post_rope) {
+      rotate_tile<NQ, ROT>(acc, g, s_freq, s_coord, pt, ph, pw);
+    }
   }
 
   if constexpr (MS > 0) {
@@ -335,7 +352,7 @@ __device__ __forceinline__ void tile_compute(const RehydrateParams& P, const Til
       const int rbase = 8 * (t >> 2) + (t & 3);
 #pragma unroll
       for (int s = 0; s < MS; ++s) {
-        if (s < Q.m_steps) {
+        if (s < T.m_steps) {
           const u32x4 ub = u_staged ? *reinterpret_cast<const u32x4*>(u_lds + t * u_rowb + 2 * (32 * s + 8 * g))
                                     : R.u[s];
           const bf16x8 b = __builtin_bit_cast(bf16x8, ub);
@@ -406,7 +423,7 @@ __device__ __forceinline__ void tile_compute(const RehydrateParams& P, const Til
 template <int NQ>
 __device__ __forceinline__ void stage_w(const TileCtx& T, uint16_t* Wt) {
   const PlaneParams& Q = *T.Q;
-  const int m_pad = 32 * Q.m_steps;
+  const int m_pad = 32 * T.m_steps;
   const int k4s = m_pad / 4;
   const int n_items = k4s * (4 * NQ);
   const uint16_t* wbase = Q.W + (int64_t)T.c * Q.w_s[0] + (int64_t)T.l * Q.w_s[1] +
@@ -421,7 +438,7 @@ __device__ __forceinline__ void stage_w(const TileCtx& T, uint16_t* Wt) {
     for (int r = 0; r < 4; ++r) {
       w[r][0] = w[r][1] = w[r][2] = w[r][3] = 0u;
       const int k = k0 + r;
-      if (in_patch && k < Q.m) {
+      if (in_patch && k < T.m) {
         const uint16_t* p = wbase + (int64_t)k * Q.w_s[3] + wcol;
         if (Q.w_vec) {
           const u32x4 v = *reinterpret_cast<const u32x4*>(p);
@@ -446,7 +463,7 @@ __device__ __forceinline__ void stage_w(const TileCtx& T, uint16_t* Wt) {
   }
 }
 
-template <int NQ, int MS, int ROT>
+template <int NQ, int MS, int ROT, bool RELOC>
 __device__ __forceinline__ void rehydrate_block(const RehydrateParams& P, const TileCtx& T, int t_begin, int t_end,
                                                 uint8_t* lds, double* s_freq, int* s_coord) {
   uint16_t* Wt = reinterpret_cast<uint16_t*>(lds);
@@ -468,12 +485,13 @@ __device__ __forceinline__ void rehydrate_block(const RehydrateParams& P, const 
   for (int tile = wave; tile < n_tiles; tile += kWaves) {
     TileRegs<NQ, MS> R;
     tile_load<NQ, MS>(T, t_begin + tile * kTileTokens, R);
-    tile_compute<NQ, MS, ROT>(P, T, t_begin + tile * kTileTokens, R, Wt, tile_lds, s_freq, s_coord);
+    tile_compute<NQ, MS, ROT, RELOC>(P, T, t_begin + tile * kTileTokens, R, Wt, tile_lds, s_freq, s_coord);
   }
 }
 
-template <int MS>
-__global__ __launch_bounds__(kThreads, MS == 4 ? 3 : 4) void rehydrate_kernel(const RehydrateParams /*by value, read in place*/) {
+// RELOC: the keys are already rotated and move by the chunk's delta
+template <int MS, bool RELOC>
+__global__ __launch_bounds__(kThreads, MS == 4 || RELOC ? 3 : 4) void rehydrate_kernel(const RehydrateParams /*by value, read in place*/) {
   const RehydrateParams& P = kernel_params<RehydrateParams>();
   extern __shared__ __align__(16) uint8_t lds_dyn[];
   __shared__ double s_freq[kMaxPairs];
@@ -503,21 +521,28 @@ __global__ __launch_bounds__(kThreads, MS == 4 ? 3 : 4) void rehydrate_kernel(co
   const ColBlock B = Q.blk[b];
   T.col0 = 8 * (int)B.col0;
   T.ldw = 32 * Q.m_steps + 8;
-  T.patched = (B.flags & kBlkPatch) && Q.m > 0;
+  T.m = Q.m;
+  if (Q.layer_rank != nullptr) {
+    const int r = Q.layer_rank[T.l];
+    T.m = r < 0 ? 0 : (r < Q.m ? r : Q.m);
+  }
+  T.m_steps = (T.m + 31) / 32;
+  T.u_vec = Q.u_vec && (T.m % 8 == 0);
+  T.patched = (B.flags & kBlkPatch) && T.m > 0;
   T.in_base = (int64_t)T.c * Q.in_s[0] + (int64_t)T.l * Q.in_s[1] + (int64_t)T.h * Q.in_s[3] + T.col0;
   T.u_base = (int64_t)T.c * Q.u_s[0] + (int64_t)T.l * Q.u_s[1] + (int64_t)T.h * Q.u_s[2];
   const int rot = (B.flags & kBlkRotate) ? (P.rope.pairing == 0 ? 1 : 2) : 0;
   switch (B.nq * 3 + rot) {
-    case 1 * 3 + 0: rehydrate_block<1, MS, 0>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
-    case 1 * 3 + 2: rehydrate_block<1, MS, 2>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
-    case 2 * 3 + 0: rehydrate_block<2, MS, 0>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
-    case 2 * 3 + 1: rehydrate_block<2, MS, 1>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
-    case 2 * 3 + 2: rehydrate_block<2, MS, 2>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
-    case 3 * 3 + 0: rehydrate_block<3, MS, 0>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
-    case 3 * 3 + 2: rehydrate_block<3, MS, 2>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
-    case 4 * 3 + 0: rehydrate_block<4, MS, 0>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
-    case 4 * 3 + 1: rehydrate_block<4, MS, 1>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
-    case 4 * 3 + 2: rehydrate_block<4, MS, 2>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
+    case 1 * 3 + 0: rehydrate_block<1, MS, 0, RELOC>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
+    case 1 * 3 + 2: rehydrate_block<1, MS, 2, RELOC>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
+    case 2 * 3 + 0: rehydrate_block<2, MS, 0, RELOC>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
+    case 2 * 3 + 1: rehydrate_block<2, MS, 1, RELOC>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
+    case 2 * 3 + 2: rehydrate_block<2, MS, 2, RELOC>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
+    case 3 * 3 + 0: rehydrate_block<3, MS, 0, RELOC>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
+    case 3 * 3 + 2: rehydrate_block<3, MS, 2, RELOC>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
+    case 4 * 3 + 0: rehydrate_block<4, MS, 0, RELOC>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
+    case 4 * 3 + 1: rehydrate_block<4, MS, 1, RELOC>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
+    case 4 * 3 + 2: rehydrate_block<4, MS, 2, RELOC>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
     default: break;                              // rejected on the host (NeoX needs an even NQ)
   }
 }
@@ -529,11 +554,20 @@ hipError_t launch_rehydrate(const RehydrateParams& p, hipStream_t s) {
   const size_t lds = (size_t)128 * (32 * ms + 8) * sizeof(uint16_t) +
                      (size_t)(kThreads / 64) * tile_lds_bytes();
   const dim3 grid((uint32_t)((int64_t)p.per_xcd * 8)), block(kThreads);
-  switch (max_steps) {
-    case 0: hipLaunchKernelGGL(rehydrate_kernel<0>, grid, block, lds, s, p); break;
-    case 1: hipLaunchKernelGGL(rehydrate_kernel<1>, grid, block, lds, s, p); break;
-    case 2: hipLaunchKernelGGL(rehydrate_kernel<2>, grid, block, lds, s, p); break;
-    default: hipLaunchKernelGGL(rehydrate_kernel<4>, grid, block, lds, s, p); break;
+  if (p.delta != nullptr) {
+    switch (max_steps) {
+      case 0: hipLaunchKernelGGL((rehydrate_kernel<0, true>), grid, block, lds, s, p); break;
+      case 1: hipLaunchKernelGGL((rehydrate_kernel<1, true>), grid, block, lds, s, p); break;
+      case 2: hipLaunchKernelGGL((rehydrate_kernel<2, true>), grid, block, lds, s, p); break;
+      default: hipLaunchKernelGGL((rehydrate_kernel<4, true>), grid, block, lds, s, p); break;
+    }
+  } else {
+    switch (max_steps) {
+      case 0: hipLaunchKernelGGL((rehydrate_kernel<0, false>), grid, block, lds, s, p); break;
+      case 1: hipLaunchKernelGGL((rehydrate_kernel<1, false>), grid, block, lds, s, p); break;
+      case 2: hipLaunchKernelGGL((rehydrate_kernel<2, false>), grid, block, lds, s, p); break;
+      default: hipLaunchKernelGGL((rehydrate_kernel<4, false>), grid, block, lds, s, p); break;
+    }
   }
   return hipGetLastError();
 }

@@ -49,6 +49,7 @@ struct PlaneParams {
   int32_t w_vec;                     // 16-byte W loads are legal
   int32_t n_blocks;
   int32_t block_base;                // index of this plane's first block within a task group
+  const int32_t* layer_rank;         // optional per-layer rank (<= m)
   ColBlock blk[kMaxBlocks];
 };
 
@@ -71,6 +72,7 @@ struct RehydrateParams {
   Placement place;
   const int32_t* chunk_pos;
   const int32_t* explicit_pos;
+  const int32_t* delta;              // relocation of already-rotated keys, or null
   int64_t explicit_cs;
   int32_t pos_mode;
   int32_t grid_w;

@@ -92,6 +92,9 @@ class RehydrateCase:
     ragged: bool = False
     post_rope: bool = False
     shared_w: bool = False
+    reloc: bool = False                # keys already rotated; move by a per-chunk delta
+    m_pe: int = 0                      # separate patch on the rope band (MLA k_pe), keys only
+    layer_rank: Optional[Tuple[int, ...]] = None   # rank used per layer (both planes)
     seed: int = 0
 
 
@@ -117,6 +120,13 @@ def run_rehydrate(case: RehydrateCase, device):
 
     Uk, Wk = factors(case.m_k)
     Uv, Wv = factors(case.m_v) if case.has_v else (None, None)
+    Upe = Wpe = None
+    if case.m_pe:
+        Upe = synth.randn_bf16_numpy((C, L, H, n, case.m_pe), 0.1, rng)
+        Wpe = synth.randn_bf16_numpy((1 if case.shared_w else C, L, H, case.m_pe, case.rope_dim), 0.1, rng)
+    delta = rng.integers(-3000, 3000, size=(C, 3)).astype(np.int32)
+    if case.sections is None:
+        delta[:, 1:] = delta[:, :1]
     n_c = (rng.integers(0, n + 1, size=C) if case.ragged else np.full(C, n)).astype(np.int32)
     if case.ragged:
         n_c[0] = n
@@ -161,6 +171,13 @@ def run_rehydrate(case: RehydrateCase, device):
               chunk_tokens=dev_i32(n_c, device) if case.ragged else None)
     status = dev_i32(np.zeros(1), device)
     kw["status"] = status
+    if case.reloc:
+        kw["delta"] = dev_i32(delta, device)
+    if case.m_pe:
+        kw.update(u_pe=dev(Upe, device), w_pe=wt(Wpe))
+    if case.layer_rank is not None:
+        lr = dev_i32(np.array(case.layer_rank), device)
+        kw.update(k_layer_rank=lr, v_layer_rank=lr, pe_layer_rank=lr)
     if case.has_v:
         kw.update(v_in=dev(V, device), u_v=dev(Uv, device) if Uv is not None else None, w_v=wt(Wv),
                   v_patch=case.patch)
@@ -194,17 +211,35 @@ def run_rehydrate(case: RehydrateCase, device):
             dst = row_base[c] + np.arange(nc)
         for l in range(L):
             touched[l, dst] = True
+            r_l = None if case.layer_rank is None else case.layer_rank[l]
+
+            def fac(Ua, Wa, width_off):
+                if Ua is None:
+                    return None, None
+                r = Ua.shape[-1] if r_l is None else min(r_l, Ua.shape[-1])
+                u_ = ref.bf16_to_f64(Ua[c, l, h, :nc, :r])
+                w_ = ref.bf16_to_f64(Wa[0 if case.shared_w else c, l, h, :r])
+                return u_, w_
+
             for h in range(H):
-                wc = 0 if case.shared_w else c
                 Kin = ref.bf16_to_f64(K[c, l, :nc, h])
-                u = ref.bf16_to_f64(Uk[c, l, h, :nc]) if Uk is not None else None
-                w = ref.bf16_to_f64(Wk[wc, l, h]) if Wk is not None else None
-                want = ref.rehydrate_k(Kin, u, w, orope, p3, case.patch[0], case.post_rope)
+                u, w = fac(Uk, Wk, 0)
+                poff = case.patch[0]
+                if case.m_pe:
+                    # two patches on disjoint columns == one patch with a block basis
+                    up, wp = fac(Upe, Wpe, 0)
+                    W_full = np.zeros((u.shape[1] + up.shape[1], D))
+                    W_full[:u.shape[1], case.patch[0]:case.patch[0] + w.shape[1]] = w
+                    W_full[u.shape[1]:, case.rope_offset:case.rope_offset + case.rope_dim] = wp
+                    u, w, poff = np.concatenate([u, up], axis=1), W_full, 0
+                if case.reloc:
+                    want = ref.relocate_k(Kin, u, w, orope, p3, delta[c], poff, case.post_rope)
+                else:
+                    want = ref.rehydrate_k(Kin, u, w, orope, p3, poff, case.post_rope)
                 assert_close(kb[l, dst, h], want, f"K c{c} l{l} h{h}")
                 if case.has_v:
                     Vin = ref.bf16_to_f64(V[c, l, :nc, h])
-                    u = ref.bf16_to_f64(Uv[c, l, h, :nc]) if Uv is not None else None
-                    w = ref.bf16_to_f64(Wv[wc, l, h]) if Wv is not None else None
+                    u, w = fac(Uv, Wv, 0)
                     assert_close(vb[l, dst, h], ref.rehydrate_v(Vin, u, w, case.patch[0]),
                                  f"V c{c} l{l} h{h}")
     assert np.all(kb[~touched] == SENTINEL), "K rows outside the destination were written"

@@ -131,6 +131,11 @@ def test_empty_call_is_a_noop():
     ("grid_w_zero", km.ERR_SHAPE),
     ("bad_pos_mode", km.ERR_SHAPE),
     ("bad_frame", km.ERR_SHAPE),
+    ("cols_unaligned", km.ERR_UNSUPPORTED),
+    ("cols_empty", km.ERR_SHAPE),
+    ("cols_outside_row", km.ERR_SHAPE),
+    ("cols_miss_band", km.ERR_SHAPE),
+    ("patch_outside_cols", km.ERR_SHAPE),
 ])
 def test_rehydrate_rejects(case, code):
     L = km.lib()
@@ -203,6 +208,16 @@ def test_rehydrate_rejects(case, code):
         a.pos_mode = 7
     elif case == "bad_frame":
         a.patch_frame = 5
+    elif case == "cols_unaligned":
+        a.plane[1].col_begin, a.plane[1].col_end = 16, 128
+    elif case == "cols_empty":
+        a.plane[1].col_begin, a.plane[1].col_end = 64, 64
+    elif case == "cols_outside_row":
+        a.plane[1].col_begin, a.plane[1].col_end = 0, 160
+    elif case == "cols_miss_band":
+        a.plane[0].col_begin, a.plane[0].col_end = 0, 64
+    elif case == "patch_outside_cols":
+        a.plane[1].col_begin, a.plane[1].col_end = 64, 128
     assert call_rehydrate(a) == code, km.last_error()
     assert km.last_error().startswith("kamera_rehydrate")
 

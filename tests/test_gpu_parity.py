@@ -49,6 +49,22 @@ REHYDRATE_CASES = {
                                                    n=61, seed=18),
     "explicit_positions": RehydrateCase(sections=(16, 24, 24), pos_mode="explicit", n=45, seed=19),
     "paged_page_size_1": RehydrateCase(paged=True, page_size=1, n=20, seed=20),
+    # survivors: keys already rotated, moved by delta with a removal patch
+    "relocate_neox_m64": RehydrateCase(reloc=True, m_k=64, m_v=64, n=70, seed=21),
+    "relocate_interleaved_post_frame": RehydrateCase(reloc=True, pairing="interleaved", theta=1e4,
+                                                     post_rope=True, seed=22),
+    "relocate_mrope_grid_paged": RehydrateCase(reloc=True, sections=(16, 24, 24), pos_mode="grid3",
+                                               paged=True, m_k=32, m_v=0, seed=23),
+    "relocate_no_patch": RehydrateCase(reloc=True, m_k=0, m_v=0, seed=24),
+    # MLA with a second, separate patch on the rope key band
+    "mla_band_patch": RehydrateCase(D=576, H=1, rope_dim=64, rope_offset=512, pairing="interleaved",
+                                    theta=1e4, patch=(0, 512), m_k=32, m_pe=16, has_v=False, n=77, seed=25),
+    "mla_band_patch_reloc_paged": RehydrateCase(D=576, H=1, rope_dim=64, rope_offset=512, pairing="neox",
+                                                theta=1e4, patch=(0, 512), m_k=32, m_pe=8, has_v=False,
+                                                reloc=True, paged=True, n=40, seed=26),
+    # deep-half patch: no factors on the shallow layers, odd ranks on others
+    "layer_rank_deep_half": RehydrateCase(L=4, layer_rank=(0, 0, 16, 16), m_k=16, m_v=16, seed=27),
+    "layer_rank_odd": RehydrateCase(L=3, layer_rank=(5, 64, 33), m_k=64, m_v=48, seed=28),
 }
 
 
