@@ -161,7 +161,10 @@ typedef struct {
  *                      out + l*out_stride[1] + slot*out_stride[2]
  *                          + h*out_stride[3]   (out_stride[0] unused)
  * Outputs must not overlap inputs (checked on the extents the host-visible
- * sizes imply).
+ * sizes imply), except exactly in place: a dense output with row_base NULL,
+ * the same base pointer and the same strides as the input (each element is
+ * then read and written by the same workgroup; two planes in place on one
+ * tensor must cover disjoint columns).
  *
  * Relocation (delta != NULL, device int32 [n_chunks][3]): the input keys are
  * already rotated, at target - delta (survivors of a window slide, Sec. 5),
@@ -261,6 +264,12 @@ int kamera_scatter_paged(const kamera_scatter_args* args, void* stream);
 int kamera_check_page_table(const int32_t* host_page_table, int32_t n_chunks,
                             int32_t pt_stride, int32_t n_tokens,
                             int32_t page_size, int32_t n_pool_pages);
+
+/* Run exactly the host-side checks of an entry point (0 kamera_rehydrate,
+ * 1 kamera_shift, 2 kamera_scatter_paged) on `args` without launching
+ * anything: KAMERA_OK when the call would be enqueued, else the error code
+ * the call would return.  Touches no device memory. */
+int kamera_validate(int32_t which, const void* args);
 
 /* Text of the last error on the calling thread ("" after a successful call);
  * valid until the next call on that thread. */

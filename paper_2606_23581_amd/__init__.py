@@ -105,7 +105,7 @@ class CScatterArgs(ctypes.Structure):
 
 
 EXPORTS = ("kamera_rehydrate", "kamera_shift", "kamera_scatter_paged", "kamera_check_page_table",
-           "kamera_last_error", "kamera_abi_version", "kamera_struct_size")
+           "kamera_validate", "kamera_last_error", "kamera_abi_version", "kamera_struct_size")
 
 _LIB = None
 
@@ -133,6 +133,8 @@ def lib() -> ctypes.CDLL:
     L.kamera_last_error.restype = ctypes.c_char_p
     L.kamera_abi_version.argtypes = []
     L.kamera_abi_version.restype = _i32
+    L.kamera_validate.argtypes = [_i32, _vp]
+    L.kamera_validate.restype = _i32
     L.kamera_struct_size.argtypes = [_i32]
     L.kamera_struct_size.restype = _i64
     sizes = {0: CRehydrateArgs, 1: CShiftArgs, 2: CScatterArgs, 3: CPlane, 4: CRope}

@@ -160,8 +160,11 @@ int pick_grid(int64_t n_tasks, int32_t& per_xcd, const char* who) {
 // kamera_rehydrate
 // ---------------------------------------------------------------------------
 
-extern "C" int kamera_rehydrate(const kamera_rehydrate_args* a, void* stream) {
+// Validation and kernel parameters of a rehydrate call; *launch is false for
+// an empty call (nothing to do).
+static int build_rehydrate(const kamera_rehydrate_args* a, kamera::RehydrateParams& P, bool& launch) {
   const char* who = "kamera_rehydrate";
+  launch = false;
   if (a == nullptr) return fail(KAMERA_ERR_NULL, "%s: args is NULL", who);
   if (a->n_chunks < 0 || a->n_layers < 0 || a->n_heads < 0 || a->n_tokens < 0)
     return fail(KAMERA_ERR_SHAPE, "%s: negative n_chunks/n_layers/n_heads/n_tokens", who);
@@ -219,7 +222,7 @@ extern "C" int kamera_rehydrate(const kamera_rehydrate_args* a, void* stream) {
   if (rc) return rc;
 
   const int64_t work = (int64_t)a->n_chunks * a->n_layers * a->n_heads * a->n_tokens;
-  if (work == 0) return ok();  // empty call: nothing to read or write
+  if (work == 0) return KAMERA_OK;  // empty call: nothing to read or write
 
   if (any_rot && a->pos_mode != KAMERA_POS_EXPLICIT && a->chunk_pos == nullptr)
     return fail(KAMERA_ERR_NULL, "%s: chunk_pos is NULL", who);
@@ -249,12 +252,21 @@ extern "C" int kamera_rehydrate(const kamera_rehydrate_args* a, void* stream) {
       } else {
         extent(r.out, r.out_stride, ein, a->head_dim, olo, ohi);
       }
+      // Exact in place is allowed: same base and strides, dense rows, no row
+      // base -- every element is then read and written by the workgroup that
+      // owns it, provided two different planes cover disjoint columns.
+      const bool same_map = !a->paged && a->row_base == nullptr && r.out == q.in &&
+                            memcmp(r.out_stride, q.in_stride, sizeof(q.in_stride)) == 0;
+      if (same_map) {
+        const int qb = q.col_begin, qe = (q.col_begin == 0 && q.col_end == 0) ? a->head_dim : q.col_end;
+        const int rb = r.col_begin, re = (r.col_begin == 0 && r.col_end == 0) ? a->head_dim : r.col_end;
+        if (o == p || qe <= rb || re <= qb) continue;
+      }
       if (overlap(ilo, ihi, olo, ohi))
         return fail(KAMERA_ERR_ALIAS, "%s: output of plane %d overlaps the input of plane %d", who, o, p);
     }
   }
 
-  kamera::RehydrateParams P;
   memset(&P, 0, sizeof(P));
   if (any_rot) fill_rope(a->rope, P.rope);
   fill_place(P.place, a->n_tokens, a->chunk_tokens, a->paged, a->row_base, a->page_table, a->pt_stride,
@@ -338,9 +350,19 @@ extern "C" int kamera_rehydrate(const kamera_rehydrate_args* a, void* stream) {
   P.n_tasks = n_tasks;
   rc = pick_grid(P.n_tasks, P.per_xcd, who);
   if (rc) return rc;
+  launch = true;
+  return KAMERA_OK;
+}
 
-  const hipError_t e = kamera::launch_rehydrate(P, static_cast<hipStream_t>(stream));
-  if (e != hipSuccess) return fail(KAMERA_ERR_HIP, "%s: launch failed: %s", who, hipGetErrorString(e));
+extern "C" int kamera_rehydrate(const kamera_rehydrate_args* a, void* stream) {
+  static thread_local kamera::RehydrateParams P;
+  bool launch = false;
+  const int rc = build_rehydrate(a, P, launch);
+  if (rc) return rc;
+  if (launch) {
+    const hipError_t e = kamera::launch_rehydrate(P, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return fail(KAMERA_ERR_HIP, "kamera_rehydrate: launch failed: %s", hipGetErrorString(e));
+  }
   return ok();
 }
 
@@ -348,8 +370,9 @@ extern "C" int kamera_rehydrate(const kamera_rehydrate_args* a, void* stream) {
 // kamera_shift
 // ---------------------------------------------------------------------------
 
-extern "C" int kamera_shift(const kamera_shift_args* a, void* stream) {
+static int build_shift(const kamera_shift_args* a, kamera::ShiftParams& P, bool& launch) {
   const char* who = "kamera_shift";
+  launch = false;
   if (a == nullptr) return fail(KAMERA_ERR_NULL, "%s: args is NULL", who);
   if (a->n_chunks < 0 || a->n_layers < 0 || a->n_heads < 0 || a->n_tokens < 0)
     return fail(KAMERA_ERR_SHAPE, "%s: negative n_chunks/n_layers/n_heads/n_tokens", who);
@@ -369,13 +392,12 @@ extern "C" int kamera_shift(const kamera_shift_args* a, void* stream) {
   rc = check_paging(a->paged, a->page_table, a->pt_stride, a->page_size, a->n_pool_pages, a->n_tokens, who);
   if (rc) return rc;
   const int64_t work = (int64_t)a->n_chunks * a->n_layers * a->n_heads * a->n_tokens;
-  if (work == 0) return ok();
+  if (work == 0) return KAMERA_OK;
   if (a->k == nullptr) return fail(KAMERA_ERR_NULL, "%s: k is NULL", who);
   if (a->delta == nullptr) return fail(KAMERA_ERR_NULL, "%s: delta is NULL", who);
   if (!aligned16(a->k) || !strides_ok(a->k_stride, 4))
     return fail(KAMERA_ERR_ALIGN, "%s: k rows must be 16-byte aligned (base %% 16, strides %% 8)", who);
 
-  kamera::ShiftParams P;
   memset(&P, 0, sizeof(P));
   fill_rope(r, P.rope);
   fill_place(P.place, a->n_tokens, a->chunk_tokens, a->paged, a->row_base, a->page_table, a->pt_stride,
@@ -396,8 +418,19 @@ extern "C" int kamera_shift(const kamera_shift_args* a, void* stream) {
   P.n_tasks = (int64_t)a->n_chunks * a->n_layers * P.n_tblk;
   rc = pick_grid(P.n_tasks, P.per_xcd, who);
   if (rc) return rc;
-  const hipError_t e = kamera::launch_shift(P, static_cast<hipStream_t>(stream));
-  if (e != hipSuccess) return fail(KAMERA_ERR_HIP, "%s: launch failed: %s", who, hipGetErrorString(e));
+  launch = true;
+  return KAMERA_OK;
+}
+
+extern "C" int kamera_shift(const kamera_shift_args* a, void* stream) {
+  static thread_local kamera::ShiftParams P;
+  bool launch = false;
+  const int rc = build_shift(a, P, launch);
+  if (rc) return rc;
+  if (launch) {
+    const hipError_t e = kamera::launch_shift(P, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return fail(KAMERA_ERR_HIP, "kamera_shift: launch failed: %s", hipGetErrorString(e));
+  }
   return ok();
 }
 
@@ -405,8 +438,9 @@ extern "C" int kamera_shift(const kamera_shift_args* a, void* stream) {
 // kamera_scatter_paged
 // ---------------------------------------------------------------------------
 
-extern "C" int kamera_scatter_paged(const kamera_scatter_args* a, void* stream) {
+static int build_scatter(const kamera_scatter_args* a, kamera::ScatterParams& P, bool& launch) {
   const char* who = "kamera_scatter_paged";
+  launch = false;
   if (a == nullptr) return fail(KAMERA_ERR_NULL, "%s: args is NULL", who);
   if (a->n_chunks < 0 || a->n_layers < 0 || a->n_tokens < 0)
     return fail(KAMERA_ERR_SHAPE, "%s: negative n_chunks/n_layers/n_tokens", who);
@@ -415,7 +449,7 @@ extern "C" int kamera_scatter_paged(const kamera_scatter_args* a, void* stream) 
   int rc = check_paging(1, a->page_table, a->pt_stride, a->page_size, a->n_pool_pages, a->n_tokens, who);
   if (rc) return rc;
   const int64_t work = (int64_t)a->n_chunks * a->n_layers * a->n_tokens;
-  if (work == 0) return ok();
+  if (work == 0) return KAMERA_OK;
   if (a->src == nullptr || a->pool == nullptr) return fail(KAMERA_ERR_NULL, "%s: src or pool is NULL", who);
   for (int k = 0; k < 3; ++k)
     if (a->src_stride_bytes[k] % 16 != 0) return fail(KAMERA_ERR_ALIGN, "%s: src strides must be multiples of 16", who);
@@ -441,7 +475,6 @@ extern "C" int kamera_scatter_paged(const kamera_scatter_args* a, void* stream) 
     if (overlap(slo, shi, plo, phi)) return fail(KAMERA_ERR_ALIAS, "%s: src overlaps the pool", who);
   }
 
-  kamera::ScatterParams P;
   memset(&P, 0, sizeof(P));
   fill_place(P.place, a->n_tokens, a->chunk_tokens, 1, nullptr, a->page_table, a->pt_stride, a->page_size,
              a->n_pool_pages, a->status);
@@ -461,9 +494,32 @@ extern "C" int kamera_scatter_paged(const kamera_scatter_args* a, void* stream) 
   P.n_tasks = (int64_t)a->n_chunks * a->n_layers * P.n_tblk;
   rc = pick_grid(P.n_tasks, P.per_xcd, who);
   if (rc) return rc;
-  const hipError_t e = kamera::launch_scatter(P, static_cast<hipStream_t>(stream));
-  if (e != hipSuccess) return fail(KAMERA_ERR_HIP, "%s: launch failed: %s", who, hipGetErrorString(e));
+  launch = true;
+  return KAMERA_OK;
+}
+
+extern "C" int kamera_scatter_paged(const kamera_scatter_args* a, void* stream) {
+  static thread_local kamera::ScatterParams P;
+  bool launch = false;
+  const int rc = build_scatter(a, P, launch);
+  if (rc) return rc;
+  if (launch) {
+    const hipError_t e = kamera::launch_scatter(P, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return fail(KAMERA_ERR_HIP, "kamera_scatter_paged: launch failed: %s", hipGetErrorString(e));
+  }
   return ok();
+}
+
+extern "C" int kamera_validate(int32_t which, const void* args) {
+  bool launch = false;
+  int rc;
+  switch (which) {
+    case 0: { static thread_local kamera::RehydrateParams P; rc = build_rehydrate(static_cast<const kamera_rehydrate_args*>(args), P, launch); break; }
+    case 1: { static thread_local kamera::ShiftParams P; rc = build_shift(static_cast<const kamera_shift_args*>(args), P, launch); break; }
+    case 2: { static thread_local kamera::ScatterParams P; rc = build_scatter(static_cast<const kamera_scatter_args*>(args), P, launch); break; }
+    default: return fail(KAMERA_ERR_SHAPE, "kamera_validate: unknown entry point %d", which);
+  }
+  return rc ? rc : ok();
 }
 
 // ---------------------------------------------------------------------------

@@ -61,6 +61,11 @@ class Workload:
     window_slots: int = 0
     delta: int = 0
     slides: int = 1
+    # survivors moved by delta with a removal patch, in place (relocation)
+    reloc: bool = False
+    # separate rank on the rope band (MLA k_pe) and deep-half patches
+    m_pe: int = 0
+    patch_from_layer: int = 0       # layers below carry no factors (rank 0)
 
     def units(self) -> int:
         return self.n_chunks * self.n_layers * self.n_heads
@@ -97,6 +102,30 @@ WORKLOADS: Dict[str, Workload] = {
         section_order="blocked", m_k=64, m_v=64, patch_dim=128, paged=True,
         page_size=16, n_pool_pages=4096, pos_mode="grid3", grid_w=32,
         seed=1005),
+    # --- the operator's other modes ---
+    # survivors of a slide on a 36-layer deepstack-style GQA model: 15 frame
+    # chunks moved back by one chunk, in place, with rank-64 removal patches
+    "gqa36l_15x1024_survivor_m64": Workload(
+        name="gqa36l_15x1024_survivor_m64", kind="rehydrate", n_chunks=15,
+        n_layers=36, n_heads=8, head_dim=128, n_tokens=1024, theta=5e6,
+        rope_dim=128, pairing=NEOX, sections=(24, 20, 20),
+        section_order="interleaved", m_k=64, m_v=64, patch_dim=128,
+        pos_mode="grid3", grid_w=32, reloc=True, delta=-1024, window_slots=16,
+        seed=1006),
+    # MLA with the extra rank-16 patch on the 64-dim rope key band
+    "mla27l_4x2048_m32_pe16": Workload(
+        name="mla27l_4x2048_m32_pe16", kind="rehydrate", n_chunks=4, n_layers=27,
+        n_heads=1, head_dim=576, n_tokens=2048, theta=1e4, rope_dim=64,
+        rope_offset=512, pairing=INTERLEAVED, m_k=32, m_v=0, m_pe=16,
+        patch_dim=512, has_v=False, seed=1007),
+    # the 80-layer paged recall with factors on the deepest 40 layers only
+    "gqa80l_64x1024_m64_mrope_paged_deephalf": Workload(
+        name="gqa80l_64x1024_m64_mrope_paged_deephalf", kind="rehydrate",
+        n_chunks=64, n_layers=80, n_heads=8, head_dim=128, n_tokens=1024,
+        theta=1e6, rope_dim=128, pairing=NEOX, sections=(16, 24, 24),
+        section_order="blocked", m_k=64, m_v=64, patch_dim=128, paged=True,
+        page_size=16, n_pool_pages=4096, pos_mode="grid3", grid_w=32,
+        patch_from_layer=40, seed=1008),
 }
 
 # order in which the workloads are listed (smallest first)
@@ -106,6 +135,14 @@ WORKLOAD_ORDER: List[str] = [
     "mha32l_window16x512_shift",
     "mla27l_4x2048_m32",
     "gqa80l_64x1024_m64_mrope_paged",
+]
+
+# workloads of the operator's other modes (relocation with a removal patch,
+# a second rank on the MLA rope band, deep-half factors)
+EXTRA_WORKLOADS: List[str] = [
+    "gqa36l_15x1024_survivor_m64",
+    "mla27l_4x2048_m32_pe16",
+    "gqa80l_64x1024_m64_mrope_paged_deephalf",
 ]
 
 
@@ -147,11 +184,16 @@ def chunk_meta(w: Workload, seed: Optional[int] = None) -> ChunkMeta:
         for s, c in enumerate(order):
             pos[c, :] = n * s
             row_base[c] = n * s
-    elif w.name == "mla27l_4x2048_m32":
+    elif w.name in ("mla27l_4x2048_m32", "mla27l_4x2048_m32_pe16"):
         p0 = rng.integers(0, 32768 - n + 1, size=C)
         pos[:] = p0[:, None]
         row_base[:] = np.arange(C) * n
-    elif w.name == "gqa80l_64x1024_m64_mrope_paged":
+    elif w.name == "gqa36l_15x1024_survivor_m64":
+        # survivor k sat at slot k + 1 of the window (frame origin 1024*(k+1) on
+        # every coordinate) and moves to slot k: all three coordinates by delta
+        pos[:] = (n * np.arange(C))[:, None]
+        delta[:] = w.delta
+    elif w.name in ("gqa80l_64x1024_m64_mrope_paged", "gqa80l_64x1024_m64_mrope_paged_deephalf"):
         s = rng.integers(1, 4097, size=C)          # temporal delta in [1, 4096]
         pos[:] = s[:, None]                        # all three coordinates advance together
         pages = (n + w.page_size - 1) // w.page_size

@@ -35,16 +35,20 @@ def algorithmic_bytes(w: Workload) -> int:
     positions are excluded.  shift: the rope band of every survivor row read
     and written.
     """
-    units = w.n_chunks * w.n_layers * w.n_heads
     n, D = w.n_tokens, w.head_dim
     if w.kind == "shift":
-        return units * n * w.rope_dim * 2 * 2
+        return w.n_chunks * w.n_layers * w.n_heads * n * w.rope_dim * 2 * 2
     planes = 2 if w.has_v else 1
-    b = planes * 2 * n * D * 2
+    rows = planes * 2 * n * D * 2
+    factors = 0
     for m in ((w.m_k, w.m_v) if w.has_v else (w.m_k,)):
         if m > 0:
-            b += (n * m + m * w.patch_dim) * 2
-    return units * b
+            factors += (n * m + m * w.patch_dim) * 2
+    if w.m_pe > 0:
+        factors += (n * w.m_pe + w.m_pe * w.rope_dim) * 2
+    patched_layers = w.n_layers - w.patch_from_layer
+    per_layer_units = w.n_chunks * w.n_heads
+    return per_layer_units * (w.n_layers * rows + patched_layers * factors)
 
 
 def _rope_spec(w: Workload):
@@ -104,20 +108,47 @@ def prepare(name: str, device="cuda", seed: Optional[int] = None, unit_major: bo
         p.extra["call"] = call
         return p
 
-    T["k_in"] = _kv_rows((C, L, n, H, D), gen, device, unit_major)
-    if w.has_v:
-        T["v_in"] = _kv_rows((C, L, n, H, D), gen, device, unit_major)
+    if w.reloc:
+        # the window's K/V, chunk-major [slot][L][n][H][D]; survivors are slots
+        # 1..15, rotated and moved in place (input = output)
+        S = w.window_slots
+        T["k_window"] = randn_bf16_device((S, L, n, H, D), 1.0, gen, device)
+        T["k_in"] = T["k_window"][1:1 + C]
+        if w.has_v:
+            T["v_window"] = randn_bf16_device((S, L, n, H, D), 1.0, gen, device)
+            T["v_in"] = T["v_window"][1:1 + C]
+    else:
+        T["k_in"] = _kv_rows((C, L, n, H, D), gen, device, unit_major)
+        if w.has_v:
+            T["v_in"] = _kv_rows((C, L, n, H, D), gen, device, unit_major)
     if w.m_k > 0:
         T["u_k"] = randn_bf16_device((C, L, H, n, w.m_k), w.u_std, gen, device)
         T["w_k"] = randn_bf16_device((C, L, H, w.m_k, w.patch_dim), w.w_std, gen, device)
     if w.has_v and w.m_v > 0:
         T["u_v"] = randn_bf16_device((C, L, H, n, w.m_v), w.u_std, gen, device)
         T["w_v"] = randn_bf16_device((C, L, H, w.m_v, w.patch_dim), w.w_std, gen, device)
+    if w.m_pe > 0:
+        T["u_pe"] = randn_bf16_device((C, L, H, n, w.m_pe), w.u_std, gen, device)
+        T["w_pe"] = randn_bf16_device((C, L, H, w.m_pe, w.rope_dim), w.w_std, gen, device)
     T["chunk_pos"] = torch.from_numpy(meta.pos).to(device)
     kw = dict(rope=rope, chunk_pos=T["chunk_pos"], u_k=T.get("u_k"), w_k=T.get("w_k"),
               k_patch=(w.patch_offset, w.patch_dim),
               pos_mode=km.POS_GRID3 if w.pos_mode == "grid3" else km.POS_LINEAR, grid_w=w.grid_w)
-    if w.paged:
+    if w.reloc:
+        T["delta"] = torch.from_numpy(meta.delta).to(device)
+        kw["delta"] = T["delta"]
+    if w.m_pe > 0:
+        kw.update(u_pe=T["u_pe"], w_pe=T["w_pe"])
+    if w.patch_from_layer > 0:
+        ranks = np.array([0 if l < w.patch_from_layer else max(w.m_k, w.m_v, w.m_pe) for l in range(L)],
+                         dtype=np.int32)
+        T["layer_rank"] = torch.from_numpy(ranks).to(device)
+        kw.update(k_layer_rank=T["layer_rank"], v_layer_rank=T["layer_rank"], pe_layer_rank=T["layer_rank"])
+    if w.reloc:
+        k_out = T["k_in"]
+        if w.has_v:
+            v_out = T["v_in"]
+    elif w.paged:
         slots = w.n_pool_pages * w.page_size
         if pool_head_major:   # [L, H, slots, D] memory, [L, slots, H, D] view
             T["k_pool"] = torch.zeros((L, H, slots, D), dtype=torch.bfloat16, device=device).transpose(1, 2)

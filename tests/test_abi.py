@@ -27,7 +27,7 @@ def declared_functions():
 def test_header_declares_the_boundary():
     names = declared_functions()
     for want in ("kamera_rehydrate", "kamera_shift", "kamera_scatter_paged", "kamera_last_error",
-                 "kamera_abi_version", "kamera_check_page_table", "kamera_struct_size"):
+                 "kamera_abi_version", "kamera_check_page_table", "kamera_struct_size", "kamera_validate"):
         assert want in names
 
 
@@ -220,6 +220,35 @@ def test_rehydrate_rejects(case, code):
         a.plane[1].col_begin, a.plane[1].col_end = 64, 128
     assert call_rehydrate(a) == code, km.last_error()
     assert km.last_error().startswith("kamera_rehydrate")
+
+
+def test_exact_in_place_is_accepted_but_shifted_overlap_is_not():
+    """In place (same base and strides, dense, no row base) passes validation;
+    any other overlap is rejected.  The in-place case is stopped right before
+    the launch by an empty token count, so nothing runs."""
+    L = km.lib()
+    a = rehydrate_args()
+    assert L.kamera_validate(0, ctypes.byref(a)) == km.OK
+    for p in range(2):
+        a.plane[p].out = a.plane[p].in_
+    assert L.kamera_validate(0, ctypes.byref(a)) == km.OK, km.last_error()
+    a = rehydrate_args()
+    a.plane[0].out = a.plane[0].in_ + 256
+    assert L.kamera_validate(0, ctypes.byref(a)) == km.ERR_ALIAS
+    # two planes in place on one tensor: only with disjoint columns
+    a = rehydrate_args()
+    a.plane[1].in_ = a.plane[0].in_
+    a.plane[0].out = a.plane[1].out = a.plane[0].in_
+    assert L.kamera_validate(0, ctypes.byref(a)) == km.ERR_ALIAS
+    a.head_dim = 256
+    a.plane[0].col_begin, a.plane[0].col_end = 0, 128
+    a.plane[1].col_begin, a.plane[1].col_end = 128, 256
+    a.plane[1].patch_offset = 128
+    for p in range(2):
+        a.plane[p].in_stride[3] = a.plane[p].out_stride[3] = 256
+        a.plane[p].in_stride[2] = a.plane[p].out_stride[2] = 4 * 256
+    assert L.kamera_validate(0, ctypes.byref(a)) == km.OK, km.last_error()
+    assert L.kamera_validate(7, ctypes.byref(a)) == km.ERR_SHAPE
 
 
 def test_error_text_is_per_thread():

@@ -35,41 +35,77 @@ def _positions(w, meta, c):
     return ref.positions_linear(int(meta.pos[c, 0]), w.n_tokens)
 
 
-def _check_rehydrate_units(p, units):
+def _inputs(p, units):
+    """The sampled units' input rows (read before the step: some workloads run in place)."""
+    w, T = p.workload, p.tensors
+    out = {}
+    for (c, l, h) in units:
+        out[(c, l, h)] = (bits(T["k_in"][c, l, :, h]), bits(T["v_in"][c, l, :, h]) if w.has_v else None)
+    return out
+
+
+def _check_rehydrate_units(p, units, inputs):
     w, T, meta = p.workload, p.tensors, p.meta
     orope = oracle_rope(harness._rope_spec(w))
     n = w.n_tokens
     for (c, l, h) in units:
         p3 = _positions(w, meta, c)
-        if w.paged:
+        patched = l >= w.patch_from_layer
+        if w.reloc:
+            ko = bits(T["k_in"][c, l, :, h])
+            dst = None
+        elif w.paged:
             dst = np.array([ref.paged_slot(meta.page_table[c], i, w.page_size) for i in range(n)])
             ko = bits(T["k_pool"][l, dst, h])
         else:
             dst = int(meta.row_base[c]) + np.arange(n)
             ko = bits(T["k_out_rows"][l, dst[0]:dst[-1] + 1, h])
-        K = ref.bf16_to_f64(bits(T["k_in"][c, l, :, h]))
-        U = ref.bf16_to_f64(bits(T["u_k"][c, l, h])) if w.m_k else None
-        W = ref.bf16_to_f64(bits(T["w_k"][c, l, h])) if w.m_k else None
-        assert_close(ko, ref.rehydrate_k(K, U, W, orope, p3, w.patch_offset), f"{w.name} K c{c} l{l} h{h}")
+        kin, vin = inputs[(c, l, h)]
+        K = ref.bf16_to_f64(kin)
+        U = ref.bf16_to_f64(bits(T["u_k"][c, l, h])) if (w.m_k and patched) else None
+        W = ref.bf16_to_f64(bits(T["w_k"][c, l, h])) if (w.m_k and patched) else None
+        off = w.patch_offset
+        if w.m_pe and patched:
+            # latent patch and rope-band patch on disjoint columns == one block patch
+            up = ref.bf16_to_f64(bits(T["u_pe"][c, l, h]))
+            wp = ref.bf16_to_f64(bits(T["w_pe"][c, l, h]))
+            Wf = np.zeros((U.shape[1] + up.shape[1], w.head_dim))
+            Wf[:U.shape[1], off:off + W.shape[1]] = W
+            Wf[U.shape[1]:, w.rope_offset:w.rope_offset + w.rope_dim] = wp
+            U, W, off = np.concatenate([U, up], axis=1), Wf, 0
+        if w.reloc:
+            want = ref.relocate_k(K, U, W, orope, p3, p.meta.delta[c], off)
+        else:
+            want = ref.rehydrate_k(K, U, W, orope, p3, off)
+        assert_close(ko, want, f"{w.name} K c{c} l{l} h{h}")
         if w.has_v:
-            vo = bits(T["v_pool"][l, dst, h]) if w.paged else bits(T["v_out_rows"][l, dst[0]:dst[-1] + 1, h])
-            V = ref.bf16_to_f64(bits(T["v_in"][c, l, :, h]))
-            U = ref.bf16_to_f64(bits(T["u_v"][c, l, h])) if w.m_v else None
-            W = ref.bf16_to_f64(bits(T["w_v"][c, l, h])) if w.m_v else None
+            if w.reloc:
+                vo = bits(T["v_in"][c, l, :, h])
+            elif w.paged:
+                vo = bits(T["v_pool"][l, dst, h])
+            else:
+                vo = bits(T["v_out_rows"][l, dst[0]:dst[-1] + 1, h])
+            V = ref.bf16_to_f64(vin)
+            U = ref.bf16_to_f64(bits(T["u_v"][c, l, h])) if (w.m_v and patched) else None
+            W = ref.bf16_to_f64(bits(T["w_v"][c, l, h])) if (w.m_v and patched) else None
             assert_close(vo, ref.rehydrate_v(V, U, W, w.patch_offset), f"{w.name} V c{c} l{l} h{h}")
 
 
 @pytest.mark.parametrize("name", ["gqa1l_256tok_m8", "gqa28l_8x1024_m16_reorder", "mla27l_4x2048_m32",
-                                  "gqa80l_64x1024_m64_mrope_paged"])
+                                  "gqa80l_64x1024_m64_mrope_paged"] + synth.EXTRA_WORKLOADS)
 def test_workload_rehydrate(device, name):
     import torch
 
     print(f"[case] workload {name}", flush=True)
     p = harness.prepare(name, device)
+    units = harness.sample_units(p.workload, 12 if p.workload.units() > 12 else p.workload.units(), seed=1)
+    if p.workload.patch_from_layer:
+        # make sure both sides of the deep-half boundary are sampled
+        units += [(0, p.workload.patch_from_layer - 1, 0), (1, p.workload.patch_from_layer, 1)]
+    inputs = _inputs(p, units)
     p.step()
     torch.cuda.synchronize()
-    units = harness.sample_units(p.workload, 12 if p.workload.units() > 12 else p.workload.units(), seed=1)
-    _check_rehydrate_units(p, units)
+    _check_rehydrate_units(p, units, inputs)
     if p.workload.paged:
         # the page table of this workload is a permutation: every slot is written exactly once,
         # and a second pass writes identical bits (no slot is hit by two tokens)
