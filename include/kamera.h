@@ -229,21 +229,23 @@ typedef struct {
   uint32_t* status;
 } kamera_shift_args;
 
-/* kamera_scatter_paged -- bit-exact copy of dense token rows into a paged
- * pool (the copy half of the conditioning switch, App. E; the pool is the
- * paged KV store the serve step writes into, Sec. 6).  Token i of chunk c,
- * layer l: row_bytes bytes from
- *   src + c*src_stride_bytes[0] + l*src_stride_bytes[1] + i*src_stride_bytes[2]
- * to pool + l*pool_stride_bytes[0] + slot*pool_stride_bytes[1], slot as in
- * kamera_rehydrate.  row_bytes and all strides: multiples of 16. */
+/* kamera_scatter_paged / kamera_gather_paged -- bit-exact copies between
+ * dense token rows and a paged pool (the copy half of the conditioning
+ * switch, App. E: the clean view is restored by a plain copy; the pool is the
+ * paged KV store the serve step writes into, Sec. 6).  For token i of chunk
+ * c, layer l the dense row is
+ *   rows + c*rows_stride_bytes[0] + l*rows_stride_bytes[1] + i*rows_stride_bytes[2]
+ * and the pool row pool + l*pool_stride_bytes[0] + slot*pool_stride_bytes[1],
+ * slot as in kamera_rehydrate; row_bytes bytes move, dense -> pool (scatter)
+ * or pool -> dense (gather).  row_bytes and all strides: multiples of 16. */
 typedef struct {
   int32_t n_chunks;
   int32_t n_layers;
   int32_t n_tokens;
   const int32_t* chunk_tokens;
   int64_t row_bytes;
-  const void* src;
-  int64_t src_stride_bytes[3];
+  void* rows;
+  int64_t rows_stride_bytes[3];
   void* pool;
   int64_t pool_stride_bytes[2];
   const int32_t* page_table;
@@ -256,6 +258,7 @@ typedef struct {
 int kamera_rehydrate(const kamera_rehydrate_args* args, void* stream);
 int kamera_shift(const kamera_shift_args* args, void* stream);
 int kamera_scatter_paged(const kamera_scatter_args* args, void* stream);
+int kamera_gather_paged(const kamera_scatter_args* args, void* stream);
 
 /* Host-side check of a page table copy (host memory, n_chunks x pt_stride,
  * the first ceil(tokens/page_size) entries of each row are used): every used
@@ -266,8 +269,10 @@ int kamera_check_page_table(const int32_t* host_page_table, int32_t n_chunks,
                             int32_t page_size, int32_t n_pool_pages);
 
 /* Run exactly the host-side checks of an entry point (0 kamera_rehydrate,
- * 1 kamera_shift, 2 kamera_scatter_paged) on `args` without launching
- * anything: KAMERA_OK when the call would be enqueued, else the error code
+ * 1 kamera_shift, 2 kamera_scatter_paged, 3 kamera_gather_paged) on `args`
+ * without launching
+ * anything (3 = kamera_gather_paged): KAMERA_OK when the call would be
+ * enqueued, else the error code
  * the call would return.  Touches no device memory. */
 int kamera_validate(int32_t which, const void* args);
 

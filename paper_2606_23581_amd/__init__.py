@@ -13,6 +13,7 @@ Entry points (same names as the C ABI):
 * ``shift``         K' = R(delta) K in place (Sec. 1, Sec. 5 survivors)
 * ``scatter_paged`` bit copy of dense token rows into page-table slots
                     (App. E clean-view overwrite, Sec. 6 paged pool)
+* ``gather_paged``  the inverse copy, pool slots back into dense rows
 """
 
 from __future__ import annotations
@@ -99,12 +100,13 @@ class CShiftArgs(ctypes.Structure):
 
 class CScatterArgs(ctypes.Structure):
     _fields_ = [("n_chunks", _i32), ("n_layers", _i32), ("n_tokens", _i32), ("chunk_tokens", _vp),
-                ("row_bytes", _i64), ("src", _vp), ("src_stride_bytes", _i64 * 3), ("pool", _vp),
+                ("row_bytes", _i64), ("rows", _vp), ("rows_stride_bytes", _i64 * 3), ("pool", _vp),
                 ("pool_stride_bytes", _i64 * 2), ("page_table", _vp), ("pt_stride", _i32),
                 ("page_size", _i32), ("n_pool_pages", _i32), ("status", _vp)]
 
 
-EXPORTS = ("kamera_rehydrate", "kamera_shift", "kamera_scatter_paged", "kamera_check_page_table",
+EXPORTS = ("kamera_rehydrate", "kamera_shift", "kamera_scatter_paged", "kamera_gather_paged",
+           "kamera_check_page_table",
            "kamera_validate", "kamera_last_error", "kamera_abi_version", "kamera_struct_size")
 
 _LIB = None
@@ -127,6 +129,8 @@ def lib() -> ctypes.CDLL:
     L.kamera_shift.restype = _i32
     L.kamera_scatter_paged.argtypes = [ctypes.POINTER(CScatterArgs), _vp]
     L.kamera_scatter_paged.restype = _i32
+    L.kamera_gather_paged.argtypes = [ctypes.POINTER(CScatterArgs), _vp]
+    L.kamera_gather_paged.restype = _i32
     L.kamera_check_page_table.argtypes = [_vp, _i32, _i32, _i32, _i32, _i32]
     L.kamera_check_page_table.restype = _i32
     L.kamera_last_error.argtypes = []
@@ -401,29 +405,36 @@ def scatter_paged(*a, stream=None, **kw) -> None:
     prepare_scatter_paged(*a, **kw).launch(stream)
 
 
-def prepare_scatter_paged(src, pool, page_table, *, page_size: int, n_pool_pages: int,
-                          chunk_tokens=None, status=None) -> Prepared:
-    """Bit copy of token rows into page-table slots (``kamera_scatter_paged``).
+def gather_paged(*a, stream=None, **kw) -> None:
+    """``kamera_gather_paged``: pool rows back into dense rows (the arguments of
+    ``prepare_scatter_paged``, with ``rows`` the destination)."""
+    prepare_scatter_paged(*a, gather=True, **kw).launch(stream)
 
-    src: [C, L, n, ...] (each token row contiguous); pool: [L, slots, ...]
-    with the same row shape and dtype.
+
+def prepare_scatter_paged(rows, pool, page_table, *, page_size: int, n_pool_pages: int,
+                          chunk_tokens=None, status=None, gather: bool = False) -> Prepared:
+    """Bit copy between dense token rows and page-table slots.
+
+    rows: [C, L, n, ...] (each token row contiguous); pool: [L, slots, ...]
+    with the same row shape and dtype.  Scatter copies rows -> pool (the
+    default), gather copies pool -> rows.
     """
     L = lib()
     _i32_dev(page_table, "page_table")
-    C, Ln, n = (int(s) for s in src.shape[:3])
+    C, Ln, n = (int(x) for x in rows.shape[:3])
     row_elems = 1
-    for s in src.shape[3:]:
-        row_elems *= int(s)
-    es = src.element_size()
-    if pool.dtype != src.dtype or tuple(pool.shape[2:]) != tuple(src.shape[3:]):
-        raise ValueError("pool rows must match src rows in shape and dtype")
+    for x in rows.shape[3:]:
+        row_elems *= int(x)
+    es = rows.element_size()
+    if pool.dtype != rows.dtype or tuple(pool.shape[2:]) != tuple(rows.shape[3:]):
+        raise ValueError("pool rows must match the dense rows in shape and dtype")
     a = CScatterArgs()
     a.n_chunks, a.n_layers, a.n_tokens = C, Ln, n
     a.chunk_tokens = _ptr(chunk_tokens)
     a.row_bytes = row_elems * es
-    a.src = _ptr(src)
+    a.rows = _ptr(rows)
     for i in range(3):
-        a.src_stride_bytes[i] = int(src.stride(i)) * es
+        a.rows_stride_bytes[i] = int(rows.stride(i)) * es
     a.pool = _ptr(pool)
     for i in range(2):
         a.pool_stride_bytes[i] = int(pool.stride(i)) * es
@@ -432,7 +443,8 @@ def prepare_scatter_paged(src, pool, page_table, *, page_size: int, n_pool_pages
     a.page_size = int(page_size)
     a.n_pool_pages = int(n_pool_pages)
     a.status = _ptr(status)
-    return Prepared(L.kamera_scatter_paged, a, (src, pool, page_table, chunk_tokens, status))
+    fn = L.kamera_gather_paged if gather else L.kamera_scatter_paged
+    return Prepared(fn, a, (rows, pool, page_table, chunk_tokens, status))
 
 
 def check_page_table(page_table_host, n_tokens: int, page_size: int, n_pool_pages: int) -> None:

@@ -438,8 +438,8 @@ extern "C" int kamera_shift(const kamera_shift_args* a, void* stream) {
 // kamera_scatter_paged
 // ---------------------------------------------------------------------------
 
-static int build_scatter(const kamera_scatter_args* a, kamera::ScatterParams& P, bool& launch) {
-  const char* who = "kamera_scatter_paged";
+static int build_scatter(const kamera_scatter_args* a, kamera::ScatterParams& P, bool& launch, bool gather) {
+  const char* who = gather ? "kamera_gather_paged" : "kamera_scatter_paged";
   launch = false;
   if (a == nullptr) return fail(KAMERA_ERR_NULL, "%s: args is NULL", who);
   if (a->n_chunks < 0 || a->n_layers < 0 || a->n_tokens < 0)
@@ -450,21 +450,21 @@ static int build_scatter(const kamera_scatter_args* a, kamera::ScatterParams& P,
   if (rc) return rc;
   const int64_t work = (int64_t)a->n_chunks * a->n_layers * a->n_tokens;
   if (work == 0) return KAMERA_OK;
-  if (a->src == nullptr || a->pool == nullptr) return fail(KAMERA_ERR_NULL, "%s: src or pool is NULL", who);
+  if (a->rows == nullptr || a->pool == nullptr) return fail(KAMERA_ERR_NULL, "%s: rows or pool is NULL", who);
   for (int k = 0; k < 3; ++k)
-    if (a->src_stride_bytes[k] % 16 != 0) return fail(KAMERA_ERR_ALIGN, "%s: src strides must be multiples of 16", who);
+    if (a->rows_stride_bytes[k] % 16 != 0) return fail(KAMERA_ERR_ALIGN, "%s: row strides must be multiples of 16", who);
   for (int k = 0; k < 2; ++k)
     if (a->pool_stride_bytes[k] % 16 != 0) return fail(KAMERA_ERR_ALIGN, "%s: pool strides must be multiples of 16", who);
-  if (!aligned16(a->src) || !aligned16(a->pool)) return fail(KAMERA_ERR_ALIGN, "%s: src/pool must be 16-byte aligned", who);
+  if (!aligned16(a->rows) || !aligned16(a->pool)) return fail(KAMERA_ERR_ALIGN, "%s: rows/pool must be 16-byte aligned", who);
   {
-    // the source rows and the pool must be different memory
+    // the dense rows and the pool must be different memory
     int64_t a0 = 0, b0 = 0;
     const int64_t ext[3] = {a->n_chunks, a->n_layers, a->n_tokens};
     for (int k = 0; k < 3; ++k) {
-      const int64_t d = (ext[k] - 1) * a->src_stride_bytes[k];
+      const int64_t d = (ext[k] - 1) * a->rows_stride_bytes[k];
       if (d < 0) a0 += d; else b0 += d;
     }
-    const uintptr_t slo = reinterpret_cast<uintptr_t>(a->src) + a0, shi = reinterpret_cast<uintptr_t>(a->src) + b0 + a->row_bytes;
+    const uintptr_t slo = reinterpret_cast<uintptr_t>(a->rows) + a0, shi = reinterpret_cast<uintptr_t>(a->rows) + b0 + a->row_bytes;
     int64_t a1 = 0, b1 = 0;
     const int64_t pext[2] = {a->n_layers, (int64_t)a->n_pool_pages * a->page_size};
     for (int k = 0; k < 2; ++k) {
@@ -472,15 +472,16 @@ static int build_scatter(const kamera_scatter_args* a, kamera::ScatterParams& P,
       if (d < 0) a1 += d; else b1 += d;
     }
     const uintptr_t plo = reinterpret_cast<uintptr_t>(a->pool) + a1, phi = reinterpret_cast<uintptr_t>(a->pool) + b1 + a->row_bytes;
-    if (overlap(slo, shi, plo, phi)) return fail(KAMERA_ERR_ALIAS, "%s: src overlaps the pool", who);
+    if (overlap(slo, shi, plo, phi)) return fail(KAMERA_ERR_ALIAS, "%s: the dense rows overlap the pool", who);
   }
 
   memset(&P, 0, sizeof(P));
   fill_place(P.place, a->n_tokens, a->chunk_tokens, 1, nullptr, a->page_table, a->pt_stride, a->page_size,
              a->n_pool_pages, a->status);
-  P.src = static_cast<const uint8_t*>(a->src);
+  P.rows = static_cast<uint8_t*>(a->rows);
   P.pool = static_cast<uint8_t*>(a->pool);
-  memcpy(P.src_s, a->src_stride_bytes, sizeof(P.src_s));
+  P.gather = gather ? 1 : 0;
+  memcpy(P.rows_s, a->rows_stride_bytes, sizeof(P.rows_s));
   memcpy(P.pool_s, a->pool_stride_bytes, sizeof(P.pool_s));
   P.row_vecs = a->row_bytes / 16;
   P.n_chunks = a->n_chunks;
@@ -498,16 +499,26 @@ static int build_scatter(const kamera_scatter_args* a, kamera::ScatterParams& P,
   return KAMERA_OK;
 }
 
-extern "C" int kamera_scatter_paged(const kamera_scatter_args* a, void* stream) {
+static int scatter_or_gather(const kamera_scatter_args* a, void* stream, bool gather) {
   static thread_local kamera::ScatterParams P;
   bool launch = false;
-  const int rc = build_scatter(a, P, launch);
+  const int rc = build_scatter(a, P, launch, gather);
   if (rc) return rc;
   if (launch) {
     const hipError_t e = kamera::launch_scatter(P, static_cast<hipStream_t>(stream));
-    if (e != hipSuccess) return fail(KAMERA_ERR_HIP, "kamera_scatter_paged: launch failed: %s", hipGetErrorString(e));
+    if (e != hipSuccess)
+      return fail(KAMERA_ERR_HIP, "%s: launch failed: %s", gather ? "kamera_gather_paged" : "kamera_scatter_paged",
+                  hipGetErrorString(e));
   }
   return ok();
+}
+
+extern "C" int kamera_scatter_paged(const kamera_scatter_args* a, void* stream) {
+  return scatter_or_gather(a, stream, false);
+}
+
+extern "C" int kamera_gather_paged(const kamera_scatter_args* a, void* stream) {
+  return scatter_or_gather(a, stream, true);
 }
 
 extern "C" int kamera_validate(int32_t which, const void* args) {
@@ -516,7 +527,12 @@ extern "C" int kamera_validate(int32_t which, const void* args) {
   switch (which) {
     case 0: { static thread_local kamera::RehydrateParams P; rc = build_rehydrate(static_cast<const kamera_rehydrate_args*>(args), P, launch); break; }
     case 1: { static thread_local kamera::ShiftParams P; rc = build_shift(static_cast<const kamera_shift_args*>(args), P, launch); break; }
-    case 2: { static thread_local kamera::ScatterParams P; rc = build_scatter(static_cast<const kamera_scatter_args*>(args), P, launch); break; }
+    case 2:
+    case 3: {
+      static thread_local kamera::ScatterParams P;
+      rc = build_scatter(static_cast<const kamera_scatter_args*>(args), P, launch, which == 3);
+      break;
+    }
     default: return fail(KAMERA_ERR_SHAPE, "kamera_validate: unknown entry point %d", which);
   }
   return rc ? rc : ok();

@@ -683,7 +683,7 @@ hipError_t launch_shift(const ShiftParams& p, hipStream_t s) {
 }
 
 // ---------------------------------------------------------------------------
-// scatter: dense rows -> page-table slots, bit for bit
+// scatter / gather: dense rows <-> page-table slots, bit for bit
 // ---------------------------------------------------------------------------
 
 constexpr int kScatterUnroll = 4;
@@ -701,8 +701,9 @@ __global__ __launch_bounds__(kThreads) void scatter_kernel(const ScatterParams /
   const int t_end = min(t_begin + P.token_block, n_c);
   const int64_t vpr = P.row_vecs;
   const int64_t total = (int64_t)(t_end - t_begin) * vpr;
-  const uint8_t* sbase = P.src + (int64_t)c * P.src_s[0] + (int64_t)l * P.src_s[1];
+  uint8_t* rbase = P.rows + (int64_t)c * P.rows_s[0] + (int64_t)l * P.rows_s[1];
   uint8_t* pbase = P.pool + (int64_t)l * P.pool_s[0];
+  const bool gather = P.gather != 0;
   for (int64_t base = threadIdx.x; base < total; base += kScatterUnroll * kThreads) {
     u32x4 v[kScatterUnroll];
     uint8_t* dp[kScatterUnroll];
@@ -715,9 +716,11 @@ __global__ __launch_bounds__(kThreads) void scatter_kernel(const ScatterParams /
         const int64_t vec = idx % vpr;
         const int64_t slot = page_slot(P.place, c, i);
         if (slot >= 0) {
-          v[u] = __builtin_nontemporal_load(
-              reinterpret_cast<const u32x4*>(sbase + (int64_t)i * P.src_s[2] + 16 * vec));
-          dp[u] = pbase + slot * P.pool_s[1] + 16 * vec;
+          uint8_t* dense = rbase + (int64_t)i * P.rows_s[2] + 16 * vec;
+          uint8_t* paged = pbase + slot * P.pool_s[1] + 16 * vec;
+          const uint8_t* sp = gather ? paged : dense;
+          dp[u] = gather ? dense : paged;
+          v[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(sp));
         }
       }
     }

@@ -104,16 +104,16 @@ struct ShiftParams {
 
 struct ScatterParams {
   Placement place;
-  const uint8_t* src;
+  uint8_t* rows;
   uint8_t* pool;
-  int64_t src_s[3];
+  int64_t rows_s[3];
   int64_t pool_s[2];
   int64_t row_vecs;                  // 16-byte vectors per row
   int32_t n_chunks, n_layers;
   int32_t token_block;
   int32_t n_tblk;
   int32_t per_xcd;
-  int32_t pad_;
+  int32_t gather;                    // 1: pool -> dense rows
   int64_t n_tasks;
 };
 

@@ -27,7 +27,8 @@ def declared_functions():
 def test_header_declares_the_boundary():
     names = declared_functions()
     for want in ("kamera_rehydrate", "kamera_shift", "kamera_scatter_paged", "kamera_last_error",
-                 "kamera_abi_version", "kamera_check_page_table", "kamera_struct_size", "kamera_validate"):
+                 "kamera_abi_version", "kamera_check_page_table", "kamera_struct_size", "kamera_validate",
+                 "kamera_gather_paged"):
         assert want in names
 
 
@@ -318,8 +319,8 @@ def scatter_args():
     a = km.CScatterArgs()
     a.n_chunks, a.n_layers, a.n_tokens = 2, 3, 40
     a.row_bytes = 2048
-    a.src = FAKE
-    a.src_stride_bytes[0], a.src_stride_bytes[1], a.src_stride_bytes[2] = 3 * 40 * 2048, 40 * 2048, 2048
+    a.rows = FAKE
+    a.rows_stride_bytes[0], a.rows_stride_bytes[1], a.rows_stride_bytes[2] = 3 * 40 * 2048, 40 * 2048, 2048
     a.pool = FAKE + (1 << 36)
     a.pool_stride_bytes[0], a.pool_stride_bytes[1] = 64 * 16 * 2048, 2048
     a.page_table = FAKE + (2 << 36)
@@ -328,24 +329,27 @@ def scatter_args():
 
 
 @pytest.mark.parametrize("case,code", [
-    ("row_bytes", km.ERR_ALIGN), ("src_null", km.ERR_NULL), ("table_null", km.ERR_NULL),
+    ("row_bytes", km.ERR_ALIGN), ("rows_null", km.ERR_NULL), ("table_null", km.ERR_NULL),
     ("short_table", km.ERR_SHAPE), ("stride", km.ERR_ALIGN), ("alias", km.ERR_ALIAS),
 ])
 def test_scatter_rejects(case, code):
     a = scatter_args()
     if case == "row_bytes":
         a.row_bytes = 2040
-    elif case == "src_null":
-        a.src = None
+    elif case == "rows_null":
+        a.rows = None
     elif case == "table_null":
         a.page_table = None
     elif case == "short_table":
         a.pt_stride = 2
     elif case == "stride":
-        a.src_stride_bytes[2] = 2056
+        a.rows_stride_bytes[2] = 2056
     elif case == "alias":
-        a.pool = a.src + 4096
+        a.pool = a.rows + 4096
     assert km.lib().kamera_scatter_paged(ctypes.byref(a), None) == code, km.last_error()
+    assert km.lib().kamera_gather_paged(ctypes.byref(a), None) == code, km.last_error()
+    assert km.last_error().startswith("kamera_gather_paged")
+    assert km.lib().kamera_validate(3, ctypes.byref(a)) == code
 
 
 def test_check_page_table():

@@ -267,6 +267,69 @@ def test_scatter_is_bit_exact(device):
     assert int(status.cpu()[0]) == 0
 
 
+def test_gather_is_bit_exact_inverse(device):
+    """Gather reads the page-table slots back into dense rows bit for bit;
+    scatter then gather returns the original rows."""
+    import paper_2606_23581_amd as km
+    import torch
+
+    print("[case] gather", flush=True)
+    rng = np.random.default_rng(51)
+    C, L, n, H, D, P = 3, 2, 45, 2, 128, 16
+    pages = (n + P - 1) // P
+    npp = C * pages + 3
+    pt = rng.permutation(npp)[: C * pages].reshape(C, pages).astype(np.int32)
+    pool_np = rng.integers(0, 1 << 16, size=(L, npp * P, H, D)).astype(np.uint16)
+    rows = dev(np.full((C, L, n, H, D), SENTINEL, np.uint16), device)
+    km.gather_paged(rows, dev(pool_np, device), dev_i32(pt, device), page_size=P, n_pool_pages=npp)
+    torch.cuda.synchronize()
+    got = bits(rows)
+    for c in range(C):
+        for i in range(n):
+            assert np.array_equal(got[c, :, i], pool_np[:, ref.paged_slot(pt[c], i, P)])
+    pool2 = dev(np.zeros((L, npp * P, H, D), np.uint16), device)
+    km.scatter_paged(rows, pool2, dev_i32(pt, device), page_size=P, n_pool_pages=npp)
+    back = dev(np.zeros((C, L, n, H, D), np.uint16), device)
+    km.gather_paged(back, pool2, dev_i32(pt, device), page_size=P, n_pool_pages=npp)
+    torch.cuda.synchronize()
+    assert np.array_equal(bits(back), got)
+
+
+def test_conditioning_switch(device):
+    """App. E: the clean view is the canonical at its position (no patch);
+    re-conditioning adds R(p) U W in place (a relocation by delta = 0); turning
+    it off again restores the clean view bit for bit."""
+    import paper_2606_23581_amd as km
+    import torch
+
+    print("[case] conditioning switch", flush=True)
+    rng = np.random.default_rng(52)
+    C, L, n, H, D, m = 2, 2, 40, 2, 128, 16
+    K = synth.randn_bf16_numpy((C, L, n, H, D), 1.0, rng)
+    U = synth.randn_bf16_numpy((C, L, H, n, m), 0.1, rng)
+    W = synth.randn_bf16_numpy((C, L, H, m, D), 0.1, rng)
+    rs = km.RopeSpec(theta=1e6, rope_dim=128)
+    p0 = np.array([[300] * 3, [7000] * 3], dtype=np.int32)
+    clean = dev(np.zeros((C, L, n, H, D), np.uint16), device)
+    km.rehydrate(dev(K, device), clean, rope=rs, chunk_pos=dev_i32(p0, device))
+    conditioned = clean.clone()
+    km.rehydrate(conditioned, conditioned, rope=rs, chunk_pos=dev_i32(p0, device), u_k=dev(U, device),
+                 w_k=dev(W, device), delta=dev_i32(np.zeros((C, 3)), device))
+    clean2 = dev(np.zeros((C, L, n, H, D), np.uint16), device)
+    km.rehydrate(dev(K, device), clean2, rope=rs, chunk_pos=dev_i32(p0, device))
+    torch.cuda.synchronize()
+    assert np.array_equal(bits(clean2), bits(clean))
+    orope = oracle_rope(rs)
+    cb = bits(conditioned)
+    for c in range(C):
+        for l in range(L):
+            for h in range(H):
+                want = ref.rehydrate_k(ref.bf16_to_f64(K[c, l, :, h]), ref.bf16_to_f64(U[c, l, h]),
+                                       ref.bf16_to_f64(W[c, l, h]), orope, ref.positions_linear(int(p0[c, 0]), n))
+                got = ref.bf16_to_f64(cb[c, l, :, h])
+                assert np.max(np.abs(got - want) / np.maximum(1, np.abs(want))) <= 2 * TOL
+
+
 def test_scatter_bad_page_is_flagged(device):
     import paper_2606_23581_amd as km
     import torch
