@@ -11,6 +11,7 @@ from .kamera_ref import (  # noqa: F401
     Rope,
     add_patch,
     bf16_to_f64,
+    form_patch,
     inv_freq,
     pair_columns,
     pair_coordinate,

@@ -275,6 +275,16 @@ def relocate_k(K: np.ndarray, U, W, rope: Rope, pos3_target: np.ndarray, delta3:
     return moved + patch
 
 
+def form_patch(delta: np.ndarray, m: int):
+    """Stored rank-m patch of a deficit Delta (n x d): the compile step of App. A
+    keeps the top-m singular triplets, returning U[:, :m] * S[:m] (n x m, the
+    singular values folded into the per-token coefficients) and Vt[:m] (m x d,
+    the basis).  U W is then the best rank-m approximation of Delta
+    (Eckart-Young).  float64, via numpy's SVD."""
+    Uf, S, Vt = np.linalg.svd(np.asarray(delta, dtype=np.float64), full_matrices=False)
+    return Uf[:, :m] * S[None, :m], Vt[:m], S
+
+
 def paged_slot(page_table_row: np.ndarray, i: int, page_size: int) -> int:
     """Physical pool slot of a chunk's token i: page_table[i // P] * P + i % P."""
     return int(page_table_row[i // page_size]) * page_size + i % page_size

@@ -443,4 +443,31 @@ def pin_relocate(ref):
         assert abs(got[i, 0] - z.real) < 1e-12 and abs(got[i, 1] - z.imag) < 1e-12
 
 
+def pin_form_patch(ref):
+    """The compile step's factors: U W is the rank-m truncation (Eckart-Young
+    residual), W has orthonormal rows, U = Delta W^T (singular values folded
+    in), a planted rank-r Delta is rebuilt exactly at m = r, and the factors
+    rehydrate Delta back through the patch path."""
+    rng = _rng(28)
+    n, d = 40, 12
+    delta = rng.standard_normal((n, d))
+    for m in (1, 5, d):
+        U, W, S = ref.form_patch(delta, m)
+        assert U.shape == (n, m) and W.shape == (m, d)
+        err = np.linalg.norm(delta - U @ W)
+        assert abs(err - math.sqrt(float(np.sum(S[m:] ** 2)))) < 1e-10
+        assert np.max(np.abs(W @ W.T - np.eye(m))) < 1e-12
+        assert np.max(np.abs(U - delta @ W.T)) < 1e-12
+        # singular values come out in descending order and match the Gram matrix eigenvalues
+        ev = np.sort(np.linalg.eigvalsh(delta.T @ delta))[::-1]
+        assert np.max(np.abs(S ** 2 - ev)) < 1e-9
+    A = rng.standard_normal((n, 3))
+    B = rng.standard_normal((3, d))
+    U, W, S = ref.form_patch(A @ B, 3)
+    assert np.max(np.abs(U @ W - A @ B)) < 1e-11
+    assert S[3] < 1e-12
+    K = rng.standard_normal((n, d))
+    assert np.max(np.abs(ref.rehydrate_v(K, U, W) - (K + A @ B))) < 1e-11
+
+
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

@@ -107,6 +107,16 @@ def _relocate_patch_at_old_position(K, U, W, rope, pos3_target, delta3, patch_of
     return moved + ref.rotate(patch, rope, ref.rope_angles(rope, old))
 
 
+def _form_patch_unscaled(delta, m):
+    Uf, S, Vt = np.linalg.svd(np.asarray(delta, dtype=np.float64), full_matrices=False)
+    return Uf[:, :m], Vt[:m], S
+
+
+def _form_patch_smallest(delta, m):
+    Uf, S, Vt = np.linalg.svd(np.asarray(delta, dtype=np.float64), full_matrices=False)
+    return Uf[:, -m:] * S[None, -m:], Vt[-m:], S
+
+
 def _shift_negated(K, rope, delta3):
     return _orig["shift_k"](K, rope, [-int(v) for v in delta3])
 
@@ -127,6 +137,8 @@ MUTANTS = {
     "page slot offset i // P": ("paged_slot", _slot_wrong),
     "shift direction negated": ("shift_k", _shift_negated),
     "removal patch rotated to the old position": ("relocate_k", _relocate_patch_at_old_position),
+    "patch forming without the singular values": ("form_patch", _form_patch_unscaled),
+    "patch forming keeps the smallest components": ("form_patch", _form_patch_smallest),
 }
 
 
