@@ -255,7 +255,43 @@ typedef struct {
   uint32_t* status;
 } kamera_scatter_args;
 
+/* kamera_form_patch -- the compile step of App. A on given deficits: for
+ * every (chunk, layer, head) unit, the top-m singular triplets of
+ * Delta (n x dim, fp32) as the stored patch
+ *   U = U_svd[:, :m] * S[:m]   (n x m, bf16, singular values folded in),
+ *   W = Vt[:m]                 (m x dim, bf16),
+ * so U W is the best rank-m approximation of Delta and (U, W) feed
+ * kamera_rehydrate directly.  The conditioned forward pass that produces
+ * Delta needs model weights and is not part of this library.
+ * Layouts: element (c, l, h, i, j) of Delta at delta + c*delta_stride[0] +
+ * l*delta_stride[1] + h*delta_stride[2] + i*delta_stride[3] + j (fp32,
+ * 16-byte aligned rows); U and W as in kamera_plane (bf16); sigma (optional,
+ * fp32) receives S[:m] at sigma + c*sigma_stride[0] + l*sigma_stride[1] +
+ * h*sigma_stride[2] + k.  Method: Gram matrix Delta^T Delta and cyclic Jacobi
+ * in fp32 (up to `sweeps` sweeps, 0 = 12), so singular vectors are accurate
+ * to ~1e-6 relative where the spectrum has a gap at m. */
+#define KAMERA_FORM_MAX_DIM 128
+typedef struct {
+  int32_t n_chunks;
+  int32_t n_layers;
+  int32_t n_heads;
+  int32_t n_tokens;            /* rows n of each Delta                          */
+  int32_t dim;                 /* columns: multiple of 4, <= KAMERA_FORM_MAX_DIM */
+  int32_t m;                   /* rank kept: 1 .. dim                           */
+  int32_t sweeps;              /* Jacobi sweep limit (0 = 12)                   */
+  int32_t pad_;
+  const float* delta;
+  int64_t delta_stride[4];
+  void* U;
+  int64_t u_stride[4];
+  void* W;
+  int64_t w_stride[4];
+  float* sigma;
+  int64_t sigma_stride[3];
+} kamera_form_args;
+
 int kamera_rehydrate(const kamera_rehydrate_args* args, void* stream);
+int kamera_form_patch(const kamera_form_args* args, void* stream);
 int kamera_shift(const kamera_shift_args* args, void* stream);
 int kamera_scatter_paged(const kamera_scatter_args* args, void* stream);
 int kamera_gather_paged(const kamera_scatter_args* args, void* stream);
@@ -269,8 +305,8 @@ int kamera_check_page_table(const int32_t* host_page_table, int32_t n_chunks,
                             int32_t page_size, int32_t n_pool_pages);
 
 /* Run exactly the host-side checks of an entry point (0 kamera_rehydrate,
- * 1 kamera_shift, 2 kamera_scatter_paged, 3 kamera_gather_paged) on `args`
- * without launching
+ * 1 kamera_shift, 2 kamera_scatter_paged, 3 kamera_gather_paged,
+ * 4 kamera_form_patch) on `args` without launching
  * anything (3 = kamera_gather_paged): KAMERA_OK when the call would be
  * enqueued, else the error code
  * the call would return.  Touches no device memory. */
@@ -281,7 +317,8 @@ int kamera_validate(int32_t which, const void* args);
 const char* kamera_last_error(void);
 int kamera_abi_version(void);
 /* sizeof of the argument structs: 0 rehydrate, 1 shift, 2 scatter, 3 plane,
- * 4 rope; -1 otherwise.  Lets a foreign-function binding check its layout. */
+ * 4 rope, 5 form; -1 otherwise.  Lets a foreign-function binding check its
+ * layout. */
 int64_t kamera_struct_size(int32_t which);
 
 #ifdef __cplusplus

@@ -14,6 +14,8 @@ Entry points (same names as the C ABI):
 * ``scatter_paged`` bit copy of dense token rows into page-table slots
                     (App. E clean-view overwrite, Sec. 6 paged pool)
 * ``gather_paged``  the inverse copy, pool slots back into dense rows
+* ``form_patch``    the compile step's truncated SVD of given deficits
+                    (App. A): U = U_svd S [:, :m], W = Vt[:m]
 """
 
 from __future__ import annotations
@@ -105,7 +107,15 @@ class CScatterArgs(ctypes.Structure):
                 ("page_size", _i32), ("n_pool_pages", _i32), ("status", _vp)]
 
 
+class CFormArgs(ctypes.Structure):
+    _fields_ = [("n_chunks", _i32), ("n_layers", _i32), ("n_heads", _i32), ("n_tokens", _i32),
+                ("dim", _i32), ("m", _i32), ("sweeps", _i32), ("pad_", _i32),
+                ("delta", _vp), ("delta_stride", _i64 * 4), ("U", _vp), ("u_stride", _i64 * 4),
+                ("W", _vp), ("w_stride", _i64 * 4), ("sigma", _vp), ("sigma_stride", _i64 * 3)]
+
+
 EXPORTS = ("kamera_rehydrate", "kamera_shift", "kamera_scatter_paged", "kamera_gather_paged",
+           "kamera_form_patch",
            "kamera_check_page_table",
            "kamera_validate", "kamera_last_error", "kamera_abi_version", "kamera_struct_size")
 
@@ -137,11 +147,13 @@ def lib() -> ctypes.CDLL:
     L.kamera_last_error.restype = ctypes.c_char_p
     L.kamera_abi_version.argtypes = []
     L.kamera_abi_version.restype = _i32
+    L.kamera_form_patch.argtypes = [ctypes.POINTER(CFormArgs), _vp]
+    L.kamera_form_patch.restype = _i32
     L.kamera_validate.argtypes = [_i32, _vp]
     L.kamera_validate.restype = _i32
     L.kamera_struct_size.argtypes = [_i32]
     L.kamera_struct_size.restype = _i64
-    sizes = {0: CRehydrateArgs, 1: CShiftArgs, 2: CScatterArgs, 3: CPlane, 4: CRope}
+    sizes = {0: CRehydrateArgs, 1: CShiftArgs, 2: CScatterArgs, 3: CPlane, 4: CRope, 5: CFormArgs}
     for k, cls in sizes.items():
         if L.kamera_struct_size(k) != ctypes.sizeof(cls):
             raise KameraUnavailable(f"struct layout mismatch for {cls.__name__}: "
@@ -445,6 +457,48 @@ def prepare_scatter_paged(rows, pool, page_table, *, page_size: int, n_pool_page
     a.status = _ptr(status)
     fn = L.kamera_gather_paged if gather else L.kamera_scatter_paged
     return Prepared(fn, a, (rows, pool, page_table, chunk_tokens, status))
+
+
+def form_patch(*a, stream=None, **kw) -> None:
+    """``kamera_form_patch``; see ``prepare_form_patch``."""
+    prepare_form_patch(*a, **kw).launch(stream)
+
+
+def prepare_form_patch(delta, U, W, *, sigma=None, sweeps: int = 0) -> Prepared:
+    """Top-m truncated SVD of every deficit (App. A compile step).
+
+    delta: fp32 [C, L, H, n, d]; U: bf16 [C, L, H, n, m] (receives U S);
+    W: bf16 [C, L, H, m, d] (receives Vt[:m]); sigma: optional fp32
+    [C, L, H, m] (receives S[:m]).  m is U's last dimension.
+    """
+    import torch
+
+    L = lib()
+    if delta.dtype != torch.float32:
+        raise TypeError(f"delta must be float32 (got {delta.dtype})")
+    _bf16(U, "U"), _bf16(W, "W")
+    C, Ln, H, n, d = (int(x) for x in delta.shape)
+    m = int(U.shape[-1])
+    if tuple(U.shape) != (C, Ln, H, n, m) or tuple(W.shape) != (C, Ln, H, m, d):
+        raise ValueError("U must be [C, L, H, n, m] and W [C, L, H, m, d]")
+    a = CFormArgs()
+    a.n_chunks, a.n_layers, a.n_heads, a.n_tokens, a.dim, a.m, a.sweeps = C, Ln, H, n, d, m, int(sweeps)
+    a.delta = _ptr(delta)
+    for i, st in enumerate(_strides(delta, 4)):
+        a.delta_stride[i] = st
+    a.U = _ptr(U)
+    for i, st in enumerate(_strides(U, 4)):
+        a.u_stride[i] = st
+    a.W = _ptr(W)
+    for i, st in enumerate(_strides(W, 4)):
+        a.w_stride[i] = st
+    if sigma is not None:
+        if sigma.dtype != torch.float32 or tuple(sigma.shape) != (C, Ln, H, m):
+            raise ValueError("sigma must be float32 [C, L, H, m]")
+        a.sigma = _ptr(sigma)
+        for i, st in enumerate(_strides(sigma, 3)):
+            a.sigma_stride[i] = st
+    return Prepared(L.kamera_form_patch, a, (delta, U, W, sigma))
 
 
 def check_page_table(page_table_host, n_tokens: int, page_size: int, n_pool_pages: int) -> None:

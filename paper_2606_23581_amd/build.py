@@ -41,6 +41,7 @@ def build(verbose: bool = False, save_temps: bool = False) -> str:
     hipcc = _hipcc()
     os.makedirs(BUILD, exist_ok=True)
     kobj = os.path.join(BUILD, "kamera_kernels.o")
+    pobj = os.path.join(BUILD, "kamera_patch.o")
     aobj = os.path.join(BUILD, "kamera_abi.o")
     common = ["-std=c++17", "-fPIC", "-I", INCLUDE, "-I", CSRC]
     kcmd = [hipcc, "-c", "-O3", f"--offload-arch={ARCH}", *NO_PACKED_FP32, *common,
@@ -49,11 +50,16 @@ def build(verbose: bool = False, save_temps: bool = False) -> str:
     if save_temps:
         kcmd.insert(2, f"-save-temps={'obj'}")
     _run(kcmd, verbose)
+    pcmd = [hipcc, "-c", "-O3", f"--offload-arch={ARCH}", *NO_PACKED_FP32, *common,
+            "-Wno-unused-command-line-argument", os.path.join(CSRC, "kamera_patch.hip"), "-o", pobj]
+    if save_temps:
+        pcmd.insert(2, "-save-temps=obj")
+    _run(pcmd, verbose)
     # the ABI layer is plain host C++: validation and launch set-up only
     _run(["g++", "-c", "-O2", "-Wall", "-Wextra", "-D__HIP_PLATFORM_AMD__", "-I", "/opt/rocm/include",
           *common, os.path.join(CSRC, "kamera_abi.cpp"), "-o", aobj], verbose)
     tmp = LIB + ".tmp"
-    _run([hipcc, "-shared", f"--offload-arch={ARCH}", "-fPIC", kobj, aobj, "-o", tmp], verbose)
+    _run([hipcc, "-shared", f"--offload-arch={ARCH}", "-fPIC", kobj, pobj, aobj, "-o", tmp], verbose)
     os.replace(tmp, LIB)
     return LIB
 

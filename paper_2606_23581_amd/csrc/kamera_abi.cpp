@@ -521,6 +521,65 @@ extern "C" int kamera_gather_paged(const kamera_scatter_args* a, void* stream) {
   return scatter_or_gather(a, stream, true);
 }
 
+// ---------------------------------------------------------------------------
+// kamera_form_patch
+// ---------------------------------------------------------------------------
+
+static int build_form(const kamera_form_args* a, kamera::FormParams& P, bool& launch) {
+  const char* who = "kamera_form_patch";
+  launch = false;
+  if (a == nullptr) return fail(KAMERA_ERR_NULL, "%s: args is NULL", who);
+  if (a->n_chunks < 0 || a->n_layers < 0 || a->n_heads < 0 || a->n_tokens < 0)
+    return fail(KAMERA_ERR_SHAPE, "%s: negative sizes", who);
+  if (a->dim <= 0 || a->dim % 4 != 0)
+    return fail(KAMERA_ERR_UNSUPPORTED, "%s: dim must be a positive multiple of 4 (got %d)", who, a->dim);
+  if (a->dim > KAMERA_FORM_MAX_DIM)
+    return fail(KAMERA_ERR_RANGE, "%s: dim %d exceeds %d", who, a->dim, KAMERA_FORM_MAX_DIM);
+  if (a->m < 1 || a->m > a->dim) return fail(KAMERA_ERR_RANGE, "%s: m = %d outside [1, dim]", who, a->m);
+  if (a->sweeps < 0) return fail(KAMERA_ERR_SHAPE, "%s: sweeps must be >= 0", who);
+  const int64_t units = (int64_t)a->n_chunks * a->n_layers * a->n_heads;
+  if (units == 0 || a->n_tokens == 0) return KAMERA_OK;
+  if (units > 0x7fffffff) return fail(KAMERA_ERR_RANGE, "%s: too many units", who);
+  if (a->delta == nullptr || a->U == nullptr || a->W == nullptr)
+    return fail(KAMERA_ERR_NULL, "%s: delta, U and W are required", who);
+  if (!aligned16(a->delta))
+    return fail(KAMERA_ERR_ALIGN, "%s: delta must be 16-byte aligned", who);
+  for (int k = 0; k < 4; ++k)
+    if (a->delta_stride[k] % 4 != 0)
+      return fail(KAMERA_ERR_ALIGN, "%s: delta strides must be multiples of 4 floats", who);
+  memset(&P, 0, sizeof(P));
+  P.delta = a->delta;
+  P.U = static_cast<uint16_t*>(a->U);
+  P.W = static_cast<uint16_t*>(a->W);
+  P.sigma = a->sigma;
+  memcpy(P.delta_s, a->delta_stride, sizeof(P.delta_s));
+  memcpy(P.u_s, a->u_stride, sizeof(P.u_s));
+  memcpy(P.w_s, a->w_stride, sizeof(P.w_s));
+  memcpy(P.sigma_s, a->sigma_stride, sizeof(P.sigma_s));
+  P.n_chunks = a->n_chunks;
+  P.n_layers = a->n_layers;
+  P.n_heads = a->n_heads;
+  P.n_tokens = a->n_tokens;
+  P.dim = a->dim;
+  P.m = a->m;
+  P.sweeps = a->sweeps == 0 ? 12 : a->sweeps;
+  P.n_units = (int32_t)units;
+  launch = true;
+  return KAMERA_OK;
+}
+
+extern "C" int kamera_form_patch(const kamera_form_args* a, void* stream) {
+  static thread_local kamera::FormParams P;
+  bool launch = false;
+  const int rc = build_form(a, P, launch);
+  if (rc) return rc;
+  if (launch) {
+    const hipError_t e = kamera::launch_form_patch(P, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return fail(KAMERA_ERR_HIP, "kamera_form_patch: launch failed: %s", hipGetErrorString(e));
+  }
+  return ok();
+}
+
 extern "C" int kamera_validate(int32_t which, const void* args) {
   bool launch = false;
   int rc;
@@ -531,6 +590,11 @@ extern "C" int kamera_validate(int32_t which, const void* args) {
     case 3: {
       static thread_local kamera::ScatterParams P;
       rc = build_scatter(static_cast<const kamera_scatter_args*>(args), P, launch, which == 3);
+      break;
+    }
+    case 4: {
+      static thread_local kamera::FormParams P;
+      rc = build_form(static_cast<const kamera_form_args*>(args), P, launch);
       break;
     }
     default: return fail(KAMERA_ERR_SHAPE, "kamera_validate: unknown entry point %d", which);
@@ -575,6 +639,7 @@ extern "C" int64_t kamera_struct_size(int32_t which) {
     case 2: return (int64_t)sizeof(kamera_scatter_args);
     case 3: return (int64_t)sizeof(kamera_plane);
     case 4: return (int64_t)sizeof(kamera_rope);
+    case 5: return (int64_t)sizeof(kamera_form_args);
     default: return -1;
   }
 }

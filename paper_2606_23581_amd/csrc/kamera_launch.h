@@ -117,7 +117,29 @@ struct ScatterParams {
   int64_t n_tasks;
 };
 
+constexpr int kFormMaxDim = 128;     // patch forming: columns of Delta
+
+struct FormParams {
+  const float* delta;
+  uint16_t* U;
+  uint16_t* W;
+  float* sigma;
+  int64_t delta_s[4];
+  int64_t u_s[4];
+  int64_t w_s[4];
+  int64_t sigma_s[3];
+  int32_t n_chunks, n_layers, n_heads;
+  int32_t n_tokens;
+  int32_t dim;
+  int32_t m;
+  int32_t sweeps;
+  int32_t n_units;
+};
+
+size_t form_lds_bytes(int dim, int m);
+
 hipError_t launch_rehydrate(const RehydrateParams& p, hipStream_t s);
+hipError_t launch_form_patch(const FormParams& p, hipStream_t s);
 hipError_t launch_shift(const ShiftParams& p, hipStream_t s);
 hipError_t launch_scatter(const ScatterParams& p, hipStream_t s);
 

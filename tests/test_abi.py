@@ -28,7 +28,7 @@ def test_header_declares_the_boundary():
     names = declared_functions()
     for want in ("kamera_rehydrate", "kamera_shift", "kamera_scatter_paged", "kamera_last_error",
                  "kamera_abi_version", "kamera_check_page_table", "kamera_struct_size", "kamera_validate",
-                 "kamera_gather_paged"):
+                 "kamera_gather_paged", "kamera_form_patch"):
         assert want in names
 
 
@@ -51,6 +51,7 @@ def test_version_and_struct_layout():
     assert L.kamera_struct_size(2) == ctypes.sizeof(km.CScatterArgs)
     assert L.kamera_struct_size(3) == ctypes.sizeof(km.CPlane)
     assert L.kamera_struct_size(4) == ctypes.sizeof(km.CRope)
+    assert L.kamera_struct_size(5) == ctypes.sizeof(km.CFormArgs)
     assert L.kamera_struct_size(99) == -1
 
 
@@ -388,3 +389,44 @@ def test_product_package_does_not_import_the_oracle():
             if f.endswith((".py", ".hip", ".cpp", ".h")):
                 text = open(os.path.join(dirpath, f)).read()
                 assert "oracle" not in text.replace("oracles", ""), f
+
+
+def form_args():
+    a = km.CFormArgs()
+    a.n_chunks, a.n_layers, a.n_heads, a.n_tokens, a.dim, a.m = 2, 3, 4, 100, 128, 16
+    a.delta = FAKE
+    for k, st in enumerate([3 * 4 * 100 * 128, 4 * 100 * 128, 100 * 128, 128]):
+        a.delta_stride[k] = st
+    a.U = FAKE + (1 << 36)
+    a.W = FAKE + (2 << 36)
+    return a
+
+
+@pytest.mark.parametrize("case,code", [
+    ("ok", km.OK), ("dim_not_4", km.ERR_UNSUPPORTED), ("dim_big", km.ERR_RANGE), ("m_zero", km.ERR_RANGE),
+    ("m_big", km.ERR_RANGE), ("null", km.ERR_NULL), ("unaligned", km.ERR_ALIGN), ("stride", km.ERR_ALIGN),
+    ("sweeps", km.ERR_SHAPE), ("negative", km.ERR_SHAPE),
+])
+def test_form_patch_validation(case, code):
+    a = form_args()
+    if case == "dim_not_4":
+        a.dim = 126
+    elif case == "dim_big":
+        a.dim = 256
+    elif case == "m_zero":
+        a.m = 0
+    elif case == "m_big":
+        a.m = 129
+    elif case == "null":
+        a.W = None
+    elif case == "unaligned":
+        a.delta = FAKE + 4
+    elif case == "stride":
+        a.delta_stride[3] = 130
+    elif case == "sweeps":
+        a.sweeps = -1
+    elif case == "negative":
+        a.n_tokens = -5
+    assert km.lib().kamera_validate(4, ctypes.byref(a)) == code, km.last_error()
+    if code != km.OK:
+        assert km.lib().kamera_form_patch(ctypes.byref(a), None) == code

@@ -345,3 +345,48 @@ def test_scatter_bad_page_is_flagged(device):
     assert int(status.cpu()[0]) & km.STATUS_BAD_PAGE
     assert np.array_equal(out[0, 16:], src[0, 0, :16])
     assert np.all(out[0, :16] == SENTINEL)
+
+
+# ---------------------------------------------------------------------------
+# compile-side patch forming
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("n,d,m", [(100, 128, 16), (1024, 128, 64), (37, 64, 8), (50, 36, 1), (64, 32, 32)])
+def test_form_patch_matches_svd(device, n, d, m):
+    """Planted deficits with a spectral gap at m (rank-m signal + small noise):
+    U W must match the fp64 truncated SVD's product, the singular values the
+    fp64 ones, W's rows must be orthonormal and the residual Eckart-Young's.
+    U and W are stored in bf16 (unit roundoff 2^-8 each), so the product's
+    relative Frobenius error is bounded by ~2 * 2^-8 plus the fp32 subspace
+    error; the bound used is 2^-6."""
+    import paper_2606_23581_amd as km
+    import torch
+
+    print(f"[case] form_patch n{n} d{d} m{m}", flush=True)
+    rng = np.random.default_rng(n * 1000 + d + m)
+    C, L, H = 2, 2, 2
+    delta = np.empty((C, L, H, n, d), np.float32)
+    for idx in np.ndindex(C, L, H):
+        A = np.linalg.qr(rng.standard_normal((n, m)))[0]
+        B = np.linalg.qr(rng.standard_normal((d, m)))[0]
+        sig = np.linspace(10.0, 2.0, m)
+        delta[idx] = (A * sig) @ B.T + 0.01 * rng.standard_normal((n, d))
+    dt = torch.from_numpy(delta).to(device)
+    U = torch.zeros((C, L, H, n, m), dtype=torch.bfloat16, device=device)
+    W = torch.zeros((C, L, H, m, d), dtype=torch.bfloat16, device=device)
+    sigma = torch.zeros((C, L, H, m), dtype=torch.float32, device=device)
+    km.form_patch(dt, U, W, sigma=sigma)
+    torch.cuda.synchronize()
+    Ub, Wb, sg = bits(U), bits(W), sigma.cpu().numpy()
+    for idx in np.ndindex(C, L, H):
+        Dl = delta[idx].astype(np.float64)
+        Ur, Wr, S = ref.form_patch(Dl, m)
+        Ug, Wg = ref.bf16_to_f64(Ub[idx]), ref.bf16_to_f64(Wb[idx])
+        prod_ref = Ur @ Wr
+        rel = np.linalg.norm(Ug @ Wg - prod_ref) / np.linalg.norm(prod_ref)
+        assert rel <= 2.0 ** -6, (idx, rel)
+        assert np.max(np.abs(sg[idx] - S[:m]) / S[:m]) <= 1e-4, (idx, sg[idx][:4], S[:4])
+        assert np.max(np.abs(Wg @ Wg.T - np.eye(m))) <= 2.0 ** -6
+        opt = np.linalg.norm(Dl - prod_ref)
+        got = np.linalg.norm(Dl - Ug @ Wg)
+        assert got <= opt + 2.0 ** -6 * np.linalg.norm(prod_ref), (idx, got, opt)
