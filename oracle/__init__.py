@@ -13,6 +13,7 @@ from .kamera_ref import (  # noqa: F401
     bf16_to_f64,
     form_patch,
     inv_freq,
+    orbit_patch,
     pair_columns,
     pair_coordinate,
     paged_slot,

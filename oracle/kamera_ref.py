@@ -285,6 +285,17 @@ def form_patch(delta: np.ndarray, m: int):
     return Uf[:, :m] * S[None, :m], Vt[:m], S
 
 
+def orbit_patch(deltas, m: int):
+    """One stored patch for every ordering of a cached chunk set (Sec. 5,
+    reorder): the deficits of the orbit's orderings (K x n x d, the held-out
+    ordering left out by the caller) are averaged and the mean is truncated to
+    rank m as in ``form_patch``.  Because the sum over the orbit of
+    ||Delta_k - P||^2 equals K ||mean - P||^2 plus a term free of P, this is
+    the rank-m patch with the least total squared error over the orbit."""
+    mean = np.mean(np.asarray(deltas, dtype=np.float64), axis=0)
+    return form_patch(mean, m)
+
+
 def paged_slot(page_table_row: np.ndarray, i: int, page_size: int) -> int:
     """Physical pool slot of a chunk's token i: page_table[i // P] * P + i % P."""
     return int(page_table_row[i // page_size]) * page_size + i % page_size

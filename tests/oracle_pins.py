@@ -470,4 +470,40 @@ def pin_form_patch(ref):
     assert np.max(np.abs(ref.rehydrate_v(K, U, W) - (K + A @ B))) < 1e-11
 
 
+def pin_orbit_patch(ref):
+    """The orbit patch: an orbit of identical deficits gives that deficit's own
+    patch; for a real orbit its total squared error over the members is below
+    that of every member's own patch, of the mean's rank-m truncation by any
+    other rank-m subspace tried, and it equals the decomposition
+    K ||mean - P||^2 + sum ||Delta_k - mean||^2."""
+    rng = _rng(29)
+    n, d, m, K = 30, 10, 3, 4
+    base = rng.standard_normal((n, d))
+    U1, W1, _ = ref.form_patch(base, m)
+    Uo, Wo, _ = ref.orbit_patch(np.stack([base] * K), m)
+    assert np.max(np.abs(Uo @ Wo - U1 @ W1)) < 1e-11
+    # a shared low-rank core plus an ordering-dependent part
+    core = rng.standard_normal((n, m)) @ rng.standard_normal((m, d)) * 3.0
+    deltas = np.stack([core + rng.standard_normal((n, d)) for _ in range(K)])
+    Uo, Wo, _ = ref.orbit_patch(deltas, m)
+    P = Uo @ Wo
+
+    def total(Q):
+        return float(sum(np.sum((dk - Q) ** 2) for dk in deltas))
+
+    mean = deltas.mean(axis=0)
+    spread = float(sum(np.sum((dk - mean) ** 2) for dk in deltas))
+    assert abs(total(P) - (K * np.sum((mean - P) ** 2) + spread)) < 1e-8 * total(P)
+    for dk in deltas:
+        Uk, Wk, _ = ref.form_patch(dk, m)
+        assert total(P) < total(Uk @ Wk)
+    for _ in range(20):
+        Q, _r = np.linalg.qr(rng.standard_normal((d, m)))
+        assert total(P) <= total(mean @ Q @ Q.T) + 1e-9
+    # the orbit mean of K scaled copies c_k Delta is the patch of mean(c_k) Delta
+    cs = np.array([0.5, 1.0, 2.0, 4.5])
+    Uo, Wo, _ = ref.orbit_patch(cs[:, None, None] * base[None], m)
+    assert np.max(np.abs(Uo @ Wo - cs.mean() * (U1 @ W1))) < 1e-10
+
+
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

@@ -117,6 +117,14 @@ def _form_patch_smallest(delta, m):
     return Uf[:, -m:] * S[None, -m:], Vt[-m:], S
 
 
+def _orbit_sum(deltas, m):
+    return ref.form_patch(np.sum(np.asarray(deltas, dtype=np.float64), axis=0), m)
+
+
+def _orbit_first(deltas, m):
+    return ref.form_patch(np.asarray(deltas, dtype=np.float64)[0], m)
+
+
 def _shift_negated(K, rope, delta3):
     return _orig["shift_k"](K, rope, [-int(v) for v in delta3])
 
@@ -139,6 +147,8 @@ MUTANTS = {
     "removal patch rotated to the old position": ("relocate_k", _relocate_patch_at_old_position),
     "patch forming without the singular values": ("form_patch", _form_patch_unscaled),
     "patch forming keeps the smallest components": ("form_patch", _form_patch_smallest),
+    "orbit patch sums instead of averaging": ("orbit_patch", _orbit_sum),
+    "orbit patch from one ordering only": ("orbit_patch", _orbit_first),
 }
 
 
