@@ -269,7 +269,13 @@ typedef struct {
  * fp32) receives S[:m] at sigma + c*sigma_stride[0] + l*sigma_stride[1] +
  * h*sigma_stride[2] + k.  Method: Gram matrix Delta^T Delta and cyclic Jacobi
  * in fp32 (up to `sweeps` sweeps, 0 = 12), so singular vectors are accurate
- * to ~1e-6 relative where the spectrum has a gap at m. */
+ * to ~1e-6 relative where the spectrum has a gap at m.
+ * Orbit patch (Sec. 5, reorder): with n_orbit = K >= 2 the deficits of K
+ * orderings of the same chunk set, at delta + o*orbit_stride (o < K), are
+ * averaged (fp32) and the mean is truncated as above: the one rank-m patch
+ * with the least total squared error over those orderings.  A held-out
+ * ordering is simply not passed.  n_orbit 0 or 1 = a single deficit.
+ * U, W and sigma must not overlap the deficits (KAMERA_ERR_ALIAS). */
 #define KAMERA_FORM_MAX_DIM 128
 typedef struct {
   int32_t n_chunks;
@@ -279,7 +285,7 @@ typedef struct {
   int32_t dim;                 /* columns: multiple of 4, <= KAMERA_FORM_MAX_DIM */
   int32_t m;                   /* rank kept: 1 .. dim                           */
   int32_t sweeps;              /* Jacobi sweep limit (0 = 12)                   */
-  int32_t pad_;
+  int32_t n_orbit;             /* deficits averaged per unit (0 or 1 = one)     */
   const float* delta;
   int64_t delta_stride[4];
   void* U;
@@ -288,6 +294,7 @@ typedef struct {
   int64_t w_stride[4];
   float* sigma;
   int64_t sigma_stride[3];
+  int64_t orbit_stride;        /* elements between orbit members of delta       */
 } kamera_form_args;
 
 int kamera_rehydrate(const kamera_rehydrate_args* args, void* stream);

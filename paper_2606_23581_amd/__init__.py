@@ -109,9 +109,10 @@ class CScatterArgs(ctypes.Structure):
 
 class CFormArgs(ctypes.Structure):
     _fields_ = [("n_chunks", _i32), ("n_layers", _i32), ("n_heads", _i32), ("n_tokens", _i32),
-                ("dim", _i32), ("m", _i32), ("sweeps", _i32), ("pad_", _i32),
+                ("dim", _i32), ("m", _i32), ("sweeps", _i32), ("n_orbit", _i32),
                 ("delta", _vp), ("delta_stride", _i64 * 4), ("U", _vp), ("u_stride", _i64 * 4),
-                ("W", _vp), ("w_stride", _i64 * 4), ("sigma", _vp), ("sigma_stride", _i64 * 3)]
+                ("W", _vp), ("w_stride", _i64 * 4), ("sigma", _vp), ("sigma_stride", _i64 * 3),
+                ("orbit_stride", _i64)]
 
 
 EXPORTS = ("kamera_rehydrate", "kamera_shift", "kamera_scatter_paged", "kamera_gather_paged",
@@ -467,9 +468,11 @@ def form_patch(*a, stream=None, **kw) -> None:
 def prepare_form_patch(delta, U, W, *, sigma=None, sweeps: int = 0) -> Prepared:
     """Top-m truncated SVD of every deficit (App. A compile step).
 
-    delta: fp32 [C, L, H, n, d]; U: bf16 [C, L, H, n, m] (receives U S);
-    W: bf16 [C, L, H, m, d] (receives Vt[:m]); sigma: optional fp32
-    [C, L, H, m] (receives S[:m]).  m is U's last dimension.
+    delta: fp32 [C, L, H, n, d], or [K, C, L, H, n, d] for an orbit patch
+    (Sec. 5, reorder: the K orderings' deficits are averaged first);
+    U: bf16 [C, L, H, n, m] (receives U S); W: bf16 [C, L, H, m, d]
+    (receives Vt[:m]); sigma: optional fp32 [C, L, H, m] (receives S[:m]).
+    m is U's last dimension.
     """
     import torch
 
@@ -477,14 +480,25 @@ def prepare_form_patch(delta, U, W, *, sigma=None, sweeps: int = 0) -> Prepared:
     if delta.dtype != torch.float32:
         raise TypeError(f"delta must be float32 (got {delta.dtype})")
     _bf16(U, "U"), _bf16(W, "W")
-    C, Ln, H, n, d = (int(x) for x in delta.shape)
+    n_orbit, orbit_stride = 0, 0
+    if delta.dim() == 6:
+        n_orbit, orbit_stride = int(delta.shape[0]), int(delta.stride(0))
+        if n_orbit == 0:
+            raise ValueError("an orbit patch needs at least one ordering's deficit")
+        delta_m = delta[0]
+    elif delta.dim() == 5:
+        delta_m = delta
+    else:
+        raise ValueError("delta must be [C, L, H, n, d] or [K, C, L, H, n, d]")
+    C, Ln, H, n, d = (int(x) for x in delta_m.shape)
     m = int(U.shape[-1])
     if tuple(U.shape) != (C, Ln, H, n, m) or tuple(W.shape) != (C, Ln, H, m, d):
         raise ValueError("U must be [C, L, H, n, m] and W [C, L, H, m, d]")
     a = CFormArgs()
     a.n_chunks, a.n_layers, a.n_heads, a.n_tokens, a.dim, a.m, a.sweeps = C, Ln, H, n, d, m, int(sweeps)
-    a.delta = _ptr(delta)
-    for i, st in enumerate(_strides(delta, 4)):
+    a.n_orbit, a.orbit_stride = n_orbit, orbit_stride
+    a.delta = _ptr(delta_m)
+    for i, st in enumerate(_strides(delta_m, 4)):
         a.delta_stride[i] = st
     a.U = _ptr(U)
     for i, st in enumerate(_strides(U, 4)):

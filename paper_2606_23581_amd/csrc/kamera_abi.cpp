@@ -143,6 +143,20 @@ void extent(const void* base, const int64_t* s, const int64_t* ext, int64_t row_
   hi = reinterpret_cast<uintptr_t>(base) + (b + row_elems) * 2;
 }
 
+// byte range [lo, hi) of an n-D strided view (element strides, elem_bytes each)
+// whose innermost rows are row_elems contiguous elements
+void span(const void* base, const int64_t* s, const int64_t* ext, int nd, int64_t row_elems, int elem_bytes,
+          uintptr_t& lo, uintptr_t& hi) {
+  int64_t a = 0, b = 0;
+  for (int k = 0; k < nd; ++k) {
+    if (ext[k] <= 0) continue;
+    const int64_t d = (ext[k] - 1) * s[k];
+    if (d < 0) a += d; else b += d;
+  }
+  lo = reinterpret_cast<uintptr_t>(base) + a * elem_bytes;
+  hi = reinterpret_cast<uintptr_t>(base) + (b + row_elems) * elem_bytes;
+}
+
 bool overlap(uintptr_t a0, uintptr_t a1, uintptr_t b0, uintptr_t b1) { return a0 < b1 && b0 < a1; }
 
 int pick_grid(int64_t n_tasks, int32_t& per_xcd, const char* who) {
@@ -537,6 +551,7 @@ static int build_form(const kamera_form_args* a, kamera::FormParams& P, bool& la
     return fail(KAMERA_ERR_RANGE, "%s: dim %d exceeds %d", who, a->dim, KAMERA_FORM_MAX_DIM);
   if (a->m < 1 || a->m > a->dim) return fail(KAMERA_ERR_RANGE, "%s: m = %d outside [1, dim]", who, a->m);
   if (a->sweeps < 0) return fail(KAMERA_ERR_SHAPE, "%s: sweeps must be >= 0", who);
+  if (a->n_orbit < 0) return fail(KAMERA_ERR_SHAPE, "%s: n_orbit must be >= 0", who);
   const int64_t units = (int64_t)a->n_chunks * a->n_layers * a->n_heads;
   if (units == 0 || a->n_tokens == 0) return KAMERA_OK;
   if (units > 0x7fffffff) return fail(KAMERA_ERR_RANGE, "%s: too many units", who);
@@ -547,6 +562,30 @@ static int build_form(const kamera_form_args* a, kamera::FormParams& P, bool& la
   for (int k = 0; k < 4; ++k)
     if (a->delta_stride[k] % 4 != 0)
       return fail(KAMERA_ERR_ALIGN, "%s: delta strides must be multiples of 4 floats", who);
+  const int32_t n_orbit = a->n_orbit > 1 ? a->n_orbit : 1;
+  if (n_orbit > 1 && a->orbit_stride % 4 != 0)
+    return fail(KAMERA_ERR_ALIGN, "%s: orbit_stride must be a multiple of 4 floats", who);
+  {
+    // outputs must not overlap any deficit that is read
+    const int64_t ext_d[5] = {a->n_chunks, a->n_layers, a->n_heads, a->n_tokens, n_orbit};
+    const int64_t s_d[5] = {a->delta_stride[0], a->delta_stride[1], a->delta_stride[2], a->delta_stride[3],
+                            n_orbit > 1 ? a->orbit_stride : 0};
+    uintptr_t d0, d1;
+    span(a->delta, s_d, ext_d, 5, a->dim, 4, d0, d1);
+    const int64_t ext_u[4] = {a->n_chunks, a->n_layers, a->n_heads, a->n_tokens};
+    const int64_t ext_w[4] = {a->n_chunks, a->n_layers, a->n_heads, a->m};
+    uintptr_t u0, u1, w0, w1;
+    span(a->U, a->u_stride, ext_u, 4, a->m, 2, u0, u1);
+    span(a->W, a->w_stride, ext_w, 4, a->dim, 2, w0, w1);
+    if (overlap(u0, u1, d0, d1) || overlap(w0, w1, d0, d1))
+      return fail(KAMERA_ERR_ALIAS, "%s: U and W must not overlap the deficits", who);
+    if (a->sigma != nullptr) {
+      const int64_t ext_s[3] = {a->n_chunks, a->n_layers, a->n_heads};
+      uintptr_t s0, s1;
+      span(a->sigma, a->sigma_stride, ext_s, 3, a->m, 4, s0, s1);
+      if (overlap(s0, s1, d0, d1)) return fail(KAMERA_ERR_ALIAS, "%s: sigma must not overlap the deficits", who);
+    }
+  }
   memset(&P, 0, sizeof(P));
   P.delta = a->delta;
   P.U = static_cast<uint16_t*>(a->U);
@@ -564,6 +603,9 @@ static int build_form(const kamera_form_args* a, kamera::FormParams& P, bool& la
   P.m = a->m;
   P.sweeps = a->sweeps == 0 ? 12 : a->sweeps;
   P.n_units = (int32_t)units;
+  P.n_orbit = n_orbit;
+  P.orbit_s = n_orbit > 1 ? a->orbit_stride : 0;
+  P.inv_orbit = 1.0f / (float)n_orbit;
   launch = true;
   return KAMERA_OK;
 }

@@ -128,12 +128,15 @@ struct FormParams {
   int64_t u_s[4];
   int64_t w_s[4];
   int64_t sigma_s[3];
+  int64_t orbit_s;                  // elements between orbit members of delta
   int32_t n_chunks, n_layers, n_heads;
   int32_t n_tokens;
   int32_t dim;
   int32_t m;
   int32_t sweeps;
   int32_t n_units;
+  int32_t n_orbit;                  // >= 1 deficits averaged per unit
+  float inv_orbit;                  // 1 / n_orbit
 };
 
 size_t form_lds_bytes(int dim, int m);

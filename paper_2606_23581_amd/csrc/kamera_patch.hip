@@ -5,10 +5,12 @@
 // One 1024-thread workgroup per (chunk, layer, head) unit, everything in LDS:
 //   1. Gram matrix G = Delta^T Delta (fp32), Delta streamed in 32-row tiles;
 //   2. cyclic Jacobi on G with the round-robin ordering: every step rotates
-//      d/2 disjoint (p, q) pairs at once (rows of G, then columns of G and of
-//      the accumulated V), sweeps until the off-diagonal mass is negligible;
+//      d/2 disjoint (p, q) pairs at once (G <- J^T G J as independent 2x2
+//      blocks, V <- V J), sweeps until the off-diagonal mass is negligible;
 //   3. rank the eigenvalues (diag G), keep the m largest;
 //   4. W[k] = V[:, order[k]]^T and U = Delta V_m, rounded to bf16.
+// With an orbit (Sec. 5, reorder) Delta is the mean of the members' deficits,
+// formed on the fly wherever a Delta tile is staged.
 // The eigenvalues of G are the squared singular values of Delta and its
 // eigenvectors the right singular vectors, so U W is the rank-m truncation.
 
@@ -49,13 +51,23 @@ __device__ __forceinline__ float block_sum(float v, float* red) {
   return s;
 }
 
+// Row i, columns [4 v4, 4 v4 + 4) of the (orbit-mean) deficit.
+__device__ __forceinline__ f32x4v load_delta4(const FormParams& P, const float* delta, int64_t i, int v4) {
+  const float* row = delta + i * P.delta_s[3] + 4 * v4;
+  f32x4v x = *reinterpret_cast<const f32x4v*>(row);
+  if (P.n_orbit > 1) {
+    for (int o = 1; o < P.n_orbit; ++o) x += *reinterpret_cast<const f32x4v*>(row + (int64_t)o * P.orbit_s);
+    x *= P.inv_orbit;
+  }
+  return x;
+}
+
 }  // namespace
 
 __global__ __launch_bounds__(kFormThreads) void form_patch_kernel(const FormParams /*by value, read in place*/) {
   const FormParams& P = *static_cast<const FormParams*>((const void*)__builtin_amdgcn_kernarg_segment_ptr());
   extern __shared__ __align__(16) float lds_f[];
-  __shared__ float s_c[64], s_s[64];
-  __shared__ int s_p[64], s_q[64];
+  __shared__ f32x4v s_pair[64];           // per pair: c, s, t, p | q << 8
   __shared__ int s_order[128];
   __shared__ float s_red[kFormThreads / 64];
 
@@ -87,7 +99,7 @@ __global__ __launch_bounds__(kFormThreads) void form_patch_kernel(const FormPara
       for (int e = tid; e < kFormTile * vec_per_row; e += kFormThreads) {
         const int r = e / vec_per_row, v4 = e % vec_per_row;
         f32x4v x = {0.f, 0.f, 0.f, 0.f};
-        if (t0 + r < n) x = *reinterpret_cast<const f32x4v*>(delta + (int64_t)(t0 + r) * P.delta_s[3] + 4 * v4);
+        if (t0 + r < n) x = load_delta4(P, delta, t0 + r, v4);
         *reinterpret_cast<f32x4v*>(T + r * d + 4 * v4) = x;
       }
       __syncthreads();
@@ -135,40 +147,99 @@ __global__ __launch_bounds__(kFormThreads) void form_patch_kernel(const FormPara
         const int pb = 1 + (d - 2 - k + step) % (d - 1);
         const int p = pa < pb ? pa : pb, q = pa < pb ? pb : pa;
         const float app = G[p * ld + p], aqq = G[q * ld + q], apq = G[p * ld + q];
-        float cc = 1.f, ss = 0.f;
+        float cc = 1.f, ss = 0.f, t = 0.f;
         if (fabsf(apq) > 1e-30f) {
+          // the smaller root of t^2 + 2 theta t - 1 = 0 zeroes G[p][q]
           const float theta = (aqq - app) / (2.f * apq);
-          const float t = (theta >= 0.f ? 1.f : -1.f) / (fabsf(theta) + sqrtf(theta * theta + 1.f));
+          t = (theta >= 0.f ? 1.f : -1.f) / (fabsf(theta) + sqrtf(theta * theta + 1.f));
           cc = 1.f / sqrtf(t * t + 1.f);
           ss = t * cc;
         }
-        s_p[k] = p;
-        s_q[k] = q;
-        s_c[k] = cc;
-        s_s[k] = ss;
+        const f32x4v pr = {cc, ss, t, __int_as_float(p | (q << 8))};
+        s_pair[k] = pr;
       }
       __syncthreads();
-      // rows p, q of G: (J^T G)
-      for (int e = tid; e < half * d; e += kFormThreads) {
-        const int k = e / d, j = e % d;
-        const int p = s_p[k], q = s_q[k];
-        const float cc = s_c[k], ss = s_s[k];
-        const float gp = G[p * ld + j], gq = G[q * ld + j];
-        G[p * ld + j] = cc * gp - ss * gq;
-        G[q * ld + j] = ss * gp + cc * gq;
-      }
-      __syncthreads();
-      // columns p, q of G and of V: (. J)
-      for (int e = tid; e < half * d; e += kFormThreads) {
-        const int k = e / d, i = e % d;
-        const int p = s_p[k], q = s_q[k];
-        const float cc = s_c[k], ss = s_s[k];
-        const float gp = G[i * ld + p], gq = G[i * ld + q];
-        G[i * ld + p] = cc * gp - ss * gq;
-        G[i * ld + q] = ss * gp + cc * gq;
-        const float vp = V[i * ld + p], vq = V[i * ld + q];
-        V[i * ld + p] = cc * vp - ss * vq;
-        V[i * ld + q] = ss * vp + cc * vq;
+      // G <- J^T G J in one pass: the pairs partition the indices, so each
+      // 2x2 block (rows of pair k, columns of pair k2) is owned by one thread
+      // (G, then V: a thread issues all its loads before its stores; the
+      // blocks and the V column pairs are disjoint, so no store is read again)
+      {
+        constexpr int kG = (kFormMaxDim / 2) * (kFormMaxDim / 2) / kFormThreads;
+        constexpr int kGb = kG / 2;                // G blocks in two batches (register budget)
+#pragma unroll
+        for (int u0 = 0; u0 < kG; u0 += kGb) {
+          float g[kGb][4];
+          f32x4v rr[kGb], rc[kGb];
+#pragma unroll
+          for (int u = 0; u < kGb; ++u) {
+            const int e = tid + (u0 + u) * kFormThreads;
+            if (e < half * half) {
+              const int k = e / half, k2 = e - k * half;
+              rr[u] = s_pair[k];
+              rc[u] = s_pair[k2];
+              const int p = __float_as_int(rr[u].w) & 0xff, q = __float_as_int(rr[u].w) >> 8;
+              const int p2 = __float_as_int(rc[u].w) & 0xff, q2 = __float_as_int(rc[u].w) >> 8;
+              g[u][0] = G[p * ld + p2];
+              g[u][1] = G[p * ld + q2];
+              g[u][2] = G[q * ld + p2];
+              g[u][3] = G[q * ld + q2];
+            }
+          }
+#pragma unroll
+          for (int u = 0; u < kGb; ++u) {
+            const int e = tid + (u0 + u) * kFormThreads;
+            if (e < half * half) {
+              const f32x4v r = rr[u], r2 = rc[u];
+              const int p = __float_as_int(r.w) & 0xff, q = __float_as_int(r.w) >> 8;
+              const int p2 = __float_as_int(r2.w) & 0xff, q2 = __float_as_int(r2.w) >> 8;
+              if (p == p2) {
+                // the pivot block: exact diagonal update, off-diagonal zeroed
+                const float apq = g[u][1];
+                G[p * ld + p] = g[u][0] - r.z * apq;
+                G[q * ld + q] = g[u][3] + r.z * apq;
+                G[p * ld + q] = 0.f;
+                G[q * ld + p] = 0.f;
+              } else {
+                const float a1 = r.x * g[u][0] - r.y * g[u][2], e1 = r.y * g[u][0] + r.x * g[u][2];
+                const float b1 = r.x * g[u][1] - r.y * g[u][3], f1 = r.y * g[u][1] + r.x * g[u][3];
+                G[p * ld + p2] = r2.x * a1 - r2.y * b1;
+                G[p * ld + q2] = r2.y * a1 + r2.x * b1;
+                G[q * ld + p2] = r2.x * e1 - r2.y * f1;
+                G[q * ld + q2] = r2.y * e1 + r2.x * f1;
+              }
+            }
+          }
+        }
+        constexpr int kV = (kFormMaxDim / 2) * kFormMaxDim / kFormThreads;
+        constexpr int kVb = kV / 2;                // V in two batches (register budget)
+#pragma unroll
+        for (int u0 = 0; u0 < kV; u0 += kVb) {
+          float v[kVb][2];
+          float vc[kVb], vs[kVb];
+          int vp[kVb], vq[kVb];
+#pragma unroll
+          for (int u = 0; u < kVb; ++u) {
+            const int e = tid + (u0 + u) * kFormThreads;
+            if (e < half * d) {
+              const int k = e / d, i = e - k * d;
+              const f32x4v r = s_pair[k];
+              vc[u] = r.x;
+              vs[u] = r.y;
+              vp[u] = i * ld + (__float_as_int(r.w) & 0xff);
+              vq[u] = i * ld + (__float_as_int(r.w) >> 8);
+              v[u][0] = V[vp[u]];
+              v[u][1] = V[vq[u]];
+            }
+          }
+#pragma unroll
+          for (int u = 0; u < kVb; ++u) {
+            const int e = tid + (u0 + u) * kFormThreads;
+            if (e < half * d) {
+              V[vp[u]] = vc[u] * v[u][0] - vs[u] * v[u][1];
+              V[vq[u]] = vs[u] * v[u][0] + vc[u] * v[u][1];
+            }
+          }
+        }
       }
       __syncthreads();
     }
@@ -212,7 +283,7 @@ __global__ __launch_bounds__(kFormThreads) void form_patch_kernel(const FormPara
     for (int e = tid; e < kFormTile * vec_per_row; e += kFormThreads) {
       const int r = e / vec_per_row, v4 = e % vec_per_row;
       f32x4v x = {0.f, 0.f, 0.f, 0.f};
-      if (t0 + r < n) x = *reinterpret_cast<const f32x4v*>(delta + (int64_t)(t0 + r) * P.delta_s[3] + 4 * v4);
+      if (t0 + r < n) x = load_delta4(P, delta, t0 + r, v4);
       *reinterpret_cast<f32x4v*>(T + r * d + 4 * v4) = x;
     }
     __syncthreads();
@@ -238,12 +309,16 @@ size_t form_lds_bytes(int dim, int m) {
 
 hipError_t launch_form_patch(const FormParams& p, hipStream_t s) {
   const size_t lds = form_lds_bytes(p.dim, p.m);
-  static bool attr_set = false;                      // idempotent: a race only repeats the call
-  if (!attr_set) {
-    const hipError_t e = hipFuncSetAttribute((const void*)form_patch_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                             (int)form_lds_bytes(kFormMaxDim, kFormMaxDim));
+  // the LDS limit is raised once per device (a race only repeats the call)
+  static bool attr_set[64] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= 64 || !attr_set[dev]) {
+    e = hipFuncSetAttribute((const void*)form_patch_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)form_lds_bytes(kFormMaxDim, kFormMaxDim));
     if (e != hipSuccess) return e;
-    attr_set = true;
+    if (dev >= 0 && dev < 64) attr_set[dev] = true;
   }
   hipLaunchKernelGGL(form_patch_kernel, dim3((uint32_t)p.n_units), dim3(kFormThreads), lds, s, p);
   return hipGetLastError();

@@ -405,7 +405,9 @@ def form_args():
 @pytest.mark.parametrize("case,code", [
     ("ok", km.OK), ("dim_not_4", km.ERR_UNSUPPORTED), ("dim_big", km.ERR_RANGE), ("m_zero", km.ERR_RANGE),
     ("m_big", km.ERR_RANGE), ("null", km.ERR_NULL), ("unaligned", km.ERR_ALIGN), ("stride", km.ERR_ALIGN),
-    ("sweeps", km.ERR_SHAPE), ("negative", km.ERR_SHAPE),
+    ("sweeps", km.ERR_SHAPE), ("negative", km.ERR_SHAPE), ("orbit_negative", km.ERR_SHAPE),
+    ("orbit_stride", km.ERR_ALIGN), ("orbit_ok", km.OK), ("u_over_delta", km.ERR_ALIAS),
+    ("w_over_orbit", km.ERR_ALIAS), ("sigma_over_delta", km.ERR_ALIAS), ("sigma_apart", km.OK),
 ])
 def test_form_patch_validation(case, code):
     a = form_args()
@@ -427,6 +429,22 @@ def test_form_patch_validation(case, code):
         a.sweeps = -1
     elif case == "negative":
         a.n_tokens = -5
+    elif case == "orbit_negative":
+        a.n_orbit = -1
+    elif case == "orbit_stride":
+        a.n_orbit, a.orbit_stride = 3, 2 * 3 * 4 * 100 * 128 + 2
+    elif case == "orbit_ok":
+        a.n_orbit, a.orbit_stride = 3, 2 * 3 * 4 * 100 * 128
+    elif case == "u_over_delta":
+        a.U = FAKE + 4 * 1000
+    elif case == "w_over_orbit":
+        # W sits in the second orbit member's deficit
+        a.n_orbit, a.orbit_stride = 2, 2 * 3 * 4 * 100 * 128
+        a.W = FAKE + 4 * (2 * 3 * 4 * 100 * 128 + 64)
+    elif case == "sigma_over_delta":
+        a.sigma = FAKE + 4 * 128
+    elif case == "sigma_apart":
+        a.sigma = FAKE + (3 << 36)
     assert km.lib().kamera_validate(4, ctypes.byref(a)) == code, km.last_error()
     if code != km.OK:
         assert km.lib().kamera_form_patch(ctypes.byref(a), None) == code

@@ -390,3 +390,41 @@ def test_form_patch_matches_svd(device, n, d, m):
         opt = np.linalg.norm(Dl - prod_ref)
         got = np.linalg.norm(Dl - Ug @ Wg)
         assert got <= opt + 2.0 ** -6 * np.linalg.norm(prod_ref), (idx, got, opt)
+
+
+@pytest.mark.parametrize("K,n,d,m", [(3, 200, 128, 16), (6, 64, 64, 8), (1, 90, 128, 32)])
+def test_orbit_patch_matches_reference(device, K, n, d, m):
+    """Orbit patch (Sec. 5, reorder): the K orderings' deficits share a
+    rank-m core with a gap; the GPU's patch must match the fp64 truncation of
+    the orbit mean, and a one-member orbit must give the plain call's bits."""
+    import paper_2606_23581_amd as km
+    import torch
+
+    print(f"[case] orbit_patch K{K} n{n} d{d} m{m}", flush=True)
+    rng = np.random.default_rng(K * 100 + m)
+    C, L, H = 2, 1, 3
+    deltas = np.empty((K, C, L, H, n, d), np.float32)
+    for idx in np.ndindex(C, L, H):
+        A = np.linalg.qr(rng.standard_normal((n, m)))[0]
+        B = np.linalg.qr(rng.standard_normal((d, m)))[0]
+        core = (A * np.linspace(10.0, 3.0, m)) @ B.T
+        for k in range(K):
+            deltas[(k,) + idx] = core + 0.05 * rng.standard_normal((n, d))
+    dt = torch.from_numpy(deltas).to(device)
+    U = torch.zeros((C, L, H, n, m), dtype=torch.bfloat16, device=device)
+    W = torch.zeros((C, L, H, m, d), dtype=torch.bfloat16, device=device)
+    km.form_patch(dt, U, W)
+    torch.cuda.synchronize()
+    Ub, Wb = bits(U), bits(W)
+    for idx in np.ndindex(C, L, H):
+        Ur, Wr, _ = ref.orbit_patch(deltas[(slice(None),) + idx].astype(np.float64), m)
+        prod_ref = Ur @ Wr
+        got = ref.bf16_to_f64(Ub[idx]) @ ref.bf16_to_f64(Wb[idx])
+        rel = np.linalg.norm(got - prod_ref) / np.linalg.norm(prod_ref)
+        assert rel <= 2.0 ** -6, (idx, rel)
+    if K == 1:
+        U2 = torch.zeros_like(U)
+        W2 = torch.zeros_like(W)
+        km.form_patch(dt[0], U2, W2)
+        torch.cuda.synchronize()
+        assert np.array_equal(bits(U2), Ub) and np.array_equal(bits(W2), Wb)
