@@ -116,6 +116,141 @@ def cpu_baseline(pool, n_workers, p, budget_s: float = 12.0):
                       f"chunks/s equivalent {gbps * 1e9 / p.bytes_per_step * w.n_chunks:.3g}"}
 
 
+# ---------------------------------------------------------------------------
+# compile-side patch forming (--op form_patch)
+# ---------------------------------------------------------------------------
+
+FP32_VECTOR_PEAK_TFLOPS = 157.3
+
+
+def _oracle_form(job):
+    import oracle as ref
+
+    delta, m = job
+    ref.form_patch(delta, m)
+    return 1
+
+
+def form_jacobi_flops(d: int, sweeps: int) -> int:
+    """Flops of ``sweeps`` cyclic Jacobi sweeps as the kernel performs them:
+    d - 1 steps per sweep, each rotating half*(half-1) off-pivot 2x2 blocks of
+    G (8 outputs of one multiply and one fused multiply-add: 24 flops) and
+    half*d row pairs of V (6 flops), plus the convergence sum (2 d^2)."""
+    half = d // 2
+    per_step = 24 * half * (half - 1) + 6 * half * d
+    return sweeps * ((d - 1) * per_step + 2 * d * d)
+
+
+def bench_form(args, pool, n_workers):
+    """One step = forming the K and the V patches of every (chunk, layer, head)
+    unit of the workload from fp32 deficits (one launch per plane)."""
+    import numpy as np
+    import torch
+
+    import paper_2606_23581_amd as km
+    from synth import WORKLOADS
+
+    w = WORKLOADS[args.workload]
+    if w.kind != "rehydrate" or w.head_dim > 128 or w.m_k == 0:
+        raise SystemExit(f"--op form_patch needs a GQA/MHA rehydrate workload with head_dim <= 128 ({w.name})")
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    C, L, H, n, d = w.n_chunks, w.n_layers, w.n_heads, w.n_tokens, w.head_dim
+    planes = [("k", w.m_k)] + ([("v", w.m_v)] if w.has_v and w.m_v else [])
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(w.seed + 7)
+    # deficits: Gaussian token coefficients on a decaying spectrum
+    # sigma_k = (1 + k)^(-1/4) in a random orthonormal basis, so that about
+    # 90% of the energy sits in the top ~80% of the components
+    sig = (1.0 + torch.arange(d, device=dev, dtype=torch.float32)) ** -0.25
+    tensors = {}
+    for name, m in planes:
+        q, _ = torch.linalg.qr(torch.randn((d, d), generator=gen, device=dev, dtype=torch.float32))
+        D = torch.empty((C, L, H, n, d), dtype=torch.float32, device=dev)
+        for c in range(C):
+            a = torch.randn((L, H, n, d), generator=gen, device=dev, dtype=torch.float32)
+            torch.matmul(a * sig, q.contiguous(), out=D[c])
+            del a
+        U = torch.empty((C, L, H, n, m), dtype=torch.bfloat16, device=dev)
+        W = torch.empty((C, L, H, m, d), dtype=torch.bfloat16, device=dev)
+        done = torch.zeros((C, L, H), dtype=torch.int32, device=dev)
+        tensors[name] = (D, U, W, done, km.prepare_form_patch(D, U, W, sweeps_done=done))
+    stream = torch.cuda.current_stream()
+
+    def step():
+        for name, _m in planes:
+            tensors[name][4].launch(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        starts[k].record(stream)
+        step()
+        ends[k].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    gpu_ms = sum(s.elapsed_time(e) for s, e in zip(starts, ends)) / args.steps
+    ms_per_step = wall * 1e3 / args.steps
+    units = C * L * H * len(planes)
+    flops = 0
+    sweeps_hist = []
+    for name, m in planes:
+        done = tensors[name][3].cpu().numpy()
+        sweeps_hist.append(done)
+        flops += 2 * n * d * d * C * L * H + 2 * n * d * m * C * L * H
+        flops += sum(form_jacobi_flops(d, int(s)) * int(cnt) for s, cnt in zip(*np.unique(done, return_counts=True)))
+    sw = np.concatenate([h.ravel() for h in sweeps_hist])
+    achieved = flops / (gpu_ms * 1e-3) / 1e12
+
+    cpu = None
+    if pool is not None:
+        D = tensors["k"][0]
+        jobs = [(D[0, 0, h].double().cpu().numpy(), w.m_k) for h in range(H)]
+        pool.map(_oracle_form, jobs, chunksize=1)      # untimed: the workers load LAPACK
+        done_n, t1 = 0, time.perf_counter()
+        while True:
+            pool.map(_oracle_form, jobs, chunksize=1)
+            done_n += len(jobs)
+            if time.perf_counter() - t1 >= args.cpu_seconds / 2:
+                break
+        dt = time.perf_counter() - t1
+        cpu = {"value": round(done_n / dt, 2), "unit": "units/s", "cores": n_workers, "kind": "oracle",
+               "sample": f"{done_n} units ({len(jobs)} distinct: chunk 0, layer 0, all heads of the K plane; "
+                         f"numpy fp64 SVD of each {n}x{d} deficit), {dt:.1f} s on {n_workers} "
+                         f"single-threaded worker processes"}
+        pool.close()
+        pool.join()
+
+    line = {
+        "metric": "patch-forming units/s (top-m truncated SVD of each deficit, compile step)",
+        "value": round(units / (ms_per_step * 1e-3), 1),
+        "unit": "units/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic fp32 deficits: N(0,1) coefficients on the spectrum (1+k)^-1/4 in a random basis",
+        "config": {"workload": f"form_patch on {w.name}", "n_chunks": C, "n_layers": L, "kv_heads": H,
+                   "tokens_per_chunk": n, "dim": d, "planes": [p for p, _ in planes],
+                   "rank": {p: m for p, m in planes}},
+        "sweeps_run": {"min": int(sw.min()), "mean": round(float(sw.mean()), 2), "max": int(sw.max())},
+        "roofline": {"bound": "alu", "achieved": round(achieved, 3), "peak": FP32_VECTOR_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(achieved / FP32_VECTOR_PEAK_TFLOPS, 4), "traffic": None,
+                     "kernel": "form_patch_kernel", "kernel_ms": round(gpu_ms / len(planes), 4),
+                     "flops_per_step": int(flops)},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
 def measured_traffic(name: str, bytes_per_launch: int):
     """HBM traffic per launch from the committed rocprofv3 counter summary, if it
     was taken on the current kernel source (else null)."""
@@ -137,6 +272,8 @@ def main():
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--op", choices=("rehydrate", "form_patch"), default="rehydrate",
+                    help="rehydrate: the serve-time hot path (default); form_patch: the compile step")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print(json.dumps({"error": "this operator benchmark runs on exactly one GPU; the work shards by "
@@ -149,6 +286,10 @@ def main():
     pool = None
     if not args.no_cpu_baseline:
         pool = mp.get_context("fork").Pool(n_workers, initializer=_worker_init)
+
+    if args.op == "form_patch":
+        bench_form(args, pool, n_workers)
+        return
 
     import torch
 

@@ -12,11 +12,17 @@
  *
  *   kamera_rehydrate     K' = R(pos) (K + U_k W_k),  V' = V + U_v W_v,
  *                        into a dense buffer or straight into a paged KV pool;
+ *                        with a per-chunk delta it relocates already-rotated
+ *                        keys and adds a (removal) patch (Sec. 5, Table evict);
  *   kamera_shift         K' = R(delta) K, in place, for keys that are already
  *                        rotated (R(delta) R(p) = R(p + delta), Sec. 1 and 3:
  *                        reorder, sliding-window survivors, Sec. 5);
  *   kamera_scatter_paged a bit copy of dense token rows into the pool slots a
- *                        page table names (the clean-view overwrite, App. E).
+ *                        page table names (the clean-view overwrite, App. E),
+ *   kamera_gather_paged  and the copy back from the pool into dense rows;
+ *   kamera_form_patch    the compile step's truncated SVD of given deficits
+ *                        (App. A), also as one orbit patch over orderings
+ *                        (Sec. 5, reorder).
  *
  * Conventions shared by every entry point
  *   - Every tensor pointer is a DEVICE pointer owned by the caller.  The
@@ -295,6 +301,8 @@ typedef struct {
   float* sigma;
   int64_t sigma_stride[3];
   int64_t orbit_stride;        /* elements between orbit members of delta       */
+  int32_t* sweeps_done;        /* optional: Jacobi sweeps each unit ran, dense
+                                  [n_chunks][n_layers][n_heads] int32          */
 } kamera_form_args;
 
 int kamera_rehydrate(const kamera_rehydrate_args* args, void* stream);
@@ -313,10 +321,9 @@ int kamera_check_page_table(const int32_t* host_page_table, int32_t n_chunks,
 
 /* Run exactly the host-side checks of an entry point (0 kamera_rehydrate,
  * 1 kamera_shift, 2 kamera_scatter_paged, 3 kamera_gather_paged,
- * 4 kamera_form_patch) on `args` without launching
- * anything (3 = kamera_gather_paged): KAMERA_OK when the call would be
- * enqueued, else the error code
- * the call would return.  Touches no device memory. */
+ * 4 kamera_form_patch) on `args` without launching anything: KAMERA_OK when
+ * the call would be enqueued, else the error code the call would return.
+ * Touches no device memory. */
 int kamera_validate(int32_t which, const void* args);
 
 /* Text of the last error on the calling thread ("" after a successful call);

@@ -112,7 +112,7 @@ class CFormArgs(ctypes.Structure):
                 ("dim", _i32), ("m", _i32), ("sweeps", _i32), ("n_orbit", _i32),
                 ("delta", _vp), ("delta_stride", _i64 * 4), ("U", _vp), ("u_stride", _i64 * 4),
                 ("W", _vp), ("w_stride", _i64 * 4), ("sigma", _vp), ("sigma_stride", _i64 * 3),
-                ("orbit_stride", _i64)]
+                ("orbit_stride", _i64), ("sweeps_done", _vp)]
 
 
 EXPORTS = ("kamera_rehydrate", "kamera_shift", "kamera_scatter_paged", "kamera_gather_paged",
@@ -465,14 +465,15 @@ def form_patch(*a, stream=None, **kw) -> None:
     prepare_form_patch(*a, **kw).launch(stream)
 
 
-def prepare_form_patch(delta, U, W, *, sigma=None, sweeps: int = 0) -> Prepared:
+def prepare_form_patch(delta, U, W, *, sigma=None, sweeps: int = 0, sweeps_done=None) -> Prepared:
     """Top-m truncated SVD of every deficit (App. A compile step).
 
     delta: fp32 [C, L, H, n, d], or [K, C, L, H, n, d] for an orbit patch
     (Sec. 5, reorder: the K orderings' deficits are averaged first);
     U: bf16 [C, L, H, n, m] (receives U S); W: bf16 [C, L, H, m, d]
     (receives Vt[:m]); sigma: optional fp32 [C, L, H, m] (receives S[:m]).
-    m is U's last dimension.
+    m is U's last dimension.  sweeps_done: optional int32 [C, L, H]
+    (contiguous), receives the Jacobi sweeps each unit ran.
     """
     import torch
 
@@ -512,7 +513,12 @@ def prepare_form_patch(delta, U, W, *, sigma=None, sweeps: int = 0) -> Prepared:
         a.sigma = _ptr(sigma)
         for i, st in enumerate(_strides(sigma, 3)):
             a.sigma_stride[i] = st
-    return Prepared(L.kamera_form_patch, a, (delta, U, W, sigma))
+    if sweeps_done is not None:
+        if (sweeps_done.dtype != torch.int32 or tuple(sweeps_done.shape) != (C, Ln, H)
+                or not sweeps_done.is_contiguous()):
+            raise ValueError("sweeps_done must be a contiguous int32 [C, L, H] tensor")
+        a.sweeps_done = _ptr(sweeps_done)
+    return Prepared(L.kamera_form_patch, a, (delta, U, W, sigma, sweeps_done))
 
 
 def check_page_table(page_table_host, n_tokens: int, page_size: int, n_pool_pages: int) -> None:

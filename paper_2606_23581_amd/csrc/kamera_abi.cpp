@@ -585,12 +585,18 @@ static int build_form(const kamera_form_args* a, kamera::FormParams& P, bool& la
       span(a->sigma, a->sigma_stride, ext_s, 3, a->m, 4, s0, s1);
       if (overlap(s0, s1, d0, d1)) return fail(KAMERA_ERR_ALIAS, "%s: sigma must not overlap the deficits", who);
     }
+    if (a->sweeps_done != nullptr) {
+      const uintptr_t c0 = reinterpret_cast<uintptr_t>(a->sweeps_done);
+      if (overlap(c0, c0 + 4 * (uintptr_t)units, d0, d1))
+        return fail(KAMERA_ERR_ALIAS, "%s: sweeps_done must not overlap the deficits", who);
+    }
   }
   memset(&P, 0, sizeof(P));
   P.delta = a->delta;
   P.U = static_cast<uint16_t*>(a->U);
   P.W = static_cast<uint16_t*>(a->W);
   P.sigma = a->sigma;
+  P.sweeps_done = a->sweeps_done;
   memcpy(P.delta_s, a->delta_stride, sizeof(P.delta_s));
   memcpy(P.u_s, a->u_stride, sizeof(P.u_s));
   memcpy(P.w_s, a->w_stride, sizeof(P.w_s));

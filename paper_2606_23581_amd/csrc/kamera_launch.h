@@ -124,6 +124,7 @@ struct FormParams {
   uint16_t* U;
   uint16_t* W;
   float* sigma;
+  int32_t* sweeps_done;             // optional, dense per unit
   int64_t delta_s[4];
   int64_t u_s[4];
   int64_t w_s[4];

@@ -128,6 +128,7 @@ __global__ __launch_bounds__(kFormThreads) void form_patch_kernel(const FormPara
 
   // ---- 2. cyclic Jacobi, round-robin pair ordering ----
   const int half = d / 2;
+  int sweeps_run = 0;
   for (int sweep = 0; sweep < P.sweeps; ++sweep) {
     // stop once the off-diagonal mass is negligible against the diagonal
     float off = 0.f, dia = 0.f;
@@ -139,6 +140,7 @@ __global__ __launch_bounds__(kFormThreads) void form_patch_kernel(const FormPara
     off = block_sum(off, s_red);
     dia = block_sum(dia, s_red);
     if (off <= 1e-9f * dia) break;             // ~(d * 4 eps)^2: the fp32 floor
+    ++sweeps_run;
     for (int step = 0; step < d - 1; ++step) {
       if (tid < half) {
         // circle method: position 0 fixed, positions 1..d-1 rotate by `step`
@@ -244,6 +246,8 @@ __global__ __launch_bounds__(kFormThreads) void form_patch_kernel(const FormPara
       __syncthreads();
     }
   }
+
+  if (P.sweeps_done != nullptr && tid == 0) P.sweeps_done[unit] = sweeps_run;
 
   // ---- 3. the m largest eigenvalues (ties by index) ----
   if (tid < d) {

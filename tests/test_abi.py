@@ -408,6 +408,7 @@ def form_args():
     ("sweeps", km.ERR_SHAPE), ("negative", km.ERR_SHAPE), ("orbit_negative", km.ERR_SHAPE),
     ("orbit_stride", km.ERR_ALIGN), ("orbit_ok", km.OK), ("u_over_delta", km.ERR_ALIAS),
     ("w_over_orbit", km.ERR_ALIAS), ("sigma_over_delta", km.ERR_ALIAS), ("sigma_apart", km.OK),
+    ("done_over_delta", km.ERR_ALIAS),
 ])
 def test_form_patch_validation(case, code):
     a = form_args()
@@ -445,6 +446,8 @@ def test_form_patch_validation(case, code):
         a.sigma = FAKE + 4 * 128
     elif case == "sigma_apart":
         a.sigma = FAKE + (3 << 36)
+    elif case == "done_over_delta":
+        a.sweeps_done = FAKE + 4 * 256
     assert km.lib().kamera_validate(4, ctypes.byref(a)) == code, km.last_error()
     if code != km.OK:
         assert km.lib().kamera_form_patch(ctypes.byref(a), None) == code

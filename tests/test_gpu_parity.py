@@ -375,8 +375,15 @@ def test_form_patch_matches_svd(device, n, d, m):
     U = torch.zeros((C, L, H, n, m), dtype=torch.bfloat16, device=device)
     W = torch.zeros((C, L, H, m, d), dtype=torch.bfloat16, device=device)
     sigma = torch.zeros((C, L, H, m), dtype=torch.float32, device=device)
-    km.form_patch(dt, U, W, sigma=sigma)
+    done = torch.full((C, L, H), -1, dtype=torch.int32, device=device)
+    km.form_patch(dt, U, W, sigma=sigma, sweeps_done=done)
     torch.cuda.synchronize()
+    # converged within the default limit of 12 sweeps, after at least one
+    assert ((done >= 1) & (done < 12)).all(), done.cpu().numpy()
+    capped = torch.full_like(done, -1)
+    km.form_patch(dt, torch.empty_like(U), torch.empty_like(W), sweeps=1, sweeps_done=capped)
+    torch.cuda.synchronize()
+    assert (capped == 1).all()
     Ub, Wb, sg = bits(U), bits(W), sigma.cpu().numpy()
     for idx in np.ndindex(C, L, H):
         Dl = delta[idx].astype(np.float64)
