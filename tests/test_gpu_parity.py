@@ -63,6 +63,8 @@ REHYDRATE_CASES = {
                                                 theta=1e4, patch=(0, 512), m_k=32, m_pe=8, has_v=False,
                                                 reloc=True, paged=True, n=40, seed=26),
     # deep-half patch: no factors on the shallow layers, odd ranks on others
+    "max_row_4096": RehydrateCase(D=4096, H=1, C=1, L=2, n=20, rope_dim=128, rope_offset=2048, m_k=8, m_v=8,
+                                  patch=(0, 4096), seed=29),
     "layer_rank_deep_half": RehydrateCase(L=4, layer_rank=(0, 0, 16, 16), m_k=16, m_v=16, seed=27),
     "layer_rank_odd": RehydrateCase(L=3, layer_rank=(5, 64, 33), m_k=64, m_v=48, seed=28),
 }
@@ -98,6 +100,71 @@ def test_rehydrate_identity_is_bit_exact(device):
             for i in range(n):
                 s = ref.paged_slot(pt[c], i, P)
                 assert np.array_equal(out[:, s], K[c, :, i]), (pairing, c, i)
+
+
+@pytest.mark.parametrize("mla", [False, True])
+def test_rehydrate_exactly_in_place(device, mla):
+    """Keys and values rebuilt in their own storage (same base and strides):
+    ragged chunks, the tokens past each chunk's count keep their bits; for MLA
+    the latent and the rope band are two planes in place on one tensor."""
+    import paper_2606_23581_amd as km
+    import torch
+
+    print(f"[case] rehydrate in place mla={mla}", flush=True)
+    rng = np.random.default_rng(31 + mla)
+    C, L, n = 3, 2, 70
+    H, D = (1, 576) if mla else (2, 128)
+    K = synth.randn_bf16_numpy((C, L, n, H, D), 1.0, rng)
+    V = None if mla else synth.randn_bf16_numpy((C, L, n, H, D), 1.0, rng)
+    pd = 512 if mla else D
+    m = 16
+    Uk = synth.randn_bf16_numpy((C, L, H, n, m), 0.1, rng)
+    Wk = synth.randn_bf16_numpy((C, L, H, m, pd), 0.1, rng)
+    n_c = np.array([n, 33, 0], dtype=np.int32)
+    p0 = rng.integers(0, 30000, size=C)
+    pos = np.repeat(p0[:, None], 3, axis=1).astype(np.int32)
+    if mla:
+        rs = km.RopeSpec(theta=1e4, rope_dim=64, rope_offset=512, pairing="interleaved")
+    else:
+        rs = km.RopeSpec(theta=1e6, rope_dim=128)
+    kt = dev(K, device)
+    kw = dict(rope=rs, chunk_pos=dev_i32(pos, device), chunk_tokens=dev_i32(n_c, device),
+              u_k=dev(Uk, device), w_k=dev(Wk, device), k_patch=(0, pd))
+    if mla:
+        Upe = synth.randn_bf16_numpy((C, L, H, n, 8), 0.1, rng)
+        Wpe = synth.randn_bf16_numpy((C, L, H, 8, 64), 0.1, rng)
+        kw.update(u_pe=dev(Upe, device), w_pe=dev(Wpe, device))
+        km.rehydrate(kt, kt, **kw)
+    else:
+        Uv = synth.randn_bf16_numpy((C, L, H, n, m), 0.1, rng)
+        Wv = synth.randn_bf16_numpy((C, L, H, m, D), 0.1, rng)
+        vt = dev(V, device)
+        km.rehydrate(kt, kt, v_in=vt, v_out=vt, u_v=dev(Uv, device), w_v=dev(Wv, device), v_patch=(0, D), **kw)
+    torch.cuda.synchronize()
+    kb = bits(kt)
+    vb = None if mla else bits(vt)
+    orope = oracle_rope(rs)
+    for c in range(C):
+        nc = int(n_c[c])
+        assert np.array_equal(kb[c, :, nc:], K[c, :, nc:]), "tokens past the chunk's count were written"
+        if not mla:
+            assert np.array_equal(vb[c, :, nc:], V[c, :, nc:])
+        p3 = ref.positions_linear(int(p0[c]), nc)
+        for l in range(L):
+            for h in range(H):
+                u = ref.bf16_to_f64(Uk[c, l, h, :nc])
+                w = ref.bf16_to_f64(Wk[c, l, h])
+                if mla:
+                    wf = np.zeros((m + 8, D))
+                    wf[:m, :512] = w
+                    wf[m:, 512:] = ref.bf16_to_f64(Wpe[c, l, h])
+                    u, w = np.concatenate([u, ref.bf16_to_f64(Upe[c, l, h, :nc])], axis=1), wf
+                want = ref.rehydrate_k(ref.bf16_to_f64(K[c, l, :nc, h]), u, w, orope, p3)
+                assert_close(kb[c, l, :nc, h], want, f"in-place K c{c} l{l} h{h}")
+                if not mla:
+                    want = ref.rehydrate_v(ref.bf16_to_f64(V[c, l, :nc, h]), ref.bf16_to_f64(Uv[c, l, h, :nc]),
+                                           ref.bf16_to_f64(Wv[c, l, h]))
+                    assert_close(vb[c, l, :nc, h], want, f"in-place V c{c} l{l} h{h}")
 
 
 def test_rehydrate_empty_call_writes_nothing(device):
