@@ -43,6 +43,20 @@ def test_library_exports_every_declared_symbol():
         assert hasattr(L, name)
 
 
+def test_plain_c_consumer(tmp_path):
+    """tests/c/abi_check.c: a C program built against include/kamera.h and
+    linked to libkamera.so checks layouts, validation and the page-table check
+    with no GPU (nothing is launched)."""
+    exe = tmp_path / "abi_check"
+    lib_dir = os.path.dirname(km.LIB_PATH)
+    subprocess.run(["gcc", "-std=c99", "-Wall", "-Werror", "-I", os.path.join(ROOT, "include"),
+                    os.path.join(ROOT, "tests", "c", "abi_check.c"), "-o", str(exe), "-L", lib_dir, "-lkamera",
+                    f"-Wl,-rpath,{lib_dir}"], check=True, capture_output=True, text=True)
+    r = subprocess.run([str(exe)], capture_output=True, text=True, timeout=60)
+    assert r.returncode == 0, r.stderr
+    assert r.stdout.strip() == "ok"
+
+
 def test_version_and_struct_layout():
     L = km.lib()
     assert L.kamera_abi_version() == 1
