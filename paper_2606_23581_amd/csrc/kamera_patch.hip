@@ -2,17 +2,25 @@
 // the top-m singular triplets of each deficit Delta (n x d) as the stored
 // patch, U = Delta V_m (the singular values folded in) and W = V_m^T.
 //
-// One 1024-thread workgroup per (chunk, layer, head) unit, everything in LDS:
-//   1. Gram matrix G = Delta^T Delta (fp32), Delta streamed in 32-row tiles;
-//   2. cyclic Jacobi on G with the round-robin ordering: every step rotates
-//      d/2 disjoint (p, q) pairs at once (G <- J^T G J as independent 2x2
-//      blocks, V <- V J), sweeps until the off-diagonal mass is negligible;
-//   3. rank the eigenvalues (diag G), keep the m largest;
+// One 1024-thread workgroup per (chunk, layer, head) unit, everything in LDS
+// (d is padded to dp, a multiple of 16, with zero rows and columns):
+//   1. Gram matrix G = Delta^T Delta on fp32 MFMA (16x16x4), Delta streamed in
+//      32-row tiles with the next tile's loads in flight during the products;
+//   2. block Jacobi on G: the indices form dp/8 blocks of 8; each step pairs
+//      the blocks round-robin (circle method) into dp/16 groups of 16
+//      indices; one wave per group runs one cyclic Jacobi sweep on the
+//      group's 16x16 principal submatrix, accumulating its rotation Q; then
+//      G <- J^T G J and V <- V J with J = diag(Q_group) as 16x16 tile
+//      products on fp32 MFMA.  Sweeps stop once the off-diagonal mass is
+//      negligible against the diagonal;
+//   3. rank the eigenvalues (diag G) of the real indices, keep the m largest;
 //   4. W[k] = V[:, order[k]]^T and U = Delta V_m, rounded to bf16.
 // With an orbit (Sec. 5, reorder) Delta is the mean of the members' deficits,
 // formed on the fly wherever a Delta tile is staged.
 // The eigenvalues of G are the squared singular values of Delta and its
 // eigenvectors the right singular vectors, so U W is the rank-m truncation.
+// Padded indices keep zero rows and columns: every rotation that touches
+// one is the identity, so they never mix with the real spectrum.
 
 #include <hip/hip_runtime.h>
 #include <math.h>
@@ -28,7 +36,34 @@ namespace {
 typedef float f32x4v __attribute__((ext_vector_type(4)));
 
 constexpr int kFormThreads = 1024;
-constexpr int kFormTile = 32;          // Delta rows per staged tile
+constexpr int kWaves = kFormThreads / 64;
+constexpr int kFormTile = 128;         // Delta rows per staged tile
+constexpr int kStageVecs = kFormTile * (kFormMaxDim / 4) / kFormThreads;   // 4-float vectors per thread
+constexpr int kBlk = 8;                // block-Jacobi block width
+constexpr int kGrp = 2 * kBlk;         // indices of one rotated group (two blocks)
+constexpr int kLdQ = kGrp + 1;         // padded row stride of a group's 16x16 scratch
+
+__host__ __device__ inline int pad16(int d) { return (d + 15) & ~15; }
+// staged Delta tile row stride: == 16 (mod 32), so the four rows one MFMA
+// operand load touches fall on disjoint banks
+__host__ __device__ inline int tile_ld(int dp) { return (dp % 32 == 16) ? dp : dp + 16; }
+
+// circle method over `n` items at `step`: the (smaller, larger) members of pair k
+__device__ __forceinline__ void circle_pair(int n, int step, int k, int& a, int& b) {
+  const int pa = k == 0 ? 0 : 1 + (k - 1 + step) % (n - 1);
+  const int pb = 1 + (n - 2 - k + step) % (n - 1);
+  a = pa < pb ? pa : pb;
+  b = pa < pb ? pb : pa;
+}
+
+// global index of local index r (0..15) of the group made of blocks (bi, bj)
+__device__ __forceinline__ int group_index(int bi, int bj, int r) {
+  return r < kBlk ? kBlk * bi + r : kBlk * bj + (r - kBlk);
+}
+
+__device__ __forceinline__ f32x4v mfma4(float a, float b, f32x4v c) {
+  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
 
 __device__ __forceinline__ uint16_t to_bf16_rne(float x) {
   typedef float f32x2 __attribute__((ext_vector_type(2)));
@@ -62,14 +97,99 @@ __device__ __forceinline__ f32x4v load_delta4(const FormParams& P, const float* 
   return x;
 }
 
+// The workgroup's dynamic LDS (one unit's working set).
+extern __shared__ __align__(16) float form_lds[];
+
+// Rotation (c, s) = (cos, sin) and t = tan that zero a[p][q] of the 2x2
+// symmetric block [[app, apq], [apq, aqq]]: t is the smaller root of
+// t^2 + 2 theta t - 1 = 0 with theta = (aqq - app) / (2 apq); no rotation
+// when apq is negligible.  Hardware reciprocal and (reciprocal) square root:
+// c^2 + s^2 = 1 to a few ulp, which is all the iteration needs.  Branch free.
+__device__ __forceinline__ void rotation(float app, float aqq, float apq, float& c, float& s, float& t) {
+  const bool act = fabsf(apq) > 1e-30f;
+  const float theta = (aqq - app) * __builtin_amdgcn_rcpf(2.f * (act ? apq : 1.f));
+  const float tt = (theta >= 0.f ? 1.f : -1.f) *
+                   __builtin_amdgcn_rcpf(fabsf(theta) + __builtin_amdgcn_sqrtf(fmaf(theta, theta, 1.f)));
+  t = act ? tt : 0.f;
+  c = __builtin_amdgcn_rsqf(fmaf(t, t, 1.f));
+  s = t * c;
+}
+
+// One cyclic Jacobi sweep, by one wave, on a group's 16x16 symmetric matrix S
+// (at form_lds + so, row stride kLdQ); Q (at form_lds + qo, identity on entry)
+// accumulates the rotations, so that on exit S = Q^T S_in Q.  Lane (kr, kc) =
+// (lane / 8, lane % 8) owns the 2x2 block of S on the rows of pair kr and the
+// columns of pair kc, and rows kr and kr + 8 of Q on the columns of pair kc;
+// it derives both pairs' rotations itself from the values it reads, so a
+// step is one round of reads followed by one round of writes.  The wave's LDS
+// accesses are performed in program order, so no barrier is needed.
+__device__ __forceinline__ void group_sweep(int so, int qo, int lane) {
+  const int kr = lane >> 3, kc = lane & 7;
+  // circle positions of both pairs at step 0; every step moves positions
+  // 1..15 on by one (position 0 stays)
+  int ra = kr == 0 ? 0 : kr, rb = 15 - kr;
+  int ca = kc == 0 ? 0 : kc, cb = 15 - kc;
+  for (int st = 0; st < kGrp - 1; ++st) {
+    const int p = min(ra, rb), q = max(ra, rb), p2 = min(ca, cb), q2 = max(ca, cb);
+    const float rpp = form_lds[so + p * kLdQ + p], rqq = form_lds[so + q * kLdQ + q];
+    const float rpq = form_lds[so + p * kLdQ + q];
+    const float cpp = form_lds[so + p2 * kLdQ + p2], cqq = form_lds[so + q2 * kLdQ + q2];
+    const float cpq = form_lds[so + p2 * kLdQ + q2];
+    const float a0 = form_lds[so + p * kLdQ + p2], b0 = form_lds[so + p * kLdQ + q2];
+    const float e0 = form_lds[so + q * kLdQ + p2], f0 = form_lds[so + q * kLdQ + q2];
+    const float qp0 = form_lds[qo + kr * kLdQ + p2], qq0 = form_lds[qo + kr * kLdQ + q2];
+    const float qp1 = form_lds[qo + (kr + 8) * kLdQ + p2], qq1 = form_lds[qo + (kr + 8) * kLdQ + q2];
+    float c1, s1, t1, c2, s2, t2;
+    rotation(rpp, rqq, rpq, c1, s1, t1);
+    rotation(cpp, cqq, cpq, c2, s2, t2);
+    const float a1 = c1 * a0 - s1 * e0, e1 = s1 * a0 + c1 * e0;
+    const float b1 = c1 * b0 - s1 * f0, f1 = s1 * b0 + c1 * f0;
+    float na = c2 * a1 - s2 * b1, nb = s2 * a1 + c2 * b1;
+    float ne = c2 * e1 - s2 * f1, nf = s2 * e1 + c2 * f1;
+    if (kr == kc) {
+      // the pivot block (same four addresses): exact diagonal update,
+      // off-diagonal zeroed
+      na = a0 - t1 * b0;
+      nf = f0 + t1 * b0;
+      nb = 0.f;
+      ne = 0.f;
+    }
+    form_lds[so + p * kLdQ + p2] = na;
+    form_lds[so + p * kLdQ + q2] = nb;
+    form_lds[so + q * kLdQ + p2] = ne;
+    form_lds[so + q * kLdQ + q2] = nf;
+    form_lds[qo + kr * kLdQ + p2] = c2 * qp0 - s2 * qq0;
+    form_lds[qo + kr * kLdQ + q2] = s2 * qp0 + c2 * qq0;
+    form_lds[qo + (kr + 8) * kLdQ + p2] = c2 * qp1 - s2 * qq1;
+    form_lds[qo + (kr + 8) * kLdQ + q2] = s2 * qp1 + c2 * qq1;
+    __builtin_amdgcn_wave_barrier();
+    ra = ra == 0 ? 0 : (ra == 15 ? 1 : ra + 1);
+    rb = rb == 15 ? 1 : rb + 1;
+    ca = ca == 0 ? 0 : (ca == 15 ? 1 : ca + 1);
+    cb = cb == 15 ? 1 : cb + 1;
+  }
+}
+
+// Rows [t0, t0 + kFormTile) of the (orbit-mean) deficit as 4-float vectors,
+// kStageVecs per thread (zero past n rows and d columns).
+__device__ __forceinline__ void load_tile(const FormParams& P, const float* delta, int t0, int n, int d,
+                                          int vec_per_row, int tid, f32x4v (&x)[kStageVecs]) {
+#pragma unroll
+  for (int u = 0; u < kStageVecs; ++u) {
+    const int e = tid + u * kFormThreads, r = e / vec_per_row, v4 = e - r * vec_per_row;
+    x[u] = (f32x4v){0.f, 0.f, 0.f, 0.f};
+    if (e < kFormTile * vec_per_row && t0 + r < n && 4 * v4 < d) x[u] = load_delta4(P, delta, t0 + r, v4);
+  }
+}
+
 }  // namespace
 
 __global__ __launch_bounds__(kFormThreads) void form_patch_kernel(const FormParams /*by value, read in place*/) {
   const FormParams& P = *static_cast<const FormParams*>((const void*)__builtin_amdgcn_kernarg_segment_ptr());
-  extern __shared__ __align__(16) float lds_f[];
-  __shared__ f32x4v s_pair[64];           // per pair: c, s, t, p | q << 8
+  float* const lds_f = form_lds;
   __shared__ int s_order[128];
-  __shared__ float s_red[kFormThreads / 64];
+  __shared__ float s_red[kWaves];
+  __shared__ int s_grp[kFormMaxDim / (2 * kBlk)];   // blocks (bi | bj << 8) of each group this step
 
   const int unit = blockIdx.x;
   if (unit >= P.n_units) return;
@@ -77,57 +197,87 @@ __global__ __launch_bounds__(kFormThreads) void form_patch_kernel(const FormPara
   const int l = (unit / P.n_heads) % P.n_layers;
   const int c = unit / (P.n_heads * P.n_layers);
   const int d = P.dim, n = P.n_tokens, m = P.m;
-  const int ld = d + 1;                      // padded LDS row stride
-  float* G = lds_f;                          // [d][d+1]
-  float* V = lds_f + d * ld;                 // [d][d+1]; holds Delta tiles in phase 1
+  const int dp = pad16(d);                   // padded size (zero rows/columns beyond d)
+  const int ld = dp + 1;                     // padded LDS row stride of G and V
+  const int nb = dp / kBlk;                  // Jacobi blocks (even)
+  const int ng = nb / 2;                     // groups rotated per step
+  const uint32_t ng_magic = (65536u + ng - 1) / ng;   // t / ng == (t * ng_magic) >> 16 for t < 128
+  float* G = lds_f;                          // [dp][ld]
+  float* V = lds_f + dp * ld;                // [dp][ld]; holds Delta tiles in phase 1
+  float* Ss = V + dp * ld;                   // [ng][16][kLdQ] group matrices
+  float* Qs = Ss + ng * kGrp * kLdQ;         // [ng][16][kLdQ] group rotations
   const float* delta = P.delta + (int64_t)c * P.delta_s[0] + (int64_t)l * P.delta_s[1] + (int64_t)h * P.delta_s[2];
   const int tid = threadIdx.x;
+  const int wave = tid >> 6, lane = tid & 63;
+  const int lj = lane >> 4, lr = lane & 15;  // MFMA operand slot (k within a step) and row/column
 
-  // ---- 1. G = Delta^T Delta: thread owns a 4x4 block (32x32 threads) ----
+  // ---- 1. G = Delta^T Delta on MFMA: wave owns up to 3 tiles (I <= J) ----
   {
-    const int bi = 4 * (tid >> 5), bj = 4 * (tid & 31);
-    const bool own = bi < d && bj < d;
-    float acc[4][4];
+    const int nt = dp / 16;
+    const int ntiles = nt * (nt + 1) / 2;
+    const int ldt = tile_ld(dp);
+    const int my_tiles = (ntiles - wave + kWaves - 1) / kWaves;   // tiles wave, wave + 16, ... (<= 3)
+    float* T = V;                            // staged tile [kFormTile][ldt]
+    int tI[3], tJ[3];
+    f32x4v acc[3];
 #pragma unroll
-    for (int a = 0; a < 4; ++a)
-#pragma unroll
-      for (int b = 0; b < 4; ++b) acc[a][b] = 0.f;
-    float* T = V;                            // staged tile [kFormTile][d]
-    const int vec_per_row = d / 4;
+    for (int u = 0; u < 3; ++u) {
+      int t = wave + u * kWaves, I = 0;
+      const int t_in = t;
+      if (t < ntiles) {
+        while (t >= nt - I) {                // row I of the upper triangle holds nt - I tiles
+          t -= nt - I;
+          ++I;
+        }
+      }
+      tI[u] = t_in < ntiles ? I : 0;         // (an idle slot reads tile (0, 0) and stores nothing)
+      tJ[u] = t_in < ntiles ? I + t : 0;
+      acc[u] = (f32x4v){0.f, 0.f, 0.f, 0.f};
+    }
+    // the tile (kFormTile rows x dp columns) is staged as 4-float vectors,
+    // kStageVecs per thread; the next tile's loads are in flight during the
+    // products on the current one
+    const int vec_per_row = dp / 4;
+    f32x4v x[kStageVecs];
+    load_tile(P, delta, 0, n, d, vec_per_row, tid, x);
     for (int t0 = 0; t0 < n; t0 += kFormTile) {
       __syncthreads();
-      for (int e = tid; e < kFormTile * vec_per_row; e += kFormThreads) {
-        const int r = e / vec_per_row, v4 = e % vec_per_row;
-        f32x4v x = {0.f, 0.f, 0.f, 0.f};
-        if (t0 + r < n) x = load_delta4(P, delta, t0 + r, v4);
-        *reinterpret_cast<f32x4v*>(T + r * d + 4 * v4) = x;
+#pragma unroll
+      for (int u = 0; u < kStageVecs; ++u) {
+        const int e = tid + u * kFormThreads, r = e / vec_per_row, v4 = e - r * vec_per_row;
+        if (e < kFormTile * vec_per_row) *reinterpret_cast<f32x4v*>(T + r * ldt + 4 * v4) = x[u];
       }
       __syncthreads();
-      if (own) {
-        for (int r = 0; r < kFormTile; ++r) {
-          const f32x4v a = *reinterpret_cast<const f32x4v*>(T + r * d + bi);
-          const f32x4v b = *reinterpret_cast<const f32x4v*>(T + r * d + bj);
+      if (t0 + kFormTile < n) load_tile(P, delta, t0 + kFormTile, n, d, vec_per_row, tid, x);
+      const int nrows = min(kFormTile, n - t0);
+      for (int kb = 0; kb < (nrows + 3) / 4; ++kb) {
+        const float* trow = T + (4 * kb + lj) * ldt + lr;
 #pragma unroll
-          for (int x = 0; x < 4; ++x)
+        for (int u = 0; u < 3; ++u)
+          if (u < my_tiles) acc[u] = mfma4(trow[16 * tI[u]], trow[16 * tJ[u]], acc[u]);
+      }
+    }
+    // lane (lj, lr) holds G[16I + 4 lj + i][16J + lr]; store it and its mirror
 #pragma unroll
-            for (int y = 0; y < 4; ++y) acc[x][y] = fmaf(a[x], b[y], acc[x][y]);
+    for (int u = 0; u < 3; ++u) {
+      if (wave + u * kWaves < ntiles) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int row = 16 * tI[u] + 4 * lj + i, col = 16 * tJ[u] + lr;
+          if (tI[u] < tJ[u] || row <= col) {
+            G[row * ld + col] = acc[u][i];
+            G[col * ld + row] = acc[u][i];
+          }
         }
       }
     }
     __syncthreads();
-    if (own) {
-#pragma unroll
-      for (int x = 0; x < 4; ++x)
-#pragma unroll
-        for (int y = 0; y < 4; ++y) G[(bi + x) * ld + bj + y] = acc[x][y];
-    }
-    // V = I
-    for (int e = tid; e < d * d; e += kFormThreads) V[(e / d) * ld + e % d] = (e / d == e % d) ? 1.f : 0.f;
+    // V = I (the staged tile is no longer needed)
+    for (int e = tid; e < dp * dp; e += kFormThreads) V[(e / dp) * ld + e % dp] = (e / dp == e % dp) ? 1.f : 0.f;
     __syncthreads();
   }
 
-  // ---- 2. cyclic Jacobi, round-robin pair ordering ----
-  const int half = d / 2;
+  // ---- 2. block Jacobi ----
   int sweeps_run = 0;
   for (int sweep = 0; sweep < P.sweeps; ++sweep) {
     // stop once the off-diagonal mass is negligible against the diagonal
@@ -141,112 +291,133 @@ __global__ __launch_bounds__(kFormThreads) void form_patch_kernel(const FormPara
     dia = block_sum(dia, s_red);
     if (off <= 1e-9f * dia) break;             // ~(d * 4 eps)^2: the fp32 floor
     ++sweeps_run;
-    for (int step = 0; step < d - 1; ++step) {
-      if (tid < half) {
-        // circle method: position 0 fixed, positions 1..d-1 rotate by `step`
-        const int k = tid;
-        const int pa = k == 0 ? 0 : 1 + (k - 1 + step) % (d - 1);
-        const int pb = 1 + (d - 2 - k + step) % (d - 1);
-        const int p = pa < pb ? pa : pb, q = pa < pb ? pb : pa;
-        const float app = G[p * ld + p], aqq = G[q * ld + q], apq = G[p * ld + q];
-        float cc = 1.f, ss = 0.f, t = 0.f;
-        if (fabsf(apq) > 1e-30f) {
-          // the smaller root of t^2 + 2 theta t - 1 = 0 zeroes G[p][q]
-          const float theta = (aqq - app) / (2.f * apq);
-          t = (theta >= 0.f ? 1.f : -1.f) / (fabsf(theta) + sqrtf(theta * theta + 1.f));
-          cc = 1.f / sqrtf(t * t + 1.f);
-          ss = t * cc;
+    for (int step = 0; step < nb - 1; ++step) {
+      // (a) one wave per group: a Jacobi sweep on the group's principal submatrix
+      if (wave < ng) {
+        int bi, bj;
+        circle_pair(nb, step, wave, bi, bj);
+        if (lane == 0) s_grp[wave] = bi | (bj << 8);
+        const int so = (int)(Ss - lds_f) + wave * kGrp * kLdQ;
+        const int qo = (int)(Qs - lds_f) + wave * kGrp * kLdQ;
+#pragma unroll
+        for (int u = 0; u < kGrp * kGrp / 64; ++u) {
+          const int e = lane + 64 * u, r = e >> 4, cc = e & 15;
+          lds_f[so + r * kLdQ + cc] = G[group_index(bi, bj, r) * ld + group_index(bi, bj, cc)];
+          lds_f[qo + r * kLdQ + cc] = r == cc ? 1.f : 0.f;
         }
-        const f32x4v pr = {cc, ss, t, __int_as_float(p | (q << 8))};
-        s_pair[k] = pr;
+        __builtin_amdgcn_wave_barrier();
+        group_sweep(so, qo, lane);
       }
       __syncthreads();
-      // G <- J^T G J in one pass: the pairs partition the indices, so each
-      // 2x2 block (rows of pair k, columns of pair k2) is owned by one thread
-      // (G, then V: a thread issues all its loads before its stores; the
-      // blocks and the V column pairs are disjoint, so no store is read again)
-      {
-        constexpr int kG = (kFormMaxDim / 2) * (kFormMaxDim / 2) / kFormThreads;
-        constexpr int kGb = kG / 2;                // G blocks in two batches (register budget)
+      // (b) G <- J^T G J: tile (a, b) becomes Q_a^T G_ab Q_b.  G stays
+      // symmetric, so only tiles a <= b are formed (up to 3 per wave, taken
+      // two at a time with their loads issued together and their MFMA chains
+      // interleaved) and each is stored with its mirror.
 #pragma unroll
-        for (int u0 = 0; u0 < kG; u0 += kGb) {
-          float g[kGb][4];
-          f32x4v rr[kGb], rc[kGb];
+      for (int u0 = 0; u0 < 4; u0 += 2) {
+        bool ok[2];
+        int rowa[2], ga[2], gb[2];
+        float gv[2][4], qv[2][4];
+        f32x4v mt[2], tt[2];
 #pragma unroll
-          for (int u = 0; u < kGb; ++u) {
-            const int e = tid + (u0 + u) * kFormThreads;
-            if (e < half * half) {
-              const int k = e / half, k2 = e - k * half;
-              rr[u] = s_pair[k];
-              rc[u] = s_pair[k2];
-              const int p = __float_as_int(rr[u].w) & 0xff, q = __float_as_int(rr[u].w) >> 8;
-              const int p2 = __float_as_int(rc[u].w) & 0xff, q2 = __float_as_int(rc[u].w) >> 8;
-              g[u][0] = G[p * ld + p2];
-              g[u][1] = G[p * ld + q2];
-              g[u][2] = G[q * ld + p2];
-              g[u][3] = G[q * ld + q2];
+        for (int u = 0; u < 2; ++u) {
+          int t = wave + (u0 + u) * kWaves, a = 0;
+          ok[u] = t < ng * (ng + 1) / 2;
+          if (ok[u]) {
+            while (t >= ng - a) {            // row a of the upper triangle holds ng - a tiles
+              t -= ng - a;
+              ++a;
             }
           }
+          const int b = ok[u] ? a + t : 0;
+          ga[u] = s_grp[a];
+          gb[u] = s_grp[b];
+          rowa[u] = a;
+          const int ai = ga[u] & 0xff, aj = ga[u] >> 8, bi = gb[u] & 0xff, bj = gb[u] >> 8;
+          const float* Qb = Qs + b * kGrp * kLdQ;
+          const int grow = group_index(ai, aj, lr);
 #pragma unroll
-          for (int u = 0; u < kGb; ++u) {
-            const int e = tid + (u0 + u) * kFormThreads;
-            if (e < half * half) {
-              const f32x4v r = rr[u], r2 = rc[u];
-              const int p = __float_as_int(r.w) & 0xff, q = __float_as_int(r.w) >> 8;
-              const int p2 = __float_as_int(r2.w) & 0xff, q2 = __float_as_int(r2.w) >> 8;
-              if (p == p2) {
-                // the pivot block: exact diagonal update, off-diagonal zeroed
-                const float apq = g[u][1];
-                G[p * ld + p] = g[u][0] - r.z * apq;
-                G[q * ld + q] = g[u][3] + r.z * apq;
-                G[p * ld + q] = 0.f;
-                G[q * ld + p] = 0.f;
-              } else {
-                const float a1 = r.x * g[u][0] - r.y * g[u][2], e1 = r.y * g[u][0] + r.x * g[u][2];
-                const float b1 = r.x * g[u][1] - r.y * g[u][3], f1 = r.y * g[u][1] + r.x * g[u][3];
-                G[p * ld + p2] = r2.x * a1 - r2.y * b1;
-                G[p * ld + q2] = r2.y * a1 + r2.x * b1;
-                G[q * ld + p2] = r2.x * e1 - r2.y * f1;
-                G[q * ld + q2] = r2.y * e1 + r2.x * f1;
+          for (int kb = 0; kb < 4; ++kb) {
+            const int k = 4 * kb + lj;
+            gv[u][kb] = G[grow * ld + group_index(bi, bj, k)];
+            qv[u][kb] = Qb[k * kLdQ + lr];
+          }
+          mt[u] = (f32x4v){0.f, 0.f, 0.f, 0.f};
+          tt[u] = (f32x4v){0.f, 0.f, 0.f, 0.f};
+        }
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+          for (int u = 0; u < 2; ++u) mt[u] = mfma4(gv[u][kb], qv[u][kb], mt[u]);
+        // T = Q_a^T M: step i sums k = 4 lj + i, whose M row this lane already holds
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          const float* Qa = Qs + rowa[u] * kGrp * kLdQ;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) qv[u][i] = Qa[(4 * lj + i) * kLdQ + lr];
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int u = 0; u < 2; ++u) tt[u] = mfma4(qv[u][i], mt[u][i], tt[u]);
+        // lane (lj, lr) holds T[4 lj + i][lr]: row of group a, column of group b
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          if (ok[u]) {
+            const int ai = ga[u] & 0xff, aj = ga[u] >> 8, bi = gb[u] & 0xff, bj = gb[u] >> 8;
+            const bool diag = ga[u] == gb[u];
+            const int gcol = group_index(bi, bj, lr);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              if (!diag || 4 * lj + i <= lr) {
+                const int grw = group_index(ai, aj, 4 * lj + i);
+                G[grw * ld + gcol] = tt[u][i];
+                G[gcol * ld + grw] = tt[u][i];
               }
             }
           }
         }
-        constexpr int kV = (kFormMaxDim / 2) * kFormMaxDim / kFormThreads;
-        constexpr int kVb = kV / 2;                // V in two batches (register budget)
+      }
+      // V <- V J: 16-row tile rt of group b's columns becomes V_tile Q_b
+      {
+        bool ok[4];
+        int rtile[4], gb[4];
+        float vv[4][4], qv[4][4];
+        f32x4v vt[4];
 #pragma unroll
-        for (int u0 = 0; u0 < kV; u0 += kVb) {
-          float v[kVb][2];
-          float vc[kVb], vs[kVb];
-          int vp[kVb], vq[kVb];
+        for (int u = 0; u < 4; ++u) {
+          const int t = wave + u * kWaves;
+          ok[u] = t < (dp / 16) * ng;
+          const int rt = ok[u] ? (int)(((uint32_t)t * ng_magic) >> 16) : 0, b = ok[u] ? t - rt * ng : 0;
+          rtile[u] = rt;
+          gb[u] = s_grp[b];
+          const int bi = gb[u] & 0xff, bj = gb[u] >> 8;
+          const float* Qb = Qs + b * kGrp * kLdQ;
 #pragma unroll
-          for (int u = 0; u < kVb; ++u) {
-            const int e = tid + (u0 + u) * kFormThreads;
-            if (e < half * d) {
-              const int k = e / d, i = e - k * d;
-              const f32x4v r = s_pair[k];
-              vc[u] = r.x;
-              vs[u] = r.y;
-              vp[u] = i * ld + (__float_as_int(r.w) & 0xff);
-              vq[u] = i * ld + (__float_as_int(r.w) >> 8);
-              v[u][0] = V[vp[u]];
-              v[u][1] = V[vq[u]];
-            }
+          for (int kb = 0; kb < 4; ++kb) {
+            const int k = 4 * kb + lj;
+            vv[u][kb] = ok[u] ? V[(16 * rt + lr) * ld + group_index(bi, bj, k)] : 0.f;
+            qv[u][kb] = Qb[k * kLdQ + lr];
           }
+          vt[u] = (f32x4v){0.f, 0.f, 0.f, 0.f};
+        }
 #pragma unroll
-          for (int u = 0; u < kVb; ++u) {
-            const int e = tid + (u0 + u) * kFormThreads;
-            if (e < half * d) {
-              V[vp[u]] = vc[u] * v[u][0] - vs[u] * v[u][1];
-              V[vq[u]] = vs[u] * v[u][0] + vc[u] * v[u][1];
-            }
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+          for (int u = 0; u < 4; ++u) vt[u] = mfma4(vv[u][kb], qv[u][kb], vt[u]);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          if (ok[u]) {
+            const int bi = gb[u] & 0xff, bj = gb[u] >> 8;
+            const int gcol = group_index(bi, bj, lr);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) V[(16 * rtile[u] + 4 * lj + i) * ld + gcol] = vt[u][i];
           }
         }
       }
       __syncthreads();
     }
   }
-
   if (P.sweeps_done != nullptr && tid == 0) P.sweeps_done[unit] = sweeps_run;
 
   // ---- 3. the m largest eigenvalues (ties by index) ----
@@ -254,8 +425,8 @@ __global__ __launch_bounds__(kFormThreads) void form_patch_kernel(const FormPara
     const float li = G[tid * ld + tid];
     int rank = 0;
     for (int j = 0; j < d; ++j) {
-      const float lj = G[j * ld + j];
-      rank += (lj > li) || (lj == li && j < tid);
+      const float lk = G[j * ld + j];
+      rank += (lk > li) || (lk == li && j < tid);
     }
     if (rank < m) s_order[rank] = tid;
   }
@@ -272,42 +443,102 @@ __global__ __launch_bounds__(kFormThreads) void form_patch_kernel(const FormPara
     P.sigma[(int64_t)c * P.sigma_s[0] + (int64_t)l * P.sigma_s[1] + (int64_t)h * P.sigma_s[2] + tid] =
         sqrtf(lam > 0.f ? lam : 0.f);
   }
-  // compact V_m [d][m] into G's space, then stream Delta tiles after it
-  float* Vm = G;                             // [d][m]
-  float* T = G + d * m;                      // [kFormTile][d]
-  __syncthreads();
-  for (int e = tid; e < d * m; e += kFormThreads) {
-    const int j = e / m, k = e % m;
-    Vm[j * m + k] = V[j * ld + s_order[k]];
-  }
-  uint16_t* Uout = P.U + (int64_t)c * P.u_s[0] + (int64_t)l * P.u_s[1] + (int64_t)h * P.u_s[2];
-  const int vec_per_row = d / 4;
-  for (int t0 = 0; t0 < n; t0 += kFormTile) {
-    __syncthreads();
-    for (int e = tid; e < kFormTile * vec_per_row; e += kFormThreads) {
-      const int r = e / vec_per_row, v4 = e % vec_per_row;
-      f32x4v x = {0.f, 0.f, 0.f, 0.f};
-      if (t0 + r < n) x = load_delta4(P, delta, t0 + r, v4);
-      *reinterpret_cast<f32x4v*>(T + r * d + 4 * v4) = x;
+  // V_m [dp][ldv] (zero beyond d rows and m columns) and a Delta tile
+  // [32][ldu] after it; V_m is gathered into registers first because it
+  // may overlap V, which is still being read
+  const int mp = pad16(m);
+  const int ldv = (mp % 32 == 16) ? mp : mp + 16;        // 4 rows x 16 columns: disjoint banks
+  const int ldu = dp + ((dp % 32 == 0) ? 2 : 18);        // 16 rows x 2 columns: disjoint banks
+  float* Vm = G;
+  float* T = G + dp * ldv;
+  {
+    constexpr int kMaxPer = kFormMaxDim * kFormMaxDim / kFormThreads;
+    float vals[kMaxPer];
+#pragma unroll
+    for (int u = 0; u < kMaxPer; ++u) {
+      const int e = tid + u * kFormThreads, j = e / mp, k = e - j * mp;
+      vals[u] = (e < dp * mp && j < d && k < m) ? V[j * ld + s_order[k]] : 0.f;
     }
     __syncthreads();
-    for (int e = tid; e < kFormTile * m; e += kFormThreads) {
-      const int r = e / m, k = e % m;
-      if (t0 + r >= n) continue;
-      float s = 0.f;
-      for (int j = 0; j < d; ++j) s = fmaf(T[r * d + j], Vm[j * m + k], s);
-      Uout[(int64_t)(t0 + r) * P.u_s[3] + k] = to_bf16_rne(s);
+#pragma unroll
+    for (int u = 0; u < kMaxPer; ++u) {
+      const int e = tid + u * kFormThreads, j = e / mp, k = e - j * mp;
+      if (e < dp * mp) Vm[j * ldv + k] = vals[u];
+    }
+  }
+  // U = Delta V_m on MFMA: the 16 x 16 output tiles of a staged tile
+  // (kFormTile / 16 row tiles x mp / 16 rank tiles), up to 4 per wave with
+  // their chains interleaved
+  uint16_t* Uout = P.U + (int64_t)c * P.u_s[0] + (int64_t)l * P.u_s[1] + (int64_t)h * P.u_s[2];
+  {
+    constexpr int kRowTiles = kFormTile / 16;
+    const int nout = kRowTiles * (mp / 16);
+    const int my_out = (nout - wave + kWaves - 1) / kWaves;        // output tiles of this wave (<= 4)
+    int ort[4], oct[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int ot = wave + u * kWaves;
+      ort[u] = ot < nout ? ot % kRowTiles : 0;
+      oct[u] = ot < nout ? ot / kRowTiles : 0;
+    }
+    const int vec_per_row = dp / 4;
+    f32x4v x[kStageVecs];
+    load_tile(P, delta, 0, n, d, vec_per_row, tid, x);
+    for (int t0 = 0; t0 < n; t0 += kFormTile) {
+      __syncthreads();
+#pragma unroll
+      for (int u = 0; u < kStageVecs; ++u) {
+        const int e = tid + u * kFormThreads, r = e / vec_per_row, v4 = e - r * vec_per_row;
+        if (e < kFormTile * vec_per_row) {
+          typedef float f32x2v __attribute__((ext_vector_type(2)));
+          f32x2v* dst = reinterpret_cast<f32x2v*>(T + r * ldu + 4 * v4);
+          dst[0] = (f32x2v){x[u][0], x[u][1]};
+          dst[1] = (f32x2v){x[u][2], x[u][3]};
+        }
+      }
+      __syncthreads();
+      if (t0 + kFormTile < n) load_tile(P, delta, t0 + kFormTile, n, d, vec_per_row, tid, x);
+      if (wave < nout) {
+        f32x4v acc[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) acc[u] = (f32x4v){0.f, 0.f, 0.f, 0.f};
+        for (int kb = 0; kb < dp / 4; ++kb) {
+          const float* ta = T + lr * ldu + 4 * kb + lj;
+          const float* vb = Vm + (4 * kb + lj) * ldv + lr;
+#pragma unroll
+          for (int u = 0; u < 4; ++u)
+            if (u < my_out) acc[u] = mfma4(ta[16 * ort[u] * ldu], vb[16 * oct[u]], acc[u]);
+        }
+        // lane (lj, lr) holds U[t0 + 16 rt + 4 lj + i][16 ct + lr]
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int col = 16 * oct[u] + lr;
+          if (wave + u * kWaves < nout && col < m) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const int row = t0 + 16 * ort[u] + 4 * lj + i;
+              if (row < n) Uout[(int64_t)row * P.u_s[3] + col] = to_bf16_rne(acc[u][i]);
+            }
+          }
+        }
+      }
     }
   }
 }
 
-// LDS floats: phase 1 needs G [d][d+1] then the Delta tile after it, phases
-// 2-3 G and V [d][d+1] each, phase 4 V_m [d][m] then the Delta tile
+// LDS floats: phase 1 G [dp][dp+1] and the staged tile [32][tile_ld]; phase 2
+// G and V [dp][dp+1] each and the groups' S and Q [16][17]; phase 4 V_m
+// [dp][ldv] and a tile [32][ldu]
 size_t form_lds_bytes(int dim, int m) {
-  const size_t d = (size_t)dim;
-  size_t f = 2 * d * (d + 1);
-  f = f > d * (d + 1) + kFormTile * d ? f : d * (d + 1) + kFormTile * d;
-  f = f > d * (size_t)m + kFormTile * d ? f : d * (size_t)m + kFormTile * d;
+  const size_t dp = (size_t)pad16(dim), ld = dp + 1, ng = dp / (2 * kBlk);
+  const size_t mp = (size_t)pad16(m);
+  const size_t ldv = (mp % 32 == 16) ? mp : mp + 16;
+  const size_t ldu = dp + ((dp % 32 == 0) ? 2 : 18);
+  const size_t f1 = dp * ld + kFormTile * (size_t)tile_ld((int)dp);
+  const size_t f2 = 2 * dp * ld + 2 * ng * kGrp * kLdQ;
+  const size_t f4 = dp * ldv + kFormTile * ldu;
+  size_t f = f1 > f2 ? f1 : f2;
+  f = f > f4 ? f : f4;
   return f * sizeof(float);
 }
 
