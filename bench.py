@@ -41,6 +41,13 @@ def kernel_source_hash() -> str:
 # ---------------------------------------------------------------------------
 
 def _worker_init():
+    """One BLAS/OpenMP thread per worker process: the environment is set before
+    numpy (and its BLAS) is first loaded in the worker, and the limit is
+    applied again to whatever is already loaded."""
+    for var in ("OPENBLAS_NUM_THREADS", "OMP_NUM_THREADS", "MKL_NUM_THREADS", "BLIS_NUM_THREADS"):
+        os.environ[var] = "1"
+    import numpy  # noqa: F401  (loads BLAS under the limit above)
+
     try:
         from threadpoolctl import threadpool_limits
 
@@ -120,7 +127,7 @@ def cpu_baseline(pool, n_workers, p, budget_s: float = 12.0):
 # compile-side patch forming (--op form_patch)
 # ---------------------------------------------------------------------------
 
-FP32_VECTOR_PEAK_TFLOPS = 157.3
+FP32_MATRIX_PEAK_TFLOPS = 157.3     # dense fp32 MFMA (the kernel's products run there)
 
 
 def _oracle_form(job):
@@ -131,14 +138,21 @@ def _oracle_form(job):
     return 1
 
 
-def form_jacobi_flops(d: int, sweeps: int) -> int:
-    """Flops of ``sweeps`` cyclic Jacobi sweeps as the kernel performs them:
-    d - 1 steps per sweep, each rotating half*(half-1) off-pivot 2x2 blocks of
-    G (8 outputs of one multiply and one fused multiply-add: 24 flops) and
-    half*d row pairs of V (6 flops), plus the convergence sum (2 d^2)."""
-    half = d // 2
-    per_step = 24 * half * (half - 1) + 6 * half * d
-    return sweeps * ((d - 1) * per_step + 2 * d * d)
+def form_flops(n: int, d: int, m: int, sweeps: int) -> int:
+    """Flops the patch-forming kernel performs on one unit (padded sizes, as
+    executed): the Gram matrix on the upper-triangle 16x16 tiles, `sweeps`
+    block-Jacobi sweeps of dp/8 - 1 steps each (one 15-step cyclic sweep of
+    24 flops per 2x2 block and 6 per rotated Q pair in each of the dp/16
+    groups, then the 16x16 tile products Q_a^T G_ab Q_b on the upper triangle
+    and V_tile Q_b, plus the convergence sum), and U = Delta V_m."""
+    dp = (d + 15) // 16 * 16
+    mp = (m + 15) // 16 * 16
+    nt, ng = dp // 16, dp // 16
+    gram = n * 512 * nt * (nt + 1) // 2
+    inner = ng * 15 * (64 * 24 + 128 * 6)
+    outer = (ng * (ng + 1) // 2) * 2 * (2 * 16 ** 3) + nt * ng * (2 * 16 ** 3)
+    per_sweep = (dp // 8 - 1) * (inner + outer) + 2 * d * d
+    return gram + sweeps * per_sweep + 2 * n * dp * mp
 
 
 def bench_form(args, pool, n_workers):
@@ -201,8 +215,7 @@ def bench_form(args, pool, n_workers):
     for name, m in planes:
         done = tensors[name][3].cpu().numpy()
         sweeps_hist.append(done)
-        flops += 2 * n * d * d * C * L * H + 2 * n * d * m * C * L * H
-        flops += sum(form_jacobi_flops(d, int(s)) * int(cnt) for s, cnt in zip(*np.unique(done, return_counts=True)))
+        flops += sum(form_flops(n, d, m, int(s)) * int(cnt) for s, cnt in zip(*np.unique(done, return_counts=True)))
     sw = np.concatenate([h.ravel() for h in sweeps_hist])
     achieved = flops / (gpu_ms * 1e-3) / 1e12
 
@@ -242,8 +255,8 @@ def bench_form(args, pool, n_workers):
                    "tokens_per_chunk": n, "dim": d, "planes": [p for p, _ in planes],
                    "rank": {p: m for p, m in planes}},
         "sweeps_run": {"min": int(sw.min()), "mean": round(float(sw.mean()), 2), "max": int(sw.max())},
-        "roofline": {"bound": "alu", "achieved": round(achieved, 3), "peak": FP32_VECTOR_PEAK_TFLOPS,
-                     "unit": "TFLOP/s", "frac": round(achieved / FP32_VECTOR_PEAK_TFLOPS, 4), "traffic": None,
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 3), "peak": FP32_MATRIX_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(achieved / FP32_MATRIX_PEAK_TFLOPS, 4), "traffic": None,
                      "kernel": "form_patch_kernel", "kernel_ms": round(gpu_ms / len(planes), 4),
                      "flops_per_step": int(flops)},
         "cpu_baseline": cpu,
