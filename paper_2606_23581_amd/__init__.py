@@ -27,6 +27,7 @@ from typing import Optional, Sequence, Tuple
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libkamera.so")
+_DEFAULT_LIB_PATH = LIB_PATH
 
 OK = 0
 ERR_NULL = -1
@@ -124,10 +125,20 @@ _LIB = None
 
 
 def lib() -> ctypes.CDLL:
-    """The loaded library; raises KameraUnavailable when it is not built."""
+    """The loaded library.  When the in-tree library has not been built yet it
+    is compiled once (hipcc, gfx950); if that is impossible, or another path
+    was configured and is missing, KameraUnavailable is raised -- there is no
+    other implementation to fall back to."""
     global _LIB
     if _LIB is not None:
         return _LIB
+    if not os.path.exists(LIB_PATH) and LIB_PATH == _DEFAULT_LIB_PATH:
+        try:
+            from . import build as _build
+
+            _build.build()
+        except Exception as e:  # no hipcc, or the compile failed
+            raise KameraUnavailable(f"{LIB_PATH} is not built and building it failed: {e}") from e
     if not os.path.exists(LIB_PATH):
         raise KameraUnavailable(f"{LIB_PATH} is not built (run __graft_entry__.build())")
     try:
