@@ -319,20 +319,32 @@ def main():
         p.step()
     torch.cuda.synchronize()
 
+    # workloads small enough to stay partly in the 256 MB MALL / L2 between
+    # steps get a 1 GiB write between timed steps (outside the events), so
+    # every step starts cold; their throughput is then taken from the events
+    flush = None
+    if p.bytes_per_step < (4 << 30):
+        flush = torch.empty((1 << 30) // 4, dtype=torch.float32, device=dev)
     starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
     ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for k in range(args.steps):
+        if flush is not None:
+            flush.fill_(float(k))
         starts[k].record(stream)
         p.step()
         ends[k].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    kernel_ms = sum(s.elapsed_time(e) for s, e in zip(starts, ends)) / args.steps
-    ms_per_step = wall * 1e3 / args.steps
+    step_ms = sorted(s.elapsed_time(e) for s, e in zip(starts, ends))
+    kernel_ms = sum(step_ms) / args.steps
+    median_ms = step_ms[len(step_ms) // 2] if len(step_ms) % 2 else 0.5 * (step_ms[len(step_ms) // 2 - 1] +
+                                                                          step_ms[len(step_ms) // 2])
+    ms_per_step = kernel_ms if flush is not None else wall * 1e3 / args.steps
     value = p.bytes_per_step / (ms_per_step * 1e-3) / 1e9
     achieved = p.bytes_per_step / (kernel_ms * 1e-3) / 1e9
+    del flush
 
     # practical ceiling on this machine: the library's own scatter kernel with an
     # identity page table is a plain row-contiguous 16-byte streaming copy
@@ -409,6 +421,9 @@ def main():
                      "frac": round(achieved / HBM_PEAK_GBPS, 4),
                      "traffic": traffic, "kernel": "rehydrate_kernel" if w.kind == "rehydrate" else "shift_kernel",
                      "kernel_ms": round(kernel_ms, 4)},
+        "timing": {"event_mean_ms": round(kernel_ms, 4), "event_median_ms": round(median_ms, 4),
+                   "event_min_ms": round(step_ms[0], 4), "wall_ms_per_step": round(wall * 1e3 / args.steps, 4),
+                   "cold_flush_bytes_between_steps": 0 if p.bytes_per_step >= (4 << 30) else (1 << 30)},
         "device_copy_GBps": None if copy_gbps is None else round(copy_gbps, 1),
         "streaming_copy_GBps": None if scatter_copy is None else round(scatter_copy, 1),
         "frac_of_streaming_copy": None if scatter_copy is None else round(value / scatter_copy, 4),

@@ -132,6 +132,10 @@ def lib() -> ctypes.CDLL:
     global _LIB
     if _LIB is not None:
         return _LIB
+    # torch ships its own HIP runtime: load it first so that the library binds
+    # to the same runtime instance torch's tensors and streams live in
+    import torch  # noqa: F401
+
     if not os.path.exists(LIB_PATH) and LIB_PATH == _DEFAULT_LIB_PATH:
         try:
             from . import build as _build

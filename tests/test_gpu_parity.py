@@ -502,3 +502,70 @@ def test_orbit_patch_matches_reference(device, K, n, d, m):
         km.form_patch(dt[0], U2, W2)
         torch.cuda.synchronize()
         assert np.array_equal(bits(U2), Ub) and np.array_equal(bits(W2), Wb)
+
+
+# ---------------------------------------------------------------------------
+# graph capture
+# ---------------------------------------------------------------------------
+
+def test_graph_capture_replays_match_eager(device):
+    """The entry points allocate, free and synchronise nothing and clear
+    nothing with a memset, so a serving loop can capture them: a rehydrate
+    into a paged pool followed by a shift of the same pages, captured in one
+    graph, replayed three times with eager work and synchronisations between
+    the replays; every replay gives the eager result bit for bit."""
+    import paper_2606_23581_amd as km
+    import torch
+
+    print("[case] graph capture rehydrate + shift", flush=True)
+    rng = np.random.default_rng(61)
+    C, L, n, H, D, m, P = 2, 2, 64, 2, 128, 16, 16
+    pages = n // P
+    npp = C * pages + 3
+    K = dev(synth.randn_bf16_numpy((C, L, n, H, D), 1.0, rng), device)
+    V = dev(synth.randn_bf16_numpy((C, L, n, H, D), 1.0, rng), device)
+    Uk = dev(synth.randn_bf16_numpy((C, L, H, n, m), 0.1, rng), device)
+    Wk = dev(synth.randn_bf16_numpy((C, L, H, m, D), 0.1, rng), device)
+    pt = dev_i32(rng.permutation(npp)[: C * pages].reshape(C, pages), device)
+    pos = dev_i32(np.repeat(rng.integers(0, 20000, size=(C, 1)), 3, axis=1), device)
+    delta = dev_i32(np.full((C, 3), -777), device)
+    rs = km.RopeSpec(theta=1e6, rope_dim=128)
+
+    def pools():
+        return (torch.zeros((L, npp * P, H, D), dtype=torch.bfloat16, device=device),
+                torch.zeros((L, npp * P, H, D), dtype=torch.bfloat16, device=device))
+
+    def calls(kp, vp):
+        return (km.prepare_rehydrate(K, kp, v_in=V, v_out=vp, rope=rs, chunk_pos=pos, u_k=Uk, w_k=Wk,
+                                     page_table=pt, page_size=P, n_pool_pages=npp),
+                km.prepare_shift(kp, delta, rope=rs, n_chunks=C, n_tokens=n, page_table=pt, page_size=P,
+                                 n_pool_pages=npp))
+
+    ke, ve = pools()
+    for call in calls(ke, ve):
+        call.launch()
+    torch.cuda.synchronize()
+    want_k, want_v = bits(ke), bits(ve)
+
+    kg, vg = pools()
+    prepared = calls(kg, vg)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        for call in prepared:          # warm-up launch outside the capture
+            call.launch(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=side):
+        for call in prepared:
+            call.launch(side)
+    for rep in range(3):
+        kg.zero_()
+        vg.zero_()
+        scratch = torch.randn(1 << 20, device=device) * rep   # unrelated eager work between replays
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert np.array_equal(bits(kg), want_k), f"replay {rep}: keys differ from the eager run"
+        assert np.array_equal(bits(vg), want_v), f"replay {rep}: values differ from the eager run"
+        del scratch
