@@ -418,7 +418,8 @@ def test_scatter_bad_page_is_flagged(device):
 # compile-side patch forming
 # ---------------------------------------------------------------------------
 
-@pytest.mark.parametrize("n,d,m", [(100, 128, 16), (1024, 128, 64), (37, 64, 8), (50, 36, 1), (64, 32, 32)])
+@pytest.mark.parametrize("n,d,m", [(100, 128, 16), (1024, 128, 64), (37, 64, 8), (50, 36, 1), (64, 32, 32),
+                                   (7, 4, 2), (130, 16, 16), (2000, 128, 128), (300, 100, 40)])
 def test_form_patch_matches_svd(device, n, d, m):
     """Planted deficits with a spectral gap at m (rank-m signal + small noise):
     U W must match the fp64 truncated SVD's product, the singular values the
