@@ -280,6 +280,23 @@ static int build_rehydrate(const kamera_rehydrate_args* a, kamera::RehydratePara
         return fail(KAMERA_ERR_ALIAS, "%s: output of plane %d overlaps the input of plane %d", who, o, p);
     }
   }
+  // two planes may write one tensor only through the same mapping on disjoint columns
+  if (a->n_planes == 2) {
+    const kamera_plane& q0 = a->plane[0];
+    const kamera_plane& q1 = a->plane[1];
+    const int64_t e_dense[4] = {a->n_chunks, a->n_layers, a->n_tokens, a->n_heads};
+    const int64_t e_pool[4] = {1, a->n_layers, (int64_t)a->n_pool_pages * a->page_size, a->n_heads};
+    uintptr_t lo0, hi0, lo1, hi1;
+    extent(q0.out, q0.out_stride, a->paged ? e_pool : e_dense, a->head_dim, lo0, hi0);
+    extent(q1.out, q1.out_stride, a->paged ? e_pool : e_dense, a->head_dim, lo1, hi1);
+    if (overlap(lo0, hi0, lo1, hi1)) {
+      const bool same_map = q0.out == q1.out && memcmp(q0.out_stride, q1.out_stride, sizeof(q0.out_stride)) == 0;
+      const int b0 = q0.col_begin, e0 = (q0.col_begin == 0 && q0.col_end == 0) ? a->head_dim : q0.col_end;
+      const int b1 = q1.col_begin, e1 = (q1.col_begin == 0 && q1.col_end == 0) ? a->head_dim : q1.col_end;
+      if (!same_map || !(e0 <= b1 || e1 <= b0))
+        return fail(KAMERA_ERR_ALIAS, "%s: the two planes' outputs overlap", who);
+    }
+  }
 
   memset(&P, 0, sizeof(P));
   if (any_rot) fill_rope(a->rope, P.rope);
@@ -317,18 +334,20 @@ static int build_rehydrate(const kamera_rehydrate_args* a, kamera::RehydratePara
     o.u_vec = q.m % 8 == 0 && aligned16(q.U) && strides_ok(q.u_stride, 4);
     o.w_vec = aligned16(q.W) && strides_ok(q.w_stride, 4);
     // column blocks: the rotated band as one block, the rest in <= 128-column pieces
-    std::vector<std::pair<int, int>> segs;  // [col0, col1)
+    std::pair<int, int> segs[3];  // [col0, col1): before the band, the band, after it
+    int nseg = 0;
     const int cb = q.col_begin, ce = (q.col_begin == 0 && q.col_end == 0) ? a->head_dim : q.col_end;
     if (q.rotate) {
       const int r0 = a->rope.rope_offset, r1 = r0 + a->rope.rope_dim;
-      if (r0 > cb) segs.push_back({cb, r0});
-      segs.push_back({r0, r1});
-      if (r1 < ce) segs.push_back({r1, ce});
+      if (r0 > cb) segs[nseg++] = {cb, r0};
+      segs[nseg++] = {r0, r1};
+      if (r1 < ce) segs[nseg++] = {r1, ce};
     } else {
-      segs.push_back({cb, ce});
+      segs[nseg++] = {cb, ce};
     }
     int nb = 0;
-    for (auto& sg : segs) {
+    for (int si = 0; si < nseg; ++si) {
+      const std::pair<int, int>& sg = segs[si];
       const bool band = q.rotate && sg.first == a->rope.rope_offset;
       for (int c0 = sg.first; c0 < sg.second; c0 += 128) {
         const int w = band ? sg.second - sg.first : std::min(128, sg.second - c0);

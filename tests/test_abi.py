@@ -246,6 +246,36 @@ def test_rehydrate_rejects(case, code):
     assert km.last_error().startswith("kamera_rehydrate")
 
 
+def test_plane_outputs_may_share_a_tensor_only_on_disjoint_columns():
+    """Two planes writing one output tensor: accepted through the same mapping on
+    disjoint column ranges (the MLA latent and its rope band), rejected when the
+    ranges intersect or the mappings differ."""
+    L = km.lib()
+
+    def two_planes(c0, c1, shift=0):
+        a = rehydrate_args()
+        a.head_dim = 256
+        a.rope = km.RopeSpec(theta=1e6, rope_dim=64, rope_offset=192).to_c()
+        for p in range(2):
+            pl = a.plane[p]
+            st = [3 * 64 * 4 * 256, 64 * 4 * 256, 4 * 256, 256]
+            for k in range(4):
+                pl.in_stride[k] = st[k]
+                pl.out_stride[k] = st[k]
+            pl.m = 16
+            pl.rotate = 1 if p == 1 else 0
+        a.plane[1].in_ = a.plane[0].in_
+        a.plane[1].out = a.plane[0].out + shift
+        (a.plane[0].col_begin, a.plane[0].col_end), (a.plane[1].col_begin, a.plane[1].col_end) = c0, c1
+        a.plane[0].patch_offset, a.plane[0].patch_dim = c0[0], c0[1] - c0[0]
+        a.plane[1].patch_offset, a.plane[1].patch_dim = c1[0], c1[1] - c1[0]
+        return a
+
+    assert L.kamera_validate(0, ctypes.byref(two_planes((0, 192), (192, 256)))) == km.OK, km.last_error()
+    assert L.kamera_validate(0, ctypes.byref(two_planes((0, 224), (192, 256)))) == km.ERR_ALIAS
+    assert L.kamera_validate(0, ctypes.byref(two_planes((0, 192), (192, 256), shift=512))) == km.ERR_ALIAS
+
+
 def test_exact_in_place_is_accepted_but_shifted_overlap_is_not():
     """In place (same base and strides, dense, no row base) passes validation;
     any other overlap is rejected.  The in-place case is stopped right before
