@@ -134,11 +134,14 @@ def _oracle_form(job):
     import oracle as ref
 
     delta, m = job
-    ref.form_patch(delta, m)
+    if delta.ndim == 3:
+        ref.orbit_patch(delta, m)
+    else:
+        ref.form_patch(delta, m)
     return 1
 
 
-def form_flops(n: int, d: int, m: int, sweeps: int) -> int:
+def form_flops(n: int, d: int, m: int, sweeps: int, orbit: int = 1) -> int:
     """Flops the patch-forming kernel performs on one unit (padded sizes, as
     executed): the Gram matrix on the upper-triangle 16x16 tiles, `sweeps`
     block-Jacobi sweeps of dp/8 - 1 steps each (one 15-step cyclic sweep of
@@ -152,7 +155,8 @@ def form_flops(n: int, d: int, m: int, sweeps: int) -> int:
     inner = ng * 15 * (64 * 24 + 128 * 6)
     outer = (ng * (ng + 1) // 2) * 2 * (2 * 16 ** 3) + nt * ng * (2 * 16 ** 3)
     per_sweep = (dp // 8 - 1) * (inner + outer) + 2 * d * d
-    return gram + sweeps * per_sweep + 2 * n * dp * mp
+    mean = 0 if orbit <= 1 else 2 * orbit * n * d          # orbit mean, formed in both passes over Delta
+    return gram + sweeps * per_sweep + 2 * n * dp * mp + mean
 
 
 def bench_form(args, pool, n_workers):
@@ -170,7 +174,8 @@ def bench_form(args, pool, n_workers):
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     C, L, H, n, d = w.n_chunks, w.n_layers, w.n_heads, w.n_tokens, w.head_dim
-    planes = [("k", w.m_k)] + ([("v", w.m_v)] if w.has_v and w.m_v else [])
+    planes = [("k", w.m_k)] + ([("v", w.m_v)] if w.has_v and w.m_v and args.orbit == 1 else [])
+    K = max(1, args.orbit)
     gen = torch.Generator(device=dev)
     gen.manual_seed(w.seed + 7)
     # deficits: Gaussian token coefficients on a decaying spectrum
@@ -180,10 +185,11 @@ def bench_form(args, pool, n_workers):
     tensors = {}
     for name, m in planes:
         q, _ = torch.linalg.qr(torch.randn((d, d), generator=gen, device=dev, dtype=torch.float32))
-        D = torch.empty((C, L, H, n, d), dtype=torch.float32, device=dev)
-        for c in range(C):
+        D = torch.empty((K, C, L, H, n, d) if K > 1 else (C, L, H, n, d), dtype=torch.float32, device=dev)
+        Dv = D.view(K * C, L, H, n, d)
+        for c in range(K * C):
             a = torch.randn((L, H, n, d), generator=gen, device=dev, dtype=torch.float32)
-            torch.matmul(a * sig, q.contiguous(), out=D[c])
+            torch.matmul(a * sig, q.contiguous(), out=Dv[c])
             del a
         U = torch.empty((C, L, H, n, m), dtype=torch.bfloat16, device=dev)
         W = torch.empty((C, L, H, m, d), dtype=torch.bfloat16, device=dev)
@@ -215,14 +221,14 @@ def bench_form(args, pool, n_workers):
     for name, m in planes:
         done = tensors[name][3].cpu().numpy()
         sweeps_hist.append(done)
-        flops += sum(form_flops(n, d, m, int(s)) * int(cnt) for s, cnt in zip(*np.unique(done, return_counts=True)))
+        flops += sum(form_flops(n, d, m, int(s), K) * int(cnt) for s, cnt in zip(*np.unique(done, return_counts=True)))
     sw = np.concatenate([h.ravel() for h in sweeps_hist])
     achieved = flops / (gpu_ms * 1e-3) / 1e12
 
     cpu = None
     if pool is not None:
         D = tensors["k"][0]
-        jobs = [(D[0, 0, h].double().cpu().numpy(), w.m_k) for h in range(H)]
+        jobs = [((D[:, 0, 0, h] if K > 1 else D[0, 0, h]).double().cpu().numpy(), w.m_k) for h in range(H)]
         pool.map(_oracle_form, jobs, chunksize=1)      # untimed: the workers load LAPACK
         done_n, t1 = 0, time.perf_counter()
         while True:
@@ -251,7 +257,8 @@ def bench_form(args, pool, n_workers):
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic fp32 deficits: N(0,1) coefficients on the spectrum (1+k)^-1/4 in a random basis",
-        "config": {"workload": f"form_patch on {w.name}", "n_chunks": C, "n_layers": L, "kv_heads": H,
+        "config": {"workload": f"form_patch on {w.name}" + (f", orbit of {K}" if K > 1 else ""),
+                   "orbit": K, "n_chunks": C, "n_layers": L, "kv_heads": H,
                    "tokens_per_chunk": n, "dim": d, "planes": [p for p, _ in planes],
                    "rank": {p: m for p, m in planes}},
         "sweeps_run": {"min": int(sw.min()), "mean": round(float(sw.mean()), 2), "max": int(sw.max())},
@@ -259,6 +266,100 @@ def bench_form(args, pool, n_workers):
                      "unit": "TFLOP/s", "frac": round(achieved / FP32_MATRIX_PEAK_TFLOPS, 4), "traffic": None,
                      "kernel": "form_patch_kernel", "kernel_ms": round(gpu_ms / len(planes), 4),
                      "flops_per_step": int(flops)},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+# ---------------------------------------------------------------------------
+# paged copies (--op scatter | gather): the copy half of the conditioning switch
+# ---------------------------------------------------------------------------
+
+def _oracle_scatter(job):
+    import oracle as ref
+
+    rows, pt_row, page_size, pool = job
+    ref.scatter_paged(rows, pt_row, page_size, pool)
+    return 1
+
+
+def bench_copy(args, pool_workers, n_workers):
+    """One step = one bit copy of every token row (all KV heads of a layer) of
+    the workload's chunks between dense rows and the pool's page-table slots:
+    rows -> pool (scatter) or pool -> rows (gather)."""
+    import numpy as np
+    import torch
+
+    import paper_2606_23581_amd as km
+    from synth import WORKLOADS, chunk_meta, randn_bf16_device
+
+    w = WORKLOADS[args.workload]
+    if not w.paged:
+        raise SystemExit(f"--op {args.op} needs a paged workload ({w.name} is not)")
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    C, L, H, n, D, P = w.n_chunks, w.n_layers, w.n_heads, w.n_tokens, w.head_dim, w.page_size
+    meta = chunk_meta(w)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(w.seed + 11)
+    rows = randn_bf16_device((C, L, n, H, D), 1.0, gen, dev, slab_dim=0)
+    pool = randn_bf16_device((L, w.n_pool_pages * P, H, D), 1.0, gen, dev, slab_dim=0)
+    pt = torch.from_numpy(meta.page_table).to(dev)
+    call = km.prepare_scatter_paged(rows, pool, pt, page_size=P, n_pool_pages=w.n_pool_pages,
+                                    gather=args.op == "gather")
+    stream = torch.cuda.current_stream()
+    for _ in range(args.warmup):
+        call.launch(stream)
+    torch.cuda.synchronize()
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        starts[k].record(stream)
+        call.launch(stream)
+        ends[k].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    kernel_ms = sum(a.elapsed_time(b) for a, b in zip(starts, ends)) / args.steps
+    ms_per_step = wall * 1e3 / args.steps
+    nbytes = 2 * C * L * n * H * D * 2
+    cpu = None
+    if pool_workers is not None:
+        pool_np = np.zeros((w.n_pool_pages * P, H * D), np.uint16)
+        rows_np = rows[0, 0].reshape(n, H * D).cpu().view(torch.int16).numpy().view(np.uint16)
+        jobs = [(rows_np, meta.page_table[c], P, pool_np) for c in range(min(C, 8))]
+        pool_workers.map(_oracle_scatter, jobs[:1], chunksize=1)
+        done, t1 = 0, time.perf_counter()
+        while True:
+            pool_workers.map(_oracle_scatter, jobs, chunksize=1)
+            done += len(jobs)
+            if time.perf_counter() - t1 >= args.cpu_seconds / 2:
+                break
+        dt = time.perf_counter() - t1
+        cpu = {"value": round(done * 2 * n * H * D * 2 / dt / 1e9, 4), "unit": "GB/s", "cores": n_workers,
+               "kind": "oracle", "sample": f"{done} (chunk, layer) row sets of {n} tokens x {H * D} bf16 "
+                                           f"(oracle scatter_paged, which copies the pool per call), {dt:.1f} s"}
+        pool_workers.close()
+        pool_workers.join()
+    achieved = nbytes / (kernel_ms * 1e-3) / 1e9
+    line = {
+        "metric": f"paged KV copy GB/s ({args.op}: all KV heads of every token row, page-table slots)",
+        "value": round(nbytes / (ms_per_step * 1e-3) / 1e9, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic N(0,1) rows; the workload's random page table",
+        "config": {"workload": f"{args.op} on {w.name}", "n_chunks": C, "n_layers": L, "kv_heads": H,
+                   "head_dim": D, "tokens_per_chunk": n, "page_size": P, "bytes_per_step": nbytes},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None, "kernel": "scatter_kernel",
+                     "kernel_ms": round(kernel_ms, 4)},
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
@@ -285,8 +386,11 @@ def main():
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
-    ap.add_argument("--op", choices=("rehydrate", "form_patch"), default="rehydrate",
-                    help="rehydrate: the serve-time hot path (default); form_patch: the compile step")
+    ap.add_argument("--op", choices=("rehydrate", "form_patch", "scatter", "gather"), default="rehydrate",
+                    help="rehydrate: the serve-time hot path (default); form_patch: the compile step; "
+                         "scatter / gather: the paged copies of the conditioning switch")
+    ap.add_argument("--orbit", type=int, default=1,
+                    help="form_patch: deficits averaged per unit (orbit patch of K orderings, K plane only)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print(json.dumps({"error": "this operator benchmark runs on exactly one GPU; the work shards by "
@@ -302,6 +406,9 @@ def main():
 
     if args.op == "form_patch":
         bench_form(args, pool, n_workers)
+        return
+    if args.op in ("scatter", "gather"):
+        bench_copy(args, pool, n_workers)
         return
 
     import torch
