@@ -127,8 +127,8 @@ __device__ __forceinline__ void group_sweep(int so, int qo, int lane) {
   const int kr = lane >> 3, kc = lane & 7;
   // circle positions of both pairs at step 0; every step moves positions
   // 1..15 on by one (position 0 stays)
-  int ra = kr == 0 ? 0 : kr, rb = 15 - kr;
-  int ca = kc == 0 ? 0 : kc, cb = 15 - kc;
+  int ra = kr, rb = 15 - kr;
+  int ca = kc, cb = 15 - kc;
   for (int st = 0; st < kGrp - 1; ++st) {
     const int p = min(ra, rb), q = max(ra, rb), p2 = min(ca, cb), q2 = max(ca, cb);
     const float rpp = form_lds[so + p * kLdQ + p], rqq = form_lds[so + q * kLdQ + q];
