@@ -182,6 +182,53 @@ __device__ __forceinline__ void load_tile(const FormParams& P, const float* delt
   }
 }
 
+// V <- V J for one block-Jacobi step: the 16-row tile rt of group b's
+// columns becomes V_tile Q_b (Q at form_lds + qo, group blocks in grp).  The
+// (dp / 16) x ng tiles are spread over waves [w0, w0 + nw), four at a time
+// with their MFMA chains interleaved; tiles are disjoint, so each is updated
+// in place by its wave.
+__device__ __forceinline__ void apply_v(float* V, int ld, int qo, const int* grp, int ng, int dp, int w0, int nw,
+                                        int wave, int lj, int lr) {
+  const int ntile = (dp / 16) * ng;
+  const uint32_t ng_magic = (65536u + ng - 1) / ng;
+  for (int t0 = wave - w0; t0 < ntile; t0 += 4 * nw) {
+    bool ok[4];
+    int rtile[4], gb[4], qb[4];
+    float vv[4][4], qv[4][4];
+    f32x4v vt[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int t = t0 + u * nw;
+      ok[u] = t < ntile;
+      const int rt = ok[u] ? (int)(((uint32_t)t * ng_magic) >> 16) : 0, b = ok[u] ? t - rt * ng : 0;
+      rtile[u] = rt;
+      gb[u] = grp[b];
+      qb[u] = qo + b * kGrp * kLdQ;
+      const int bi = gb[u] & 0xff, bj = gb[u] >> 8;
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb) {
+        const int k = 4 * kb + lj;
+        vv[u][kb] = ok[u] ? V[(16 * rt + lr) * ld + group_index(bi, bj, k)] : 0.f;
+        qv[u][kb] = form_lds[qb[u] + k * kLdQ + lr];
+      }
+      vt[u] = (f32x4v){0.f, 0.f, 0.f, 0.f};
+    }
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+      for (int u = 0; u < 4; ++u) vt[u] = mfma4(vv[u][kb], qv[u][kb], vt[u]);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      if (ok[u]) {
+        const int bi = gb[u] & 0xff, bj = gb[u] >> 8;
+        const int gcol = group_index(bi, bj, lr);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) V[(16 * rtile[u] + 4 * lj + i) * ld + gcol] = vt[u][i];
+      }
+    }
+  }
+}
+
 }  // namespace
 
 __global__ __launch_bounds__(kFormThreads) void form_patch_kernel(const FormParams /*by value, read in place*/) {
@@ -189,7 +236,7 @@ __global__ __launch_bounds__(kFormThreads) void form_patch_kernel(const FormPara
   float* const lds_f = form_lds;
   __shared__ int s_order[128];
   __shared__ float s_red[kWaves];
-  __shared__ int s_grp[kFormMaxDim / (2 * kBlk)];   // blocks (bi | bj << 8) of each group this step
+  __shared__ int s_grp[2][kFormMaxDim / (2 * kBlk)];   // blocks (bi | bj << 8) of each group, this and last step
 
   const int unit = blockIdx.x;
   if (unit >= P.n_units) return;
@@ -205,7 +252,7 @@ __global__ __launch_bounds__(kFormThreads) void form_patch_kernel(const FormPara
   float* G = lds_f;                          // [dp][ld]
   float* V = lds_f + dp * ld;                // [dp][ld]; holds Delta tiles in phase 1
   float* Ss = V + dp * ld;                   // [ng][16][kLdQ] group matrices
-  float* Qs = Ss + ng * kGrp * kLdQ;         // [ng][16][kLdQ] group rotations
+  float* Qs2 = Ss + ng * kGrp * kLdQ;        // [2][ng][16][kLdQ] group rotations of this and the last step
   const float* delta = P.delta + (int64_t)c * P.delta_s[0] + (int64_t)l * P.delta_s[1] + (int64_t)h * P.delta_s[2];
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63;
@@ -278,7 +325,12 @@ __global__ __launch_bounds__(kFormThreads) void form_patch_kernel(const FormPara
   }
 
   // ---- 2. block Jacobi ----
+  // Each step's V <- V J is deferred to the next step's first phase, where the
+  // waves without a group to solve apply it while the others run their inner
+  // sweeps; the Q buffers and group lists alternate between steps.
   int sweeps_run = 0;
+  int cur = 0;                                 // buffer of the step being formed
+  bool pending = false;                        // V still owes the previous step's rotation
   for (int sweep = 0; sweep < P.sweeps; ++sweep) {
     // stop once the off-diagonal mass is negligible against the diagonal
     float off = 0.f, dia = 0.f;
@@ -292,11 +344,14 @@ __global__ __launch_bounds__(kFormThreads) void form_patch_kernel(const FormPara
     if (off <= 1e-9f * dia) break;             // ~(d * 4 eps)^2: the fp32 floor
     ++sweeps_run;
     for (int step = 0; step < nb - 1; ++step) {
-      // (a) one wave per group: a Jacobi sweep on the group's principal submatrix
+      float* Qs = Qs2 + cur * ng * kGrp * kLdQ;
+      const int* grp = s_grp[cur];
+      // (a) one wave per group: a Jacobi sweep on the group's principal
+      // submatrix; the remaining waves apply the previous step to V
       if (wave < ng) {
         int bi, bj;
         circle_pair(nb, step, wave, bi, bj);
-        if (lane == 0) s_grp[wave] = bi | (bj << 8);
+        if (lane == 0) s_grp[cur][wave] = bi | (bj << 8);
         const int so = (int)(Ss - lds_f) + wave * kGrp * kLdQ;
         const int qo = (int)(Qs - lds_f) + wave * kGrp * kLdQ;
 #pragma unroll
@@ -307,6 +362,9 @@ __global__ __launch_bounds__(kFormThreads) void form_patch_kernel(const FormPara
         }
         __builtin_amdgcn_wave_barrier();
         group_sweep(so, qo, lane);
+      } else if (pending) {
+        apply_v(V, ld, (int)(Qs2 - lds_f) + (cur ^ 1) * ng * kGrp * kLdQ, s_grp[cur ^ 1], ng, dp, ng,
+                kWaves - ng, wave, lj, lr);
       }
       __syncthreads();
       // (b) G <- J^T G J: tile (a, b) becomes Q_a^T G_ab Q_b.  G stays
@@ -330,8 +388,8 @@ __global__ __launch_bounds__(kFormThreads) void form_patch_kernel(const FormPara
             }
           }
           const int b = ok[u] ? a + t : 0;
-          ga[u] = s_grp[a];
-          gb[u] = s_grp[b];
+          ga[u] = grp[a];
+          gb[u] = grp[b];
           rowa[u] = a;
           const int ai = ga[u] & 0xff, aj = ga[u] >> 8, bi = gb[u] & 0xff, bj = gb[u] >> 8;
           const float* Qb = Qs + b * kGrp * kLdQ;
@@ -378,45 +436,16 @@ __global__ __launch_bounds__(kFormThreads) void form_patch_kernel(const FormPara
           }
         }
       }
-      // V <- V J: 16-row tile rt of group b's columns becomes V_tile Q_b
-      {
-        bool ok[4];
-        int rtile[4], gb[4];
-        float vv[4][4], qv[4][4];
-        f32x4v vt[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int t = wave + u * kWaves;
-          ok[u] = t < (dp / 16) * ng;
-          const int rt = ok[u] ? (int)(((uint32_t)t * ng_magic) >> 16) : 0, b = ok[u] ? t - rt * ng : 0;
-          rtile[u] = rt;
-          gb[u] = s_grp[b];
-          const int bi = gb[u] & 0xff, bj = gb[u] >> 8;
-          const float* Qb = Qs + b * kGrp * kLdQ;
-#pragma unroll
-          for (int kb = 0; kb < 4; ++kb) {
-            const int k = 4 * kb + lj;
-            vv[u][kb] = ok[u] ? V[(16 * rt + lr) * ld + group_index(bi, bj, k)] : 0.f;
-            qv[u][kb] = Qb[k * kLdQ + lr];
-          }
-          vt[u] = (f32x4v){0.f, 0.f, 0.f, 0.f};
-        }
-#pragma unroll
-        for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-          for (int u = 0; u < 4; ++u) vt[u] = mfma4(vv[u][kb], qv[u][kb], vt[u]);
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          if (ok[u]) {
-            const int bi = gb[u] & 0xff, bj = gb[u] >> 8;
-            const int gcol = group_index(bi, bj, lr);
-#pragma unroll
-            for (int i = 0; i < 4; ++i) V[(16 * rtile[u] + 4 * lj + i) * ld + gcol] = vt[u][i];
-          }
-        }
-      }
       __syncthreads();
+      pending = true;
+      cur ^= 1;
     }
+  }
+  if (pending) {
+    // the last step's rotation of V
+    apply_v(V, ld, (int)(Qs2 - lds_f) + (cur ^ 1) * ng * kGrp * kLdQ, s_grp[cur ^ 1], ng, dp, 0, kWaves, wave, lj,
+            lr);
+    __syncthreads();
   }
   if (P.sweeps_done != nullptr && tid == 0) P.sweeps_done[unit] = sweeps_run;
 
@@ -526,16 +555,16 @@ __global__ __launch_bounds__(kFormThreads) void form_patch_kernel(const FormPara
   }
 }
 
-// LDS floats: phase 1 G [dp][dp+1] and the staged tile [32][tile_ld]; phase 2
-// G and V [dp][dp+1] each and the groups' S and Q [16][17]; phase 4 V_m
-// [dp][ldv] and a tile [32][ldu]
+// LDS floats: phase 1 G [dp][dp+1] and the staged tile [kFormTile][tile_ld];
+// phase 2 G and V [dp][dp+1] each, the groups' S [16][17] and two sets of
+// their Q [16][17]; phase 4 V_m [dp][ldv] and a tile [kFormTile][ldu]
 size_t form_lds_bytes(int dim, int m) {
   const size_t dp = (size_t)pad16(dim), ld = dp + 1, ng = dp / (2 * kBlk);
   const size_t mp = (size_t)pad16(m);
   const size_t ldv = (mp % 32 == 16) ? mp : mp + 16;
   const size_t ldu = dp + ((dp % 32 == 0) ? 2 : 18);
   const size_t f1 = dp * ld + kFormTile * (size_t)tile_ld((int)dp);
-  const size_t f2 = 2 * dp * ld + 2 * ng * kGrp * kLdQ;
+  const size_t f2 = 2 * dp * ld + 3 * ng * kGrp * kLdQ;
   const size_t f4 = dp * ldv + kFormTile * ldu;
   size_t f = f1 > f2 ? f1 : f2;
   f = f > f4 ? f : f4;
