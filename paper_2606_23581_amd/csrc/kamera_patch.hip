@@ -47,6 +47,9 @@ __host__ __device__ inline int pad16(int d) { return (d + 15) & ~15; }
 // staged Delta tile row stride: == 16 (mod 32), so the four rows one MFMA
 // operand load touches fall on disjoint banks
 __host__ __device__ inline int tile_ld(int dp) { return (dp % 32 == 16) ? dp : dp + 16; }
+// row stride of G and V: == 2 (mod 32), so an MFMA operand load of 16 rows
+// x 2 columns (half a wave) and a 16-row tile's row pieces fall on distinct banks
+__host__ __device__ inline int gv_ld(int dp) { return dp + ((2 - dp) % 32 + 32) % 32; }
 
 // circle method over `n` items at `step`: the (smaller, larger) members of pair k
 __device__ __forceinline__ void circle_pair(int n, int step, int k, int& a, int& b) {
@@ -245,7 +248,7 @@ __global__ __launch_bounds__(kFormThreads) void form_patch_kernel(const FormPara
   const int c = unit / (P.n_heads * P.n_layers);
   const int d = P.dim, n = P.n_tokens, m = P.m;
   const int dp = pad16(d);                   // padded size (zero rows/columns beyond d)
-  const int ld = dp + 1;                     // padded LDS row stride of G and V
+  const int ld = gv_ld(dp);                  // padded LDS row stride of G and V
   const int nb = dp / kBlk;                  // Jacobi blocks (even)
   const int ng = nb / 2;                     // groups rotated per step
   const uint32_t ng_magic = (65536u + ng - 1) / ng;   // t / ng == (t * ng_magic) >> 16 for t < 128
@@ -555,11 +558,11 @@ __global__ __launch_bounds__(kFormThreads) void form_patch_kernel(const FormPara
   }
 }
 
-// LDS floats: phase 1 G [dp][dp+1] and the staged tile [kFormTile][tile_ld];
-// phase 2 G and V [dp][dp+1] each, the groups' S [16][17] and two sets of
+// LDS floats: phase 1 G [dp][gv_ld] and the staged tile [kFormTile][tile_ld];
+// phase 2 G and V [dp][gv_ld] each, the groups' S [16][17] and two sets of
 // their Q [16][17]; phase 4 V_m [dp][ldv] and a tile [kFormTile][ldu]
 size_t form_lds_bytes(int dim, int m) {
-  const size_t dp = (size_t)pad16(dim), ld = dp + 1, ng = dp / (2 * kBlk);
+  const size_t dp = (size_t)pad16(dim), ld = (size_t)gv_ld((int)dp), ng = dp / (2 * kBlk);
   const size_t mp = (size_t)pad16(m);
   const size_t ldv = (mp % 32 == 16) ? mp : mp + 16;
   const size_t ldu = dp + ((dp % 32 == 0) ? 2 : 18);
