@@ -2,9 +2,12 @@
 //
 // rehydrate: K' = R(pos)(K + U W), V' = V + U_v W_v  (Eq. eq:operator, Sec. 3;
 //            serve step of App. A).  One grouped launch over
-//            (plane, chunk, layer, head, token block, column block).
+//            (plane, chunk, layer, head, token block, column block).  With a
+//            per-chunk delta the keys are already rotated and move by delta
+//            with a (removal) patch added at the target (Sec. 5, Table evict).
 // shift:     K' = R(delta) K in place (R(delta) R(p) = R(p + delta), Sec. 1).
-// scatter:   bit copy of token rows into page-table slots (App. E, Sec. 6).
+// scatter:   bit copy of token rows into page-table slots and back (App. E,
+//            Sec. 6).
 //
 // Register layout of a rehydrate tile.  A wave owns 16 tokens x one column
 // block of 32*NQ columns (NQ <= 4).  The rank-m patch U W is computed as
@@ -18,8 +21,10 @@
 // token row.  The accumulators are seeded with K (fp32), the MFMAs add U W on
 // top, and the rotation pairs are lane-local: NeoX partner of chunk q is
 // chunk q + NQ/2, interleaved partners are adjacent accumulator elements.
-// Nothing goes through LDS except W (transposed once per workgroup) and the
-// per-pair frequencies.
+// LDS holds W^T (transposed once per workgroup), the per-pair frequencies and
+// one padded 16-row buffer per wave: tiles pass through it between the
+// row-contiguous global loads/stores (4 rows x 256 B per instruction) and the
+// MFMA register layout, and U rows take the same route.
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>

@@ -132,6 +132,7 @@ __device__ __forceinline__ void group_sweep(int so, int qo, int lane) {
   // 1..15 on by one (position 0 stays)
   int ra = kr, rb = 15 - kr;
   int ca = kc, cb = 15 - kc;
+#pragma unroll 3
   for (int st = 0; st < kGrp - 1; ++st) {
     const int p = min(ra, rb), q = max(ra, rb), p2 = min(ca, cb), q2 = max(ca, cb);
     const float rpp = form_lds[so + p * kLdQ + p], rqq = form_lds[so + q * kLdQ + q];
