@@ -65,6 +65,16 @@ REHYDRATE_CASES = {
     # deep-half patch: no factors on the shallow layers, odd ranks on others
     "max_row_4096": RehydrateCase(D=4096, H=1, C=1, L=2, n=20, rope_dim=128, rope_offset=2048, m_k=8, m_v=8,
                                   patch=(0, 4096), seed=29),
+    "relocate_layer_rank_post_frame": RehydrateCase(reloc=True, post_rope=True, L=3, layer_rank=(0, 32, 7), m_k=32,
+                                                    m_v=32, seed=40),
+    "post_rope_grid_paged_shared": RehydrateCase(post_rope=True, sections=(16, 24, 24), pos_mode="grid3", grid_w=8,
+                                                 paged=True, shared_w=True, C=3, seed=41),
+    "mla_band_patch_layer_rank_shared": RehydrateCase(D=576, H=1, rope_dim=64, rope_offset=512, pairing="interleaved",
+                                                      theta=1e4, patch=(0, 512), has_v=False, m_k=32, m_v=0, m_pe=16,
+                                                      L=3, layer_rank=(16, 0, 48), shared_w=True, seed=42),
+    "explicit_ragged_paged_rank_100": RehydrateCase(pos_mode="explicit", sections=(24, 20, 20),
+                                                    section_order="interleaved", ragged=True, paged=True,
+                                                    page_size=7, m_k=100, m_v=3, n=77, C=3, seed=43),
     "layer_rank_deep_half": RehydrateCase(L=4, layer_rank=(0, 0, 16, 16), m_k=16, m_v=16, seed=27),
     "layer_rank_odd": RehydrateCase(L=3, layer_rank=(5, 64, 33), m_k=64, m_v=48, seed=28),
 }
