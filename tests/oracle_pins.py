@@ -240,6 +240,31 @@ def pin_full_rank_patch(ref):
     assert np.max(np.abs(out[:, d:] - (V[:, d:] + dK))) < 1e-15
 
 
+def pin_band_patch_composition(ref):
+    """MLA row [latent | rope key]: a latent patch (rank m on the latent
+    columns) and a separate rope-band patch (rank m_pe on the band, in the
+    stored frame) applied in turn equal one patch with the block basis
+    diag(W_lat, W_pe) and concatenated coefficients [U_lat | U_pe]; the latent
+    columns never rotate and only the band carries R(p) (k_pe' =
+    R(p)(k_pe + U_pe W_pe), checked by complex arithmetic)."""
+    rng = _rng(31)
+    n, dl, dr, m, mp = 9, 16, 8, 3, 2
+    K = rng.standard_normal((n, dl + dr))
+    Ul, Wl = rng.standard_normal((n, m)), rng.standard_normal((m, dl))
+    Up, Wp = rng.standard_normal((n, mp)), rng.standard_normal((mp, dr))
+    rope = ref.Rope(theta=1e4, rope_dim=dr, pairing="interleaved", rope_offset=dl)
+    pos = _lin_pos(77, n)
+    Wb = np.zeros((m + mp, dl + dr))
+    Wb[:m, :dl] = Wl
+    Wb[m:, dl:] = Wp
+    one = ref.rehydrate_k(K, np.concatenate([Ul, Up], axis=1), Wb, rope, pos)
+    staged = ref.rehydrate_k(ref.add_patch(K, Up, Wp, dl), Ul, Wl, rope, pos)
+    assert np.max(np.abs(one - staged)) < 1e-12
+    assert np.max(np.abs(one[:, :dl] - (K[:, :dl] + Ul @ Wl))) < 1e-12
+    band = K[:, dl:] + Up @ Wp
+    assert np.max(np.abs(one[:, dl:] - complex_rope_interleaved(band, np.arange(n) + 77, 1e4))) < 1e-10
+
+
 def pin_identity_index(ref):
     """Position 0 and no patch: cos 0 = 1, sin 0 = 0, so the stored bits come
     back unchanged."""
