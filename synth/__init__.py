@@ -12,8 +12,11 @@ datasets and model weights are not available, so every tensor here is a
 seeded stand-in with those shapes: K, V (and the MLA latent and rope key)
 ~ N(0, 1), patch coefficients U and bases W ~ N(0, 0.1^2), all rounded to bf16.
 
-``WORKLOADS`` lists the five operator workloads the benchmark and the parity
-tests use, from a one-layer GQA chunk up to the 80-layer paged recall.
+``WORKLOADS`` lists the operator workloads the benchmark and the parity tests
+use: five from a one-layer GQA chunk up to the 80-layer paged recall
+(``WORKLOAD_ORDER``), and three for the operator's other modes -- relocation
+with a removal patch, the MLA rope-band patch and deep-half factors
+(``EXTRA_WORKLOADS``).
 """
 
 from __future__ import annotations
