@@ -191,8 +191,8 @@ __device__ __forceinline__ void load_tile(const FormParams& P, const float* delt
 // (dp / 16) x ng tiles are spread over waves [w0, w0 + nw), four at a time
 // with their MFMA chains interleaved; tiles are disjoint, so each is updated
 // in place by its wave.
-__device__ __forceinline__ void apply_v(float* V, int ld, int qo, const int* grp, int ng, int dp, int w0, int nw,
-                                        int wave, int lj, int lr) {
+__device__ __forceinline__ void apply_v(float* V, int ld, int qo, const int* grp, const int* ident, int ng, int dp,
+                                        int w0, int nw, int wave, int lj, int lr) {
   const int ntile = (dp / 16) * ng;
   const uint32_t ng_magic = (65536u + ng - 1) / ng;
   for (int t0 = wave - w0; t0 < ntile; t0 += 4 * nw) {
@@ -205,6 +205,7 @@ __device__ __forceinline__ void apply_v(float* V, int ld, int qo, const int* grp
       const int t = t0 + u * nw;
       ok[u] = t < ntile;
       const int rt = ok[u] ? (int)(((uint32_t)t * ng_magic) >> 16) : 0, b = ok[u] ? t - rt * ng : 0;
+      ok[u] = ok[u] && !ident[b];            // Q_b = I leaves the tile as it is
       rtile[u] = rt;
       gb[u] = grp[b];
       qb[u] = qo + b * kGrp * kLdQ;
@@ -217,6 +218,7 @@ __device__ __forceinline__ void apply_v(float* V, int ld, int qo, const int* grp
       }
       vt[u] = (f32x4v){0.f, 0.f, 0.f, 0.f};
     }
+    if (!ok[0] && !ok[1] && !ok[2] && !ok[3]) continue;
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
@@ -241,6 +243,7 @@ __global__ __launch_bounds__(kFormThreads) void form_patch_kernel(const FormPara
   __shared__ int s_order[128];
   __shared__ float s_red[kWaves];
   __shared__ int s_grp[2][kFormMaxDim / (2 * kBlk)];   // blocks (bi | bj << 8) of each group, this and last step
+  __shared__ int s_ident[2][kFormMaxDim / (2 * kBlk)]; // group kept Q = I, this and last step
 
   const int unit = blockIdx.x;
   if (unit >= P.n_units) return;
@@ -358,17 +361,26 @@ __global__ __launch_bounds__(kFormThreads) void form_patch_kernel(const FormPara
         if (lane == 0) s_grp[cur][wave] = bi | (bj << 8);
         const int so = (int)(Ss - lds_f) + wave * kGrp * kLdQ;
         const int qo = (int)(Qs - lds_f) + wave * kGrp * kLdQ;
+        float goff = 0.f;
 #pragma unroll
         for (int u = 0; u < kGrp * kGrp / 64; ++u) {
           const int e = lane + 64 * u, r = e >> 4, cc = e & 15;
-          lds_f[so + r * kLdQ + cc] = G[group_index(bi, bj, r) * ld + group_index(bi, bj, cc)];
+          const float g = G[group_index(bi, bj, r) * ld + group_index(bi, bj, cc)];
+          lds_f[so + r * kLdQ + cc] = g;
           lds_f[qo + r * kLdQ + cc] = r == cc ? 1.f : 0.f;
+          if (r != cc) goff += g * g;
         }
+        for (int o = 32; o > 0; o >>= 1) goff += __shfl_xor(goff, o, 64);
+        // a group whose block is already diagonal to well below the
+        // convergence test (at most 120 such groups per sweep stay under it)
+        // keeps Q = I, and the tile products it would leave unchanged are skipped
+        const bool skip = goff <= 1e-12f * dia;
+        if (lane == 0) s_ident[cur][wave] = skip ? 1 : 0;
         __builtin_amdgcn_wave_barrier();
-        group_sweep(so, qo, lane);
+        if (!skip) group_sweep(so, qo, lane);
       } else if (pending) {
-        apply_v(V, ld, (int)(Qs2 - lds_f) + (cur ^ 1) * ng * kGrp * kLdQ, s_grp[cur ^ 1], ng, dp, ng,
-                kWaves - ng, wave, lj, lr);
+        apply_v(V, ld, (int)(Qs2 - lds_f) + (cur ^ 1) * ng * kGrp * kLdQ, s_grp[cur ^ 1], s_ident[cur ^ 1], ng, dp,
+                ng, kWaves - ng, wave, lj, lr);
       }
       __syncthreads();
       // (b) G <- J^T G J: tile (a, b) becomes Q_a^T G_ab Q_b.  G stays
@@ -392,6 +404,7 @@ __global__ __launch_bounds__(kFormThreads) void form_patch_kernel(const FormPara
             }
           }
           const int b = ok[u] ? a + t : 0;
+          ok[u] = ok[u] && !(s_ident[cur][a] && s_ident[cur][b]);   // both sides kept Q = I
           ga[u] = grp[a];
           gb[u] = grp[b];
           rowa[u] = a;
@@ -407,6 +420,7 @@ __global__ __launch_bounds__(kFormThreads) void form_patch_kernel(const FormPara
           mt[u] = (f32x4v){0.f, 0.f, 0.f, 0.f};
           tt[u] = (f32x4v){0.f, 0.f, 0.f, 0.f};
         }
+        if (!ok[0] && !ok[1]) continue;
 #pragma unroll
         for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
@@ -447,8 +461,8 @@ __global__ __launch_bounds__(kFormThreads) void form_patch_kernel(const FormPara
   }
   if (pending) {
     // the last step's rotation of V
-    apply_v(V, ld, (int)(Qs2 - lds_f) + (cur ^ 1) * ng * kGrp * kLdQ, s_grp[cur ^ 1], ng, dp, 0, kWaves, wave, lj,
-            lr);
+    apply_v(V, ld, (int)(Qs2 - lds_f) + (cur ^ 1) * ng * kGrp * kLdQ, s_grp[cur ^ 1], s_ident[cur ^ 1], ng, dp, 0,
+            kWaves, wave, lj, lr);
     __syncthreads();
   }
   if (P.sweeps_done != nullptr && tid == 0) P.sweeps_done[unit] = sweeps_run;
