@@ -142,8 +142,9 @@ def _oracle_form(job):
 
 
 def form_flops(n: int, d: int, m: int, sweeps: int, orbit: int = 1) -> int:
-    """Flops the patch-forming kernel performs on one unit (padded sizes, as
-    executed): the Gram matrix on the upper-triangle 16x16 tiles, `sweeps`
+    """Flops of the patch-forming kernel on one unit (padded sizes, every group
+    and tile counted, including those the kernel skips once a group is already
+    diagonal, so an upper bound on the executed work): the Gram matrix on the upper-triangle 16x16 tiles, `sweeps`
     block-Jacobi sweeps of dp/8 - 1 steps each (one 15-step cyclic sweep of
     24 flops per 2x2 block and 6 per rotated Q pair in each of the dp/16
     groups, then the 16x16 tile products Q_a^T G_ab Q_b on the upper triangle
