@@ -326,6 +326,20 @@ int kamera_check_page_table(const int32_t* host_page_table, int32_t n_chunks,
  * Touches no device memory. */
 int kamera_validate(int32_t which, const void* args);
 
+/* Which kernel kamera_rehydrate would launch for `args`, after exactly its
+ * host-side checks: KAMERA_PLAN_PER_HEAD (one workgroup per plane, chunk,
+ * layer, head, token block and column block), KAMERA_PLAN_ROW_GROUP (one
+ * workgroup per plane, chunk, layer and token block taking every head of a
+ * token row, so that a pool page is written as one contiguous run; chosen for
+ * rows of <= 8 heads of 128 columns, rank <= 64, linear or grid positions, no
+ * relocation, paged output or dense output without row_base), KAMERA_PLAN_NONE
+ * for a call with nothing to do, or the negative error code the call would
+ * return.  Touches no device memory.  Both kernels compute the same bits. */
+#define KAMERA_PLAN_NONE 0
+#define KAMERA_PLAN_PER_HEAD 1
+#define KAMERA_PLAN_ROW_GROUP 2
+int kamera_rehydrate_plan(const kamera_rehydrate_args* args);
+
 /* Text of the last error on the calling thread ("" after a successful call);
  * valid until the next call on that thread. */
 const char* kamera_last_error(void);

@@ -49,6 +49,9 @@ POS_GRID3 = 1
 POS_EXPLICIT = 2
 PATCH_PRE_ROPE = 0
 PATCH_POST_ROPE = 1
+PLAN_NONE = 0
+PLAN_PER_HEAD = 1
+PLAN_ROW_GROUP = 2
 
 
 class KameraUnavailable(RuntimeError):
@@ -119,7 +122,8 @@ class CFormArgs(ctypes.Structure):
 EXPORTS = ("kamera_rehydrate", "kamera_shift", "kamera_scatter_paged", "kamera_gather_paged",
            "kamera_form_patch",
            "kamera_check_page_table",
-           "kamera_validate", "kamera_last_error", "kamera_abi_version", "kamera_struct_size")
+           "kamera_validate", "kamera_rehydrate_plan", "kamera_last_error", "kamera_abi_version",
+           "kamera_struct_size")
 
 _LIB = None
 
@@ -167,6 +171,8 @@ def lib() -> ctypes.CDLL:
     L.kamera_form_patch.restype = _i32
     L.kamera_validate.argtypes = [_i32, _vp]
     L.kamera_validate.restype = _i32
+    L.kamera_rehydrate_plan.argtypes = [ctypes.POINTER(CRehydrateArgs)]
+    L.kamera_rehydrate_plan.restype = _i32
     L.kamera_struct_size.argtypes = [_i32]
     L.kamera_struct_size.restype = _i64
     sizes = {0: CRehydrateArgs, 1: CShiftArgs, 2: CScatterArgs, 3: CPlane, 4: CRope, 5: CFormArgs}
@@ -307,6 +313,14 @@ class Prepared:
 def rehydrate(*a, stream=None, **kw) -> None:
     """``kamera_rehydrate``; see ``prepare_rehydrate`` for the arguments."""
     prepare_rehydrate(*a, **kw).launch(stream)
+
+
+def rehydrate_plan(prepared: "Prepared") -> int:
+    """``kamera_rehydrate_plan`` of a prepared rehydrate call: PLAN_PER_HEAD or
+    PLAN_ROW_GROUP (the kernel the call launches), PLAN_NONE, or an error."""
+    rc = lib().kamera_rehydrate_plan(ctypes.byref(prepared.args))
+    _check(min(rc, 0))
+    return rc
 
 
 def prepare_rehydrate(k_in, k_out, *, rope: RopeSpec, chunk_pos=None, v_in=None, v_out=None,

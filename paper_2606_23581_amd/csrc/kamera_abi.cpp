@@ -365,6 +365,48 @@ static int build_rehydrate(const kamera_rehydrate_args* a, kamera::RehydratePara
     o.n_blocks = nb;
     units += (int64_t)a->n_chunks * a->n_layers * a->n_heads * nb;
   }
+  // Rows of <= 8 heads of 128 columns, one block per head, rank <= 64 and
+  // no relocation: one workgroup takes every head of a token row, so a pool
+  // page is written as one contiguous run.
+  bool rows = P.delta == nullptr && a->n_heads <= kamera::kRgMaxHeads && a->head_dim == 128 &&
+              (!any_rot || a->pos_mode != KAMERA_POS_EXPLICIT) && (a->paged || a->row_base == nullptr);
+  for (int p = 0; p < a->n_planes && rows; ++p) {
+    kamera::PlaneParams& o = P.plane[p];
+    const kamera::ColBlock& b = o.blk[0];
+    rows = o.n_blocks == 1 && b.col0 == 0 && b.nq == 4 && o.m_steps <= 2 &&
+           (o.m == 0 || (o.patch_lo == 0 && o.patch_hi == 128 && o.u_vec));
+    for (int d = 0; d < 4 && rows; ++d) rows = o.in_s[d] >= 0 && o.out_s[d] >= 0 && (o.m == 0 || o.u_s[d] >= 0);
+    if (!rows) break;
+    // the buffer instructions of that kernel take 32-bit byte offsets within
+    // one (chunk, layer) slab, or within one layer of the pool
+    const int64_t n1 = a->n_tokens - 1, h1 = a->n_heads - 1;
+    const int64_t in_rec = (n1 * o.in_s[2] + h1 * o.in_s[3] + 128) * 2;
+    const int64_t u_rec = o.m > 0 ? (h1 * o.u_s[2] + n1 * o.u_s[3] + o.m) * 2 : 0;
+    const int64_t rows_out = a->paged ? (int64_t)a->n_pool_pages * a->page_size - 1 : n1;
+    const int64_t out_rec = (rows_out * o.out_s[2] + h1 * o.out_s[3] + 128) * 2;
+    const int64_t lim = 0x7ffffff0;
+    rows = in_rec <= lim && u_rec <= lim && out_rec <= lim;
+    o.in_rec = (int32_t)in_rec;
+    o.u_rec = (int32_t)u_rec;
+    o.out_rec = (int32_t)out_rec;
+  }
+  if (rows) {
+    int tb = 1024;
+    while (tb > 64 && (int64_t)a->n_planes * a->n_chunks * a->n_layers * ceil_div(a->n_tokens, tb) < 2048) tb /= 2;
+    tb = (int)std::min<int64_t>(tb, ceil_div(a->n_tokens, 64) * 64);
+    P.row_group = 1;
+    P.token_block = tb;
+    P.n_tblk = (int32_t)ceil_div(a->n_tokens, tb);
+    P.blocks_per_group = a->n_planes;
+    const int64_t n_tasks = (int64_t)a->n_planes * a->n_chunks * a->n_layers * P.n_tblk;
+    if (n_tasks >= (int64_t)1 << 31)
+      return fail(KAMERA_ERR_RANGE, "%s: %lld tasks exceed one launch", who, (long long)n_tasks);
+    P.n_tasks = n_tasks;
+    rc = pick_grid(P.n_tasks, P.per_xcd, who);
+    if (rc) return rc;
+    launch = true;
+    return KAMERA_OK;
+  }
   // token block: as large as possible while keeping >= 16 workgroups per CU
   int tb = 1024;
   while (tb > 64 && units * ceil_div(a->n_tokens, tb) < 4096) tb /= 2;
@@ -667,6 +709,16 @@ extern "C" int kamera_validate(int32_t which, const void* args) {
     default: return fail(KAMERA_ERR_SHAPE, "kamera_validate: unknown entry point %d", which);
   }
   return rc ? rc : ok();
+}
+
+extern "C" int kamera_rehydrate_plan(const kamera_rehydrate_args* a) {
+  static thread_local kamera::RehydrateParams P;
+  bool launch = false;
+  const int rc = build_rehydrate(a, P, launch);
+  if (rc) return rc;
+  ok();
+  if (!launch) return KAMERA_PLAN_NONE;
+  return P.row_group ? KAMERA_PLAN_ROW_GROUP : KAMERA_PLAN_PER_HEAD;
 }
 
 // ---------------------------------------------------------------------------

@@ -12,6 +12,7 @@ constexpr int kThreads = 256;        // 4 wave64 per workgroup
 constexpr int kTileTokens = 16;      // tokens per wave tile (MFMA N dimension)
 constexpr int kMaxBlocks = 36;       // column blocks per row (head_dim <= 4096)
 constexpr int kMaxPairs = 64;        // rotated pairs (rope_dim <= 128)
+constexpr int kRgMaxHeads = 8;       // heads of a row taken by one row-group workgroup
 
 enum BlockFlags : int { kBlkPatch = 1, kBlkRotate = 2 };
 
@@ -50,6 +51,8 @@ struct PlaneParams {
   int32_t n_blocks;
   int32_t block_base;                // index of this plane's first block within a task group
   const int32_t* layer_rank;         // optional per-layer rank (<= m)
+  int32_t in_rec, u_rec, out_rec;    // row-group form: bytes of one (chunk, layer) input / U slab and
+  int32_t pad_;                      // of one output slab (a layer's pool when paged)
   ColBlock blk[kMaxBlocks];
 };
 
@@ -83,7 +86,7 @@ struct RehydrateParams {
   int32_t n_tblk;                    // token blocks per chunk
   int32_t per_xcd;                   // tasks per XCD slice of the grid
   int32_t blocks_per_group;          // column blocks of all planes for one (chunk, layer, head, token block)
-  int32_t pad2_;
+  int32_t row_group;                 // 1: one workgroup per (plane, chunk, layer, token block), all heads
   int64_t n_tasks;
 };
 

@@ -95,6 +95,10 @@ class RehydrateCase:
     reloc: bool = False                # keys already rotated; move by a per-chunk delta
     m_pe: int = 0                      # separate patch on the rope band (MLA k_pe), keys only
     layer_rank: Optional[Tuple[int, ...]] = None   # rank used per layer (both planes)
+    row_base: bool = True              # dense output: chunks at permuted row bases, else chunk c at rows c*n..
+    in_place: bool = False             # dense output without row_base written over the input
+    unit_major: bool = False           # input memory [C, L, H, n, D] (rows of one head contiguous)
+    plan: Optional[int] = None         # kernel kamera_rehydrate_plan must report for the case
     seed: int = 0
 
 
@@ -146,16 +150,39 @@ def run_rehydrate(case: RehydrateCase, device):
         pt = rng.permutation(n_pool_pages)[: C * pages].reshape(C, pages).astype(np.int32)
         slots = n_pool_pages * case.page_size
         out_shape = (L, slots, H, D)
-    else:
+    elif case.row_base:
         row_base = (rng.permutation(C) * (n + 3)).astype(np.int32)
         rows = int(row_base.max()) + n + 3
         out_shape = (L, rows, H, D)
+    else:
+        # chunk c at rows c*n .. c*n + n - 1 of a [L, C*n, H, D] buffer, seen as [C, L, n, H, D]
+        row_base = (np.arange(C) * n).astype(np.int32)
+        out_shape = (L, C * n, H, D)
+    assert not case.in_place or (not case.paged and not case.row_base and not case.ragged)
 
     rs = km.RopeSpec(theta=case.theta, rope_dim=case.rope_dim, pairing=case.pairing,
                      rope_offset=case.rope_offset, sections=case.sections,
                      section_order=case.section_order)
-    k_out = dev(np.full(out_shape, SENTINEL, np.uint16), device)
-    v_out = dev(np.full(out_shape, SENTINEL, np.uint16), device) if case.has_v else None
+    def chunk_rows(X):
+        # [C, L, n, H, D] numpy -> its [L, C*n, H, D] memory
+        return np.ascontiguousarray(X.transpose(1, 0, 2, 3, 4).reshape(L, C * n, H, D))
+
+    def rows_view(t):
+        # a [L, C*n, H, D] device buffer as the [C, L, n, H, D] tensor the call takes
+        st = t.stride()
+        return t.as_strided((C, L, n, H, D), (n * st[1], st[0], st[1], st[2], st[3]))
+
+    def dev_in(X):
+        if case.unit_major:
+            return dev(np.ascontiguousarray(X.transpose(0, 1, 3, 2, 4)), device).permute(0, 1, 3, 2, 4)
+        return dev(X, device)
+
+    if case.in_place:
+        k_out = dev(chunk_rows(K), device)
+        v_out = dev(chunk_rows(V), device) if case.has_v else None
+    else:
+        k_out = dev(np.full(out_shape, SENTINEL, np.uint16), device)
+        v_out = dev(np.full(out_shape, SENTINEL, np.uint16), device) if case.has_v else None
 
     def wt(W):
         if W is None:
@@ -179,15 +206,22 @@ def run_rehydrate(case: RehydrateCase, device):
         lr = dev_i32(np.array(case.layer_rank), device)
         kw.update(k_layer_rank=lr, v_layer_rank=lr, pe_layer_rank=lr)
     if case.has_v:
-        kw.update(v_in=dev(V, device), u_v=dev(Uv, device) if Uv is not None else None, w_v=wt(Wv),
-                  v_patch=case.patch)
+        kw.update(v_in=rows_view(v_out) if case.in_place else dev_in(V),
+                  u_v=dev(Uv, device) if Uv is not None else None, w_v=wt(Wv), v_patch=case.patch)
     if case.paged:
         kw.update(page_table=dev_i32(pt, device), page_size=case.page_size, n_pool_pages=n_pool_pages)
-        km.rehydrate(dev(K, device), k_out, v_out=v_out, **kw)
-    else:
+        prep = km.prepare_rehydrate(dev_in(K), k_out, v_out=v_out, **kw)
+    elif case.row_base:
         ko = k_out.unsqueeze(0).expand(C, *out_shape)
         vo = v_out.unsqueeze(0).expand(C, *out_shape) if case.has_v else None
-        km.rehydrate(dev(K, device), ko, v_out=vo, row_base=dev_i32(row_base, device), **kw)
+        prep = km.prepare_rehydrate(dev_in(K), ko, v_out=vo, row_base=dev_i32(row_base, device), **kw)
+    else:
+        ko = rows_view(k_out)
+        vo = rows_view(v_out) if case.has_v else None
+        prep = km.prepare_rehydrate(ko if case.in_place else dev_in(K), ko, v_out=vo, **kw)
+    if case.plan is not None:
+        assert km.rehydrate_plan(prep) == case.plan
+    prep.launch()
     import torch
 
     torch.cuda.synchronize()

@@ -77,6 +77,29 @@ REHYDRATE_CASES = {
                                                     page_size=7, m_k=100, m_v=3, n=77, C=3, seed=43),
     "layer_rank_deep_half": RehydrateCase(L=4, layer_rank=(0, 0, 16, 16), m_k=16, m_v=16, seed=27),
     "layer_rank_odd": RehydrateCase(L=3, layer_rank=(5, 64, 33), m_k=64, m_v=48, seed=28),
+    # the row-group kernel (all heads of a token row per workgroup) and where it is not used
+    "rows_h8_mrope_grid_paged_m64": RehydrateCase(H=8, n=100, sections=(16, 24, 24), pos_mode="grid3", grid_w=32,
+                                                  paged=True, m_k=64, m_v=64, p0_range=(1, 4097),
+                                                  plan=2, seed=50),
+    "rows_h3_interleaved_page24_ragged": RehydrateCase(pairing="interleaved", theta=1e4, paged=True, page_size=24,
+                                                       ragged=True, C=4, n=90, m_k=40, m_v=8, plan=2, seed=51),
+    "rows_h1_dense_rope_only": RehydrateCase(H=1, row_base=False, m_k=0, m_v=0, plan=2, seed=52),
+    "rows_h8_dense_in_place": RehydrateCase(H=8, row_base=False, in_place=True, m_k=32, m_v=16, n=70,
+                                            plan=2, seed=53),
+    "rows_layer_rank_odd_paged": RehydrateCase(L=3, layer_rank=(20, 0, 64), m_k=64, m_v=64, paged=True,
+                                               plan=2, seed=54),
+    "rows_post_rope_unit_major": RehydrateCase(H=4, post_rope=True, unit_major=True, paged=True, plan=2, seed=55),
+    "rows_unit_major_long_blocks": RehydrateCase(H=8, C=1, L=1, n=1100, unit_major=True, paged=True, m_k=64,
+                                                 m_v=64, sections=(16, 24, 24), pos_mode="grid3",
+                                                 plan=2, seed=56),
+    "rows_shared_basis_v_patch_only": RehydrateCase(H=2, shared_w=True, C=3, m_k=0, m_v=24, paged=True,
+                                                    plan=2, seed=57),
+    "rows_one_token": RehydrateCase(H=8, n=1, paged=True, plan=2, seed=58),
+    "rows_k_only": RehydrateCase(H=8, has_v=False, row_base=False, m_k=48, n=33, plan=2, seed=59),
+    "per_head_row_base": RehydrateCase(H=8, m_k=64, m_v=64, plan=1, seed=60),
+    "per_head_explicit_paged": RehydrateCase(H=8, pos_mode="explicit", paged=True, plan=1, seed=61),
+    "per_head_rank_72_paged": RehydrateCase(H=8, m_k=72, m_v=8, paged=True, plan=1, seed=62),
+    "per_head_9_heads_paged": RehydrateCase(H=9, paged=True, plan=1, seed=63),
 }
 
 
@@ -189,25 +212,40 @@ def test_rehydrate_empty_call_writes_nothing(device):
     assert np.all(bits(out) == SENTINEL)
 
 
-def test_rehydrate_bad_page_is_flagged_not_written(device):
-    """A page number outside the pool is skipped by the kernel and flagged."""
+@pytest.mark.parametrize("kernel", ["per_head", "row_group"])
+def test_rehydrate_bad_page_is_flagged_not_written(device, kernel):
+    """A page number outside the pool is skipped by the kernel and flagged
+    (explicit positions take the per-head kernel, linear ones the row-group
+    kernel)."""
     import paper_2606_23581_amd as km
     import torch
 
-    print("[case] rehydrate bad page", flush=True)
+    print(f"[case] rehydrate bad page {kernel}", flush=True)
     rng = np.random.default_rng(31)
     C, L, n, H, D, P = 1, 1, 32, 2, 128, 16
     K = synth.randn_bf16_numpy((C, L, n, H, D), 1.0, rng)
     pt = np.array([[1, 7]], dtype=np.int32)       # page 7 is outside a 3-page pool
     pool = dev(np.full((L, 3 * P, H, D), SENTINEL, np.uint16), device)
     status = dev_i32(np.zeros(1), device)
-    km.rehydrate(dev(K, device), pool, rope=km.RopeSpec(theta=1e4, rope_dim=128),
-                 pos_mode=km.POS_EXPLICIT, explicit_pos=dev_i32(np.zeros((C, n, 3)), device),
-                 page_table=dev_i32(pt, device), page_size=P, n_pool_pages=3, status=status)
+    rs = km.RopeSpec(theta=1e4, rope_dim=128)
+    if kernel == "per_head":
+        pos = dict(pos_mode=km.POS_EXPLICIT, explicit_pos=dev_i32(np.zeros((C, n, 3)), device))
+    else:
+        pos = dict(pos_mode=km.POS_LINEAR, chunk_pos=dev_i32(np.zeros((C, 3)), device))
+    prep = km.prepare_rehydrate(dev(K, device), pool, rope=rs, page_table=dev_i32(pt, device), page_size=P,
+                                n_pool_pages=3, status=status, **pos)
+    assert km.rehydrate_plan(prep) == (km.PLAN_PER_HEAD if kernel == "per_head" else km.PLAN_ROW_GROUP)
+    prep.launch()
     torch.cuda.synchronize()
     assert int(status.cpu()[0]) & km.STATUS_BAD_PAGE
     out = bits(pool)
-    assert np.array_equal(out[0, P:2 * P], K[0, 0, :P])     # page 1 written (position 0: identity)
+    if kernel == "per_head":
+        assert np.array_equal(out[0, P:2 * P], K[0, 0, :P])     # page 1 written (position 0: identity)
+    else:
+        for h in range(H):                                      # page 1 holds tokens 0..15 at positions 0..15
+            want = ref.rehydrate_k(ref.bf16_to_f64(K[0, 0, :P, h]), None, None, oracle_rope(rs),
+                                   ref.positions_linear(0, P))
+            assert_close(out[0, P:2 * P, h], want, f"page 1 h{h}")
     assert np.all(out[0, :P] == SENTINEL) and np.all(out[0, 2 * P:] == SENTINEL)
 
 

@@ -166,6 +166,11 @@ def test_workload_window_slides(device):
     rng = np.random.default_rng(5)
     gen = torch.Generator(device=device)
     gen.manual_seed(77)
+    # slot S-1 survives every one of the slides: its chained drift is measured
+    # against one direct shift by slides * delta
+    last = w.window_slots - 1
+    assert all(last in synth.window_survivor_slots(w, k) for k in range(w.slides))
+    chain0 = bits(T["window"][w.n_layers - 1, last * n:(last + 1) * n])
     for k in range(w.slides):
         p.extra["set_slide"](k)
         slots = synth.window_survivor_slots(w, k)
@@ -185,5 +190,16 @@ def test_workload_window_slides(device):
         fresh = synth.randn_bf16_device((w.n_layers, n, w.n_heads, w.head_dim), 1.0, gen, device)
         T["window"][:, evict * n:(evict + 1) * n].copy_(fresh)
         del fresh
+    chained = ref.bf16_to_f64(bits(T["window"][w.n_layers - 1, last * n:(last + 1) * n]))
+    total = w.slides * w.delta
+    drift = 0.0
+    for h in range(w.n_heads):
+        direct = ref.shift_k(ref.bf16_to_f64(chain0[:, h]), orope, (total,) * 3)
+        drift = max(drift, float(np.max(np.abs(chained[:, h] - direct) / np.maximum(1, np.abs(direct)))))
+    # reported: each slide rounds to bf16 once, so the drift grows at most
+    # linearly in the number of slides; the bound below is only a sanity check
+    print(f"[drift] {w.slides} chained slides vs one shift by {total}: "
+          f"max rel err {drift:.3e} = {drift / 2.0 ** -8:.2f} x the bf16 unit roundoff 2^-8", flush=True)
+    assert drift <= w.slides * 2.0 ** -7
     del p
     _free()
