@@ -503,6 +503,11 @@ def main():
         pool.join()
 
     traffic = measured_traffic(w.name, p.bytes_per_step)
+    if w.kind == "rehydrate":
+        plan = km.rehydrate_plan(p.extra["call"])
+        kernel_name = "rehydrate_rows_kernel" if plan == km.PLAN_ROW_GROUP else "rehydrate_kernel"
+    else:
+        kernel_name = "shift_kernel"
     line = {
         "metric": "rehydrated KV GB/s (rotate + rank-m patch) and % of HBM peak; chunks/s",
         "value": round(value, 2),
@@ -527,7 +532,7 @@ def main():
         "chunks_per_s": round(w.n_chunks / (ms_per_step * 1e-3), 1),
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBPS, 4),
-                     "traffic": traffic, "kernel": "rehydrate_kernel" if w.kind == "rehydrate" else "shift_kernel",
+                     "traffic": traffic, "kernel": kernel_name,
                      "kernel_ms": round(kernel_ms, 4)},
         "timing": {"event_mean_ms": round(kernel_ms, 4), "event_median_ms": round(median_ms, 4),
                    "event_min_ms": round(step_ms[0], 4), "wall_ms_per_step": round(wall * 1e3 / args.steps, 4),

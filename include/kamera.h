@@ -54,7 +54,7 @@
 extern "C" {
 #endif
 
-#define KAMERA_ABI_VERSION 1
+#define KAMERA_ABI_VERSION 2
 
 /* Largest patch rank m accepted (>= the 128-wide head, so a full-rank patch
  * that reproduces any Delta K exactly can be applied). */
@@ -96,6 +96,25 @@ typedef enum {
   KAMERA_POS_EXPLICIT = 2  /* token i of chunk c at explicit_pos[c*explicit_
                               chunk_stride + i*3 + (0,1,2)]                   */
 } kamera_pos_mode;
+
+/* Which rehydrate kernel a call uses.  Both compute the same bits.
+ * PER_HEAD: one workgroup per (plane, chunk, layer, head, token block, column
+ * block); any row layout.  ROW_GROUP: one workgroup per (plane, chunk, layer,
+ * token block) taking every head of a token row, so that a 16-token pool page
+ * is written as one contiguous run; possible for rows of <= 8 heads of 128
+ * columns (one block per head, the rope band if any being the whole head),
+ * rank <= 64 in whole 16-byte U chunks, linear or grid positions, no
+ * relocation, and byte offsets below 2^31 within one (chunk, layer) slab or
+ * one layer of the pool.  AUTO takes ROW_GROUP where it was measured faster on
+ * MI355X: 8 heads, >= 1024 tokens per chunk and >= 2048 workgroups of 1024
+ * tokens (e.g. 64 chunks x 80 layers x K and V); the per-head kernel keeps
+ * small grids and narrower rows.  A ROW_GROUP request that is not possible
+ * falls back to PER_HEAD. */
+typedef enum {
+  KAMERA_KERNEL_AUTO = 0,
+  KAMERA_KERNEL_PER_HEAD = 1,
+  KAMERA_KERNEL_ROW_GROUP = 2
+} kamera_kernel_choice;
 
 typedef enum {
   KAMERA_PATCH_PRE_ROPE = 0,  /* K' = R(pos)(K + U W): the patch lives in the
@@ -204,6 +223,7 @@ typedef struct {
   int32_t n_pool_pages;
   uint32_t* status;            /* optional device word, bits OR-ed in          */
   const int32_t* delta;        /* optional: relocation of rotated keys         */
+  int32_t kernel;              /* kamera_kernel_choice (0: AUTO)               */
 } kamera_rehydrate_args;
 
 /* kamera_shift -- K' = R(delta_c) K in place on the rope band of every token
@@ -326,15 +346,11 @@ int kamera_check_page_table(const int32_t* host_page_table, int32_t n_chunks,
  * Touches no device memory. */
 int kamera_validate(int32_t which, const void* args);
 
-/* Which kernel kamera_rehydrate would launch for `args`, after exactly its
- * host-side checks: KAMERA_PLAN_PER_HEAD (one workgroup per plane, chunk,
- * layer, head, token block and column block), KAMERA_PLAN_ROW_GROUP (one
- * workgroup per plane, chunk, layer and token block taking every head of a
- * token row, so that a pool page is written as one contiguous run; chosen for
- * rows of <= 8 heads of 128 columns, rank <= 64, linear or grid positions, no
- * relocation, paged output or dense output without row_base), KAMERA_PLAN_NONE
- * for a call with nothing to do, or the negative error code the call would
- * return.  Touches no device memory.  Both kernels compute the same bits. */
+/* Which kernel kamera_rehydrate would launch for `args` (see
+ * kamera_kernel_choice), after exactly its host-side checks:
+ * KAMERA_PLAN_PER_HEAD, KAMERA_PLAN_ROW_GROUP, KAMERA_PLAN_NONE for a call
+ * with nothing to do, or the negative error code the call would return.
+ * Touches no device memory. */
 #define KAMERA_PLAN_NONE 0
 #define KAMERA_PLAN_PER_HEAD 1
 #define KAMERA_PLAN_ROW_GROUP 2

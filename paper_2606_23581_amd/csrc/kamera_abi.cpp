@@ -188,6 +188,8 @@ static int build_rehydrate(const kamera_rehydrate_args* a, kamera::RehydratePara
     return fail(KAMERA_ERR_RANGE, "%s: head_dim %d exceeds %d", who, a->head_dim, KAMERA_MAX_HEAD_DIM);
   if (a->n_planes != 1 && a->n_planes != 2)
     return fail(KAMERA_ERR_SHAPE, "%s: n_planes must be 1 or 2 (got %d)", who, a->n_planes);
+  if (a->kernel != KAMERA_KERNEL_AUTO && a->kernel != KAMERA_KERNEL_PER_HEAD && a->kernel != KAMERA_KERNEL_ROW_GROUP)
+    return fail(KAMERA_ERR_SHAPE, "%s: unknown kernel choice %d", who, a->kernel);
   if (a->patch_frame != KAMERA_PATCH_PRE_ROPE && a->patch_frame != KAMERA_PATCH_POST_ROPE)
     return fail(KAMERA_ERR_SHAPE, "%s: unknown patch_frame %d", who, a->patch_frame);
   bool any_rot = false;
@@ -368,8 +370,14 @@ static int build_rehydrate(const kamera_rehydrate_args* a, kamera::RehydratePara
   // Rows of <= 8 heads of 128 columns, one block per head, rank <= 64 and
   // no relocation: one workgroup takes every head of a token row, so a pool
   // page is written as one contiguous run.
-  bool rows = P.delta == nullptr && a->n_heads <= kamera::kRgMaxHeads && a->head_dim == 128 &&
-              (!any_rot || a->pos_mode != KAMERA_POS_EXPLICIT) && (a->paged || a->row_base == nullptr);
+  // AUTO takes it where it measured faster: full 8-head rows and a grid of
+  // >= 2048 workgroups of 1024 tokens; smaller grids keep the per-head kernel.
+  const int64_t big_grid = (int64_t)a->n_planes * a->n_chunks * a->n_layers * ceil_div(a->n_tokens, 1024);
+  const bool want_rows = a->kernel == KAMERA_KERNEL_ROW_GROUP ||
+                         (a->kernel == KAMERA_KERNEL_AUTO && a->n_heads == kamera::kRgMaxHeads &&
+                          a->n_tokens >= 1024 && big_grid >= 2048);
+  bool rows = want_rows && P.delta == nullptr && a->n_heads <= kamera::kRgMaxHeads && a->head_dim == 128 &&
+              (!any_rot || a->pos_mode != KAMERA_POS_EXPLICIT);
   for (int p = 0; p < a->n_planes && rows; ++p) {
     kamera::PlaneParams& o = P.plane[p];
     const kamera::ColBlock& b = o.blk[0];
@@ -378,7 +386,8 @@ static int build_rehydrate(const kamera_rehydrate_args* a, kamera::RehydratePara
     for (int d = 0; d < 4 && rows; ++d) rows = o.in_s[d] >= 0 && o.out_s[d] >= 0 && (o.m == 0 || o.u_s[d] >= 0);
     if (!rows) break;
     // the buffer instructions of that kernel take 32-bit byte offsets within
-    // one (chunk, layer) slab, or within one layer of the pool
+    // one (chunk, layer) slab (dense output: from the chunk's row base on), or
+    // within one layer of the pool
     const int64_t n1 = a->n_tokens - 1, h1 = a->n_heads - 1;
     const int64_t in_rec = (n1 * o.in_s[2] + h1 * o.in_s[3] + 128) * 2;
     const int64_t u_rec = o.m > 0 ? (h1 * o.u_s[2] + n1 * o.u_s[3] + o.m) * 2 : 0;

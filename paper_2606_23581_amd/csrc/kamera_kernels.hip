@@ -555,7 +555,7 @@ __global__ __launch_bounds__(kThreads, MS == 4 || RELOC ? 3 : 4) void rehydrate_
 // ---------------------------------------------------------------------------
 // rehydrate, row-group form: rows of <= 8 heads of 128 columns with one
 // 128-column block per head (the rope band, if any, is the whole head), rank
-// <= 64, positions linear or on a grid.  A workgroup of 8 waves owns (plane,
+// <= 64, positions linear or on a grid, no relocation.  A workgroup of 8 waves owns (plane,
 // chunk, layer, token block) for every head of the row; wave h computes head
 // h in the register layout of the per-head kernel above (lane (g, t) holds
 // chunks g, g+4, g+8, g+12 of token t).  Per 16-token tile all heads move
@@ -991,7 +991,11 @@ __global__ __launch_bounds__(kRgThreads, 1) void rehydrate_rows_kernel(const Reh
   T.s_o3 = (int)Q.out_s[3];
   T.rin = rg_rsrc(Q.in + (int64_t)T.c * Q.in_s[0] + (int64_t)T.l * Q.in_s[1], Q.in_rec);
   T.ru = rg_rsrc(Q.U != nullptr ? Q.U + (int64_t)T.c * Q.u_s[0] + (int64_t)T.l * Q.u_s[1] : Q.in, Q.U != nullptr ? Q.u_rec : 0);
-  T.rout = rg_rsrc(Q.out + (P.place.paged ? 0 : (int64_t)T.c * Q.out_s[0]) + (int64_t)T.l * Q.out_s[1], Q.out_rec);
+  // paged: the layer's pool; dense: the chunk's rows from its row base on
+  const int64_t out_base = P.place.paged ? 0
+                           : (int64_t)T.c * Q.out_s[0] +
+                                 (int64_t)(P.place.row_base ? P.place.row_base[T.c] : 0) * Q.out_s[2];
+  T.rout = rg_rsrc(Q.out + out_base + (int64_t)T.l * Q.out_s[1], Q.out_rec);
   T.cp0 = T.cp1 = T.cp2 = 0.0;
   if (P.chunk_pos != nullptr) {
     T.cp0 = (double)P.chunk_pos[3 * T.c];

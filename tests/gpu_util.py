@@ -98,6 +98,7 @@ class RehydrateCase:
     row_base: bool = True              # dense output: chunks at permuted row bases, else chunk c at rows c*n..
     in_place: bool = False             # dense output without row_base written over the input
     unit_major: bool = False           # input memory [C, L, H, n, D] (rows of one head contiguous)
+    kernel: int = 0                    # kamera_kernel_choice requested (0: AUTO)
     plan: Optional[int] = None         # kernel kamera_rehydrate_plan must report for the case
     seed: int = 0
 
@@ -195,7 +196,7 @@ def run_rehydrate(case: RehydrateCase, device):
               pos_mode={"linear": km.POS_LINEAR, "grid3": km.POS_GRID3, "explicit": km.POS_EXPLICIT}[case.pos_mode],
               grid_w=case.grid_w, chunk_pos=dev_i32(pos, device),
               explicit_pos=dev_i32(explicit, device) if explicit is not None else None,
-              chunk_tokens=dev_i32(n_c, device) if case.ragged else None)
+              chunk_tokens=dev_i32(n_c, device) if case.ragged else None, kernel=case.kernel)
     status = dev_i32(np.zeros(1), device)
     kw["status"] = status
     if case.reloc:

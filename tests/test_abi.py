@@ -67,7 +67,7 @@ def test_plain_c_consumer(tmp_path):
 
 def test_version_and_struct_layout():
     L = km.lib()
-    assert L.kamera_abi_version() == 1
+    assert L.kamera_abi_version() == 2
     assert L.kamera_struct_size(0) == ctypes.sizeof(km.CRehydrateArgs)
     assert L.kamera_struct_size(1) == ctypes.sizeof(km.CShiftArgs)
     assert L.kamera_struct_size(2) == ctypes.sizeof(km.CScatterArgs)
@@ -124,6 +124,89 @@ def test_empty_call_is_a_noop():
     a.n_tokens = 0
     assert call_rehydrate(a) == km.OK
     assert km.last_error() == ""
+
+
+def _plan_case(case):
+    a = rehydrate_args()
+    a.kernel = km.KERNEL_ROW_GROUP
+    if case == "auto_small":
+        a.kernel = km.KERNEL_AUTO
+    elif case == "per_head_requested":
+        a.kernel = km.KERNEL_PER_HEAD
+    elif case == "kernel_choice_unknown":
+        a.kernel = 7
+    elif case in ("auto_recall", "auto_recall_4_heads", "auto_recall_short_chunks"):
+        # 64 chunks x 80 layers of 8 heads x 1024 tokens, token-major rows
+        a.kernel = km.KERNEL_AUTO
+        H = 4 if case == "auto_recall_4_heads" else 8
+        n = 512 if case == "auto_recall_short_chunks" else 1024
+        a.n_chunks, a.n_layers, a.n_heads, a.n_tokens = 64, 80, H, n
+        for p in range(2):
+            strides = [80 * n * H * 128, n * H * 128, H * 128, 128]
+            us = [80 * H * n * 16, H * n * 16, n * 16, 16]
+            ws = [80 * H * 16 * 128, H * 16 * 128, 16 * 128, 128]
+            for k in range(4):
+                a.plane[p].in_stride[k] = a.plane[p].out_stride[k] = strides[k]
+                a.plane[p].u_stride[k], a.plane[p].w_stride[k] = us[k], ws[k]
+    elif case == "heads_9":
+        a.n_heads = 9
+    elif case == "rank_72":
+        for p in range(2):
+            a.plane[p].m = 72
+            a.plane[p].u_stride[2], a.plane[p].u_stride[3] = 64 * 72, 72
+    elif case == "rank_12":
+        a.plane[0].m = 12
+    elif case == "explicit":
+        a.pos_mode = km.POS_EXPLICIT
+        a.explicit_pos = FAKE + 0x200000000
+    elif case == "relocation":
+        a.delta = FAKE + 0x300000000
+    elif case == "head_dim_256":
+        a.head_dim = 256
+        a.rope = km.RopeSpec(theta=1e6, rope_dim=128, rope_offset=128).to_c()
+    elif case == "partial_band":
+        a.rope = km.RopeSpec(theta=1e6, rope_dim=64, rope_offset=64).to_c()
+    elif case == "patch_64":
+        a.plane[0].patch_offset, a.plane[0].patch_dim = 32, 64
+    elif case == "offsets_past_2g":
+        for p in range(2):
+            a.plane[p].in_stride[2] = 1 << 26
+    elif case == "empty":
+        a.n_tokens = 0
+    elif case == "invalid":
+        a.plane[0].m = -1
+    return a
+
+
+@pytest.mark.parametrize("case,plan", [
+    ("default", km.PLAN_ROW_GROUP),
+    ("auto_small", km.PLAN_PER_HEAD),
+    ("per_head_requested", km.PLAN_PER_HEAD),
+    ("kernel_choice_unknown", km.ERR_SHAPE),
+    ("auto_recall", km.PLAN_ROW_GROUP),
+    ("auto_recall_4_heads", km.PLAN_PER_HEAD),
+    ("auto_recall_short_chunks", km.PLAN_PER_HEAD),
+    ("heads_9", km.PLAN_PER_HEAD),
+    ("rank_72", km.PLAN_PER_HEAD),
+    ("rank_12", km.PLAN_PER_HEAD),
+    ("explicit", km.PLAN_PER_HEAD),
+    ("relocation", km.PLAN_PER_HEAD),
+    ("head_dim_256", km.PLAN_PER_HEAD),
+    ("partial_band", km.PLAN_PER_HEAD),
+    ("patch_64", km.PLAN_PER_HEAD),
+    ("offsets_past_2g", km.PLAN_PER_HEAD),
+    ("empty", km.PLAN_NONE),
+    ("invalid", km.ERR_RANGE),
+])
+def test_rehydrate_plan_picks_the_kernel(case, plan):
+    """kamera_rehydrate_plan runs the call's host checks and names the kernel:
+    the row-group kernel, when requested, only for rows of <= 8 heads x 128
+    columns with one block per head, rank <= 64 in whole 16-byte U chunks, no
+    explicit positions or relocation, and every byte offset below 2^31; AUTO
+    takes it only for 8-head rows on a grid of >= 2048 1024-token blocks."""
+    a = _plan_case(case)
+    assert km.lib().kamera_rehydrate_plan(ctypes.byref(a)) == plan
+    assert km.lib().kamera_validate(0, ctypes.byref(a)) == min(plan, 0)
 
 
 @pytest.mark.parametrize("case,code", [
