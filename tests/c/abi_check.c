@@ -89,6 +89,18 @@ int main(void) {
   a.rope.n_sections = 2;
   CHECK(kamera_rehydrate(&a, NULL) == KAMERA_ERR_SHAPE);
 
+  /* kernel plan: AUTO keeps this small grid on the per-head kernel; the
+   * row-group kernel when requested; an unknown choice is rejected */
+  fill_rehydrate(&a);
+  CHECK(kamera_rehydrate_plan(&a) == KAMERA_PLAN_PER_HEAD);
+  a.kernel = KAMERA_KERNEL_ROW_GROUP;
+  CHECK(kamera_rehydrate_plan(&a) == KAMERA_PLAN_ROW_GROUP);
+  a.kernel = 9;
+  CHECK(kamera_rehydrate_plan(&a) == KAMERA_ERR_SHAPE);
+  fill_rehydrate(&a);
+  a.n_tokens = 0;
+  CHECK(kamera_rehydrate_plan(&a) == KAMERA_PLAN_NONE);
+
   /* page-table check on a host copy: 2 chunks x 3 pages of 16 tokens */
   int32_t pt[6] = {5, 1, 2, 0, 4, 3};
   CHECK(kamera_check_page_table(pt, 2, 3, 40, 16, 6) == KAMERA_OK);
