@@ -28,12 +28,24 @@ if ROOT not in sys.path:
 HBM_PEAK_GBPS = 8000.0
 DEFAULT_WORKLOAD = "gqa80l_64x1024_m64_mrope_paged"
 PROFILES = os.path.join(ROOT, "profiles")
-KERNEL_SRC = os.path.join(ROOT, "paper_2606_23581_amd", "csrc", "kamera_kernels.hip")
+CSRC = os.path.join(ROOT, "paper_2606_23581_amd", "csrc")
+# the source files each measured kernel is built from (its own file, the shared
+# device helpers and the launch-parameter structs)
+KERNEL_SOURCES = {
+    "rehydrate_rows_kernel": ("kamera_rows.hip", "kamera_device.h", "kamera_launch.h"),
+    "rehydrate_kernel": ("kamera_kernels.hip", "kamera_device.h", "kamera_launch.h"),
+    "shift_kernel": ("kamera_kernels.hip", "kamera_device.h", "kamera_launch.h"),
+    "scatter_kernel": ("kamera_kernels.hip", "kamera_device.h", "kamera_launch.h"),
+}
 
 
-def kernel_source_hash() -> str:
-    with open(KERNEL_SRC, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+def kernel_source_hash(kernel: str) -> str:
+    """sha256[:16] over the kernel's source files, in order."""
+    h = hashlib.sha256()
+    for name in KERNEL_SOURCES[kernel]:
+        with open(os.path.join(CSRC, name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 # ---------------------------------------------------------------------------
@@ -366,15 +378,15 @@ def bench_copy(args, pool_workers, n_workers):
     print(json.dumps(line), flush=True)
 
 
-def measured_traffic(name: str, bytes_per_launch: int):
+def measured_traffic(name: str, kernel: str):
     """HBM traffic per launch from the committed rocprofv3 counter summary, if it
-    was taken on the current kernel source (else null)."""
+    was taken on this kernel as its sources stand (else null)."""
     path = os.path.join(PROFILES, f"traffic_{name}.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
         d = json.load(f)
-    if d.get("kernel_source_sha256_16") != kernel_source_hash():
+    if f"::{kernel}<" not in d.get("kernel", "") or d.get("kernel_source_sha256_16") != kernel_source_hash(kernel):
         return None
     return d.get("hbm_bytes_per_launch")
 
@@ -502,12 +514,12 @@ def main():
         pool.close()
         pool.join()
 
-    traffic = measured_traffic(w.name, p.bytes_per_step)
     if w.kind == "rehydrate":
         plan = km.rehydrate_plan(p.extra["call"])
         kernel_name = "rehydrate_rows_kernel" if plan == km.PLAN_ROW_GROUP else "rehydrate_kernel"
     else:
         kernel_name = "shift_kernel"
+    traffic = measured_traffic(w.name, kernel_name)
     line = {
         "metric": "rehydrated KV GB/s (rotate + rank-m patch) and % of HBM peak; chunks/s",
         "value": round(value, 2),

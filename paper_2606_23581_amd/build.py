@@ -36,30 +36,36 @@ def _run(cmd, verbose):
     return res
 
 
+DEVICE_SOURCES = ("kamera_kernels.hip", "kamera_rows.hip", "kamera_patch.hip")
+
+
 def build(verbose: bool = False, save_temps: bool = False) -> str:
-    """Compile the kernels and the host ABI layer and link libkamera.so."""
+    """Compile the kernels and the host ABI layer (the objects in parallel) and
+    link libkamera.so."""
+    from concurrent.futures import ThreadPoolExecutor
+
     hipcc = _hipcc()
     os.makedirs(BUILD, exist_ok=True)
-    kobj = os.path.join(BUILD, "kamera_kernels.o")
-    pobj = os.path.join(BUILD, "kamera_patch.o")
-    aobj = os.path.join(BUILD, "kamera_abi.o")
     common = ["-std=c++17", "-fPIC", "-I", INCLUDE, "-I", CSRC]
-    kcmd = [hipcc, "-c", "-O3", f"--offload-arch={ARCH}", *NO_PACKED_FP32, *common,
-            "-Wno-unused-command-line-argument",
-            os.path.join(CSRC, "kamera_kernels.hip"), "-o", kobj]
-    if save_temps:
-        kcmd.insert(2, f"-save-temps={'obj'}")
-    _run(kcmd, verbose)
-    pcmd = [hipcc, "-c", "-O3", f"--offload-arch={ARCH}", *NO_PACKED_FP32, *common,
-            "-Wno-unused-command-line-argument", os.path.join(CSRC, "kamera_patch.hip"), "-o", pobj]
-    if save_temps:
-        pcmd.insert(2, "-save-temps=obj")
-    _run(pcmd, verbose)
+    cmds, objs = [], []
+    for src in DEVICE_SOURCES:
+        obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
+        cmd = [hipcc, "-c", "-O3", f"--offload-arch={ARCH}", *NO_PACKED_FP32, *common,
+               "-Wno-unused-command-line-argument", os.path.join(CSRC, src), "-o", obj]
+        if save_temps:
+            cmd.insert(2, "-save-temps=obj")
+        cmds.append(cmd)
+        objs.append(obj)
     # the ABI layer is plain host C++: validation and launch set-up only
-    _run(["g++", "-c", "-O2", "-Wall", "-Wextra", "-D__HIP_PLATFORM_AMD__", "-I", "/opt/rocm/include",
-          *common, os.path.join(CSRC, "kamera_abi.cpp"), "-o", aobj], verbose)
+    aobj = os.path.join(BUILD, "kamera_abi.o")
+    cmds.append(["g++", "-c", "-O2", "-Wall", "-Wextra", "-D__HIP_PLATFORM_AMD__", "-I", "/opt/rocm/include",
+                 *common, os.path.join(CSRC, "kamera_abi.cpp"), "-o", aobj])
+    objs.append(aobj)
+    with ThreadPoolExecutor(max_workers=len(cmds)) as ex:
+        for f in [ex.submit(_run, c, verbose) for c in cmds]:
+            f.result()
     tmp = LIB + ".tmp"
-    _run([hipcc, "-shared", f"--offload-arch={ARCH}", "-fPIC", kobj, pobj, aobj, "-o", tmp], verbose)
+    _run([hipcc, "-shared", f"--offload-arch={ARCH}", "-fPIC", *objs, "-o", tmp], verbose)
     os.replace(tmp, LIB)
     return LIB
 

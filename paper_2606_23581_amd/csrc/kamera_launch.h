@@ -146,6 +146,7 @@ struct FormParams {
 size_t form_lds_bytes(int dim, int m);
 
 hipError_t launch_rehydrate(const RehydrateParams& p, hipStream_t s);
+hipError_t launch_rehydrate_rows(const RehydrateParams& p, hipStream_t s);
 hipError_t launch_form_patch(const FormParams& p, hipStream_t s);
 hipError_t launch_shift(const ShiftParams& p, hipStream_t s);
 hipError_t launch_scatter(const ScatterParams& p, hipStream_t s);
