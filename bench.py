@@ -156,17 +156,19 @@ def _oracle_form(job):
 def form_flops(n: int, d: int, m: int, sweeps: int, orbit: int = 1) -> int:
     """Flops of the patch-forming kernel on one unit (padded sizes, every group
     and tile counted, including those the kernel skips once a group is already
-    diagonal, so an upper bound on the executed work): the Gram matrix on the upper-triangle 16x16 tiles, `sweeps`
-    block-Jacobi sweeps of dp/8 - 1 steps each (one 15-step cyclic sweep of
-    24 flops per 2x2 block and 6 per rotated Q pair in each of the dp/16
-    groups, then the 16x16 tile products Q_a^T G_ab Q_b on the upper triangle
-    and V_tile Q_b, plus the convergence sum), and U = Delta V_m."""
+    diagonal, so an upper bound on the executed work): the Gram matrix on the
+    upper-triangle 16x16 tiles, `sweeps` block-Jacobi sweeps of dp/8 - 1 steps
+    each (one 15-step cyclic sweep of 24 flops per 2x2 block and 6 per rotated
+    Q pair in each of the dp/16 groups -- which also yields the diagonal tiles
+    of the rotated G -- then the 16x16 tile products Q_a^T G_ab Q_b on the
+    strict upper triangle and V_tile Q_b, plus the convergence sum), and
+    U = Delta V_m."""
     dp = (d + 15) // 16 * 16
     mp = (m + 15) // 16 * 16
     nt, ng = dp // 16, dp // 16
     gram = n * 512 * nt * (nt + 1) // 2
     inner = ng * 15 * (64 * 24 + 128 * 6)
-    outer = (ng * (ng + 1) // 2) * 2 * (2 * 16 ** 3) + nt * ng * (2 * 16 ** 3)
+    outer = (ng * (ng - 1) // 2) * 2 * (2 * 16 ** 3) + nt * ng * (2 * 16 ** 3)
     per_sweep = (dp // 8 - 1) * (inner + outer) + 2 * d * d
     mean = 0 if orbit <= 1 else 2 * orbit * n * d          # orbit mean, formed in both passes over Delta
     return gram + sweeps * per_sweep + 2 * n * dp * mp + mean

@@ -126,15 +126,20 @@ __device__ __forceinline__ void rotation(float app, float aqq, float apq, float&
 // it derives both pairs' rotations itself from the values it reads, so a
 // step is one round of reads followed by one round of writes.  The wave's LDS
 // accesses are performed in program order, so no barrier is needed.
-__device__ __forceinline__ void group_sweep(int so, int qo, int lane) {
+__device__ __forceinline__ void group_sweep(int so, int qo, int lane, float* G, int ld, int bi, int bj) {
   const int kr = lane >> 3, kc = lane & 7;
   // circle positions of both pairs at step 0; every step moves positions
   // 1..15 on by one (position 0 stays)
   int ra = kr, rb = 15 - kr;
   int ca = kc, cb = 15 - kc;
+  int p = 0, q = 0, p2 = 0, q2 = 0;
+  float na = 0.f, nb = 0.f, ne = 0.f, nf = 0.f;
 #pragma unroll 3
   for (int st = 0; st < kGrp - 1; ++st) {
-    const int p = min(ra, rb), q = max(ra, rb), p2 = min(ca, cb), q2 = max(ca, cb);
+    p = min(ra, rb);
+    q = max(ra, rb);
+    p2 = min(ca, cb);
+    q2 = max(ca, cb);
     const float rpp = form_lds[so + p * kLdQ + p], rqq = form_lds[so + q * kLdQ + q];
     const float rpq = form_lds[so + p * kLdQ + q];
     const float cpp = form_lds[so + p2 * kLdQ + p2], cqq = form_lds[so + q2 * kLdQ + q2];
@@ -148,8 +153,10 @@ __device__ __forceinline__ void group_sweep(int so, int qo, int lane) {
     rotation(cpp, cqq, cpq, c2, s2, t2);
     const float a1 = c1 * a0 - s1 * e0, e1 = s1 * a0 + c1 * e0;
     const float b1 = c1 * b0 - s1 * f0, f1 = s1 * b0 + c1 * f0;
-    float na = c2 * a1 - s2 * b1, nb = s2 * a1 + c2 * b1;
-    float ne = c2 * e1 - s2 * f1, nf = s2 * e1 + c2 * f1;
+    na = c2 * a1 - s2 * b1;
+    nb = s2 * a1 + c2 * b1;
+    ne = c2 * e1 - s2 * f1;
+    nf = s2 * e1 + c2 * f1;
     if (kr == kc) {
       // the pivot block (same four addresses): exact diagonal update,
       // off-diagonal zeroed
@@ -171,6 +178,21 @@ __device__ __forceinline__ void group_sweep(int so, int qo, int lane) {
     rb = rb == 15 ? 1 : rb + 1;
     ca = ca == 0 ? 0 : (ca == 15 ? 1 : ca + 1);
     cb = cb == 15 ? 1 : cb + 1;
+  }
+  // The last step wrote every entry of S = Q^T G_gg Q: the group's diagonal
+  // tile of the rotated G.  Lanes on and above the pair diagonal store their
+  // 2x2 block with its mirror, so G stays exactly symmetric.
+  if (kr <= kc) {
+    const int gp = group_index(bi, bj, p), gq = group_index(bi, bj, q);
+    const int gp2 = group_index(bi, bj, p2), gq2 = group_index(bi, bj, q2);
+    G[gp * ld + gp2] = na;
+    G[gp * ld + gq2] = nb;
+    G[gq * ld + gp2] = ne;
+    G[gq * ld + gq2] = nf;
+    G[gp2 * ld + gp] = na;
+    G[gq2 * ld + gp] = nb;
+    G[gp2 * ld + gq] = ne;
+    G[gq2 * ld + gq] = nf;
   }
 }
 
@@ -377,33 +399,35 @@ __global__ __launch_bounds__(kFormThreads) void form_patch_kernel(const FormPara
         const bool skip = goff <= 1e-12f * dia;
         if (lane == 0) s_ident[cur][wave] = skip ? 1 : 0;
         __builtin_amdgcn_wave_barrier();
-        if (!skip) group_sweep(so, qo, lane);
+        if (!skip) group_sweep(so, qo, lane, G, ld, bi, bj);
       } else if (pending) {
         apply_v(V, ld, (int)(Qs2 - lds_f) + (cur ^ 1) * ng * kGrp * kLdQ, s_grp[cur ^ 1], s_ident[cur ^ 1], ng, dp,
                 ng, kWaves - ng, wave, lj, lr);
       }
       __syncthreads();
-      // (b) G <- J^T G J: tile (a, b) becomes Q_a^T G_ab Q_b.  G stays
-      // symmetric, so only tiles a <= b are formed (up to 3 per wave, taken
-      // two at a time with their loads issued together and their MFMA chains
-      // interleaved) and each is stored with its mirror.
-#pragma unroll
-      for (int u0 = 0; u0 < 4; u0 += 2) {
+      // (b) G <- J^T G J.  The diagonal tiles (a, a) are the groups' rotated
+      // blocks Q_a^T G_aa Q_a, written by their inner sweeps.  An off-diagonal
+      // tile (a < b) becomes Q_a^T G_ab Q_b on MFMA and is stored with its
+      // mirror, so G stays exactly symmetric: at most ng (ng - 1) / 2 = 28 of
+      // them, two per wave, their loads issued together and their MFMA chains
+      // interleaved.
+      {
+        const int ntile = ng * (ng - 1) / 2;
         bool ok[2];
         int rowa[2], ga[2], gb[2];
         float gv[2][4], qv[2][4];
         f32x4v mt[2], tt[2];
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
-          int t = wave + (u0 + u) * kWaves, a = 0;
-          ok[u] = t < ng * (ng + 1) / 2;
+          int t = wave + u * kWaves, a = 0;
+          ok[u] = t < ntile;
           if (ok[u]) {
-            while (t >= ng - a) {            // row a of the upper triangle holds ng - a tiles
-              t -= ng - a;
+            while (t >= ng - 1 - a) {        // row a of the strict upper triangle holds ng - 1 - a tiles
+              t -= ng - 1 - a;
               ++a;
             }
           }
-          const int b = ok[u] ? a + t : 0;
+          const int b = ok[u] ? a + 1 + t : 0;
           ok[u] = ok[u] && !(s_ident[cur][a] && s_ident[cur][b]);   // both sides kept Q = I
           ga[u] = grp[a];
           gb[u] = grp[b];
@@ -420,32 +444,30 @@ __global__ __launch_bounds__(kFormThreads) void form_patch_kernel(const FormPara
           mt[u] = (f32x4v){0.f, 0.f, 0.f, 0.f};
           tt[u] = (f32x4v){0.f, 0.f, 0.f, 0.f};
         }
-        if (!ok[0] && !ok[1]) continue;
+        if (ok[0] || ok[1]) {
 #pragma unroll
-        for (int kb = 0; kb < 4; ++kb)
+          for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-          for (int u = 0; u < 2; ++u) mt[u] = mfma4(gv[u][kb], qv[u][kb], mt[u]);
-        // T = Q_a^T M: step i sums k = 4 lj + i, whose M row this lane already holds
+            for (int u = 0; u < 2; ++u) mt[u] = mfma4(gv[u][kb], qv[u][kb], mt[u]);
+          // T = Q_a^T M: step i sums k = 4 lj + i, whose M row this lane already holds
 #pragma unroll
-        for (int u = 0; u < 2; ++u) {
-          const float* Qa = Qs + rowa[u] * kGrp * kLdQ;
+          for (int u = 0; u < 2; ++u) {
+            const float* Qa = Qs + rowa[u] * kGrp * kLdQ;
 #pragma unroll
-          for (int i = 0; i < 4; ++i) qv[u][i] = Qa[(4 * lj + i) * kLdQ + lr];
-        }
+            for (int i = 0; i < 4; ++i) qv[u][i] = Qa[(4 * lj + i) * kLdQ + lr];
+          }
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+          for (int i = 0; i < 4; ++i)
 #pragma unroll
-          for (int u = 0; u < 2; ++u) tt[u] = mfma4(qv[u][i], mt[u][i], tt[u]);
-        // lane (lj, lr) holds T[4 lj + i][lr]: row of group a, column of group b
+            for (int u = 0; u < 2; ++u) tt[u] = mfma4(qv[u][i], mt[u][i], tt[u]);
+          // lane (lj, lr) holds T[4 lj + i][lr]: row of group a, column of group b
 #pragma unroll
-        for (int u = 0; u < 2; ++u) {
-          if (ok[u]) {
-            const int ai = ga[u] & 0xff, aj = ga[u] >> 8, bi = gb[u] & 0xff, bj = gb[u] >> 8;
-            const bool diag = ga[u] == gb[u];
-            const int gcol = group_index(bi, bj, lr);
+          for (int u = 0; u < 2; ++u) {
+            if (ok[u]) {
+              const int ai = ga[u] & 0xff, aj = ga[u] >> 8, bi = gb[u] & 0xff, bj = gb[u] >> 8;
+              const int gcol = group_index(bi, bj, lr);
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              if (!diag || 4 * lj + i <= lr) {
+              for (int i = 0; i < 4; ++i) {
                 const int grw = group_index(ai, aj, 4 * lj + i);
                 G[grw * ld + gcol] = tt[u][i];
                 G[gcol * ld + grw] = tt[u][i];
