@@ -105,11 +105,14 @@ typedef enum {
  * columns (one block per head, the rope band if any being the whole head),
  * rank <= 64 in whole 16-byte U chunks, linear or grid positions, no
  * relocation, and byte offsets below 2^31 within one (chunk, layer) slab or
- * one layer of the pool.  AUTO takes ROW_GROUP where it was measured faster on
- * MI355X: 8 heads, >= 1024 tokens per chunk and >= 2048 workgroups of 1024
- * tokens (e.g. 64 chunks x 80 layers x K and V); the per-head kernel keeps
- * small grids and narrower rows.  A ROW_GROUP request that is not possible
- * falls back to PER_HEAD. */
+ * one layer of the pool.  A row-group workgroup takes 8 heads (one per CU),
+ * or 4 (two per CU; rows of <= 4 heads, or 8 heads in two groups).  AUTO
+ * takes ROW_GROUP where it was measured faster on MI355X, counting g = planes
+ * x chunks x layers x 1024-token blocks, for chunks of >= 1024 tokens: 8
+ * heads with g >= 2048 (8 per workgroup) or 1024 <= g < 2048 (4 per
+ * workgroup); 4 heads with 1024 <= g < 4096.  Smaller grids, shorter chunks
+ * and other head counts keep PER_HEAD.  A ROW_GROUP request that is not
+ * possible falls back to PER_HEAD. */
 typedef enum {
   KAMERA_KERNEL_AUTO = 0,
   KAMERA_KERNEL_PER_HEAD = 1,

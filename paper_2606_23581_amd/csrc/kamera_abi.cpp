@@ -368,15 +368,24 @@ static int build_rehydrate(const kamera_rehydrate_args* a, kamera::RehydratePara
     units += (int64_t)a->n_chunks * a->n_layers * a->n_heads * nb;
   }
   // Rows of <= 8 heads of 128 columns, one block per head, rank <= 64 and
-  // no relocation: one workgroup takes every head of a token row, so a pool
-  // page is written as one contiguous run.
-  // AUTO takes it where it measured faster: full 8-head rows and a grid of
-  // >= 2048 workgroups of 1024 tokens; smaller grids keep the per-head kernel.
-  const int64_t big_grid = (int64_t)a->n_planes * a->n_chunks * a->n_layers * ceil_div(a->n_tokens, 1024);
-  const bool want_rows = a->kernel == KAMERA_KERNEL_ROW_GROUP ||
-                         (a->kernel == KAMERA_KERNEL_AUTO && a->n_heads == kamera::kRgMaxHeads &&
-                          a->n_tokens >= 1024 && big_grid >= 2048);
-  bool rows = want_rows && P.delta == nullptr && a->n_heads <= kamera::kRgMaxHeads && a->head_dim == 128 &&
+  // no relocation can take the row-group kernel: a workgroup takes hw = 4 or
+  // 8 heads of a token row, so it writes them as one contiguous run (a whole
+  // pool page at 8 heads).  AUTO follows where it measured faster than the
+  // per-head kernel (g = plane x chunk x layer x 1024-token blocks):
+  //   8 heads: g >= 2048 -> hw 8 (one workgroup per CU); 1024 <= g < 2048 ->
+  //   hw 4 (two head groups, two workgroups per CU);
+  //   4 heads: 1024 <= g < 4096 -> hw 4;
+  //   everything else (small grids, chunks under 1024 tokens, other head
+  //   counts) keeps the per-head kernel.
+  const int64_t g1024 = (int64_t)a->n_planes * a->n_chunks * a->n_layers * ceil_div(a->n_tokens, 1024);
+  int hw = 0;
+  if (a->kernel == KAMERA_KERNEL_ROW_GROUP) {
+    hw = a->n_heads <= 4 ? 4 : 8;
+  } else if (a->kernel == KAMERA_KERNEL_AUTO && a->n_tokens >= 1024) {
+    if (a->n_heads == 8) hw = g1024 >= 2048 ? 8 : (g1024 >= 1024 ? 4 : 0);
+    else if (a->n_heads == 4) hw = g1024 >= 1024 && g1024 < 4096 ? 4 : 0;
+  }
+  bool rows = hw > 0 && P.delta == nullptr && a->n_heads <= kamera::kRgMaxHeads && a->head_dim == 128 &&
               (!any_rot || a->pos_mode != KAMERA_POS_EXPLICIT);
   for (int p = 0; p < a->n_planes && rows; ++p) {
     kamera::PlaneParams& o = P.plane[p];
@@ -400,14 +409,18 @@ static int build_rehydrate(const kamera_rehydrate_args* a, kamera::RehydratePara
     o.out_rec = (int32_t)out_rec;
   }
   if (rows) {
+    // a workgroup takes 4 heads (two workgroups per CU) or 8 (one per CU)
+    const int64_t groups = (int64_t)a->n_planes * ceil_div(a->n_heads, hw) * a->n_chunks * a->n_layers;
+    const int64_t want = 2048 * (8 / hw);
     int tb = 1024;
-    while (tb > 64 && (int64_t)a->n_planes * a->n_chunks * a->n_layers * ceil_div(a->n_tokens, tb) < 2048) tb /= 2;
+    while (tb > 64 && groups * ceil_div(a->n_tokens, tb) < want) tb /= 2;
     tb = (int)std::min<int64_t>(tb, ceil_div(a->n_tokens, 64) * 64);
-    P.row_group = 1;
+    P.row_group = hw;
+    P.n_hgroups = (int32_t)ceil_div(a->n_heads, hw);
     P.token_block = tb;
     P.n_tblk = (int32_t)ceil_div(a->n_tokens, tb);
     P.blocks_per_group = a->n_planes;
-    const int64_t n_tasks = (int64_t)a->n_planes * a->n_chunks * a->n_layers * P.n_tblk;
+    const int64_t n_tasks = groups * P.n_tblk;
     if (n_tasks >= (int64_t)1 << 31)
       return fail(KAMERA_ERR_RANGE, "%s: %lld tasks exceed one launch", who, (long long)n_tasks);
     P.n_tasks = n_tasks;

@@ -86,7 +86,9 @@ struct RehydrateParams {
   int32_t n_tblk;                    // token blocks per chunk
   int32_t per_xcd;                   // tasks per XCD slice of the grid
   int32_t blocks_per_group;          // column blocks of all planes for one (chunk, layer, head, token block)
-  int32_t row_group;                 // 1: one workgroup per (plane, chunk, layer, token block), all heads
+  int32_t row_group;                 // 0: per-head kernel; 4 or 8: heads per row-group workgroup
+  int32_t n_hgroups;                 // row-group: head groups per row
+  int32_t pad3_;
   int64_t n_tasks;
 };
 

@@ -28,23 +28,24 @@ namespace kamera {
 // without waiting for the tile issued after it.
 // ---------------------------------------------------------------------------
 
+// HW (4 or 8) heads per workgroup, one wave each: 64 * HW threads.
 constexpr int kRgDepth = 2;                                // tiles in flight per thread
-constexpr int kRgThreads = 512;                            // one wave per head
-constexpr int kRgHeads = kRgMaxHeads;
 constexpr int kRgKRow = 256 + kRowPad;                     // LDS bytes per (head, token) K row
 __host__ __device__ constexpr int rg_u_row(int ms) { return 64 * ms + kRowPad; }
-__host__ __device__ constexpr int rg_buf_bytes(int ms) {
-  return kRgHeads * kTileTokens * (kRgKRow + rg_u_row(ms));
+__host__ __device__ constexpr int rg_buf_bytes(int ms, int hw) {
+  return hw * kTileTokens * (kRgKRow + rg_u_row(ms));
 }
 constexpr int kRgWtRow = 64 * 2 + kRowPad;                 // W^T staging row: 64 ranks + pad
 constexpr int kRgMaxBlock = 1024;                          // tokens per row-group task
-__host__ __device__ constexpr int rg_lds_bytes(int ms) {
-  return (2 * rg_buf_bytes(ms) > 4 * 128 * kRgWtRow ? 2 * rg_buf_bytes(ms) : 4 * 128 * kRgWtRow) +
+__host__ __device__ constexpr int rg_lds_bytes(int ms, int hw) {
+  return (2 * rg_buf_bytes(ms, hw) > 4 * 128 * kRgWtRow ? 2 * rg_buf_bytes(ms, hw) : 4 * 128 * kRgWtRow) +
          kRgMaxBlock * 4;
 }
 
-constexpr int kRgKVec = kRgHeads * kTileTokens * 16 / kRgThreads;   // K vectors per thread and tile
-constexpr int kRgUVec = kRgHeads * kTileTokens * 8 / kRgThreads;    // U vectors (rank 64)
+// per thread and tile: HW * 16 tokens * 16 K chunks over 64 * HW threads,
+// and HW * 16 tokens * (up to 8) U chunks
+constexpr int kRgKVec = 4;
+constexpr int kRgUVec = 2;
 
 struct RgRegs {              // one tile's global loads, in flight until the LDS write
   u32x4 k[kRgKVec];
@@ -56,7 +57,9 @@ constexpr int kRgBufWord3 = 0x00020000;                    // raw buffer, 32-bit
 
 struct RgTask {
   const PlaneParams* Q;
-  int c, l, n_c, H;
+  int c, l, n_c;
+  int H;                     // heads of this workgroup (<= HW)
+  int h0;                    // their first head in the row
   int m, m_steps;            // rank at this layer
   int t_end;                 // end of the task's token block
   bool in_head_major;        // rows of one head lie closer together than the heads
@@ -72,7 +75,8 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t rg_rsrc(const void* p, int64_t
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, kRgBufWord3);
 }
 
-// 16-byte vector v of a tile (16 tokens x H heads x 16 chunks) -> (head, token)
+// 16-byte vector v of a tile (16 tokens x H heads x 16 chunks) -> (head, token),
+// heads counted from the workgroup's first
 __device__ __forceinline__ void rg_vec(int v, int H, bool head_major, int& h, int& t) {
   if (head_major) {
     h = v >> 8;
@@ -83,13 +87,14 @@ __device__ __forceinline__ void rg_vec(int v, int H, bool head_major, int& h, in
   }
 }
 
-template <int MS>
+template <int MS, int HW>
 __device__ __forceinline__ void rg_load(const RgTask& T, int i0, RgRegs& R) {
+  constexpr int NT = 64 * HW;
   const int tid = threadIdx.x;
   const int nv = T.H * kTileTokens * 16;
 #pragma unroll
   for (int k = 0; k < kRgKVec; ++k) {
-    const int v = tid + kRgThreads * k;
+    const int v = tid + NT * k;
     int h, t;
     rg_vec(v, T.H, T.in_head_major, h, t);
     const int i = i0 + t;
@@ -100,7 +105,7 @@ __device__ __forceinline__ void rg_load(const RgTask& T, int i0, RgRegs& R) {
     const int cpr = 4 * (T.m_steps > 0 ? T.m_steps : 1);   // 16-byte chunks per U row (rank padded to 32)
 #pragma unroll
     for (int k = 0; k < kRgUVec; ++k) {
-      const int v = tid + kRgThreads * k;
+      const int v = tid + NT * k;
       const int h = v / (kTileTokens * cpr), t = (v / cpr) % kTileTokens, c = v % cpr;
       const int i = i0 + t;
       const uint32_t off = (h < T.H && 8 * c < T.m && i < T.t_end)
@@ -110,13 +115,14 @@ __device__ __forceinline__ void rg_load(const RgTask& T, int i0, RgRegs& R) {
   }
 }
 
-template <int MS>
+template <int MS, int HW>
 __device__ __forceinline__ void rg_to_lds(const RgTask& T, const RgRegs& R, uint8_t* buf) {
+  constexpr int NT = 64 * HW;
   const int tid = threadIdx.x;
   const int nv = T.H * kTileTokens * 16;
 #pragma unroll
   for (int k = 0; k < kRgKVec; ++k) {
-    const int v = tid + kRgThreads * k;
+    const int v = tid + NT * k;
     int h, t;
     rg_vec(v, T.H, T.in_head_major, h, t);
     if (v < nv) *reinterpret_cast<u32x4*>(buf + (h * kTileTokens + t) * kRgKRow + 16 * (v & 15)) = R.k[k];
@@ -126,7 +132,7 @@ __device__ __forceinline__ void rg_to_lds(const RgTask& T, const RgRegs& R, uint
       const int cpr = 4 * T.m_steps;
 #pragma unroll
       for (int k = 0; k < kRgUVec; ++k) {
-        const int v = tid + kRgThreads * k;
+        const int v = tid + NT * k;
         const int h = v / (kTileTokens * cpr), t = (v / cpr) % kTileTokens, c = v % cpr;
         // a layer rank that is not a multiple of 8 ends inside a chunk: the
         // ranks past it are cleared (the plane's U rows hold m >= 8c + 8 ranks)
@@ -140,7 +146,7 @@ __device__ __forceinline__ void rg_to_lds(const RgTask& T, const RgRegs& R, uint
           u = u32x4{wv[0], wv[1], wv[2], wv[3]};
         }
         if (h < T.H)
-          *reinterpret_cast<u32x4*>(buf + kRgHeads * kTileTokens * kRgKRow + (h * kTileTokens + t) * rg_u_row(MS) +
+          *reinterpret_cast<u32x4*>(buf + HW * kTileTokens * kRgKRow + (h * kTileTokens + t) * rg_u_row(MS) +
                                     16 * c) = u;
       }
     }
@@ -193,7 +199,7 @@ __device__ __forceinline__ void rg_rotate(f32x4 (&acc)[8], int g, const double* 
 }
 
 // one wave: head h of the tile in LDS, result written back in place
-template <int MS, int ROT>
+template <int MS, int ROT, int HW>
 __device__ __forceinline__ void rg_compute(const RehydrateParams& P, const RgTask& T, int i0, int h,
                                            const u32x4 (&wa)[8][MS > 0 ? MS : 1], uint8_t* buf,
                                            const double* s_freq, const int* s_coord) {
@@ -228,7 +234,7 @@ __device__ __forceinline__ void rg_compute(const RehydrateParams& P, const RgTas
     if (P.patch_post_rope) rg_rotate<ROT>(acc, g, s_freq, s_coord, pt, ph, pw);
   }
   if constexpr (MS > 0) {
-    const uint8_t* urow = buf + kRgHeads * kTileTokens * kRgKRow + (h * kTileTokens + t) * rg_u_row(MS);
+    const uint8_t* urow = buf + HW * kTileTokens * kRgKRow + (h * kTileTokens + t) * rg_u_row(MS);
 #pragma unroll
     for (int k = 0; k < MS; ++k) {
       if (k < T.m_steps) {
@@ -255,13 +261,15 @@ __device__ __forceinline__ void rg_compute(const RehydrateParams& P, const RgTas
 
 // store phase: every thread writes four 16-byte pieces of the tile's rows;
 // s_page holds the pool page of every token of the block (-1: not written)
+template <int HW>
 __device__ __forceinline__ void rg_store(const RehydrateParams& P, const RgTask& T, int t_begin, int i0,
                                          const uint8_t* buf, const int* s_page) {
+  constexpr int NT = 64 * HW;
   const int tid = threadIdx.x;
   const int nv = T.H * kTileTokens * 16;
 #pragma unroll
   for (int k = 0; k < kRgKVec; ++k) {
-    const int v = tid + kRgThreads * k;
+    const int v = tid + NT * k;
     int h, t;
     rg_vec(v, T.H, T.out_head_major, h, t);
     const int i = i0 + t;
@@ -279,10 +287,12 @@ __device__ __forceinline__ void rg_store(const RehydrateParams& P, const RgTask&
   }
 }
 
-// W rows of one staging item: head h, ranks k0..k0+3, columns colb..colb+7
+// W rows of one staging item: head h (of the workgroup), ranks k0..k0+3,
+// columns colb..colb+7
 __device__ __forceinline__ void rg_load_w(const RgTask& T, int h, int k0, int colb, uint32_t (&w)[4][4]) {
   const PlaneParams& Q = *T.Q;
-  const uint16_t* wbase = Q.W + (int64_t)T.c * Q.w_s[0] + (int64_t)T.l * Q.w_s[1] + (int64_t)h * Q.w_s[2];
+  const uint16_t* wbase =
+      Q.W + (int64_t)T.c * Q.w_s[0] + (int64_t)T.l * Q.w_s[1] + (int64_t)(T.h0 + h) * Q.w_s[2];
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
     w[r][0] = w[r][1] = w[r][2] = w[r][3] = 0u;
@@ -315,22 +325,24 @@ __device__ __forceinline__ void rg_put_w(int hq, int k0, int colb, const uint32_
   }
 }
 
-template <int MS, int ROT>
+template <int MS, int ROT, int HW>
 __device__ __forceinline__ void rg_run(const RehydrateParams& P, const RgTask& T, int t_begin, int t_end,
                                        uint8_t* lds, const double* s_freq, const int* s_coord) {
+  constexpr int NT = 64 * HW;
+  constexpr int kIpt = 1024 / NT;               // W staging items per thread and round of 4 heads
   const int tid = threadIdx.x;
   const int h = tid >> 6;                       // wave = head
   const int lane = tid & 63;
   const bool active = h < T.H;
   const int n_tiles = (t_end - t_begin + kTileTokens - 1) / kTileTokens;
-  int* s_page = reinterpret_cast<int*>(lds + rg_lds_bytes(MS) - kRgMaxBlock * 4);
+  int* s_page = reinterpret_cast<int*>(lds + rg_lds_bytes(MS, HW) - kRgMaxBlock * 4);
 
   // set-up loads, in flight together: the block's pool pages, the first
-  // tiles and the W rows of heads 0..3 (two staging items per thread)
-  int page[kRgMaxBlock / kRgThreads];
+  // tiles and the W rows of the first four heads
+  int page[kRgMaxBlock / NT];
 #pragma unroll
-  for (int k = 0; k < kRgMaxBlock / kRgThreads; ++k) {
-    const int j = t_begin + tid + kRgThreads * k;
+  for (int k = 0; k < kRgMaxBlock / NT; ++k) {
+    const int j = t_begin + tid + NT * k;
     page[k] = -1;
     if (P.place.paged && j < t_end) {
       page[k] = P.place.page_table[(int64_t)T.c * P.place.pt_stride + j / P.place.page_size];
@@ -343,35 +355,35 @@ __device__ __forceinline__ void rg_run(const RehydrateParams& P, const RgTask& T
   RgRegs R[kRgDepth];
 #pragma unroll
   for (int d = 0; d < kRgDepth; ++d)
-    if (d < n_tiles) rg_load<MS>(T, t_begin + d * kTileTokens, R[d]);
-  // staging item = (head, rank quad, column chunk); item tid + 512 * r
-  const int k0 = 4 * ((tid >> 4) & 15), colb = 8 * (tid & 15), hq = tid >> 8;   // hq in {0, 1}
+    if (d < n_tiles) rg_load<MS, HW>(T, t_begin + d * kTileTokens, R[d]);
+  // staging item = (head of the round, rank quad, column chunk); the thread's
+  // items are tid + NT * j, i.e. heads (tid >> 8) + j * NT / 256 of the round
+  const int k0 = 4 * ((tid >> 4) & 15), colb = 8 * (tid & 15), hr = tid >> 8;
   const bool w_item = MS > 0 && T.m_steps > 0 && k0 < 32 * T.m_steps;
-  uint32_t w[2][4][4];
+  uint32_t w[kIpt][4][4];
   if (w_item) {
-    rg_load_w(T, hq, k0, colb, w[0]);
-    rg_load_w(T, hq + 2, k0, colb, w[1]);
+#pragma unroll
+    for (int j = 0; j < kIpt; ++j) rg_load_w(T, hr + j * (NT / 256), k0, colb, w[j]);
   }
 #pragma unroll
-  for (int k = 0; k < kRgMaxBlock / kRgThreads; ++k)
-    if (P.place.paged && t_begin + tid + kRgThreads * k < t_end) s_page[tid + kRgThreads * k] = page[k];
+  for (int k = 0; k < kRgMaxBlock / NT; ++k)
+    if (P.place.paged && t_begin + tid + NT * k < t_end) s_page[tid + NT * k] = page[k];
 
   // W^T into registers: A operand of M-tile mt, K-step k for lane (g, t):
   // column 8*(t/4) + t%4 + 32*(mt/2) + 4*(mt%2), ranks 32k + 8g .. +7.
-  // Two rounds of four heads through LDS: round r holds heads 4r + hq and
-  // 4r + 2 + hq of the thread's items.
+  // Rounds of four heads through LDS: round r holds heads 4r .. 4r + 3.
   u32x4 wa[8][MS > 0 ? MS : 1];
   if constexpr (MS > 0) {
     const int g = lane >> 4, t = lane & 15;
 #pragma unroll
-    for (int round = 0; round < 2; ++round) {
-      if (round == 1 && w_item) {
-        rg_load_w(T, hq + 4, k0, colb, w[0]);
-        rg_load_w(T, hq + 6, k0, colb, w[1]);
+    for (int round = 0; round < HW / 4; ++round) {
+      if (round > 0 && w_item) {
+#pragma unroll
+        for (int j = 0; j < kIpt; ++j) rg_load_w(T, 4 * round + hr + j * (NT / 256), k0, colb, w[j]);
       }
       if (w_item) {
-        rg_put_w(hq, k0, colb, w[0], lds);
-        rg_put_w(hq + 2, k0, colb, w[1], lds);
+#pragma unroll
+        for (int j = 0; j < kIpt; ++j) rg_put_w(hr + j * (NT / 256), k0, colb, w[j], lds);
       }
       __syncthreads();
       if ((h >> 2) == round) {
@@ -393,13 +405,13 @@ __device__ __forceinline__ void rg_run(const RehydrateParams& P, const RgTask& T
   // uses set tt % kRgDepth and buffer tt % 2; two barriers per tile
   auto step = [&](int tt, RgRegs& R) {
     const int i0 = t_begin + tt * kTileTokens;
-    uint8_t* buf = lds + (tt & 1) * rg_buf_bytes(MS);
-    rg_to_lds<MS>(T, R, buf);
-    if (tt + kRgDepth < n_tiles) rg_load<MS>(T, i0 + kRgDepth * kTileTokens, R);
+    uint8_t* buf = lds + (tt & 1) * rg_buf_bytes(MS, HW);
+    rg_to_lds<MS, HW>(T, R, buf);
+    if (tt + kRgDepth < n_tiles) rg_load<MS, HW>(T, i0 + kRgDepth * kTileTokens, R);
     __syncthreads();
-    if (active) rg_compute<MS, ROT>(P, T, i0, h, wa, buf, s_freq, s_coord);
+    if (active) rg_compute<MS, ROT, HW>(P, T, i0, h, wa, buf, s_freq, s_coord);
     __syncthreads();
-    rg_store(P, T, t_begin, i0, buf, s_page);
+    rg_store<HW>(P, T, t_begin, i0, buf, s_page);
   };
   for (int tile = 0; tile < n_tiles; tile += kRgDepth) {
 #pragma unroll
@@ -408,8 +420,8 @@ __device__ __forceinline__ void rg_run(const RehydrateParams& P, const RgTask& T
   }
 }
 
-template <int MS>
-__global__ __launch_bounds__(kRgThreads, 1) void rehydrate_rows_kernel(const RehydrateParams /*by value, read in place*/) {
+template <int MS, int HW>
+__global__ __launch_bounds__(64 * HW, 8 / HW) void rehydrate_rows_kernel(const RehydrateParams /*by value, read in place*/) {
   const RehydrateParams& P = kernel_params<RehydrateParams>();
   extern __shared__ __align__(16) uint8_t lds_dyn[];
   __shared__ double s_freq[kMaxPairs];
@@ -417,9 +429,12 @@ __global__ __launch_bounds__(kRgThreads, 1) void rehydrate_rows_kernel(const Reh
 
   const int64_t task = xcd_task(P.per_xcd);
   if (task >= P.n_tasks) return;
-  // the planes (K, V) of one (chunk, layer, token block) are adjacent tasks
+  // the planes (K, V) and head groups of one (chunk, layer, token block) are
+  // adjacent tasks
   const int pl = (int)(task % P.n_planes);
   int64_t rem = task / P.n_planes;
+  const int hg = (int)(rem % P.n_hgroups);
+  rem /= P.n_hgroups;
   const int tb = (int)(rem % P.n_tblk);
   rem /= P.n_tblk;
   RgTask T;
@@ -427,7 +442,8 @@ __global__ __launch_bounds__(kRgThreads, 1) void rehydrate_rows_kernel(const Reh
   const PlaneParams& Q = *T.Q;
   T.l = (int)(rem % P.n_layers);
   T.c = (int)(rem / P.n_layers);
-  T.H = P.n_heads;
+  T.h0 = hg * HW;
+  T.H = min(HW, P.n_heads - T.h0);
   T.n_c = chunk_len(P.place, T.c);
   const int t_begin = tb * P.token_block;
   if (t_begin >= T.n_c) return;                 // uniform: the whole workgroup leaves
@@ -447,13 +463,18 @@ __global__ __launch_bounds__(kRgThreads, 1) void rehydrate_rows_kernel(const Reh
   T.s_u3 = (int)Q.u_s[3];
   T.s_o2 = (int)Q.out_s[2];
   T.s_o3 = (int)Q.out_s[3];
-  T.rin = rg_rsrc(Q.in + (int64_t)T.c * Q.in_s[0] + (int64_t)T.l * Q.in_s[1], Q.in_rec);
-  T.ru = rg_rsrc(Q.U != nullptr ? Q.U + (int64_t)T.c * Q.u_s[0] + (int64_t)T.l * Q.u_s[1] : Q.in, Q.U != nullptr ? Q.u_rec : 0);
+  // the slabs start at the workgroup's first head
+  T.rin = rg_rsrc(Q.in + (int64_t)T.c * Q.in_s[0] + (int64_t)T.l * Q.in_s[1] + (int64_t)T.h0 * Q.in_s[3],
+                  Q.in_rec - 2 * (int64_t)T.h0 * Q.in_s[3]);
+  T.ru = rg_rsrc(Q.U != nullptr ? Q.U + (int64_t)T.c * Q.u_s[0] + (int64_t)T.l * Q.u_s[1] + (int64_t)T.h0 * Q.u_s[2]
+                                : Q.in,
+                 Q.U != nullptr ? Q.u_rec - 2 * (int64_t)T.h0 * Q.u_s[2] : 0);
   // paged: the layer's pool; dense: the chunk's rows from its row base on
   const int64_t out_base = P.place.paged ? 0
                            : (int64_t)T.c * Q.out_s[0] +
                                  (int64_t)(P.place.row_base ? P.place.row_base[T.c] : 0) * Q.out_s[2];
-  T.rout = rg_rsrc(Q.out + out_base + (int64_t)T.l * Q.out_s[1], Q.out_rec);
+  T.rout = rg_rsrc(Q.out + out_base + (int64_t)T.l * Q.out_s[1] + (int64_t)T.h0 * Q.out_s[3],
+                   Q.out_rec - 2 * (int64_t)T.h0 * Q.out_s[3]);
   T.cp0 = T.cp1 = T.cp2 = 0.0;
   if (P.chunk_pos != nullptr) {
     T.cp0 = (double)P.chunk_pos[3 * T.c];
@@ -463,46 +484,52 @@ __global__ __launch_bounds__(kRgThreads, 1) void rehydrate_rows_kernel(const Reh
   const int rot = (Q.blk[0].flags & kBlkRotate) ? (P.rope.pairing == 0 ? 1 : 2) : 0;
   if (rot != 0) {
     const int half = P.rope.rope_dim / 2;
-    for (int j = threadIdx.x; j < half; j += kRgThreads) {
+    for (int j = threadIdx.x; j < half; j += 64 * HW) {
       s_freq[j] = P.rope.rev_freq[j];
       s_coord[j] = P.rope.coord[j];
     }
   }
   switch (rot) {
-    case 0: rg_run<MS, 0>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
-    case 1: rg_run<MS, 1>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
-    default: rg_run<MS, 2>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
+    case 0: rg_run<MS, 0, HW>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
+    case 1: rg_run<MS, 1, HW>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
+    default: rg_run<MS, 2, HW>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
   }
 }
 
-hipError_t launch_rehydrate_rows(const RehydrateParams& p, hipStream_t s) {
-  int max_steps = 0;
-  for (int k = 0; k < p.n_planes; ++k) max_steps = max_steps > p.plane[k].m_steps ? max_steps : p.plane[k].m_steps;
-  const dim3 grid((uint32_t)((int64_t)p.per_xcd * 8));
-  // the LDS limit is raised once per device (a race only repeats the calls)
+template <int MS, int HW>
+hipError_t launch_rows(const RehydrateParams& p, hipStream_t s) {
+  // the LDS limit is raised once per device and instantiation (a race only
+  // repeats the call)
   static bool attr_set[64] = {};
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
   if (dev < 0 || dev >= 64 || !attr_set[dev]) {
-    e = hipFuncSetAttribute((const void*)rehydrate_rows_kernel<0>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                            rg_lds_bytes(0));
-    if (e == hipSuccess)
-      e = hipFuncSetAttribute((const void*)rehydrate_rows_kernel<1>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                              rg_lds_bytes(1));
-    if (e == hipSuccess)
-      e = hipFuncSetAttribute((const void*)rehydrate_rows_kernel<2>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                              rg_lds_bytes(2));
+    e = hipFuncSetAttribute((const void*)rehydrate_rows_kernel<MS, HW>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            rg_lds_bytes(MS, HW));
     if (e != hipSuccess) return e;
     if (dev >= 0 && dev < 64) attr_set[dev] = true;
   }
-  const dim3 rblock(kRgThreads);
-  switch (max_steps) {
-    case 0: hipLaunchKernelGGL((rehydrate_rows_kernel<0>), grid, rblock, rg_lds_bytes(0), s, p); break;
-    case 1: hipLaunchKernelGGL((rehydrate_rows_kernel<1>), grid, rblock, rg_lds_bytes(1), s, p); break;
-    default: hipLaunchKernelGGL((rehydrate_rows_kernel<2>), grid, rblock, rg_lds_bytes(2), s, p); break;
-  }
+  const dim3 grid((uint32_t)((int64_t)p.per_xcd * 8)), block(64 * HW);
+  hipLaunchKernelGGL((rehydrate_rows_kernel<MS, HW>), grid, block, rg_lds_bytes(MS, HW), s, p);
   return hipGetLastError();
+}
+
+hipError_t launch_rehydrate_rows(const RehydrateParams& p, hipStream_t s) {
+  int max_steps = 0;
+  for (int k = 0; k < p.n_planes; ++k) max_steps = max_steps > p.plane[k].m_steps ? max_steps : p.plane[k].m_steps;
+  if (p.row_group == 4) {
+    switch (max_steps) {
+      case 0: return launch_rows<0, 4>(p, s);
+      case 1: return launch_rows<1, 4>(p, s);
+      default: return launch_rows<2, 4>(p, s);
+    }
+  }
+  switch (max_steps) {
+    case 0: return launch_rows<0, 8>(p, s);
+    case 1: return launch_rows<1, 8>(p, s);
+    default: return launch_rows<2, 8>(p, s);
+  }
 }
 
 }  // namespace kamera

@@ -129,6 +129,14 @@ WORKLOADS: Dict[str, Workload] = {
         section_order="blocked", m_k=64, m_v=64, patch_dim=128, paged=True,
         page_size=16, n_pool_pages=4096, pos_mode="grid3", grid_w=32,
         patch_from_layer=40, seed=1008),
+    # a mid-size paged recall: 16 frame chunks on a 32-layer model, rank 32
+    "gqa32l_16x1024_m32_mrope_paged": Workload(
+        name="gqa32l_16x1024_m32_mrope_paged", kind="rehydrate", n_chunks=16,
+        n_layers=32, n_heads=8, head_dim=128, n_tokens=1024, theta=1e6,
+        rope_dim=128, pairing=NEOX, sections=(16, 24, 24),
+        section_order="blocked", m_k=32, m_v=32, patch_dim=128, paged=True,
+        page_size=16, n_pool_pages=1024, pos_mode="grid3", grid_w=32,
+        seed=1009),
 }
 
 # order in which the workloads are listed (smallest first)
@@ -141,11 +149,12 @@ WORKLOAD_ORDER: List[str] = [
 ]
 
 # workloads of the operator's other modes (relocation with a removal patch,
-# a second rank on the MLA rope band, deep-half factors)
+# a second rank on the MLA rope band, deep-half factors) and a mid-size recall
 EXTRA_WORKLOADS: List[str] = [
     "gqa36l_15x1024_survivor_m64",
     "mla27l_4x2048_m32_pe16",
     "gqa80l_64x1024_m64_mrope_paged_deephalf",
+    "gqa32l_16x1024_m32_mrope_paged",
 ]
 
 
@@ -196,7 +205,8 @@ def chunk_meta(w: Workload, seed: Optional[int] = None) -> ChunkMeta:
         # every coordinate) and moves to slot k: all three coordinates by delta
         pos[:] = (n * np.arange(C))[:, None]
         delta[:] = w.delta
-    elif w.name in ("gqa80l_64x1024_m64_mrope_paged", "gqa80l_64x1024_m64_mrope_paged_deephalf"):
+    elif w.name in ("gqa80l_64x1024_m64_mrope_paged", "gqa80l_64x1024_m64_mrope_paged_deephalf",
+                    "gqa32l_16x1024_m32_mrope_paged"):
         s = rng.integers(1, 4097, size=C)          # temporal delta in [1, 4096]
         pos[:] = s[:, None]                        # all three coordinates advance together
         pages = (n + w.page_size - 1) // w.page_size

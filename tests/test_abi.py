@@ -135,16 +135,18 @@ def _plan_case(case):
         a.kernel = km.KERNEL_PER_HEAD
     elif case == "kernel_choice_unknown":
         a.kernel = 7
-    elif case in ("auto_recall", "auto_recall_4_heads", "auto_recall_short_chunks"):
-        # 64 chunks x 80 layers of 8 heads x 1024 tokens, token-major rows
+    elif case.startswith("auto_"):
+        # chunks x layers of H heads x n tokens, token-major rows
         a.kernel = km.KERNEL_AUTO
-        H = 4 if case == "auto_recall_4_heads" else 8
-        n = 512 if case == "auto_recall_short_chunks" else 1024
-        a.n_chunks, a.n_layers, a.n_heads, a.n_tokens = 64, 80, H, n
+        C, Ln, H, n = {"auto_recall": (64, 80, 8, 1024), "auto_recall_4_heads": (64, 80, 4, 1024),
+                       "auto_recall_short_chunks": (64, 80, 8, 512), "auto_mid_8_heads": (16, 32, 8, 1024),
+                       "auto_mid_4_heads": (16, 32, 4, 1024), "auto_small_8_heads": (8, 28, 8, 1024),
+                       "auto_6_heads": (64, 80, 6, 1024)}[case]
+        a.n_chunks, a.n_layers, a.n_heads, a.n_tokens = C, Ln, H, n
         for p in range(2):
-            strides = [80 * n * H * 128, n * H * 128, H * 128, 128]
-            us = [80 * H * n * 16, H * n * 16, n * 16, 16]
-            ws = [80 * H * 16 * 128, H * 16 * 128, 16 * 128, 128]
+            strides = [Ln * n * H * 128, n * H * 128, H * 128, 128]
+            us = [Ln * H * n * 16, H * n * 16, n * 16, 16]
+            ws = [Ln * H * 16 * 128, H * 16 * 128, 16 * 128, 128]
             for k in range(4):
                 a.plane[p].in_stride[k] = a.plane[p].out_stride[k] = strides[k]
                 a.plane[p].u_stride[k], a.plane[p].w_stride[k] = us[k], ws[k]
@@ -186,6 +188,10 @@ def _plan_case(case):
     ("auto_recall", km.PLAN_ROW_GROUP),
     ("auto_recall_4_heads", km.PLAN_PER_HEAD),
     ("auto_recall_short_chunks", km.PLAN_PER_HEAD),
+    ("auto_mid_8_heads", km.PLAN_ROW_GROUP),
+    ("auto_mid_4_heads", km.PLAN_ROW_GROUP),
+    ("auto_small_8_heads", km.PLAN_PER_HEAD),
+    ("auto_6_heads", km.PLAN_PER_HEAD),
     ("heads_9", km.PLAN_PER_HEAD),
     ("rank_72", km.PLAN_PER_HEAD),
     ("rank_12", km.PLAN_PER_HEAD),
@@ -203,7 +209,8 @@ def test_rehydrate_plan_picks_the_kernel(case, plan):
     the row-group kernel, when requested, only for rows of <= 8 heads x 128
     columns with one block per head, rank <= 64 in whole 16-byte U chunks, no
     explicit positions or relocation, and every byte offset below 2^31; AUTO
-    takes it only for 8-head rows on a grid of >= 2048 1024-token blocks."""
+    takes it for 8-head rows on >= 1024 (plane, chunk, layer, 1024-token
+    block) units and for 4-head rows on 1024 .. 4095 of them."""
     a = _plan_case(case)
     assert km.lib().kamera_rehydrate_plan(ctypes.byref(a)) == plan
     assert km.lib().kamera_validate(0, ctypes.byref(a)) == min(plan, 0)

@@ -96,9 +96,18 @@ def _check_rehydrate_units(p, units, inputs):
 def test_workload_rehydrate(device, name):
     import torch
 
+    import paper_2606_23581_amd as km
+
     print(f"[case] workload {name}", flush=True)
     p = harness.prepare(name, device)
+    # the kernel AUTO picks: row groups of 8 heads for the 80-layer recalls,
+    # of 4 heads (two per 8-head row) for the mid-size one, per head elsewhere
+    rows = {"gqa80l_64x1024_m64_mrope_paged", "gqa80l_64x1024_m64_mrope_paged_deephalf",
+            "gqa32l_16x1024_m32_mrope_paged"}
+    assert km.rehydrate_plan(p.extra["call"]) == (km.PLAN_ROW_GROUP if name in rows else km.PLAN_PER_HEAD)
     units = harness.sample_units(p.workload, 12 if p.workload.units() > 12 else p.workload.units(), seed=1)
+    if p.workload.n_heads == 8:
+        units += [(0, 0, 3), (0, 0, 4)]       # both sides of a 4-head group boundary
     if p.workload.patch_from_layer:
         # make sure both sides of the deep-half boundary are sampled
         units += [(0, p.workload.patch_from_layer - 1, 0), (1, p.workload.patch_from_layer, 1)]
