@@ -1,7 +1,8 @@
 // gfx950 row-group rehydrate kernel of the Kamera operator:
 // K' = R(pos)(K + U W), V' = V + U_v W_v  (Eq. eq:operator, Sec. 3; serve
 // step of App. A) for rows of <= 8 heads, one workgroup per (plane, chunk,
-// layer, token block) writing every head of a token row together.
+// layer, token block, group of heads) writing its heads of a token row
+// together.
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -11,21 +12,21 @@
 namespace kamera {
 
 // ---------------------------------------------------------------------------
-// rehydrate, row-group form: rows of <= 8 heads of 128 columns with one
-// 128-column block per head (the rope band, if any, is the whole head), rank
-// <= 64, positions linear or on a grid, no relocation.  A workgroup of 8 waves owns (plane,
-// chunk, layer, token block) for every head of the row; wave h computes head
-// h in the register layout of the per-head kernel (kamera_kernels.hip; lane (g, t) holds
-// chunks g, g+4, g+8, g+12 of token t).  Per 16-token tile all heads move
+// Rows of <= 8 heads of 128 columns with one 128-column block per head (the
+// rope band, if any, is the whole head), rank <= 64, positions linear or on a
+// grid, no relocation.  A workgroup of HW = 4 or 8 waves owns (plane, chunk,
+// layer, token block, group of HW heads); wave h computes head h of the group
+// in the register layout of the per-head kernel (kamera_kernels.hip: lane
+// (g, t) holds chunks g, g+4, g+8, g+12 of token t).  Per 16-token tile the
+// group's heads move
 //   HBM -> registers (two tiles in flight) -> LDS -> MFMA layout -> LDS -> HBM
-// and the store phase writes every token's whole row of heads: a pool page of
-// 16 tokens is written as one contiguous run instead of one 256-byte piece
-// per head.  W^T of every head sits in registers for the whole token block,
-// and the block's page numbers in LDS.  Tile loads and stores are buffer
-// instructions whose out-of-range lanes (ragged tails, missing heads, pages
-// outside the pool) read zeros or write nothing, so the tile loop issues the
-// same memory instructions on every path and a tile's loads are awaited
-// without waiting for the tile issued after it.
+// and the store phase writes every token's row of the group's heads: with 8
+// heads a pool page of 16 tokens is one contiguous 32 KiB run instead of one
+// 256-byte piece per head.  W^T of every head sits in registers for the whole
+// token block, and the block's page numbers in LDS.  Tile loads and stores are
+// buffer instructions whose out-of-range lanes (ragged tails, missing heads,
+// pages outside the pool) read zeros or write nothing, so the tile loop issues
+// the same memory instructions on every path.
 // ---------------------------------------------------------------------------
 
 // HW (4 or 8) heads per workgroup, one wave each: 64 * HW threads.
