@@ -259,6 +259,26 @@ __device__ __forceinline__ void apply_v(float* V, int ld, int qo, const int* grp
 
 }  // namespace
 
+// nk k-steps of NS interleaved 16x16x4 MFMA chains: step k of chain u takes
+// its A operand at pa[k * sa + oa[u]] and its B operand at pb[k * sb + ob[u]]
+// (this lane's element).  No branch inside, so the loads of a step run ahead
+// of its MFMAs.
+template <int NS, int N>
+__device__ __forceinline__ void mfma_steps(const float* pa, int sa, const int (&oa)[N], const float* pb, int sb,
+                                           const int (&ob)[N], int nk, f32x4v (&acc)[N]) {
+#pragma unroll 4
+  for (int k = 0; k < nk; ++k) {
+    float a[NS], b[NS];
+#pragma unroll
+    for (int u = 0; u < NS; ++u) {
+      a[u] = pa[k * sa + oa[u]];
+      b[u] = pb[k * sb + ob[u]];
+    }
+#pragma unroll
+    for (int u = 0; u < NS; ++u) acc[u] = mfma4(a[u], b[u], acc[u]);
+  }
+}
+
 __global__ __launch_bounds__(kFormThreads) void form_patch_kernel(const FormParams /*by value, read in place*/) {
   const FormParams& P = *static_cast<const FormParams*>((const void*)__builtin_amdgcn_kernarg_segment_ptr());
   float* const lds_f = form_lds;
@@ -325,13 +345,20 @@ __global__ __launch_bounds__(kFormThreads) void form_patch_kernel(const FormPara
       }
       __syncthreads();
       if (t0 + kFormTile < n) load_tile(P, delta, t0 + kFormTile, n, d, vec_per_row, tid, x);
-      const int nrows = min(kFormTile, n - t0);
-      for (int kb = 0; kb < (nrows + 3) / 4; ++kb) {
-        const float* trow = T + (4 * kb + lj) * ldt + lr;
+      // the slot count is the same on every lane: one scalar branch picks a
+      // loop without branches, whose loads run ahead of its MFMAs; rows past n
+      // are staged as zeros, so every tile takes all k-steps
+      const int my = __builtin_amdgcn_readfirstlane(my_tiles);
+      const float* trow = T + lj * ldt + lr;
+      int oa[3], ob[3];
 #pragma unroll
-        for (int u = 0; u < 3; ++u)
-          if (u < my_tiles) acc[u] = mfma4(trow[16 * tI[u]], trow[16 * tJ[u]], acc[u]);
+      for (int u = 0; u < 3; ++u) {
+        oa[u] = 16 * tI[u];
+        ob[u] = 16 * tJ[u];
       }
+      if (my == 3) mfma_steps<3>(trow, 4 * ldt, oa, trow, 4 * ldt, ob, kFormTile / 4, acc);
+      else if (my == 2) mfma_steps<2>(trow, 4 * ldt, oa, trow, 4 * ldt, ob, kFormTile / 4, acc);
+      else if (my == 1) mfma_steps<1>(trow, 4 * ldt, oa, trow, 4 * ldt, ob, kFormTile / 4, acc);
     }
     // lane (lj, lr) holds G[16I + 4 lj + i][16J + lr]; store it and its mirror
 #pragma unroll
@@ -571,13 +598,20 @@ __global__ __launch_bounds__(kFormThreads) void form_patch_kernel(const FormPara
         f32x4v acc[4];
 #pragma unroll
         for (int u = 0; u < 4; ++u) acc[u] = (f32x4v){0.f, 0.f, 0.f, 0.f};
-        for (int kb = 0; kb < dp / 4; ++kb) {
-          const float* ta = T + lr * ldu + 4 * kb + lj;
-          const float* vb = Vm + (4 * kb + lj) * ldv + lr;
+        // as in the Gram: a scalar slot count picks a loop without branches
+        const int my = __builtin_amdgcn_readfirstlane(my_out);
+        const float* ta = T + lr * ldu + lj;
+        const float* vb = Vm + lj * ldv + lr;
+        int oa[4], ob[4];
 #pragma unroll
-          for (int u = 0; u < 4; ++u)
-            if (u < my_out) acc[u] = mfma4(ta[16 * ort[u] * ldu], vb[16 * oct[u]], acc[u]);
+        for (int u = 0; u < 4; ++u) {
+          oa[u] = 16 * ort[u] * ldu;
+          ob[u] = 16 * oct[u];
         }
+        if (my == 4) mfma_steps<4>(ta, 4, oa, vb, 4 * ldv, ob, dp / 4, acc);
+        else if (my == 3) mfma_steps<3>(ta, 4, oa, vb, 4 * ldv, ob, dp / 4, acc);
+        else if (my == 2) mfma_steps<2>(ta, 4, oa, vb, 4 * ldv, ob, dp / 4, acc);
+        else if (my == 1) mfma_steps<1>(ta, 4, oa, vb, 4 * ldv, ob, dp / 4, acc);
         // lane (lj, lr) holds U[t0 + 16 rt + 4 lj + i][16 ct + lr]
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
