@@ -61,7 +61,7 @@ REH_FIELDS = ["n_chunks", "n_layers", "n_heads", "head_dim", "n_tokens", "patch_
               "rope.rope_dim", "rope.rope_offset", "rope.pairing", "rope.n_sections", "rope.section_order",
               "p0.m", "p0.rotate", "p0.patch_offset", "p0.patch_dim", "p0.col_begin", "p0.col_end",
               "p1.m", "p1.rotate", "p1.col_begin", "p1.col_end", "p0.in_stride.2", "p1.out_stride.1",
-              "p0.in_", "p0.out", "p1.in_", "p1.out", "p0.U", "p1.W", "chunk_pos", "page_table"]
+              "p0.in_", "p0.out", "p1.in_", "p1.out", "p0.U", "p1.W", "chunk_pos", "page_table", "kernel"]
 
 
 def _set(a, field, value):
@@ -94,6 +94,11 @@ def test_rehydrate_validation_never_misbehaves(edits):
     rc = L.kamera_validate(0, ctypes.byref(a))
     assert rc in CODES
     assert (km.last_error() == "") == (rc == km.OK), (rc, km.last_error())
+    # the plan agrees with validation: an error code, or a kernel (none for an empty call)
+    plan = L.kamera_rehydrate_plan(ctypes.byref(a))
+    assert plan == rc if rc != km.OK else plan in (km.PLAN_NONE, km.PLAN_PER_HEAD, km.PLAN_ROW_GROUP)
+    if rc == km.OK:
+        assert a.kernel in (km.KERNEL_AUTO, km.KERNEL_PER_HEAD, km.KERNEL_ROW_GROUP)
     if not edits:
         assert rc == km.OK
     if rc == km.OK and min(a.n_chunks, a.n_layers, a.n_heads, a.n_tokens) > 0:
