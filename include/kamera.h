@@ -116,7 +116,8 @@ typedef enum {
 typedef enum {
   KAMERA_KERNEL_AUTO = 0,
   KAMERA_KERNEL_PER_HEAD = 1,
-  KAMERA_KERNEL_ROW_GROUP = 2
+  KAMERA_KERNEL_ROW_GROUP = 2,   /* 8 heads per workgroup (4 for rows of <= 4) */
+  KAMERA_KERNEL_ROW_GROUP4 = 3   /* 4 heads per workgroup, also for wider rows */
 } kamera_kernel_choice;
 
 typedef enum {

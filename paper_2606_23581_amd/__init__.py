@@ -52,6 +52,7 @@ PATCH_POST_ROPE = 1
 KERNEL_AUTO = 0
 KERNEL_PER_HEAD = 1
 KERNEL_ROW_GROUP = 2
+KERNEL_ROW_GROUP4 = 3
 PLAN_NONE = 0
 PLAN_PER_HEAD = 1
 PLAN_ROW_GROUP = 2
@@ -349,7 +350,7 @@ def prepare_rehydrate(k_in, k_out, *, rope: RopeSpec, chunk_pos=None, v_in=None,
     the row splits into two planes, [0, rope_offset) patched by u_k/w_k and the
     band patched by u_pe/w_pe ([C, L, H, n, m_pe], [C, L, H, m_pe, rope_dim]).
     *_layer_rank: int32 [L] device tensors lowering the rank per layer.
-    kernel: KERNEL_AUTO, KERNEL_PER_HEAD or KERNEL_ROW_GROUP (same results).
+    kernel: KERNEL_AUTO, KERNEL_PER_HEAD, KERNEL_ROW_GROUP or KERNEL_ROW_GROUP4 (same results).
     """
     L = lib()
     _bf16(k_in, "k_in"), _bf16(k_out, "k_out"), _bf16(v_in, "v_in"), _bf16(v_out, "v_out")

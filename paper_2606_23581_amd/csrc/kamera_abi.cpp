@@ -188,7 +188,7 @@ static int build_rehydrate(const kamera_rehydrate_args* a, kamera::RehydratePara
     return fail(KAMERA_ERR_RANGE, "%s: head_dim %d exceeds %d", who, a->head_dim, KAMERA_MAX_HEAD_DIM);
   if (a->n_planes != 1 && a->n_planes != 2)
     return fail(KAMERA_ERR_SHAPE, "%s: n_planes must be 1 or 2 (got %d)", who, a->n_planes);
-  if (a->kernel != KAMERA_KERNEL_AUTO && a->kernel != KAMERA_KERNEL_PER_HEAD && a->kernel != KAMERA_KERNEL_ROW_GROUP)
+  if (a->kernel < KAMERA_KERNEL_AUTO || a->kernel > KAMERA_KERNEL_ROW_GROUP4)
     return fail(KAMERA_ERR_SHAPE, "%s: unknown kernel choice %d", who, a->kernel);
   if (a->patch_frame != KAMERA_PATCH_PRE_ROPE && a->patch_frame != KAMERA_PATCH_POST_ROPE)
     return fail(KAMERA_ERR_SHAPE, "%s: unknown patch_frame %d", who, a->patch_frame);
@@ -381,6 +381,8 @@ static int build_rehydrate(const kamera_rehydrate_args* a, kamera::RehydratePara
   int hw = 0;
   if (a->kernel == KAMERA_KERNEL_ROW_GROUP) {
     hw = a->n_heads <= 4 ? 4 : 8;
+  } else if (a->kernel == KAMERA_KERNEL_ROW_GROUP4) {
+    hw = 4;
   } else if (a->kernel == KAMERA_KERNEL_AUTO && a->n_tokens >= 1024) {
     if (a->n_heads == 8) hw = g1024 >= 2048 ? 8 : (g1024 >= 1024 ? 4 : 0);
     else if (a->n_heads == 4) hw = g1024 >= 1024 && g1024 < 4096 ? 4 : 0;

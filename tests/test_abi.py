@@ -135,6 +135,8 @@ def _plan_case(case):
         a.kernel = km.KERNEL_PER_HEAD
     elif case == "kernel_choice_unknown":
         a.kernel = 7
+    elif case == "row_group4_requested":
+        a.kernel = km.KERNEL_ROW_GROUP4
     elif case.startswith("auto_"):
         # chunks x layers of H heads x n tokens, token-major rows
         a.kernel = km.KERNEL_AUTO
@@ -185,6 +187,7 @@ def _plan_case(case):
     ("auto_small", km.PLAN_PER_HEAD),
     ("per_head_requested", km.PLAN_PER_HEAD),
     ("kernel_choice_unknown", km.ERR_SHAPE),
+    ("row_group4_requested", km.PLAN_ROW_GROUP),
     ("auto_recall", km.PLAN_ROW_GROUP),
     ("auto_recall_4_heads", km.PLAN_PER_HEAD),
     ("auto_recall_short_chunks", km.PLAN_PER_HEAD),

@@ -98,7 +98,7 @@ def test_rehydrate_validation_never_misbehaves(edits):
     plan = L.kamera_rehydrate_plan(ctypes.byref(a))
     assert plan == rc if rc != km.OK else plan in (km.PLAN_NONE, km.PLAN_PER_HEAD, km.PLAN_ROW_GROUP)
     if rc == km.OK:
-        assert a.kernel in (km.KERNEL_AUTO, km.KERNEL_PER_HEAD, km.KERNEL_ROW_GROUP)
+        assert a.kernel in (km.KERNEL_AUTO, km.KERNEL_PER_HEAD, km.KERNEL_ROW_GROUP, km.KERNEL_ROW_GROUP4)
     if not edits:
         assert rc == km.OK
     if rc == km.OK and min(a.n_chunks, a.n_layers, a.n_heads, a.n_tokens) > 0:

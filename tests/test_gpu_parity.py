@@ -99,6 +99,15 @@ REHYDRATE_CASES = {
     "rows_k_only": RehydrateCase(H=8, has_v=False, row_base=False, m_k=48, n=33, kernel=2, plan=2, seed=59),
     "rows_row_base_m64": RehydrateCase(H=8, m_k=64, m_v=64, kernel=2, plan=2, seed=60),
     "rows_row_base_h4_ragged": RehydrateCase(H=4, ragged=True, C=3, n=130, m_k=16, m_v=16, kernel=2, plan=2, seed=64),
+    # 8-head rows in two 4-head groups (the mid-size grids' form)
+    "rows4_h8_row_base_ragged": RehydrateCase(H=8, ragged=True, C=3, n=130, m_k=64, m_v=32, kernel=3, plan=2,
+                                              seed=66),
+    "rows4_h8_mrope_grid_paged": RehydrateCase(H=8, n=100, sections=(16, 24, 24), pos_mode="grid3", grid_w=32,
+                                               paged=True, m_k=64, m_v=64, kernel=3, plan=2, seed=67),
+    "rows4_h8_in_place": RehydrateCase(H=8, row_base=False, in_place=True, m_k=16, m_v=16, n=70,
+                                                  kernel=3, plan=2, seed=68),
+    "rows4_h6_post_rope_paged": RehydrateCase(H=6, post_rope=True, pairing="interleaved", theta=1e4, paged=True,
+                                              page_size=8, kernel=3, plan=2, seed=69),
     "per_head_reloc": RehydrateCase(H=8, reloc=True, kernel=2, plan=1, seed=65),
     "per_head_explicit_paged": RehydrateCase(H=8, pos_mode="explicit", paged=True, kernel=2, plan=1, seed=61),
     "per_head_rank_72_paged": RehydrateCase(H=8, m_k=72, m_v=8, paged=True, kernel=2, plan=1, seed=62),
