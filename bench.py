@@ -518,7 +518,8 @@ def main():
 
     if w.kind == "rehydrate":
         plan = km.rehydrate_plan(p.extra["call"])
-        kernel_name = "rehydrate_rows_kernel" if plan == km.PLAN_ROW_GROUP else "rehydrate_kernel"
+        kernel_name = ("rehydrate_rows_kernel" if plan in (km.PLAN_ROW_GROUP, km.PLAN_ROW_GROUP4)
+                       else "rehydrate_kernel")
     else:
         kernel_name = "shift_kernel"
     traffic = measured_traffic(w.name, kernel_name)

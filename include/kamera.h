@@ -103,15 +103,15 @@ typedef enum {
  * token block) taking every head of a token row, so that a 16-token pool page
  * is written as one contiguous run; possible for rows of <= 8 heads of 128
  * columns (one block per head, the rope band if any being the whole head),
- * rank <= 64 in whole 16-byte U chunks, linear or grid positions, no
- * relocation, and byte offsets below 2^31 within one (chunk, layer) slab or
- * one layer of the pool.  A row-group workgroup takes 8 heads (one per CU),
+ * rank <= 64 in whole 16-byte U chunks, linear or grid positions (with or
+ * without relocation), and byte offsets below 2^31 within one (chunk, layer)
+ * slab or one layer of the pool.  A row-group workgroup takes 8 heads (one per CU),
  * or 4 (two per CU; rows of <= 4 heads, or 8 heads in two groups).  AUTO
  * takes ROW_GROUP where it was measured faster on MI355X, counting g = planes
  * x chunks x layers x 1024-token blocks, for chunks of >= 1024 tokens: 8
- * heads with g >= 2048 (8 per workgroup) or 1024 <= g < 2048 (4 per
- * workgroup); 4 heads with 1024 <= g < 4096.  Smaller grids, shorter chunks
- * and other head counts keep PER_HEAD.  A ROW_GROUP request that is not
+ * heads with g >= 2048 (8 per workgroup; 4 with relocation) or 1024 <= g <
+ * 2048 (4 per workgroup); 4 heads with 1024 <= g < 4096.  Smaller grids,
+ * shorter chunks and other head counts keep PER_HEAD.  A ROW_GROUP request that is not
  * possible falls back to PER_HEAD. */
 typedef enum {
   KAMERA_KERNEL_AUTO = 0,
@@ -352,12 +352,15 @@ int kamera_validate(int32_t which, const void* args);
 
 /* Which kernel kamera_rehydrate would launch for `args` (see
  * kamera_kernel_choice), after exactly its host-side checks:
- * KAMERA_PLAN_PER_HEAD, KAMERA_PLAN_ROW_GROUP, KAMERA_PLAN_NONE for a call
- * with nothing to do, or the negative error code the call would return.
+ * KAMERA_PLAN_PER_HEAD, KAMERA_PLAN_ROW_GROUP (8 heads per workgroup),
+ * KAMERA_PLAN_ROW_GROUP4 (4 heads per workgroup), KAMERA_PLAN_NONE for a call
+ * with nothing to do, or the negative error code the call would return.  A
+ * positive plan equals the kamera_kernel_choice that requests that kernel.
  * Touches no device memory. */
 #define KAMERA_PLAN_NONE 0
 #define KAMERA_PLAN_PER_HEAD 1
 #define KAMERA_PLAN_ROW_GROUP 2
+#define KAMERA_PLAN_ROW_GROUP4 3
 int kamera_rehydrate_plan(const kamera_rehydrate_args* args);
 
 /* Text of the last error on the calling thread ("" after a successful call);

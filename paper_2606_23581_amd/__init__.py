@@ -56,6 +56,7 @@ KERNEL_ROW_GROUP4 = 3
 PLAN_NONE = 0
 PLAN_PER_HEAD = 1
 PLAN_ROW_GROUP = 2
+PLAN_ROW_GROUP4 = 3
 
 
 class KameraUnavailable(RuntimeError):
@@ -321,8 +322,9 @@ def rehydrate(*a, stream=None, **kw) -> None:
 
 
 def rehydrate_plan(prepared: "Prepared") -> int:
-    """``kamera_rehydrate_plan`` of a prepared rehydrate call: PLAN_PER_HEAD or
-    PLAN_ROW_GROUP (the kernel the call launches), PLAN_NONE, or an error."""
+    """``kamera_rehydrate_plan`` of a prepared rehydrate call: PLAN_PER_HEAD,
+    PLAN_ROW_GROUP or PLAN_ROW_GROUP4 (the kernel the call launches, with 8 or
+    4 heads per row-group workgroup), PLAN_NONE, or an error."""
     rc = lib().kamera_rehydrate_plan(ctypes.byref(prepared.args))
     _check(min(rc, 0))
     return rc

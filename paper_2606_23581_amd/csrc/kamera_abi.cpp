@@ -367,13 +367,15 @@ static int build_rehydrate(const kamera_rehydrate_args* a, kamera::RehydratePara
     o.n_blocks = nb;
     units += (int64_t)a->n_chunks * a->n_layers * a->n_heads * nb;
   }
-  // Rows of <= 8 heads of 128 columns, one block per head, rank <= 64 and
-  // no relocation can take the row-group kernel: a workgroup takes hw = 4 or
+  // Rows of <= 8 heads of 128 columns, one block per head and rank <= 64 can
+  // take the row-group kernel: a workgroup takes hw = 4 or
   // 8 heads of a token row, so it writes them as one contiguous run (a whole
   // pool page at 8 heads).  AUTO follows where it measured faster than the
   // per-head kernel (g = plane x chunk x layer x 1024-token blocks):
   //   8 heads: g >= 2048 -> hw 8 (one workgroup per CU); 1024 <= g < 2048 ->
-  //   hw 4 (two head groups, two workgroups per CU);
+  //   hw 4 (two head groups, two workgroups per CU); with relocation hw 4
+  //   for every g >= 1024 (the relocating 8-head variant runs out of
+  //   registers: it trails the per-head kernel, the 4-head one leads it);
   //   4 heads: 1024 <= g < 4096 -> hw 4;
   //   everything else (small grids, chunks under 1024 tokens, other head
   //   counts) keeps the per-head kernel.
@@ -384,10 +386,10 @@ static int build_rehydrate(const kamera_rehydrate_args* a, kamera::RehydratePara
   } else if (a->kernel == KAMERA_KERNEL_ROW_GROUP4) {
     hw = 4;
   } else if (a->kernel == KAMERA_KERNEL_AUTO && a->n_tokens >= 1024) {
-    if (a->n_heads == 8) hw = g1024 >= 2048 ? 8 : (g1024 >= 1024 ? 4 : 0);
+    if (a->n_heads == 8) hw = g1024 >= 2048 && !a->delta ? 8 : (g1024 >= 1024 ? 4 : 0);
     else if (a->n_heads == 4) hw = g1024 >= 1024 && g1024 < 4096 ? 4 : 0;
   }
-  bool rows = hw > 0 && P.delta == nullptr && a->n_heads <= kamera::kRgMaxHeads && a->head_dim == 128 &&
+  bool rows = hw > 0 && a->n_heads <= kamera::kRgMaxHeads && a->head_dim == 128 &&
               (!any_rot || a->pos_mode != KAMERA_POS_EXPLICIT);
   for (int p = 0; p < a->n_planes && rows; ++p) {
     kamera::PlaneParams& o = P.plane[p];
@@ -742,7 +744,8 @@ extern "C" int kamera_rehydrate_plan(const kamera_rehydrate_args* a) {
   if (rc) return rc;
   ok();
   if (!launch) return KAMERA_PLAN_NONE;
-  return P.row_group ? KAMERA_PLAN_ROW_GROUP : KAMERA_PLAN_PER_HEAD;
+  if (P.row_group == 0) return KAMERA_PLAN_PER_HEAD;
+  return P.row_group == 4 ? KAMERA_PLAN_ROW_GROUP4 : KAMERA_PLAN_ROW_GROUP;
 }
 
 // ---------------------------------------------------------------------------

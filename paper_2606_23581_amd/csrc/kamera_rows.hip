@@ -14,7 +14,7 @@ namespace kamera {
 // ---------------------------------------------------------------------------
 // Rows of <= 8 heads of 128 columns with one 128-column block per head (the
 // rope band, if any, is the whole head), rank <= 64, positions linear or on a
-// grid, no relocation.  A workgroup of HW = 4 or 8 waves owns (plane, chunk,
+// grid, with or without the relocation of already-rotated keys.  A workgroup of HW = 4 or 8 waves owns (plane, chunk,
 // layer, token block, group of HW heads); wave h computes head h of the group
 // in the register layout of the per-head kernel (kamera_kernels.hip: lane
 // (g, t) holds chunks g, g+4, g+8, g+12 of token t).  Per 16-token tile the
@@ -69,6 +69,7 @@ struct RgTask {
   int s_u3, s_u2;            // U token / head strides
   int s_o2, s_o3;            // output row (slot) / head strides
   double cp0, cp1, cp2;      // chunk position (t, h, w) of token 0
+  double dt, dh, dw;         // relocation: the chunk's move of already-rotated keys
   __amdgpu_buffer_rsrc_t rin, ru, rout;   // (chunk, layer) slabs of input, U and output
 };
 
@@ -200,7 +201,7 @@ __device__ __forceinline__ void rg_rotate(f32x4 (&acc)[8], int g, const double* 
 }
 
 // one wave: head h of the tile in LDS, result written back in place
-template <int MS, int ROT, int HW>
+template <int MS, int ROT, int HW, bool RELOC>
 __device__ __forceinline__ void rg_compute(const RehydrateParams& P, const RgTask& T, int i0, int h,
                                            const u32x4 (&wa)[8][MS > 0 ? MS : 1], uint8_t* buf,
                                            const double* s_freq, const int* s_coord) {
@@ -232,7 +233,18 @@ __device__ __forceinline__ void rg_compute(const RehydrateParams& P, const RgTas
       ph = T.cp1 + (double)(i / P.grid_w);
       pw = T.cp2 + (double)(i % P.grid_w);
     }
-    if (P.patch_post_rope) rg_rotate<ROT>(acc, g, s_freq, s_coord, pt, ph, pw);
+    // rotation before the patch, as in the per-head kernel:
+    //   post-rope frame:          R(p) K           (+ U W after)
+    //   relocation, post-rope:    R(delta) K       (+ U W after)
+    //   relocation, pre-rope:     R(delta - p) K, the stored frame (+ U W, then R(p))
+    if constexpr (RELOC) {
+      if (P.patch_post_rope)
+        rg_rotate<ROT>(acc, g, s_freq, s_coord, T.dt, T.dh, T.dw);
+      else
+        rg_rotate<ROT>(acc, g, s_freq, s_coord, T.dt - pt, T.dh - ph, T.dw - pw);
+    } else if (P.patch_post_rope) {
+      rg_rotate<ROT>(acc, g, s_freq, s_coord, pt, ph, pw);
+    }
   }
   if constexpr (MS > 0) {
     const uint8_t* urow = buf + HW * kTileTokens * kRgKRow + (h * kTileTokens + t) * rg_u_row(MS);
@@ -326,7 +338,7 @@ __device__ __forceinline__ void rg_put_w(int hq, int k0, int colb, const uint32_
   }
 }
 
-template <int MS, int ROT, int HW>
+template <int MS, int ROT, int HW, bool RELOC>
 __device__ __forceinline__ void rg_run(const RehydrateParams& P, const RgTask& T, int t_begin, int t_end,
                                        uint8_t* lds, const double* s_freq, const int* s_coord) {
   constexpr int NT = 64 * HW;
@@ -410,7 +422,7 @@ __device__ __forceinline__ void rg_run(const RehydrateParams& P, const RgTask& T
     rg_to_lds<MS, HW>(T, R, buf);
     if (tt + kRgDepth < n_tiles) rg_load<MS, HW>(T, i0 + kRgDepth * kTileTokens, R);
     __syncthreads();
-    if (active) rg_compute<MS, ROT, HW>(P, T, i0, h, wa, buf, s_freq, s_coord);
+    if (active) rg_compute<MS, ROT, HW, RELOC>(P, T, i0, h, wa, buf, s_freq, s_coord);
     __syncthreads();
     rg_store<HW>(P, T, t_begin, i0, buf, s_page);
   };
@@ -421,7 +433,8 @@ __device__ __forceinline__ void rg_run(const RehydrateParams& P, const RgTask& T
   }
 }
 
-template <int MS, int HW>
+// RELOC: the keys are already rotated and move by the chunk's delta
+template <int MS, int HW, bool RELOC>
 __global__ __launch_bounds__(64 * HW, 8 / HW) void rehydrate_rows_kernel(const RehydrateParams /*by value, read in place*/) {
   const RehydrateParams& P = kernel_params<RehydrateParams>();
   extern __shared__ __align__(16) uint8_t lds_dyn[];
@@ -477,6 +490,12 @@ __global__ __launch_bounds__(64 * HW, 8 / HW) void rehydrate_rows_kernel(const R
   T.rout = rg_rsrc(Q.out + out_base + (int64_t)T.l * Q.out_s[1] + (int64_t)T.h0 * Q.out_s[3],
                    Q.out_rec - 2 * (int64_t)T.h0 * Q.out_s[3]);
   T.cp0 = T.cp1 = T.cp2 = 0.0;
+  T.dt = T.dh = T.dw = 0.0;
+  if (RELOC) {
+    T.dt = (double)P.delta[3 * T.c];
+    T.dh = (double)P.delta[3 * T.c + 1];
+    T.dw = (double)P.delta[3 * T.c + 2];
+  }
   if (P.chunk_pos != nullptr) {
     T.cp0 = (double)P.chunk_pos[3 * T.c];
     T.cp1 = (double)P.chunk_pos[3 * T.c + 1];
@@ -491,13 +510,13 @@ __global__ __launch_bounds__(64 * HW, 8 / HW) void rehydrate_rows_kernel(const R
     }
   }
   switch (rot) {
-    case 0: rg_run<MS, 0, HW>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
-    case 1: rg_run<MS, 1, HW>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
-    default: rg_run<MS, 2, HW>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
+    case 0: rg_run<MS, 0, HW, RELOC>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
+    case 1: rg_run<MS, 1, HW, RELOC>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
+    default: rg_run<MS, 2, HW, RELOC>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
   }
 }
 
-template <int MS, int HW>
+template <int MS, int HW, bool RELOC>
 hipError_t launch_rows(const RehydrateParams& p, hipStream_t s) {
   // the LDS limit is raised once per device and instantiation (a race only
   // repeats the call)
@@ -506,31 +525,36 @@ hipError_t launch_rows(const RehydrateParams& p, hipStream_t s) {
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
   if (dev < 0 || dev >= 64 || !attr_set[dev]) {
-    e = hipFuncSetAttribute((const void*)rehydrate_rows_kernel<MS, HW>, hipFuncAttributeMaxDynamicSharedMemorySize,
+    e = hipFuncSetAttribute((const void*)rehydrate_rows_kernel<MS, HW, RELOC>, hipFuncAttributeMaxDynamicSharedMemorySize,
                             rg_lds_bytes(MS, HW));
     if (e != hipSuccess) return e;
     if (dev >= 0 && dev < 64) attr_set[dev] = true;
   }
   const dim3 grid((uint32_t)((int64_t)p.per_xcd * 8)), block(64 * HW);
-  hipLaunchKernelGGL((rehydrate_rows_kernel<MS, HW>), grid, block, rg_lds_bytes(MS, HW), s, p);
+  hipLaunchKernelGGL((rehydrate_rows_kernel<MS, HW, RELOC>), grid, block, rg_lds_bytes(MS, HW), s, p);
   return hipGetLastError();
+}
+
+template <bool RELOC>
+hipError_t launch_rows_reloc(const RehydrateParams& p, hipStream_t s, int max_steps) {
+  if (p.row_group == 4) {
+    switch (max_steps) {
+      case 0: return launch_rows<0, 4, RELOC>(p, s);
+      case 1: return launch_rows<1, 4, RELOC>(p, s);
+      default: return launch_rows<2, 4, RELOC>(p, s);
+    }
+  }
+  switch (max_steps) {
+    case 0: return launch_rows<0, 8, RELOC>(p, s);
+    case 1: return launch_rows<1, 8, RELOC>(p, s);
+    default: return launch_rows<2, 8, RELOC>(p, s);
+  }
 }
 
 hipError_t launch_rehydrate_rows(const RehydrateParams& p, hipStream_t s) {
   int max_steps = 0;
   for (int k = 0; k < p.n_planes; ++k) max_steps = max_steps > p.plane[k].m_steps ? max_steps : p.plane[k].m_steps;
-  if (p.row_group == 4) {
-    switch (max_steps) {
-      case 0: return launch_rows<0, 4>(p, s);
-      case 1: return launch_rows<1, 4>(p, s);
-      default: return launch_rows<2, 4>(p, s);
-    }
-  }
-  switch (max_steps) {
-    case 0: return launch_rows<0, 8>(p, s);
-    case 1: return launch_rows<1, 8>(p, s);
-    default: return launch_rows<2, 8>(p, s);
-  }
+  return p.delta != nullptr ? launch_rows_reloc<true>(p, s, max_steps) : launch_rows_reloc<false>(p, s, max_steps);
 }
 
 }  // namespace kamera

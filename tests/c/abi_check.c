@@ -93,8 +93,10 @@ int main(void) {
    * row-group kernel when requested; an unknown choice is rejected */
   fill_rehydrate(&a);
   CHECK(kamera_rehydrate_plan(&a) == KAMERA_PLAN_PER_HEAD);
-  a.kernel = KAMERA_KERNEL_ROW_GROUP;
-  CHECK(kamera_rehydrate_plan(&a) == KAMERA_PLAN_ROW_GROUP);
+  a.kernel = KAMERA_KERNEL_ROW_GROUP;   /* 4 heads: one 4-head group per row */
+  CHECK(kamera_rehydrate_plan(&a) == KAMERA_PLAN_ROW_GROUP4);
+  a.kernel = KAMERA_KERNEL_ROW_GROUP4;
+  CHECK(kamera_rehydrate_plan(&a) == KAMERA_PLAN_ROW_GROUP4);
   a.kernel = 9;
   CHECK(kamera_rehydrate_plan(&a) == KAMERA_ERR_SHAPE);
   fill_rehydrate(&a);

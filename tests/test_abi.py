@@ -137,10 +137,14 @@ def _plan_case(case):
         a.kernel = 7
     elif case == "row_group4_requested":
         a.kernel = km.KERNEL_ROW_GROUP4
-    elif case.startswith("auto_"):
+    elif case.startswith("auto_") or case == "row_group_8_heads":
         # chunks x layers of H heads x n tokens, token-major rows
-        a.kernel = km.KERNEL_AUTO
-        C, Ln, H, n = {"auto_recall": (64, 80, 8, 1024), "auto_recall_4_heads": (64, 80, 4, 1024),
+        if case != "row_group_8_heads":
+            a.kernel = km.KERNEL_AUTO
+        if case == "auto_recall_relocation":
+            a.delta = FAKE + 0x300000000
+        C, Ln, H, n = {"auto_recall": (64, 80, 8, 1024), "auto_recall_relocation": (64, 80, 8, 1024),
+                       "row_group_8_heads": (2, 3, 8, 64), "auto_recall_4_heads": (64, 80, 4, 1024),
                        "auto_recall_short_chunks": (64, 80, 8, 512), "auto_mid_8_heads": (16, 32, 8, 1024),
                        "auto_mid_4_heads": (16, 32, 4, 1024), "auto_small_8_heads": (8, 28, 8, 1024),
                        "auto_6_heads": (64, 80, 6, 1024)}[case]
@@ -183,23 +187,25 @@ def _plan_case(case):
 
 
 @pytest.mark.parametrize("case,plan", [
-    ("default", km.PLAN_ROW_GROUP),
+    ("default", km.PLAN_ROW_GROUP4),
+    ("row_group_8_heads", km.PLAN_ROW_GROUP),
     ("auto_small", km.PLAN_PER_HEAD),
     ("per_head_requested", km.PLAN_PER_HEAD),
     ("kernel_choice_unknown", km.ERR_SHAPE),
-    ("row_group4_requested", km.PLAN_ROW_GROUP),
+    ("row_group4_requested", km.PLAN_ROW_GROUP4),
     ("auto_recall", km.PLAN_ROW_GROUP),
     ("auto_recall_4_heads", km.PLAN_PER_HEAD),
     ("auto_recall_short_chunks", km.PLAN_PER_HEAD),
-    ("auto_mid_8_heads", km.PLAN_ROW_GROUP),
-    ("auto_mid_4_heads", km.PLAN_ROW_GROUP),
+    ("auto_recall_relocation", km.PLAN_ROW_GROUP4),
+    ("auto_mid_8_heads", km.PLAN_ROW_GROUP4),
+    ("auto_mid_4_heads", km.PLAN_ROW_GROUP4),
     ("auto_small_8_heads", km.PLAN_PER_HEAD),
     ("auto_6_heads", km.PLAN_PER_HEAD),
     ("heads_9", km.PLAN_PER_HEAD),
     ("rank_72", km.PLAN_PER_HEAD),
     ("rank_12", km.PLAN_PER_HEAD),
     ("explicit", km.PLAN_PER_HEAD),
-    ("relocation", km.PLAN_PER_HEAD),
+    ("relocation", km.PLAN_ROW_GROUP4),
     ("head_dim_256", km.PLAN_PER_HEAD),
     ("partial_band", km.PLAN_PER_HEAD),
     ("patch_64", km.PLAN_PER_HEAD),
@@ -211,9 +217,11 @@ def test_rehydrate_plan_picks_the_kernel(case, plan):
     """kamera_rehydrate_plan runs the call's host checks and names the kernel:
     the row-group kernel, when requested, only for rows of <= 8 heads x 128
     columns with one block per head, rank <= 64 in whole 16-byte U chunks, no
-    explicit positions or relocation, and every byte offset below 2^31; AUTO
-    takes it for 8-head rows on >= 1024 (plane, chunk, layer, 1024-token
-    block) units and for 4-head rows on 1024 .. 4095 of them."""
+    explicit positions, and every byte offset below 2^31, with 8 heads per
+    workgroup for wider rows and 4 for rows of <= 4 heads; AUTO takes it for
+    8-head rows on >= 1024 (plane, chunk, layer, 1024-token block) units (8
+    heads per workgroup from 2048 on, unless relocating) and for 4-head rows
+    on 1024 .. 4095 of them."""
     a = _plan_case(case)
     assert km.lib().kamera_rehydrate_plan(ctypes.byref(a)) == plan
     assert km.lib().kamera_validate(0, ctypes.byref(a)) == min(plan, 0)

@@ -96,7 +96,7 @@ def test_rehydrate_validation_never_misbehaves(edits):
     assert (km.last_error() == "") == (rc == km.OK), (rc, km.last_error())
     # the plan agrees with validation: an error code, or a kernel (none for an empty call)
     plan = L.kamera_rehydrate_plan(ctypes.byref(a))
-    assert plan == rc if rc != km.OK else plan in (km.PLAN_NONE, km.PLAN_PER_HEAD, km.PLAN_ROW_GROUP)
+    assert plan == rc if rc != km.OK else plan in (km.PLAN_NONE, km.PLAN_PER_HEAD, km.PLAN_ROW_GROUP, km.PLAN_ROW_GROUP4)
     if rc == km.OK:
         assert a.kernel in (km.KERNEL_AUTO, km.KERNEL_PER_HEAD, km.KERNEL_ROW_GROUP, km.KERNEL_ROW_GROUP4)
     if not edits:

@@ -83,32 +83,38 @@ REHYDRATE_CASES = {
                                                   paged=True, m_k=64, m_v=64, p0_range=(1, 4097),
                                                   kernel=2, plan=2, seed=50),
     "rows_h3_interleaved_page24_ragged": RehydrateCase(pairing="interleaved", theta=1e4, paged=True, page_size=24,
-                                                       ragged=True, C=4, n=90, m_k=40, m_v=8, kernel=2, plan=2, seed=51),
-    "rows_h1_dense_rope_only": RehydrateCase(H=1, row_base=False, m_k=0, m_v=0, kernel=2, plan=2, seed=52),
+                                                       ragged=True, C=4, n=90, m_k=40, m_v=8, kernel=2, plan=3, seed=51),
+    "rows_h1_dense_rope_only": RehydrateCase(H=1, row_base=False, m_k=0, m_v=0, kernel=2, plan=3, seed=52),
     "rows_h8_dense_in_place": RehydrateCase(H=8, row_base=False, in_place=True, m_k=32, m_v=16, n=70,
                                             kernel=2, plan=2, seed=53),
     "rows_layer_rank_odd_paged": RehydrateCase(L=3, layer_rank=(20, 0, 64), m_k=64, m_v=64, paged=True,
-                                               kernel=2, plan=2, seed=54),
-    "rows_post_rope_unit_major": RehydrateCase(H=4, post_rope=True, unit_major=True, paged=True, kernel=2, plan=2, seed=55),
+                                               kernel=2, plan=3, seed=54),
+    "rows_post_rope_unit_major": RehydrateCase(H=4, post_rope=True, unit_major=True, paged=True, kernel=2, plan=3, seed=55),
     "rows_unit_major_long_blocks": RehydrateCase(H=8, C=1, L=1, n=1100, unit_major=True, paged=True, m_k=64,
                                                  m_v=64, sections=(16, 24, 24), pos_mode="grid3",
                                                  kernel=2, plan=2, seed=56),
     "rows_shared_basis_v_patch_only": RehydrateCase(H=2, shared_w=True, C=3, m_k=0, m_v=24, paged=True,
-                                                    kernel=2, plan=2, seed=57),
+                                                    kernel=2, plan=3, seed=57),
     "rows_one_token": RehydrateCase(H=8, n=1, paged=True, kernel=2, plan=2, seed=58),
     "rows_k_only": RehydrateCase(H=8, has_v=False, row_base=False, m_k=48, n=33, kernel=2, plan=2, seed=59),
     "rows_row_base_m64": RehydrateCase(H=8, m_k=64, m_v=64, kernel=2, plan=2, seed=60),
-    "rows_row_base_h4_ragged": RehydrateCase(H=4, ragged=True, C=3, n=130, m_k=16, m_v=16, kernel=2, plan=2, seed=64),
+    "rows_row_base_h4_ragged": RehydrateCase(H=4, ragged=True, C=3, n=130, m_k=16, m_v=16, kernel=2, plan=3, seed=64),
     # 8-head rows in two 4-head groups (the mid-size grids' form)
-    "rows4_h8_row_base_ragged": RehydrateCase(H=8, ragged=True, C=3, n=130, m_k=64, m_v=32, kernel=3, plan=2,
+    "rows4_h8_row_base_ragged": RehydrateCase(H=8, ragged=True, C=3, n=130, m_k=64, m_v=32, kernel=3, plan=3,
                                               seed=66),
     "rows4_h8_mrope_grid_paged": RehydrateCase(H=8, n=100, sections=(16, 24, 24), pos_mode="grid3", grid_w=32,
-                                               paged=True, m_k=64, m_v=64, kernel=3, plan=2, seed=67),
+                                               paged=True, m_k=64, m_v=64, kernel=3, plan=3, seed=67),
     "rows4_h8_in_place": RehydrateCase(H=8, row_base=False, in_place=True, m_k=16, m_v=16, n=70,
-                                                  kernel=3, plan=2, seed=68),
+                                                  kernel=3, plan=3, seed=68),
     "rows4_h6_post_rope_paged": RehydrateCase(H=6, post_rope=True, pairing="interleaved", theta=1e4, paged=True,
-                                              page_size=8, kernel=3, plan=2, seed=69),
-    "per_head_reloc": RehydrateCase(H=8, reloc=True, kernel=2, plan=1, seed=65),
+                                              page_size=8, kernel=3, plan=3, seed=69),
+    "rows_reloc_h8_m64": RehydrateCase(H=8, reloc=True, m_k=64, m_v=64, n=70, kernel=2, plan=2, seed=65),
+    "rows4_reloc_mrope_grid_paged_post_frame": RehydrateCase(H=8, reloc=True, post_rope=True, sections=(24, 20, 20),
+                                                             section_order="interleaved", pos_mode="grid3",
+                                                             paged=True, m_k=32, m_v=0, kernel=3, plan=3,
+                                                             seed=70),
+    "rows_reloc_in_place_no_patch": RehydrateCase(H=4, reloc=True, row_base=False, in_place=True, m_k=0, m_v=0,
+                                                  kernel=2, plan=3, seed=71),
     "per_head_explicit_paged": RehydrateCase(H=8, pos_mode="explicit", paged=True, kernel=2, plan=1, seed=61),
     "per_head_rank_72_paged": RehydrateCase(H=8, m_k=72, m_v=8, paged=True, kernel=2, plan=1, seed=62),
     "per_head_9_heads_paged": RehydrateCase(H=9, paged=True, kernel=2, plan=1, seed=63),
@@ -246,7 +252,7 @@ def test_rehydrate_bad_page_is_flagged_not_written(device, kernel):
         pos = dict(pos_mode=km.POS_LINEAR, chunk_pos=dev_i32(np.zeros((C, 3)), device))
     prep = km.prepare_rehydrate(dev(K, device), pool, rope=rs, page_table=dev_i32(pt, device), page_size=P,
                                 n_pool_pages=3, status=status, kernel=km.KERNEL_ROW_GROUP, **pos)
-    assert km.rehydrate_plan(prep) == (km.PLAN_PER_HEAD if kernel == "per_head" else km.PLAN_ROW_GROUP)
+    assert km.rehydrate_plan(prep) == (km.PLAN_PER_HEAD if kernel == "per_head" else km.PLAN_ROW_GROUP4)
     prep.launch()
     torch.cuda.synchronize()
     assert int(status.cpu()[0]) & km.STATUS_BAD_PAGE

@@ -101,10 +101,13 @@ def test_workload_rehydrate(device, name):
     print(f"[case] workload {name}", flush=True)
     p = harness.prepare(name, device)
     # the kernel AUTO picks: row groups of 8 heads for the 80-layer recalls,
-    # of 4 heads (two per 8-head row) for the mid-size one, per head elsewhere
-    rows = {"gqa80l_64x1024_m64_mrope_paged", "gqa80l_64x1024_m64_mrope_paged_deephalf",
-            "gqa32l_16x1024_m32_mrope_paged"}
-    assert km.rehydrate_plan(p.extra["call"]) == (km.PLAN_ROW_GROUP if name in rows else km.PLAN_PER_HEAD)
+    # of 4 heads (two per 8-head row) for the mid-size recall and the window
+    # survivors, per head elsewhere
+    plan = {"gqa80l_64x1024_m64_mrope_paged": km.PLAN_ROW_GROUP,
+            "gqa80l_64x1024_m64_mrope_paged_deephalf": km.PLAN_ROW_GROUP,
+            "gqa32l_16x1024_m32_mrope_paged": km.PLAN_ROW_GROUP4,
+            "gqa36l_15x1024_survivor_m64": km.PLAN_ROW_GROUP4}
+    assert km.rehydrate_plan(p.extra["call"]) == plan.get(name, km.PLAN_PER_HEAD)
     units = harness.sample_units(p.workload, 12 if p.workload.units() > 12 else p.workload.units(), seed=1)
     if p.workload.n_heads == 8:
         units += [(0, 0, 3), (0, 0, 4)]       # both sides of a 4-head group boundary
