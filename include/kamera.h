@@ -107,11 +107,10 @@ typedef enum {
  * without relocation), and byte offsets below 2^31 within one (chunk, layer)
  * slab or one layer of the pool.  A row-group workgroup takes 8 heads (one per CU),
  * or 4 (two per CU; rows of <= 4 heads, or 8 heads in two groups).  AUTO
- * takes ROW_GROUP where it was measured faster on MI355X, counting g = planes
- * x chunks x layers x 1024-token blocks, for chunks of >= 1024 tokens: 8
- * heads with g >= 2048 (8 per workgroup; 4 with relocation) or 1024 <= g <
- * 2048 (4 per workgroup); 4 heads with 1024 <= g < 4096.  Smaller grids,
- * shorter chunks and other head counts keep PER_HEAD.  A ROW_GROUP request that is not
+ * takes ROW_GROUP4 where it was measured faster on MI355X: rows of 4 or 8
+ * heads, chunks of >= 256 tokens and >= 2^22 rows in all (planes x chunks x
+ * layers x tokens x heads).  Fewer rows, shorter chunks and other head
+ * counts keep PER_HEAD.  A ROW_GROUP or ROW_GROUP4 request that is not
  * possible falls back to PER_HEAD. */
 typedef enum {
   KAMERA_KERNEL_AUTO = 0,

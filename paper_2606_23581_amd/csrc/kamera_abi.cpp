@@ -368,26 +368,24 @@ static int build_rehydrate(const kamera_rehydrate_args* a, kamera::RehydratePara
     units += (int64_t)a->n_chunks * a->n_layers * a->n_heads * nb;
   }
   // Rows of <= 8 heads of 128 columns, one block per head and rank <= 64 can
-  // take the row-group kernel: a workgroup takes hw = 4 or
-  // 8 heads of a token row, so it writes them as one contiguous run (a whole
-  // pool page at 8 heads).  AUTO follows where it measured faster than the
-  // per-head kernel (g = plane x chunk x layer x 1024-token blocks):
-  //   8 heads: g >= 2048 -> hw 8 (one workgroup per CU); 1024 <= g < 2048 ->
-  //   hw 4 (two head groups, two workgroups per CU); with relocation hw 4
-  //   for every g >= 1024 (the relocating 8-head variant runs out of
-  //   registers: it trails the per-head kernel, the 4-head one leads it);
-  //   4 heads: 1024 <= g < 4096 -> hw 4;
-  //   everything else (small grids, chunks under 1024 tokens, other head
-  //   counts) keeps the per-head kernel.
-  const int64_t g1024 = (int64_t)a->n_planes * a->n_chunks * a->n_layers * ceil_div(a->n_tokens, 1024);
+  // take the row-group kernel: a workgroup takes hw = 4 or 8 heads of a token
+  // row, so it writes them as one contiguous run (a whole pool page at 8
+  // heads).  AUTO follows where it measured faster than the per-head kernel,
+  // averaged over several placements of the buffers in HBM: rows of 4 or 8
+  // heads, chunks of >= 256 tokens and >= 2^22 rows in all (planes x chunks x
+  // layers x tokens x heads) take groups of 4 heads (two workgroups per CU);
+  // 8-head groups never led them by more than the spread of placements and
+  // trail them when relocating (they run out of registers).  Fewer rows, where
+  // a task's set-up is paid over too few tiles, shorter chunks and other head
+  // counts keep the per-head kernel.
+  const double n_rows = (double)a->n_planes * a->n_chunks * a->n_layers * a->n_tokens * a->n_heads;
   int hw = 0;
   if (a->kernel == KAMERA_KERNEL_ROW_GROUP) {
     hw = a->n_heads <= 4 ? 4 : 8;
   } else if (a->kernel == KAMERA_KERNEL_ROW_GROUP4) {
     hw = 4;
-  } else if (a->kernel == KAMERA_KERNEL_AUTO && a->n_tokens >= 1024) {
-    if (a->n_heads == 8) hw = g1024 >= 2048 && !a->delta ? 8 : (g1024 >= 1024 ? 4 : 0);
-    else if (a->n_heads == 4) hw = g1024 >= 1024 && g1024 < 4096 ? 4 : 0;
+  } else if (a->kernel == KAMERA_KERNEL_AUTO) {
+    hw = (a->n_heads == 4 || a->n_heads == 8) && a->n_tokens >= 256 && n_rows >= 4194304.0 ? 4 : 0;
   }
   bool rows = hw > 0 && a->n_heads <= kamera::kRgMaxHeads && a->head_dim == 128 &&
               (!any_rot || a->pos_mode != KAMERA_POS_EXPLICIT);

@@ -69,8 +69,18 @@ def _kv_rows(shape, gen, device, unit_major: bool):
     return randn_bf16_device(shape, 1.0, gen, device)
 
 
+def _u_rows(shape, std, gen, device, token_major: bool):
+    """Patch factors U of one workload, [C, L, H, n, m] as the operator sees
+    it.  With ``token_major`` the memory is [C, L, n, H, m]: the factors of
+    every head of a token row are adjacent, like the rows themselves."""
+    C, L, H, n, m = shape
+    if token_major:
+        return randn_bf16_device((C, L, n, H, m), std, gen, device).permute(0, 1, 3, 2, 4)
+    return randn_bf16_device(shape, std, gen, device)
+
+
 def prepare(name: str, device="cuda", seed: Optional[int] = None, unit_major: bool = True,
-            pool_head_major: bool = False) -> Prepared:
+            pool_head_major: bool = False, u_token_major: bool = False) -> Prepared:
     import torch
 
     import paper_2606_23581_amd as km
@@ -122,10 +132,10 @@ def prepare(name: str, device="cuda", seed: Optional[int] = None, unit_major: bo
         if w.has_v:
             T["v_in"] = _kv_rows((C, L, n, H, D), gen, device, unit_major)
     if w.m_k > 0:
-        T["u_k"] = randn_bf16_device((C, L, H, n, w.m_k), w.u_std, gen, device)
+        T["u_k"] = _u_rows((C, L, H, n, w.m_k), w.u_std, gen, device, u_token_major)
         T["w_k"] = randn_bf16_device((C, L, H, w.m_k, w.patch_dim), w.w_std, gen, device)
     if w.has_v and w.m_v > 0:
-        T["u_v"] = randn_bf16_device((C, L, H, n, w.m_v), w.u_std, gen, device)
+        T["u_v"] = _u_rows((C, L, H, n, w.m_v), w.u_std, gen, device, u_token_major)
         T["w_v"] = randn_bf16_device((C, L, H, w.m_v, w.patch_dim), w.w_std, gen, device)
     if w.m_pe > 0:
         T["u_pe"] = randn_bf16_device((C, L, H, n, w.m_pe), w.u_std, gen, device)

@@ -144,8 +144,10 @@ def _plan_case(case):
         if case == "auto_recall_relocation":
             a.delta = FAKE + 0x300000000
         C, Ln, H, n = {"auto_recall": (64, 80, 8, 1024), "auto_recall_relocation": (64, 80, 8, 1024),
+                       "auto_recall_128_token_chunks": (64, 80, 8, 128), "auto_2_22_rows": (16, 32, 4, 1024),
+                       "auto_below_2_22_rows": (16, 32, 4, 1023),
                        "row_group_8_heads": (2, 3, 8, 64), "auto_recall_4_heads": (64, 80, 4, 1024),
-                       "auto_recall_short_chunks": (64, 80, 8, 512), "auto_mid_8_heads": (16, 32, 8, 1024),
+                       "auto_recall_short_chunks": (64, 80, 8, 256), "auto_mid_8_heads": (16, 32, 8, 1024),
                        "auto_mid_4_heads": (16, 32, 4, 1024), "auto_small_8_heads": (8, 28, 8, 1024),
                        "auto_6_heads": (64, 80, 6, 1024)}[case]
         a.n_chunks, a.n_layers, a.n_heads, a.n_tokens = C, Ln, H, n
@@ -193,9 +195,12 @@ def _plan_case(case):
     ("per_head_requested", km.PLAN_PER_HEAD),
     ("kernel_choice_unknown", km.ERR_SHAPE),
     ("row_group4_requested", km.PLAN_ROW_GROUP4),
-    ("auto_recall", km.PLAN_ROW_GROUP),
-    ("auto_recall_4_heads", km.PLAN_PER_HEAD),
-    ("auto_recall_short_chunks", km.PLAN_PER_HEAD),
+    ("auto_recall", km.PLAN_ROW_GROUP4),
+    ("auto_recall_4_heads", km.PLAN_ROW_GROUP4),
+    ("auto_recall_short_chunks", km.PLAN_ROW_GROUP4),
+    ("auto_recall_128_token_chunks", km.PLAN_PER_HEAD),
+    ("auto_2_22_rows", km.PLAN_ROW_GROUP4),
+    ("auto_below_2_22_rows", km.PLAN_PER_HEAD),
     ("auto_recall_relocation", km.PLAN_ROW_GROUP4),
     ("auto_mid_8_heads", km.PLAN_ROW_GROUP4),
     ("auto_mid_4_heads", km.PLAN_ROW_GROUP4),
@@ -218,10 +223,9 @@ def test_rehydrate_plan_picks_the_kernel(case, plan):
     the row-group kernel, when requested, only for rows of <= 8 heads x 128
     columns with one block per head, rank <= 64 in whole 16-byte U chunks, no
     explicit positions, and every byte offset below 2^31, with 8 heads per
-    workgroup for wider rows and 4 for rows of <= 4 heads; AUTO takes it for
-    8-head rows on >= 1024 (plane, chunk, layer, 1024-token block) units (8
-    heads per workgroup from 2048 on, unless relocating) and for 4-head rows
-    on 1024 .. 4095 of them."""
+    workgroup for wider rows and 4 for rows of <= 4 heads; AUTO takes it, with
+    4 heads per workgroup, for rows of 4 or 8 heads, chunks of >= 256 tokens
+    and >= 2^22 rows (planes x chunks x layers x tokens x heads)."""
     a = _plan_case(case)
     assert km.lib().kamera_rehydrate_plan(ctypes.byref(a)) == plan
     assert km.lib().kamera_validate(0, ctypes.byref(a)) == min(plan, 0)
