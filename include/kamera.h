@@ -192,7 +192,15 @@ typedef struct {
  * sizes imply), except exactly in place: a dense output with row_base NULL,
  * the same base pointer and the same strides as the input (each element is
  * then read and written by the same workgroup; two planes in place on one
- * tensor must cover disjoint columns).
+ * tensor must cover disjoint columns).  The two planes' outputs must not
+ * overlap each other either, except (a) one tensor through the same mapping
+ * on disjoint columns, or (b) interleaved rows: the same out_stride, all of
+ * them >= 0, the layer (and for dense output the chunk) stride a multiple of
+ * the row stride out_stride[2], and the bases d elements apart with
+ * span <= |d| and |d| + span <= out_stride[2], span = (n_heads - 1) *
+ * out_stride[3] + head_dim -- e.g. a pool [layer][slot][K|V][head][dim] in
+ * which the K and V rows of a slot are adjacent, so that a page of both
+ * planes is one contiguous run.
  *
  * Relocation (delta != NULL, device int32 [n_chunks][3]): the input keys are
  * already rotated, at target - delta (survivors of a window slide, Sec. 5),

@@ -174,6 +174,28 @@ int pick_grid(int64_t n_tasks, int32_t& per_xcd, const char* who) {
 // kamera_rehydrate
 // ---------------------------------------------------------------------------
 
+// The two planes' outputs interleave by rows without sharing an element: the
+// same strides (none negative); every offset a plane writes to is a multiple of
+// the row stride r plus a position inside one row's span (all heads of the
+// row); the bases are d elements apart with span <= |d| <= r - span, so a row
+// of one plane lies in the gap between two rows of the other.
+static bool interleaved_rows(const kamera_rehydrate_args* a) {
+  const kamera_plane& q0 = a->plane[0];
+  const kamera_plane& q1 = a->plane[1];
+  if (memcmp(q0.out_stride, q1.out_stride, sizeof(q0.out_stride)) != 0) return false;
+  const int64_t* s = q0.out_stride;
+  for (int k = 0; k < 4; ++k)
+    if (s[k] < 0) return false;
+  const int64_t r = s[2];
+  if (r <= 0 || s[1] % r != 0 || (!a->paged && s[0] % r != 0)) return false;
+  const int64_t span = (int64_t)(a->n_heads - 1) * s[3] + a->head_dim;
+  const uintptr_t p0 = (uintptr_t)q0.out, p1 = (uintptr_t)q1.out;
+  const uintptr_t gap = p0 > p1 ? p0 - p1 : p1 - p0;
+  if (gap % 2 != 0) return false;
+  const int64_t d = (int64_t)(gap / 2);
+  return span <= d && d + span <= r;
+}
+
 // Validation and kernel parameters of a rehydrate call; *launch is false for
 // an empty call (nothing to do).
 static int build_rehydrate(const kamera_rehydrate_args* a, kamera::RehydrateParams& P, bool& launch) {
@@ -282,7 +304,8 @@ static int build_rehydrate(const kamera_rehydrate_args* a, kamera::RehydratePara
         return fail(KAMERA_ERR_ALIAS, "%s: output of plane %d overlaps the input of plane %d", who, o, p);
     }
   }
-  // two planes may write one tensor only through the same mapping on disjoint columns
+  // two planes may write one tensor only through the same mapping on disjoint
+  // columns, or with interleaved rows (interleaved_rows)
   if (a->n_planes == 2) {
     const kamera_plane& q0 = a->plane[0];
     const kamera_plane& q1 = a->plane[1];
@@ -295,7 +318,7 @@ static int build_rehydrate(const kamera_rehydrate_args* a, kamera::RehydratePara
       const bool same_map = q0.out == q1.out && memcmp(q0.out_stride, q1.out_stride, sizeof(q0.out_stride)) == 0;
       const int b0 = q0.col_begin, e0 = (q0.col_begin == 0 && q0.col_end == 0) ? a->head_dim : q0.col_end;
       const int b1 = q1.col_begin, e1 = (q1.col_begin == 0 && q1.col_end == 0) ? a->head_dim : q1.col_end;
-      if (!same_map || !(e0 <= b1 || e1 <= b0))
+      if ((!same_map || !(e0 <= b1 || e1 <= b0)) && !interleaved_rows(a))
         return fail(KAMERA_ERR_ALIAS, "%s: the two planes' outputs overlap", who);
     }
   }

@@ -80,7 +80,8 @@ def _u_rows(shape, std, gen, device, token_major: bool):
 
 
 def prepare(name: str, device="cuda", seed: Optional[int] = None, unit_major: bool = True,
-            pool_head_major: bool = False, u_token_major: bool = False) -> Prepared:
+            pool_head_major: bool = False, u_token_major: bool = False,
+            separate_pools: bool = False) -> Prepared:
     import torch
 
     import paper_2606_23581_amd as km
@@ -160,18 +161,23 @@ def prepare(name: str, device="cuda", seed: Optional[int] = None, unit_major: bo
             v_out = T["v_in"]
     elif w.paged:
         slots = w.n_pool_pages * w.page_size
-        if pool_head_major:   # [L, H, slots, D] memory, [L, slots, H, D] view
+        if w.has_v and not pool_head_major and not separate_pools:
+            # one pool [L, slots, K|V, H, D]: the K and V rows of a slot are
+            # adjacent, so a 16-token page of both planes is one 64 KiB run
+            T["kv_pool"] = torch.zeros((L, slots, 2, H, D), dtype=torch.bfloat16, device=device)
+            T["k_pool"], T["v_pool"] = T["kv_pool"][:, :, 0], T["kv_pool"][:, :, 1]
+        elif pool_head_major:   # [L, H, slots, D] memory, [L, slots, H, D] view
             T["k_pool"] = torch.zeros((L, H, slots, D), dtype=torch.bfloat16, device=device).transpose(1, 2)
+            if w.has_v:
+                T["v_pool"] = torch.zeros((L, H, slots, D), dtype=torch.bfloat16, device=device).transpose(1, 2)
         else:
             T["k_pool"] = torch.zeros((L, slots, H, D), dtype=torch.bfloat16, device=device)
+            if w.has_v:
+                T["v_pool"] = torch.zeros((L, slots, H, D), dtype=torch.bfloat16, device=device)
         T["page_table"] = torch.from_numpy(meta.page_table).to(device)
         kw.update(page_table=T["page_table"], page_size=w.page_size, n_pool_pages=w.n_pool_pages)
         k_out = T["k_pool"]
         if w.has_v:
-            if pool_head_major:
-                T["v_pool"] = torch.zeros((L, H, slots, D), dtype=torch.bfloat16, device=device).transpose(1, 2)
-            else:
-                T["v_pool"] = torch.zeros((L, slots, H, D), dtype=torch.bfloat16, device=device)
             v_out = T["v_pool"]
     else:
         rows = int(meta.row_base.max()) + n

@@ -98,6 +98,7 @@ class RehydrateCase:
     row_base: bool = True              # dense output: chunks at permuted row bases, else chunk c at rows c*n..
     in_place: bool = False             # dense output without row_base written over the input
     unit_major: bool = False           # input memory [C, L, H, n, D] (rows of one head contiguous)
+    kv_interleaved: bool = False       # K and V outputs in one tensor [L, rows, K|V, H, D]
     kernel: int = 0                    # kamera_kernel_choice requested (0: AUTO)
     plan: Optional[int] = None         # kernel kamera_rehydrate_plan must report for the case
     seed: int = 0
@@ -181,6 +182,10 @@ def run_rehydrate(case: RehydrateCase, device):
     if case.in_place:
         k_out = dev(chunk_rows(K), device)
         v_out = dev(chunk_rows(V), device) if case.has_v else None
+    elif case.kv_interleaved:
+        assert case.has_v
+        kv_out = dev(np.full((*out_shape[:2], 2, *out_shape[2:]), SENTINEL, np.uint16), device)
+        k_out, v_out = kv_out[:, :, 0], kv_out[:, :, 1]
     else:
         k_out = dev(np.full(out_shape, SENTINEL, np.uint16), device)
         v_out = dev(np.full(out_shape, SENTINEL, np.uint16), device) if case.has_v else None

@@ -231,6 +231,62 @@ def test_rehydrate_plan_picks_the_kernel(case, plan):
     assert km.lib().kamera_validate(0, ctypes.byref(a)) == min(plan, 0)
 
 
+def _interleaved_case(case):
+    """Both planes write one tensor [C][L][n][K|V][H][D] (dense) or a pool
+    [L][slot][K|V][H][D] (paged): H = 4, D = 128, so a row of one plane spans
+    512 elements and the row stride is 1024."""
+    a = rehydrate_args()
+    C, Ln, n, H, D = 2, 3, 64, 4, 128
+    base = FAKE + 20 * (1 << 34)
+    r, d = 2 * H * D, H * D
+    if case.startswith("paged"):
+        a.paged, a.page_size, a.n_pool_pages, a.pt_stride = 1, 16, 8, 4
+        a.page_table = FAKE + 0x400000000
+        st = [0, 8 * 16 * r, r, D]
+    else:
+        st = [Ln * n * r, n * r, r, D]
+    outs = [base, base + 2 * d]
+    if case == "dense_v_first":
+        outs = outs[::-1]
+    elif case == "dense_gap_short":
+        outs[1] = base + 2 * (d // 2)
+    elif case == "dense_gap_long":
+        outs[1] = base + 2 * (d + d // 2)
+    elif case == "dense_gap_odd_bytes":
+        outs[1] = base + 2 * d + 1
+    for p in range(2):
+        a.plane[p].out = outs[p]
+        for k in range(4):
+            a.plane[p].out_stride[k] = st[k]
+    if case == "dense_strides_differ":
+        a.plane[1].out_stride[2] = r + D
+    elif case == "dense_layer_stride_not_rows":
+        for p in range(2):
+            a.plane[p].out_stride[1] = n * r + d
+            a.plane[p].out_stride[0] = Ln * (n * r + d)
+    return a
+
+
+@pytest.mark.parametrize("case,code", [
+    ("dense", km.OK),
+    ("dense_v_first", km.OK),
+    ("paged", km.OK),
+    ("dense_gap_short", km.ERR_ALIAS),
+    ("dense_gap_long", km.ERR_ALIAS),
+    ("dense_gap_odd_bytes", km.ERR_ALIGN),
+    ("dense_strides_differ", km.ERR_ALIAS),
+    ("dense_layer_stride_not_rows", km.ERR_ALIAS),
+])
+def test_interleaved_plane_outputs(case, code):
+    """The K and V planes may write one tensor with their rows interleaved (the
+    rows of one plane in the gaps between the rows of the other); any other
+    overlap of the two outputs is rejected."""
+    a = _interleaved_case(case)
+    assert km.lib().kamera_validate(0, ctypes.byref(a)) == code, km.last_error()
+    if code == km.ERR_ALIAS:
+        assert "outputs overlap" in km.last_error()
+
+
 @pytest.mark.parametrize("case,code", [
     ("null_args", km.ERR_NULL),
     ("negative", km.ERR_SHAPE),

@@ -115,6 +115,14 @@ REHYDRATE_CASES = {
                                                              seed=70),
     "rows_reloc_in_place_no_patch": RehydrateCase(H=4, reloc=True, row_base=False, in_place=True, m_k=0, m_v=0,
                                                   kernel=2, plan=3, seed=71),
+    # K and V written into one tensor with their rows interleaved ([L, slot, K|V, H, D])
+    "rows4_kv_interleaved_pool": RehydrateCase(H=8, paged=True, m_k=64, m_v=64, sections=(16, 24, 24),
+                                               pos_mode="grid3", grid_w=32, n=100, kernel=3, plan=3, seed=72,
+                                               kv_interleaved=True),
+    "rows_kv_interleaved_dense": RehydrateCase(H=8, row_base=False, m_k=32, m_v=16, n=70, kernel=2, plan=2,
+                                               seed=73, kv_interleaved=True),
+    "per_head_kv_interleaved_row_base_ragged": RehydrateCase(H=4, ragged=True, C=3, n=130, m_k=16, m_v=8,
+                                                             kernel=1, plan=1, seed=74, kv_interleaved=True),
     "per_head_explicit_paged": RehydrateCase(H=8, pos_mode="explicit", paged=True, kernel=2, plan=1, seed=61),
     "per_head_rank_72_paged": RehydrateCase(H=8, m_k=72, m_v=8, paged=True, kernel=2, plan=1, seed=62),
     "per_head_9_heads_paged": RehydrateCase(H=9, paged=True, kernel=2, plan=1, seed=63),
