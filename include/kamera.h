@@ -200,7 +200,9 @@ typedef struct {
  * span <= |d| and |d| + span <= out_stride[2], span = (n_heads - 1) *
  * out_stride[3] + head_dim -- e.g. a pool [layer][slot][K|V][head][dim] in
  * which the K and V rows of a slot are adjacent, so that a page of both
- * planes is one contiguous run.
+ * planes is one contiguous run.  By the same rule a dense output may
+ * interleave with the other plane's input (one tensor [chunk][layer][token]
+ * [K|V][head][dim] rehydrated in place, each plane exactly in place).
  *
  * Relocation (delta != NULL, device int32 [n_chunks][3]): the input keys are
  * already rotated, at target - delta (survivors of a window slide, Sec. 5),

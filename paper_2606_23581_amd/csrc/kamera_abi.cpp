@@ -174,22 +174,22 @@ int pick_grid(int64_t n_tasks, int32_t& per_xcd, const char* who) {
 // kamera_rehydrate
 // ---------------------------------------------------------------------------
 
-// The two planes' outputs interleave by rows without sharing an element: the
-// same strides (none negative); every offset a plane writes to is a multiple of
-// the row stride r plus a position inside one row's span (all heads of the
-// row); the bases are d elements apart with span <= |d| <= r - span, so a row
-// of one plane lies in the gap between two rows of the other.
-static bool interleaved_rows(const kamera_rehydrate_args* a) {
-  const kamera_plane& q0 = a->plane[0];
-  const kamera_plane& q1 = a->plane[1];
-  if (memcmp(q0.out_stride, q1.out_stride, sizeof(q0.out_stride)) != 0) return false;
-  const int64_t* s = q0.out_stride;
+// Two row sets of one call, each at base + c*s[0] + l*s[1] + row*s[2] + h*s[3]
+// + [0, head_dim) (s[0] unused for a pool), interleave without sharing an
+// element: the same strides (none negative); every offset is a multiple of the
+// row stride r plus a position inside one row's span (all heads of the row);
+// the bases are d elements apart with span <= |d| <= r - span, so a row of one
+// set lies in the gap between two rows of the other.  This admits two planes
+// written into one tensor [.., row, K|V, head, dim], also in place.
+static bool interleaved_rows(const kamera_rehydrate_args* a, const void* b0, const int64_t* s0, const void* b1,
+                             const int64_t* s1, bool chunk_stride_used) {
+  if (memcmp(s0, s1, 4 * sizeof(int64_t)) != 0) return false;
   for (int k = 0; k < 4; ++k)
-    if (s[k] < 0) return false;
-  const int64_t r = s[2];
-  if (r <= 0 || s[1] % r != 0 || (!a->paged && s[0] % r != 0)) return false;
-  const int64_t span = (int64_t)(a->n_heads - 1) * s[3] + a->head_dim;
-  const uintptr_t p0 = (uintptr_t)q0.out, p1 = (uintptr_t)q1.out;
+    if (s0[k] < 0) return false;
+  const int64_t r = s0[2];
+  if (r <= 0 || s0[1] % r != 0 || (chunk_stride_used && s0[0] % r != 0)) return false;
+  const int64_t span = (int64_t)(a->n_heads - 1) * s0[3] + a->head_dim;
+  const uintptr_t p0 = (uintptr_t)b0, p1 = (uintptr_t)b1;
   const uintptr_t gap = p0 > p1 ? p0 - p1 : p1 - p0;
   if (gap % 2 != 0) return false;
   const int64_t d = (int64_t)(gap / 2);
@@ -300,6 +300,9 @@ static int build_rehydrate(const kamera_rehydrate_args* a, kamera::RehydratePara
         const int rb = r.col_begin, re = (r.col_begin == 0 && r.col_end == 0) ? a->head_dim : r.col_end;
         if (o == p || qe <= rb || re <= qb) continue;
       }
+      // the other plane's input may interleave with this output by rows (one
+      // tensor [.., row, K|V, head, dim] rehydrated in place)
+      if (o != p && !a->paged && interleaved_rows(a, r.out, r.out_stride, q.in, q.in_stride, true)) continue;
       if (overlap(ilo, ihi, olo, ohi))
         return fail(KAMERA_ERR_ALIAS, "%s: output of plane %d overlaps the input of plane %d", who, o, p);
     }
@@ -318,7 +321,8 @@ static int build_rehydrate(const kamera_rehydrate_args* a, kamera::RehydratePara
       const bool same_map = q0.out == q1.out && memcmp(q0.out_stride, q1.out_stride, sizeof(q0.out_stride)) == 0;
       const int b0 = q0.col_begin, e0 = (q0.col_begin == 0 && q0.col_end == 0) ? a->head_dim : q0.col_end;
       const int b1 = q1.col_begin, e1 = (q1.col_begin == 0 && q1.col_end == 0) ? a->head_dim : q1.col_end;
-      if ((!same_map || !(e0 <= b1 || e1 <= b0)) && !interleaved_rows(a))
+      if ((!same_map || !(e0 <= b1 || e1 <= b0)) &&
+          !interleaved_rows(a, q0.out, q0.out_stride, q1.out, q1.out_stride, !a->paged))
         return fail(KAMERA_ERR_ALIAS, "%s: the two planes' outputs overlap", who);
     }
   }

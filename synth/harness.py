@@ -82,6 +82,9 @@ def _u_rows(shape, std, gen, device, token_major: bool):
 def prepare(name: str, device="cuda", seed: Optional[int] = None, unit_major: bool = True,
             pool_head_major: bool = False, u_token_major: bool = False,
             separate_pools: bool = False) -> Prepared:
+    """Device tensors and the prepared call of one workload.  The paged pool
+    and the relocation window hold K and V interleaved by rows (one tensor
+    [.., slot or token, K|V, H, D]) unless ``separate_pools``."""
     import torch
 
     import paper_2606_23581_amd as km
@@ -123,10 +126,16 @@ def prepare(name: str, device="cuda", seed: Optional[int] = None, unit_major: bo
         # the window's K/V, chunk-major [slot][L][n][H][D]; survivors are slots
         # 1..15, rotated and moved in place (input = output)
         S = w.window_slots
-        T["k_window"] = randn_bf16_device((S, L, n, H, D), 1.0, gen, device)
+        if w.has_v and not separate_pools:
+            # one window [slot][L][n][K|V][H][D]: the K and V rows of a token adjacent
+            T["kv_window"] = randn_bf16_device((S, L, n, 2, H, D), 1.0, gen, device)
+            T["k_window"], T["v_window"] = T["kv_window"][:, :, :, 0], T["kv_window"][:, :, :, 1]
+        else:
+            T["k_window"] = randn_bf16_device((S, L, n, H, D), 1.0, gen, device)
+            if w.has_v:
+                T["v_window"] = randn_bf16_device((S, L, n, H, D), 1.0, gen, device)
         T["k_in"] = T["k_window"][1:1 + C]
         if w.has_v:
-            T["v_window"] = randn_bf16_device((S, L, n, H, D), 1.0, gen, device)
             T["v_in"] = T["v_window"][1:1 + C]
     else:
         T["k_in"] = _kv_rows((C, L, n, H, D), gen, device, unit_major)

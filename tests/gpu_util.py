@@ -179,7 +179,10 @@ def run_rehydrate(case: RehydrateCase, device):
             return dev(np.ascontiguousarray(X.transpose(0, 1, 3, 2, 4)), device).permute(0, 1, 3, 2, 4)
         return dev(X, device)
 
-    if case.in_place:
+    if case.in_place and case.kv_interleaved:
+        kv_out = dev(np.stack([chunk_rows(K), chunk_rows(V)], axis=2), device)
+        k_out, v_out = kv_out[:, :, 0], kv_out[:, :, 1]
+    elif case.in_place:
         k_out = dev(chunk_rows(K), device)
         v_out = dev(chunk_rows(V), device) if case.has_v else None
     elif case.kv_interleaved:

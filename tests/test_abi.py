@@ -258,6 +258,14 @@ def _interleaved_case(case):
         a.plane[p].out = outs[p]
         for k in range(4):
             a.plane[p].out_stride[k] = st[k]
+    if case.startswith("dense_in_place"):
+        # each plane exactly in place on one tensor [C][L][n][K|V][H][D]
+        if case == "dense_in_place_gap_short":
+            outs[1] = base + 2 * (d // 2)
+        for p in range(2):
+            a.plane[p].out = a.plane[p].in_ = outs[p]
+            for k in range(4):
+                a.plane[p].in_stride[k] = st[k]
     if case == "dense_strides_differ":
         a.plane[1].out_stride[2] = r + D
     elif case == "dense_layer_stride_not_rows":
@@ -276,15 +284,17 @@ def _interleaved_case(case):
     ("dense_gap_odd_bytes", km.ERR_ALIGN),
     ("dense_strides_differ", km.ERR_ALIAS),
     ("dense_layer_stride_not_rows", km.ERR_ALIAS),
+    ("dense_in_place", km.OK),
+    ("dense_in_place_gap_short", km.ERR_ALIAS),
 ])
 def test_interleaved_plane_outputs(case, code):
     """The K and V planes may write one tensor with their rows interleaved (the
-    rows of one plane in the gaps between the rows of the other); any other
-    overlap of the two outputs is rejected."""
+    rows of one plane in the gaps between the rows of the other), also each
+    plane in place on such a tensor; any other overlap is rejected."""
     a = _interleaved_case(case)
     assert km.lib().kamera_validate(0, ctypes.byref(a)) == code, km.last_error()
     if code == km.ERR_ALIAS:
-        assert "outputs overlap" in km.last_error()
+        assert "overlap" in km.last_error()
 
 
 @pytest.mark.parametrize("case,code", [

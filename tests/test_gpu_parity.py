@@ -123,6 +123,12 @@ REHYDRATE_CASES = {
                                                seed=73, kv_interleaved=True),
     "per_head_kv_interleaved_row_base_ragged": RehydrateCase(H=4, ragged=True, C=3, n=130, m_k=16, m_v=8,
                                                              kernel=1, plan=1, seed=74, kv_interleaved=True),
+    "rows4_reloc_kv_interleaved_in_place": RehydrateCase(H=8, reloc=True, row_base=False, in_place=True, m_k=64,
+                                                         m_v=64, n=70, sections=(24, 20, 20),
+                                                         section_order="interleaved", pos_mode="grid3",
+                                                         kernel=3, plan=3, seed=75, kv_interleaved=True),
+    "per_head_kv_interleaved_in_place": RehydrateCase(row_base=False, in_place=True, m_k=16, m_v=16, n=90,
+                                                      kernel=1, plan=1, seed=76, kv_interleaved=True),
     "per_head_explicit_paged": RehydrateCase(H=8, pos_mode="explicit", paged=True, kernel=2, plan=1, seed=61),
     "per_head_rank_72_paged": RehydrateCase(H=8, m_k=72, m_v=8, paged=True, kernel=2, plan=1, seed=62),
     "per_head_9_heads_paged": RehydrateCase(H=9, paged=True, kernel=2, plan=1, seed=63),
