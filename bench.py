@@ -380,6 +380,27 @@ def bench_copy(args, pool_workers, n_workers):
     print(json.dumps(line), flush=True)
 
 
+def _layout(p) -> dict:
+    """Memory order of the workload's tensors as the call sees them."""
+    T, w = p.tensors, p.workload
+    out = {}
+    if "kv_pool" in T:
+        out["pool"] = "[layer][slot][K|V][head][dim]"
+    elif "k_pool" in T:
+        out["pool"] = "[layer][slot][head][dim] per plane"
+    if "kv_window" in T:
+        out["window"] = "[slot][layer][token][K|V][head][dim], in place"
+    elif "window" in T or "k_window" in T:
+        out["window"] = "[slot][layer][token][head][dim], in place"
+    if "k_out_rows" in T:
+        out["out"] = "[layer][row][head][dim] per plane, chunk c from its row base"
+    if w.kind == "rehydrate" and "k_window" not in T and "kv_window" not in T:
+        k = T["k_in"]
+        out["kv_in"] = ("[chunk][layer][head][token][dim]" if k.stride(2) == k.shape[4]
+                        else "[chunk][layer][token][head][dim]")
+    return out
+
+
 def measured_traffic(name: str, kernel: str):
     """HBM traffic per launch from the committed rocprofv3 counter summary, if it
     was taken on this kernel as its sources stand (else null)."""
@@ -542,6 +563,7 @@ def main():
                    "rank_k": w.m_k, "rank_v": w.m_v, "rope": {"theta": w.theta, "dim": w.rope_dim,
                                                               "pairing": w.pairing, "sections": w.sections},
                    "paged": w.paged, "page_size": w.page_size if w.paged else None,
+                   "layout": _layout(p),
                    "algorithmic_bytes_per_step": p.bytes_per_step},
         "pct_hbm_peak": round(100.0 * value / HBM_PEAK_GBPS, 2),
         "chunks_per_s": round(w.n_chunks / (ms_per_step * 1e-3), 1),
