@@ -70,7 +70,7 @@ typedef enum {
   KAMERA_ERR_ALIGN = -3,       /* pointer or stride breaks 16-byte row alignment */
   KAMERA_ERR_RANGE = -4,       /* a size or rank beyond the supported maximum    */
   KAMERA_ERR_ALIAS = -5,       /* an output overlaps an input it must not        */
-  KAMERA_ERR_UNSUPPORTED = -6, /* a valid request this build does not implement  */
+  KAMERA_ERR_UNSUPPORTED = -6, /* a valid request this library does not implement */
   KAMERA_ERR_HIP = -7          /* the HIP runtime refused the launch             */
 } kamera_status;
 

@@ -26,7 +26,7 @@ def require_gpu():
         pytest.skip("no GPU")
     import paper_2606_23581_amd as km
 
-    km.lib()  # a missing library on a GPU machine is a failure, not a skip
+    km.lib()  # a missing library where a GPU is present is a failure, not a skip
     return torch.device("cuda:0")
 
 
