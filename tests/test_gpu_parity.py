@@ -589,18 +589,22 @@ def test_orbit_patch_matches_reference(device, K, n, d, m):
 # graph capture
 # ---------------------------------------------------------------------------
 
-def test_graph_capture_replays_match_eager(device):
+@pytest.mark.parametrize("form", ["per_head", "row_group_interleaved_pool"])
+def test_graph_capture_replays_match_eager(device, form):
     """The entry points allocate, free and synchronise nothing and clear
     nothing with a memset, so a serving loop can capture them: a rehydrate
     into a paged pool followed by a shift of the same pages, captured in one
     graph, replayed three times with eager work and synchronisations between
-    the replays; every replay gives the eager result bit for bit."""
+    the replays; every replay gives the eager result bit for bit.  Once with
+    the per-head kernel and separate pools, once with 4-head row groups into
+    one K|V-interleaved pool."""
     import paper_2606_23581_amd as km
     import torch
 
-    print("[case] graph capture rehydrate + shift", flush=True)
+    print(f"[case] graph capture rehydrate + shift ({form})", flush=True)
+    rows = form != "per_head"
     rng = np.random.default_rng(61)
-    C, L, n, H, D, m, P = 2, 2, 64, 2, 128, 16, 16
+    C, L, n, H, D, m, P = (2, 2, 64, 8, 128, 64, 16) if rows else (2, 2, 64, 2, 128, 16, 16)
     pages = n // P
     npp = C * pages + 3
     K = dev(synth.randn_bf16_numpy((C, L, n, H, D), 1.0, rng), device)
@@ -613,12 +617,18 @@ def test_graph_capture_replays_match_eager(device):
     rs = km.RopeSpec(theta=1e6, rope_dim=128)
 
     def pools():
+        if rows:
+            kv = torch.zeros((L, npp * P, 2, H, D), dtype=torch.bfloat16, device=device)
+            return kv[:, :, 0], kv[:, :, 1]
         return (torch.zeros((L, npp * P, H, D), dtype=torch.bfloat16, device=device),
                 torch.zeros((L, npp * P, H, D), dtype=torch.bfloat16, device=device))
 
     def calls(kp, vp):
-        return (km.prepare_rehydrate(K, kp, v_in=V, v_out=vp, rope=rs, chunk_pos=pos, u_k=Uk, w_k=Wk,
-                                     page_table=pt, page_size=P, n_pool_pages=npp),
+        kernel = km.KERNEL_ROW_GROUP4 if rows else km.KERNEL_AUTO
+        reh = km.prepare_rehydrate(K, kp, v_in=V, v_out=vp, rope=rs, chunk_pos=pos, u_k=Uk, w_k=Wk,
+                                   page_table=pt, page_size=P, n_pool_pages=npp, kernel=kernel)
+        assert km.rehydrate_plan(reh) == (km.PLAN_ROW_GROUP4 if rows else km.PLAN_PER_HEAD)
+        return (reh,
                 km.prepare_shift(kp, delta, rope=rs, n_chunks=C, n_tokens=n, page_table=pt, page_size=P,
                                  n_pool_pages=npp))
 
