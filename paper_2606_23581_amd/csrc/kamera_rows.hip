@@ -441,7 +441,11 @@ __global__ __launch_bounds__(64 * HW, 8 / HW) void rehydrate_rows_kernel(const R
   __shared__ double s_freq[kMaxPairs];
   __shared__ int s_coord[kMaxPairs];
 
-  const int64_t task = xcd_task(P.per_xcd);
+  // Consecutive workgroups go to consecutive XCDs, and here consecutive tasks
+  // too: no two tasks share data that an XCD's L2 could keep, so the eight
+  // XCDs work side by side on neighbouring rows instead of on eight distant
+  // ranges (0.5-5% faster on the paged recalls than XCD-contiguous ranges).
+  const int64_t task = blockIdx.x;
   if (task >= P.n_tasks) return;
   // the planes (K, V) and head groups of one (chunk, layer, token block) are
   // adjacent tasks
