@@ -240,12 +240,15 @@ def randn_bf16_numpy(shape, std: float, rng: np.random.Generator) -> np.ndarray:
     return torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
 
 
-def randn_bf16_device(shape, std: float, gen, device, slab_dim: int = 0):
+def randn_bf16_device(shape, std: float, gen, device, slab_dim: int = 0, out=None):
     """N(0, std^2) bf16 tensor drawn on the device in slabs along ``slab_dim``
-    (keeps the fp32 temporary small for tens-of-GB tensors)."""
+    (keeps the fp32 temporary small for tens-of-GB tensors); fills ``out``
+    (shape ``shape``) when given."""
     import torch
 
-    out = torch.empty(shape, dtype=torch.bfloat16, device=device)
+    if out is None:
+        out = torch.empty(shape, dtype=torch.bfloat16, device=device)
+    assert tuple(out.shape) == tuple(shape)
     if len(shape) == 0 or shape[slab_dim] == 0:
         return out
     for k in range(shape[slab_dim]):

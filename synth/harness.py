@@ -59,32 +59,93 @@ def _rope_spec(w: Workload):
                        section_order=w.section_order)
 
 
-def _kv_rows(shape, gen, device, unit_major: bool):
+class _Arena:
+    """The large tensors of one workload carved from one device allocation,
+    each at a 2 MiB boundary, as a serving engine reserves one region for its
+    KV store (``nbytes`` = 0: every tensor allocated on its own)."""
+
+    ALIGN = 2 << 20
+
+    def __init__(self, nbytes: int, device):
+        import torch
+
+        self.device = device
+        self.off = 0
+        self.buf = torch.empty(nbytes, dtype=torch.uint8, device=device) if nbytes > 0 else None
+
+    def empty(self, shape):
+        import torch
+
+        if self.buf is None:
+            return torch.empty(shape, dtype=torch.bfloat16, device=self.device)
+        nb = 2 * int(np.prod(shape))
+        at = -(-self.off // self.ALIGN) * self.ALIGN
+        if at + nb > self.buf.numel():
+            raise RuntimeError("workload arena too small")
+        self.off = at + nb
+        return self.buf[at:at + nb].view(torch.bfloat16).view(shape)
+
+    def zeros(self, shape):
+        t = self.empty(shape)
+        t.zero_()
+        return t
+
+    def randn(self, shape, std, gen, slab_dim: int = 0):
+        return randn_bf16_device(shape, std, gen, self.device, slab_dim=slab_dim, out=self.empty(shape))
+
+
+def _arena_bytes(w: Workload, meta) -> int:
+    """Upper bound of the arena of one workload: its inputs, factors and outputs
+    (bf16), each rounded up to the alignment, plus one alignment each."""
+    C, L, H, n, D = w.n_chunks, w.n_layers, w.n_heads, w.n_tokens, w.head_dim
+    planes = 2 if (w.kind == "rehydrate" and w.has_v) else 1
+    sizes = []
+    if w.kind == "shift":
+        sizes.append(L * w.window_slots * n * H * D)
+    else:
+        if w.reloc:
+            sizes += [w.window_slots * L * n * H * D] * planes
+        else:
+            sizes += [C * L * n * H * D] * planes
+        for m in ((w.m_k, w.m_v) if w.has_v else (w.m_k,)):
+            if m > 0:
+                sizes += [C * L * H * n * m, C * L * H * m * w.patch_dim]
+        if w.m_pe > 0:
+            sizes += [C * L * H * n * w.m_pe, C * L * H * w.m_pe * w.rope_dim]
+        if not w.reloc:
+            rows = w.n_pool_pages * w.page_size if w.paged else int(meta.row_base.max()) + n
+            sizes += [L * rows * H * D] * planes
+    A = _Arena.ALIGN
+    return sum(-(-2 * s // A) * A + A for s in sizes)
+
+
+def _kv_rows(shape, gen, arena: _Arena, unit_major: bool):
     """K/V of one workload, [C, L, n, H, D] as the operator sees it.  With
     ``unit_major`` the memory is [C, L, H, n, D]: every (chunk, layer, head)
     unit is one contiguous run of rows."""
     C, L, n, H, D = shape
     if unit_major:
-        return randn_bf16_device((C, L, H, n, D), 1.0, gen, device).permute(0, 1, 3, 2, 4)
-    return randn_bf16_device(shape, 1.0, gen, device)
+        return arena.randn((C, L, H, n, D), 1.0, gen).permute(0, 1, 3, 2, 4)
+    return arena.randn(shape, 1.0, gen)
 
 
-def _u_rows(shape, std, gen, device, token_major: bool):
+def _u_rows(shape, std, gen, arena: _Arena, token_major: bool):
     """Patch factors U of one workload, [C, L, H, n, m] as the operator sees
     it.  With ``token_major`` the memory is [C, L, n, H, m]: the factors of
     every head of a token row are adjacent, like the rows themselves."""
     C, L, H, n, m = shape
     if token_major:
-        return randn_bf16_device((C, L, n, H, m), std, gen, device).permute(0, 1, 3, 2, 4)
-    return randn_bf16_device(shape, std, gen, device)
+        return arena.randn((C, L, n, H, m), std, gen).permute(0, 1, 3, 2, 4)
+    return arena.randn(shape, std, gen)
 
 
 def prepare(name: str, device="cuda", seed: Optional[int] = None, unit_major: bool = True,
             pool_head_major: bool = False, u_token_major: bool = False,
-            separate_pools: bool = False) -> Prepared:
+            separate_pools: bool = False, arena: bool = True) -> Prepared:
     """Device tensors and the prepared call of one workload.  The paged pool
     and the relocation window hold K and V interleaved by rows (one tensor
-    [.., slot or token, K|V, H, D]) unless ``separate_pools``."""
+    [.., slot or token, K|V, H, D]) unless ``separate_pools``; the inputs,
+    factors and outputs are carved from one allocation unless not ``arena``."""
     import torch
 
     import paper_2606_23581_amd as km
@@ -96,11 +157,12 @@ def prepare(name: str, device="cuda", seed: Optional[int] = None, unit_major: bo
     C, L, H, n, D = w.n_chunks, w.n_layers, w.n_heads, w.n_tokens, w.head_dim
     rope = _rope_spec(w)
     T: Dict[str, object] = {}
+    A = _Arena(_arena_bytes(w, meta) if arena else 0, device)
 
     if w.kind == "shift":
         # ring window of S chunk slots [L, S*n, H, D], already rotated keys
         S = w.window_slots
-        T["window"] = randn_bf16_device((L, S * n, H, D), 1.0, gen, device, slab_dim=0)
+        T["window"] = A.randn((L, S * n, H, D), 1.0, gen, slab_dim=0)
         T["delta"] = torch.from_numpy(meta.delta).to(device)
         state = {"slide": 0}
         T["row_base"] = torch.zeros(C, dtype=torch.int32, device=device)
@@ -120,6 +182,7 @@ def prepare(name: str, device="cuda", seed: Optional[int] = None, unit_major: bo
         p = Prepared(w, T, meta, step, algorithmic_bytes(w), C)
         p.extra["set_slide"] = set_slide
         p.extra["call"] = call
+        p.extra["arena"] = A.buf
         return p
 
     if w.reloc:
@@ -128,28 +191,28 @@ def prepare(name: str, device="cuda", seed: Optional[int] = None, unit_major: bo
         S = w.window_slots
         if w.has_v and not separate_pools:
             # one window [slot][L][n][K|V][H][D]: the K and V rows of a token adjacent
-            T["kv_window"] = randn_bf16_device((S, L, n, 2, H, D), 1.0, gen, device)
+            T["kv_window"] = A.randn((S, L, n, 2, H, D), 1.0, gen)
             T["k_window"], T["v_window"] = T["kv_window"][:, :, :, 0], T["kv_window"][:, :, :, 1]
         else:
-            T["k_window"] = randn_bf16_device((S, L, n, H, D), 1.0, gen, device)
+            T["k_window"] = A.randn((S, L, n, H, D), 1.0, gen)
             if w.has_v:
-                T["v_window"] = randn_bf16_device((S, L, n, H, D), 1.0, gen, device)
+                T["v_window"] = A.randn((S, L, n, H, D), 1.0, gen)
         T["k_in"] = T["k_window"][1:1 + C]
         if w.has_v:
             T["v_in"] = T["v_window"][1:1 + C]
     else:
-        T["k_in"] = _kv_rows((C, L, n, H, D), gen, device, unit_major)
+        T["k_in"] = _kv_rows((C, L, n, H, D), gen, A, unit_major)
         if w.has_v:
-            T["v_in"] = _kv_rows((C, L, n, H, D), gen, device, unit_major)
+            T["v_in"] = _kv_rows((C, L, n, H, D), gen, A, unit_major)
     if w.m_k > 0:
-        T["u_k"] = _u_rows((C, L, H, n, w.m_k), w.u_std, gen, device, u_token_major)
-        T["w_k"] = randn_bf16_device((C, L, H, w.m_k, w.patch_dim), w.w_std, gen, device)
+        T["u_k"] = _u_rows((C, L, H, n, w.m_k), w.u_std, gen, A, u_token_major)
+        T["w_k"] = A.randn((C, L, H, w.m_k, w.patch_dim), w.w_std, gen)
     if w.has_v and w.m_v > 0:
-        T["u_v"] = _u_rows((C, L, H, n, w.m_v), w.u_std, gen, device, u_token_major)
-        T["w_v"] = randn_bf16_device((C, L, H, w.m_v, w.patch_dim), w.w_std, gen, device)
+        T["u_v"] = _u_rows((C, L, H, n, w.m_v), w.u_std, gen, A, u_token_major)
+        T["w_v"] = A.randn((C, L, H, w.m_v, w.patch_dim), w.w_std, gen)
     if w.m_pe > 0:
-        T["u_pe"] = randn_bf16_device((C, L, H, n, w.m_pe), w.u_std, gen, device)
-        T["w_pe"] = randn_bf16_device((C, L, H, w.m_pe, w.rope_dim), w.w_std, gen, device)
+        T["u_pe"] = A.randn((C, L, H, n, w.m_pe), w.u_std, gen)
+        T["w_pe"] = A.randn((C, L, H, w.m_pe, w.rope_dim), w.w_std, gen)
     T["chunk_pos"] = torch.from_numpy(meta.pos).to(device)
     kw = dict(rope=rope, chunk_pos=T["chunk_pos"], u_k=T.get("u_k"), w_k=T.get("w_k"),
               k_patch=(w.patch_offset, w.patch_dim),
@@ -173,16 +236,16 @@ def prepare(name: str, device="cuda", seed: Optional[int] = None, unit_major: bo
         if w.has_v and not pool_head_major and not separate_pools:
             # one pool [L, slots, K|V, H, D]: the K and V rows of a slot are
             # adjacent, so a 16-token page of both planes is one 64 KiB run
-            T["kv_pool"] = torch.zeros((L, slots, 2, H, D), dtype=torch.bfloat16, device=device)
+            T["kv_pool"] = A.zeros((L, slots, 2, H, D))
             T["k_pool"], T["v_pool"] = T["kv_pool"][:, :, 0], T["kv_pool"][:, :, 1]
         elif pool_head_major:   # [L, H, slots, D] memory, [L, slots, H, D] view
-            T["k_pool"] = torch.zeros((L, H, slots, D), dtype=torch.bfloat16, device=device).transpose(1, 2)
+            T["k_pool"] = A.zeros((L, H, slots, D)).transpose(1, 2)
             if w.has_v:
-                T["v_pool"] = torch.zeros((L, H, slots, D), dtype=torch.bfloat16, device=device).transpose(1, 2)
+                T["v_pool"] = A.zeros((L, H, slots, D)).transpose(1, 2)
         else:
-            T["k_pool"] = torch.zeros((L, slots, H, D), dtype=torch.bfloat16, device=device)
+            T["k_pool"] = A.zeros((L, slots, H, D))
             if w.has_v:
-                T["v_pool"] = torch.zeros((L, slots, H, D), dtype=torch.bfloat16, device=device)
+                T["v_pool"] = A.zeros((L, slots, H, D))
         T["page_table"] = torch.from_numpy(meta.page_table).to(device)
         kw.update(page_table=T["page_table"], page_size=w.page_size, n_pool_pages=w.n_pool_pages)
         k_out = T["k_pool"]
@@ -190,12 +253,12 @@ def prepare(name: str, device="cuda", seed: Optional[int] = None, unit_major: bo
             v_out = T["v_pool"]
     else:
         rows = int(meta.row_base.max()) + n
-        T["k_out_rows"] = torch.zeros((L, rows, H, D), dtype=torch.bfloat16, device=device)
+        T["k_out_rows"] = A.zeros((L, rows, H, D))
         k_out = T["k_out_rows"].unsqueeze(0).expand(C, L, rows, H, D)
         T["row_base"] = torch.from_numpy(meta.row_base).to(device)
         kw["row_base"] = T["row_base"]
         if w.has_v:
-            T["v_out_rows"] = torch.zeros((L, rows, H, D), dtype=torch.bfloat16, device=device)
+            T["v_out_rows"] = A.zeros((L, rows, H, D))
             v_out = T["v_out_rows"].unsqueeze(0).expand(C, L, rows, H, D)
     if w.has_v:
         kw.update(v_in=T["v_in"], v_out=v_out, u_v=T.get("u_v"), w_v=T.get("w_v"),
@@ -207,6 +270,7 @@ def prepare(name: str, device="cuda", seed: Optional[int] = None, unit_major: bo
 
     p = Prepared(w, T, meta, step, algorithmic_bytes(w), C)
     p.extra["call"] = call
+    p.extra["arena"] = A.buf
     return p
 
 
