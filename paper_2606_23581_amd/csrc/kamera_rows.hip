@@ -200,28 +200,82 @@ __device__ __forceinline__ void rg_rotate(f32x4 (&acc)[8], int g, const double* 
   }
 }
 
+// relocation: acc += R(delta) K for the head row at krow, with the chunk's
+// (cos, sin) of delta per pair from s_dcs (R(delta) is the same for every
+// token of the chunk); the element-to-pair layout is that of rg_rotate
+template <int ROT>
+__device__ __forceinline__ void rg_add_turned(f32x4 (&acc)[8], int g, const uint8_t* krow, const float* s_dcs) {
+  u32x4 kc[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) kc[q] = *reinterpret_cast<const u32x4*>(krow + 16 * (g + 4 * q));
+  auto kv = [&](int mt, int k) -> float {
+    const u32x4& w = kc[mt >> 1];
+    const uint32_t u = (mt & 1) ? (k < 2 ? w.z : w.w) : (k < 2 ? w.x : w.y);
+    return (k & 1) ? bf_hi(u) : bf_lo(u);
+  };
+  int jb = 8 * g;
+  asm volatile("" : "+v"(jb));
+  if constexpr (ROT == 0) {
+#pragma unroll
+    for (int mt = 0; mt < 8; ++mt)
+#pragma unroll
+      for (int k = 0; k < 4; ++k) acc[mt][k] += kv(mt, k);
+  } else if constexpr (ROT == 1) {
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int j = jb + 32 * q + e;
+        const float cs = s_dcs[2 * j], sn = s_dcs[2 * j + 1];
+        const int ax = 2 * q + (e >> 2), ay = 2 * (q + 2) + (e >> 2), k = e & 3;
+        const float x = kv(ax, k), y = kv(ay, k);
+        acc[ax][k] += x * cs - y * sn;
+        acc[ay][k] += x * sn + y * cs;
+      }
+    }
+  } else {
+#pragma unroll
+    for (int mt = 0; mt < 8; ++mt) {
+#pragma unroll
+      for (int k = 0; k < 4; k += 2) {
+        const int j = (jb >> 1) + 16 * (mt >> 1) + 2 * (mt & 1) + (k >> 1);
+        const float cs = s_dcs[2 * j], sn = s_dcs[2 * j + 1];
+        const float x = kv(mt, k), y = kv(mt, k + 1);
+        acc[mt][k] += x * cs - y * sn;
+        acc[mt][k + 1] += x * sn + y * cs;
+      }
+    }
+  }
+}
+
 // one wave: head h of the tile in LDS, result written back in place
 template <int MS, int ROT, int HW, bool RELOC>
 __device__ __forceinline__ void rg_compute(const RehydrateParams& P, const RgTask& T, int i0, int h,
                                            const u32x4 (&wa)[8][MS > 0 ? MS : 1], uint8_t* buf,
-                                           const double* s_freq, const int* s_coord) {
+                                           const double* s_freq, const int* s_coord, const float* s_dcs) {
   const int lane = threadIdx.x & 63;
   const int g = lane >> 4, t = lane & 15;
   uint8_t* krow = buf + (h * kTileTokens + t) * kRgKRow;
-  u32x4 kc[4];
-#pragma unroll
-  for (int q = 0; q < 4; ++q) kc[q] = *reinterpret_cast<const u32x4*>(krow + 16 * (g + 4 * q));
   f32x4 acc[8];
+  if constexpr (RELOC) {
+    // the patch accumulates alone; the keys are added, turned, at the end
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    acc[2 * q][0] = bf_lo(kc[q].x);
-    acc[2 * q][1] = bf_hi(kc[q].x);
-    acc[2 * q][2] = bf_lo(kc[q].y);
-    acc[2 * q][3] = bf_hi(kc[q].y);
-    acc[2 * q + 1][0] = bf_lo(kc[q].z);
-    acc[2 * q + 1][1] = bf_hi(kc[q].z);
-    acc[2 * q + 1][2] = bf_lo(kc[q].w);
-    acc[2 * q + 1][3] = bf_hi(kc[q].w);
+    for (int mt = 0; mt < 8; ++mt) acc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  } else {
+    u32x4 kc[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) kc[q] = *reinterpret_cast<const u32x4*>(krow + 16 * (g + 4 * q));
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      acc[2 * q][0] = bf_lo(kc[q].x);
+      acc[2 * q][1] = bf_hi(kc[q].x);
+      acc[2 * q][2] = bf_lo(kc[q].y);
+      acc[2 * q][3] = bf_hi(kc[q].y);
+      acc[2 * q + 1][0] = bf_lo(kc[q].z);
+      acc[2 * q + 1][1] = bf_hi(kc[q].z);
+      acc[2 * q + 1][2] = bf_lo(kc[q].w);
+      acc[2 * q + 1][3] = bf_hi(kc[q].w);
+    }
   }
   const int i = i0 + t;
   double pt = 0.0, ph = 0.0, pw = 0.0;
@@ -233,17 +287,9 @@ __device__ __forceinline__ void rg_compute(const RehydrateParams& P, const RgTas
       ph = T.cp1 + (double)(i / P.grid_w);
       pw = T.cp2 + (double)(i % P.grid_w);
     }
-    // rotation before the patch, as in the per-head kernel:
-    //   post-rope frame:          R(p) K           (+ U W after)
-    //   relocation, post-rope:    R(delta) K       (+ U W after)
-    //   relocation, pre-rope:     R(delta - p) K, the stored frame (+ U W, then R(p))
-    if constexpr (RELOC) {
-      if (P.patch_post_rope)
-        rg_rotate<ROT>(acc, g, s_freq, s_coord, T.dt, T.dh, T.dw);
-      else
-        rg_rotate<ROT>(acc, g, s_freq, s_coord, T.dt - pt, T.dh - ph, T.dw - pw);
-    } else if (P.patch_post_rope) {
-      rg_rotate<ROT>(acc, g, s_freq, s_coord, pt, ph, pw);
+    // post-rope frame: R(p) K before the patch (+ U W after)
+    if constexpr (!RELOC) {
+      if (P.patch_post_rope) rg_rotate<ROT>(acc, g, s_freq, s_coord, pt, ph, pw);
     }
   }
   if constexpr (MS > 0) {
@@ -258,7 +304,16 @@ __device__ __forceinline__ void rg_compute(const RehydrateParams& P, const RgTas
       }
     }
   }
-  if constexpr (ROT != 0) {
+  if constexpr (RELOC) {
+    // relocation of keys already turned to p - delta (Sec. 5):
+    //   stored frame:    R(p) (R(delta - p) K + U W) = R(delta) K + R(p) U W
+    //   post-rope frame: R(delta) K + U W
+    // so the only per-token angles are those of the patch term
+    if constexpr (ROT != 0) {
+      if (!P.patch_post_rope && MS > 0 && T.m_steps > 0) rg_rotate<ROT>(acc, g, s_freq, s_coord, pt, ph, pw);
+    }
+    rg_add_turned<ROT>(acc, g, krow, s_dcs);
+  } else if constexpr (ROT != 0) {
     if (!P.patch_post_rope) rg_rotate<ROT>(acc, g, s_freq, s_coord, pt, ph, pw);
   }
 #pragma unroll
@@ -340,7 +395,7 @@ __device__ __forceinline__ void rg_put_w(int hq, int k0, int colb, const uint32_
 
 template <int MS, int ROT, int HW, bool RELOC>
 __device__ __forceinline__ void rg_run(const RehydrateParams& P, const RgTask& T, int t_begin, int t_end,
-                                       uint8_t* lds, const double* s_freq, const int* s_coord) {
+                                       uint8_t* lds, const double* s_freq, const int* s_coord, const float* s_dcs) {
   constexpr int NT = 64 * HW;
   constexpr int kIpt = 1024 / NT;               // W staging items per thread and round of 4 heads
   const int tid = threadIdx.x;
@@ -422,7 +477,7 @@ __device__ __forceinline__ void rg_run(const RehydrateParams& P, const RgTask& T
     rg_to_lds<MS, HW>(T, R, buf);
     if (tt + kRgDepth < n_tiles) rg_load<MS, HW>(T, i0 + kRgDepth * kTileTokens, R);
     __syncthreads();
-    if (active) rg_compute<MS, ROT, HW, RELOC>(P, T, i0, h, wa, buf, s_freq, s_coord);
+    if (active) rg_compute<MS, ROT, HW, RELOC>(P, T, i0, h, wa, buf, s_freq, s_coord, s_dcs);
     __syncthreads();
     rg_store<HW>(P, T, t_begin, i0, buf, s_page);
   };
@@ -440,6 +495,7 @@ __global__ __launch_bounds__(64 * HW, 8 / HW) void rehydrate_rows_kernel(const R
   extern __shared__ __align__(16) uint8_t lds_dyn[];
   __shared__ double s_freq[kMaxPairs];
   __shared__ int s_coord[kMaxPairs];
+  __shared__ float s_dcs[2 * kMaxPairs];        // relocation: cos, sin of delta per pair
 
   // Consecutive workgroups go to consecutive XCDs, and here consecutive tasks
   // too: no two tasks share data that an XCD's L2 could keep, so the eight
@@ -511,12 +567,19 @@ __global__ __launch_bounds__(64 * HW, 8 / HW) void rehydrate_rows_kernel(const R
     for (int j = threadIdx.x; j < half; j += 64 * HW) {
       s_freq[j] = P.rope.rev_freq[j];
       s_coord[j] = P.rope.coord[j];
+      if constexpr (RELOC) {
+        const int sc = P.rope.coord[j];
+        float sn, cs;
+        sincos_rev(sc == 0 ? T.dt : (sc == 1 ? T.dh : T.dw), P.rope.rev_freq[j], sn, cs);
+        s_dcs[2 * j] = cs;
+        s_dcs[2 * j + 1] = sn;
+      }
     }
   }
   switch (rot) {
-    case 0: rg_run<MS, 0, HW, RELOC>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
-    case 1: rg_run<MS, 1, HW, RELOC>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
-    default: rg_run<MS, 2, HW, RELOC>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
+    case 0: rg_run<MS, 0, HW, RELOC>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord, s_dcs); break;
+    case 1: rg_run<MS, 1, HW, RELOC>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord, s_dcs); break;
+    default: rg_run<MS, 2, HW, RELOC>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord, s_dcs); break;
   }
 }
 

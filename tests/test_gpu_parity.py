@@ -129,6 +129,14 @@ REHYDRATE_CASES = {
                                                          kernel=3, plan=3, seed=75, kv_interleaved=True),
     "per_head_kv_interleaved_in_place": RehydrateCase(row_base=False, in_place=True, m_k=16, m_v=16, n=90,
                                                       kernel=1, plan=1, seed=76, kv_interleaved=True),
+    # relocation with interleaved pairing, and with a layer of rank 0 (the patch
+    # term, and with it the per-token rotation, is absent there)
+    "rows4_reloc_interleaved_pairing": RehydrateCase(H=8, reloc=True, pairing="interleaved", theta=1e4,
+                                                     m_k=16, m_v=16, n=50, paged=True, kernel=3, plan=3,
+                                                     seed=77, kv_interleaved=True),
+    "rows4_reloc_layer_rank_0_64": RehydrateCase(H=4, reloc=True, L=2, layer_rank=(0, 64), m_k=64, m_v=64,
+                                                 sections=(16, 24, 24), pos_mode="grid3", n=40, kernel=3,
+                                                 plan=3, seed=78),
     "per_head_explicit_paged": RehydrateCase(H=8, pos_mode="explicit", paged=True, kernel=2, plan=1, seed=61),
     "per_head_rank_72_paged": RehydrateCase(H=8, m_k=72, m_v=8, paged=True, kernel=2, plan=1, seed=62),
     "per_head_9_heads_paged": RehydrateCase(H=9, paged=True, kernel=2, plan=1, seed=63),
