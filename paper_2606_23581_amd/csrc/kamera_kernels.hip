@@ -110,6 +110,51 @@ __device__ __forceinline__ void rotate_tile(f32x4 (&acc)[2 * NQ], int g, const d
   }
 }
 
+// relocation: acc += R(delta) K for the lane's K chunks kc, with the chunk's
+// (cos, sin) of delta per pair from s_dcs; the element-to-pair layout is that
+// of rotate_tile (no rotation where rotate_tile rotates nothing)
+template <int NQ, int ROT>
+__device__ __forceinline__ void add_turned_tile(f32x4 (&acc)[2 * NQ], int g, const u32x4 (&kc)[NQ],
+                                                const float* s_dcs) {
+  auto kv = [&](int mt, int k) -> float {
+    const u32x4& w = kc[mt >> 1];
+    const uint32_t u = (mt & 1) ? (k < 2 ? w.z : w.w) : (k < 2 ? w.x : w.y);
+    return (k & 1) ? bf_hi(u) : bf_lo(u);
+  };
+  if constexpr (ROT == 1 && NQ % 2 == 0) {
+#pragma unroll
+    for (int q = 0; q < NQ / 2; ++q) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int j = 8 * g + 32 * q + e;
+        const float cs = s_dcs[2 * j], sn = s_dcs[2 * j + 1];
+        const int ax = 2 * q + (e >> 2), ay = 2 * (q + NQ / 2) + (e >> 2), k = e & 3;
+        const float x = kv(ax, k), y = kv(ay, k);
+        acc[ax][k] += x * cs - y * sn;
+        acc[ay][k] += x * sn + y * cs;
+      }
+    }
+  } else if constexpr (ROT == 2) {
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+#pragma unroll
+      for (int e = 0; e < 8; e += 2) {
+        const int j = 4 * g + 16 * q + (e >> 1);
+        const float cs = s_dcs[2 * j], sn = s_dcs[2 * j + 1];
+        const int a = 2 * q + (e >> 2), k = e & 3;
+        const float x = kv(a, k), y = kv(a, k + 1);
+        acc[a][k] += x * cs - y * sn;
+        acc[a][k + 1] += x * sn + y * cs;
+      }
+    }
+  } else {
+#pragma unroll
+    for (int mt = 0; mt < 2 * NQ; ++mt)
+#pragma unroll
+      for (int k = 0; k < 4; ++k) acc[mt][k] += kv(mt, k);
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Tile I/O.  Global memory is accessed row-contiguously: one load or store
 // instruction of a wave covers 64 consecutive 16-byte chunks, i.e. whole
@@ -201,7 +246,11 @@ template <int NQ, int MS, int ROT, bool RELOC>
 __device__ __forceinline__ void tile_compute(const RehydrateParams& P, const TileCtx& T, int i0,
                                              const TileRegs<NQ, MS>& R, const uint16_t* __restrict__ Wt,
                                              uint8_t* tile_lds, const double* s_freq,
-                                             const int* s_coord) {
+                                             const int* s_coord, const float* s_dcs) {
+  // relocation up to rank 64 as R(delta) K + R(p) U W (one set of per-token
+  // angles, K kept in registers across the patch); at rank 128, where those
+  // registers would spill, as R(p) (R(delta - p) K + U W)
+  constexpr bool kOneAngle = RELOC && MS <= 2;
   const PlaneParams& Q = *T.Q;
   const int lane = threadIdx.x & 63;
   const int g = lane >> 4;
@@ -239,6 +288,10 @@ __device__ __forceinline__ void tile_compute(const RehydrateParams& P, const Til
   }
 
   f32x4 acc[2 * NQ];
+  if constexpr (kOneAngle) {
+#pragma unroll
+    for (int mt = 0; mt < 2 * NQ; ++mt) acc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  } else {
 #pragma unroll
   for (int q = 0; q < NQ; ++q) {
     acc[2 * q][0] = bf_lo(kc[q].x);
@@ -249,6 +302,7 @@ __device__ __forceinline__ void tile_compute(const RehydrateParams& P, const Til
     acc[2 * q + 1][1] = bf_hi(kc[q].z);
     acc[2 * q + 1][2] = bf_lo(kc[q].w);
     acc[2 * q + 1][3] = bf_hi(kc[q].w);
+  }
   }
 
   const int i = i0 + t;
@@ -261,14 +315,14 @@ __device__ __forceinline__ void tile_compute(const RehydrateParams& P, const Til
     //   relocation, post-rope:      R(delta) K      (+ U W after)
     //   relocation, pre-rope:       R(-(p - delta)) K, the stored frame
     //                               (+ U W, then R(p) below)
-    if constexpr (RELOC) {
+    if constexpr (RELOC && !kOneAngle) {
       const double dt = (double)P.delta[3 * T.c], dh = (double)P.delta[3 * T.c + 1],
                    dw = (double)P.delta[3 * T.c + 2];
       if (P.patch_post_rope)
         rotate_tile<NQ, ROT>(acc, g, s_freq, s_coord, dt, dh, dw);
       else
         rotate_tile<NQ, ROT>(acc, g, s_freq, s_coord, dt - pt, dh - ph, dw - pw);
-    } else if (P.patch_post_rope) {
+    } else if (!RELOC && P.patch_post_rope) {
       rotate_tile<NQ, ROT>(acc, g, s_freq, s_coord, pt, ph, pw);
     }
   }
@@ -294,7 +348,12 @@ __device__ __forceinline__ void tile_compute(const RehydrateParams& P, const Til
     }
   }
 
-  if constexpr (ROT != 0) {
+  if constexpr (kOneAngle) {
+    if constexpr (ROT != 0) {
+      if (!P.patch_post_rope && MS > 0 && T.patched) rotate_tile<NQ, ROT>(acc, g, s_freq, s_coord, pt, ph, pw);
+    }
+    add_turned_tile<NQ, ROT>(acc, g, kc, s_dcs);
+  } else if constexpr (ROT != 0) {
     if (!P.patch_post_rope) rotate_tile<NQ, ROT>(acc, g, s_freq, s_coord, pt, ph, pw);
   }
 
@@ -392,7 +451,7 @@ __device__ __forceinline__ void stage_w(const TileCtx& T, uint16_t* Wt) {
 
 template <int NQ, int MS, int ROT, bool RELOC>
 __device__ __forceinline__ void rehydrate_block(const RehydrateParams& P, const TileCtx& T, int t_begin, int t_end,
-                                                uint8_t* lds, double* s_freq, int* s_coord) {
+                                                uint8_t* lds, double* s_freq, int* s_coord, float* s_dcs) {
   uint16_t* Wt = reinterpret_cast<uint16_t*>(lds);
   const int wave = threadIdx.x >> 6;
   uint8_t* tile_lds = lds + 128 * (32 * MS + 8) * 2 + wave * tile_lds_bytes();
@@ -412,12 +471,19 @@ __device__ __forceinline__ void rehydrate_block(const RehydrateParams& P, const 
     for (int j = threadIdx.x; j < half; j += kThreads) {
       s_freq[j] = P.rope.rev_freq[j];
       s_coord[j] = P.rope.coord[j];
+      if constexpr (RELOC && MS <= 2) {
+        const int sc = P.rope.coord[j];
+        float sn, cs;
+        sincos_rev((double)P.delta[3 * T.c + (sc == 0 ? 0 : (sc == 1 ? 1 : 2))], P.rope.rev_freq[j], sn, cs);
+        s_dcs[2 * j] = cs;
+        s_dcs[2 * j + 1] = sn;
+      }
     }
   }
   __syncthreads();
   for (int tile = wave; tile < n_tiles; tile += kWaves) {
     if (!kEarly) tile_load<NQ, MS>(T, t_begin + tile * kTileTokens, R);
-    tile_compute<NQ, MS, ROT, RELOC>(P, T, t_begin + tile * kTileTokens, R, Wt, tile_lds, s_freq, s_coord);
+    tile_compute<NQ, MS, ROT, RELOC>(P, T, t_begin + tile * kTileTokens, R, Wt, tile_lds, s_freq, s_coord, s_dcs);
     if (kEarly && tile + kWaves < n_tiles) tile_load<NQ, MS>(T, t_begin + (tile + kWaves) * kTileTokens, R);
   }
 }
@@ -429,6 +495,7 @@ __global__ __launch_bounds__(kThreads, MS == 4 || RELOC ? 3 : 4) void rehydrate_
   extern __shared__ __align__(16) uint8_t lds_dyn[];
   __shared__ double s_freq[kMaxPairs];
   __shared__ int s_coord[kMaxPairs];
+  __shared__ float s_dcs[2 * kMaxPairs];        // relocation: cos, sin of delta per pair
 
   const int64_t task = xcd_task(P.per_xcd);
   if (task >= P.n_tasks) return;
@@ -466,16 +533,16 @@ __global__ __launch_bounds__(kThreads, MS == 4 || RELOC ? 3 : 4) void rehydrate_
   T.u_base = (int64_t)T.c * Q.u_s[0] + (int64_t)T.l * Q.u_s[1] + (int64_t)T.h * Q.u_s[2];
   const int rot = (B.flags & kBlkRotate) ? (P.rope.pairing == 0 ? 1 : 2) : 0;
   switch (B.nq * 3 + rot) {
-    case 1 * 3 + 0: rehydrate_block<1, MS, 0, RELOC>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
-    case 1 * 3 + 2: rehydrate_block<1, MS, 2, RELOC>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
-    case 2 * 3 + 0: rehydrate_block<2, MS, 0, RELOC>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
-    case 2 * 3 + 1: rehydrate_block<2, MS, 1, RELOC>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
-    case 2 * 3 + 2: rehydrate_block<2, MS, 2, RELOC>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
-    case 3 * 3 + 0: rehydrate_block<3, MS, 0, RELOC>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
-    case 3 * 3 + 2: rehydrate_block<3, MS, 2, RELOC>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
-    case 4 * 3 + 0: rehydrate_block<4, MS, 0, RELOC>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
-    case 4 * 3 + 1: rehydrate_block<4, MS, 1, RELOC>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
-    case 4 * 3 + 2: rehydrate_block<4, MS, 2, RELOC>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord); break;
+    case 1 * 3 + 0: rehydrate_block<1, MS, 0, RELOC>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord, s_dcs); break;
+    case 1 * 3 + 2: rehydrate_block<1, MS, 2, RELOC>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord, s_dcs); break;
+    case 2 * 3 + 0: rehydrate_block<2, MS, 0, RELOC>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord, s_dcs); break;
+    case 2 * 3 + 1: rehydrate_block<2, MS, 1, RELOC>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord, s_dcs); break;
+    case 2 * 3 + 2: rehydrate_block<2, MS, 2, RELOC>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord, s_dcs); break;
+    case 3 * 3 + 0: rehydrate_block<3, MS, 0, RELOC>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord, s_dcs); break;
+    case 3 * 3 + 2: rehydrate_block<3, MS, 2, RELOC>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord, s_dcs); break;
+    case 4 * 3 + 0: rehydrate_block<4, MS, 0, RELOC>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord, s_dcs); break;
+    case 4 * 3 + 1: rehydrate_block<4, MS, 1, RELOC>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord, s_dcs); break;
+    case 4 * 3 + 2: rehydrate_block<4, MS, 2, RELOC>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord, s_dcs); break;
     default: break;                              // rejected on the host (NeoX needs an even NQ)
   }
 }
