@@ -123,7 +123,9 @@ typedef enum {
   KAMERA_PATCH_PRE_ROPE = 0,  /* K' = R(pos)(K + U W): the patch lives in the
                                  stored, position-free frame (Sec. 3)         */
   KAMERA_PATCH_POST_ROPE = 1  /* K' = R(pos) K + U W: the literal form of
-                                 Eq. eq:operator                              */
+                                 Eq. eq:operator, and the frame of a key
+                                 deficit taken against R(pos) K as App. A's
+                                 compile step does (see kamera_form_patch)    */
 } kamera_patch_frame;
 
 /* RoPE variant (Sec. 3 content | RoPE split; Fig. fig:unify for M-RoPE).
@@ -299,9 +301,21 @@ typedef struct {
  * Delta (n x dim, fp32) as the stored patch
  *   U = U_svd[:, :m] * S[:m]   (n x m, bf16, singular values folded in),
  *   W = Vt[:m]                 (m x dim, bf16),
- * so U W is the best rank-m approximation of Delta and (U, W) feed
- * kamera_rehydrate directly.  The conditioned forward pass that produces
- * Delta needs model weights and is not part of this library.
+ * so U W is the best rank-m approximation of Delta.  The conditioned forward
+ * pass that produces Delta needs model weights and is not part of this
+ * library.
+ * Frame of the factors: U W lives in the frame Delta was taken in, and the
+ * kamera_rehydrate call that applies it must use the same frame.
+ *   - App. A takes the key deficit against the canonical keys already turned
+ *     to the target, Delta = K_cond - R(p) K: the rotated frame.  Such
+ *     factors are applied with KAMERA_PATCH_POST_ROPE, K' = R(p) K + U W, at
+ *     the positions p they were formed at.
+ *   - For the default KAMERA_PATCH_PRE_ROPE, K' = R(p)(K + U W), turn each
+ *     token's deficit back first, Delta_i <- R(-p_i) Delta_i (row i at its
+ *     position p_i); the patch formed from that serves every position.
+ *   Applying rotated-frame factors with KAMERA_PATCH_PRE_ROPE rotates the
+ *   patch a second time and gives wrong keys.  Values and the MLA latent are
+ *   never rotated, so for them the two frames coincide.
  * Layouts: element (c, l, h, i, j) of Delta at delta + c*delta_stride[0] +
  * l*delta_stride[1] + h*delta_stride[2] + i*delta_stride[3] + j (fp32,
  * 16-byte aligned rows); U and W as in kamera_plane (bf16); sigma (optional,

@@ -4,6 +4,8 @@
 
 #include <stdint.h>
 
+#include <atomic>
+
 #include <hip/hip_runtime_api.h>
 
 namespace kamera {
@@ -146,6 +148,22 @@ struct FormParams {
 };
 
 size_t form_lds_bytes(int dim, int m);
+
+// Raises a kernel's dynamic-LDS limit on the current device the first time it
+// is launched there.  `done` is the caller's per-device flag array (one per
+// kernel instantiation); two threads that race on a first launch both make
+// the same idempotent attribute call.
+constexpr int kMaxDevices = 64;
+inline hipError_t ensure_lds_limit(const void* fn, int bytes, std::atomic<bool> (&done)[kMaxDevices]) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  const bool cached = dev >= 0 && dev < kMaxDevices;
+  if (cached && done[dev].load(std::memory_order_acquire)) return hipSuccess;
+  e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+  if (e == hipSuccess && cached) done[dev].store(true, std::memory_order_release);
+  return e;
+}
 
 hipError_t launch_rehydrate(const RehydrateParams& p, hipStream_t s);
 hipError_t launch_rehydrate_rows(const RehydrateParams& p, hipStream_t s);

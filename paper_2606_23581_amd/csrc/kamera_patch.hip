@@ -647,17 +647,10 @@ size_t form_lds_bytes(int dim, int m) {
 
 hipError_t launch_form_patch(const FormParams& p, hipStream_t s) {
   const size_t lds = form_lds_bytes(p.dim, p.m);
-  // the LDS limit is raised once per device (a race only repeats the call)
-  static bool attr_set[64] = {};
-  int dev = 0;
-  hipError_t e = hipGetDevice(&dev);
+  static std::atomic<bool> lds_set[kMaxDevices];
+  const hipError_t e =
+      ensure_lds_limit((const void*)form_patch_kernel, (int)form_lds_bytes(kFormMaxDim, kFormMaxDim), lds_set);
   if (e != hipSuccess) return e;
-  if (dev < 0 || dev >= 64 || !attr_set[dev]) {
-    e = hipFuncSetAttribute((const void*)form_patch_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
-                            (int)form_lds_bytes(kFormMaxDim, kFormMaxDim));
-    if (e != hipSuccess) return e;
-    if (dev >= 0 && dev < 64) attr_set[dev] = true;
-  }
   hipLaunchKernelGGL(form_patch_kernel, dim3((uint32_t)p.n_units), dim3(kFormThreads), lds, s, p);
   return hipGetLastError();
 }

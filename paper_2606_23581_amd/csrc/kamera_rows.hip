@@ -585,18 +585,9 @@ __global__ __launch_bounds__(64 * HW, 8 / HW) void rehydrate_rows_kernel(const R
 
 template <int MS, int HW, bool RELOC>
 hipError_t launch_rows(const RehydrateParams& p, hipStream_t s) {
-  // the LDS limit is raised once per device and instantiation (a race only
-  // repeats the call)
-  static bool attr_set[64] = {};
-  int dev = 0;
-  hipError_t e = hipGetDevice(&dev);
+  static std::atomic<bool> lds_set[kMaxDevices];
+  const hipError_t e = ensure_lds_limit((const void*)rehydrate_rows_kernel<MS, HW, RELOC>, rg_lds_bytes(MS, HW), lds_set);
   if (e != hipSuccess) return e;
-  if (dev < 0 || dev >= 64 || !attr_set[dev]) {
-    e = hipFuncSetAttribute((const void*)rehydrate_rows_kernel<MS, HW, RELOC>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                            rg_lds_bytes(MS, HW));
-    if (e != hipSuccess) return e;
-    if (dev >= 0 && dev < 64) attr_set[dev] = true;
-  }
   const dim3 grid((uint32_t)((int64_t)p.per_xcd * 8)), block(64 * HW);
   hipLaunchKernelGGL((rehydrate_rows_kernel<MS, HW, RELOC>), grid, block, rg_lds_bytes(MS, HW), s, p);
   return hipGetLastError();

@@ -140,6 +140,17 @@ REHYDRATE_CASES = {
     "per_head_explicit_paged": RehydrateCase(H=8, pos_mode="explicit", paged=True, kernel=2, plan=1, seed=61),
     "per_head_rank_72_paged": RehydrateCase(H=8, m_k=72, m_v=8, paged=True, kernel=2, plan=1, seed=62),
     "per_head_9_heads_paged": RehydrateCase(H=9, paged=True, kernel=2, plan=1, seed=63),
+    # relocation above rank 64 on the per-head kernel: the two-rotation form
+    # R(p)(R(delta - p) K + U W) (rank steps of 4 x 32), both frames
+    "relocate_rank_72_per_head": RehydrateCase(reloc=True, m_k=72, m_v=8, n=70, kernel=1, plan=1, seed=66),
+    "relocate_rank_72_post_frame_paged": RehydrateCase(reloc=True, m_k=72, m_v=72, post_rope=True, paged=True,
+                                                       pairing="interleaved", theta=1e4, n=50, kernel=1, plan=1,
+                                                       seed=67),
+    "relocate_rank_128_per_head": RehydrateCase(reloc=True, m_k=128, m_v=128, n=48, C=1, L=1, H=2, kernel=1, plan=1,
+                                                seed=68),
+    "relocate_rank_128_post_frame_mrope": RehydrateCase(reloc=True, m_k=128, m_v=100, post_rope=True,
+                                                        sections=(16, 24, 24), pos_mode="grid3", grid_w=8, n=40,
+                                                        C=2, L=1, H=2, kernel=1, plan=1, seed=69),
 }
 
 
@@ -591,6 +602,95 @@ def test_orbit_patch_matches_reference(device, K, n, d, m):
         km.form_patch(dt[0], U2, W2)
         torch.cuda.synchronize()
         assert np.array_equal(bits(U2), Ub) and np.array_equal(bits(W2), Wb)
+
+
+@pytest.mark.parametrize("kernel", [1, 3])
+def test_form_patch_then_rehydrate_in_both_frames(device, kernel):
+    """The compile step feeds the serve step (App. A): a key deficit is
+    planted, its patch formed on the GPU and applied by kamera_rehydrate.
+
+    * rotated frame (App. A takes the deficit against R(p) K): a rank-m
+      Delta_post, formed as is and applied with KAMERA_PATCH_POST_ROPE,
+      rebuilds R(p) K + Delta_post;
+    * stored frame: a deficit that is rank m before rotation, handed over as
+      App. A would see it (R(p) Delta_pre) and turned back per token by
+      R(-p_i) before forming, applied with KAMERA_PATCH_PRE_ROPE, rebuilds
+      R(p)(K + Delta_pre);
+    * rotated-frame factors applied in the stored frame rotate the patch
+      twice and miss the target.
+
+    Each output is checked element by element against the oracle run on the
+    GPU-formed factors (the parity bar), and against the target keys within
+    2 x 2^-7 (the output's bf16 rounding plus that of the two factors)."""
+    import paper_2606_23581_amd as km
+    import torch
+
+    print(f"[case] form_patch -> rehydrate frames kernel {kernel}", flush=True)
+    rng = np.random.default_rng(4242 + kernel)
+    C, L, H, n, D, m = 2, 2, 4, 256, 128, 16
+    rs = km.RopeSpec(theta=1e6, rope_dim=D, pairing="neox")
+    orope = oracle_rope(rs)
+    p0 = rng.integers(0, 30000, size=C)
+    pos = np.zeros((C, 3), np.int32)
+    pos[:, 0] = p0
+    pos3 = [ref.positions_linear(int(p0[c]), n) for c in range(C)]
+    K = synth.randn_bf16_numpy((C, L, n, H, D), 1.0, rng)
+
+    def planted():
+        A = np.linalg.qr(rng.standard_normal((n, m)))[0]
+        B = np.linalg.qr(rng.standard_normal((D, m)))[0]
+        return (A * np.linspace(12.0, 4.0, m)) @ B.T          # entries ~0.3
+
+    d_post = np.empty((C, L, H, n, D))
+    d_pre = np.empty((C, L, H, n, D))
+    d_pre_rotated = np.empty((C, L, H, n, D))                 # what App. A would hand over
+    for c, l, h in np.ndindex(C, L, H):
+        d_post[c, l, h] = planted()
+        d_pre[c, l, h] = planted()
+        d_pre_rotated[c, l, h] = ref.rotate(d_pre[c, l, h], orope, ref.rope_angles(orope, pos3[c]))
+    # the caller's conversion to the stored frame: R(-p_i) per token
+    d_back = np.empty_like(d_pre_rotated)
+    for c, l, h in np.ndindex(C, L, H):
+        d_back[c, l, h] = ref.rotate(d_pre_rotated[c, l, h], orope, ref.rope_angles(orope, -pos3[c]))
+
+    kin = dev(K, device)
+    cpos = dev_i32(pos, device)
+
+    def form(deficit):
+        U = torch.zeros((C, L, H, n, m), dtype=torch.bfloat16, device=device)
+        W = torch.zeros((C, L, H, m, D), dtype=torch.bfloat16, device=device)
+        km.form_patch(torch.from_numpy(deficit.astype(np.float32)).to(device), U, W)
+        return U, W
+
+    def apply(U, W, frame):
+        out = dev(np.full((C, L, n, H, D), SENTINEL, np.uint16), device)
+        km.rehydrate(kin, out, rope=rs, chunk_pos=cpos, u_k=U, w_k=W, patch_frame=frame, kernel=kernel)
+        torch.cuda.synchronize()
+        return bits(out), bits(U), bits(W)
+
+    cases = {
+        "rotated frame, POST_ROPE": (d_post, km.PATCH_POST_ROPE, True),
+        "stored frame, PRE_ROPE": (d_back, km.PATCH_PRE_ROPE, False),
+    }
+    for what, (deficit, frame, post) in cases.items():
+        got, Ub, Wb = apply(*form(deficit), frame)
+        for c, l, h in np.ndindex(C, L, H):
+            Kf = ref.bf16_to_f64(K[c, l, :, h])
+            Ug, Wg = ref.bf16_to_f64(Ub[c, l, h]), ref.bf16_to_f64(Wb[c, l, h])
+            want = ref.rehydrate_k(Kf, Ug, Wg, orope, pos3[c], patch_after_rope=post)
+            assert_close(got[c, l, :, h], want, f"{what} c{c} l{l} h{h}")
+            rotated = ref.rehydrate_k(Kf, None, None, orope, pos3[c])
+            target = rotated + (d_post[c, l, h] if post else d_pre_rotated[c, l, h])
+            err = np.abs(ref.bf16_to_f64(got[c, l, :, h]) - target) / np.maximum(1.0, np.abs(target))
+            assert err.max() <= 2 * TOL, (what, c, l, h, float(err.max()))
+    # the hazard the frame flag guards against
+    got, _, _ = apply(*form(d_post), km.PATCH_PRE_ROPE)
+    worst = 0.0
+    for c, l, h in np.ndindex(C, L, H):
+        target = ref.rehydrate_k(ref.bf16_to_f64(K[c, l, :, h]), None, None, orope, pos3[c]) + d_post[c, l, h]
+        err = np.abs(ref.bf16_to_f64(got[c, l, :, h]) - target) / np.maximum(1.0, np.abs(target))
+        worst = max(worst, float(err.max()))
+    assert worst > 8 * TOL, worst
 
 
 # ---------------------------------------------------------------------------
