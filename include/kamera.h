@@ -54,7 +54,7 @@
 extern "C" {
 #endif
 
-#define KAMERA_ABI_VERSION 2
+#define KAMERA_ABI_VERSION 3
 
 /* Largest patch rank m accepted (>= the 128-wide head, so a full-rank patch
  * that reproduces any Delta K exactly can be applied). */
@@ -108,10 +108,11 @@ typedef enum {
  * slab or one layer of the pool.  A row-group workgroup takes 8 heads (one per CU),
  * or 4 (two per CU; rows of <= 4 heads, or 8 heads in two groups).  AUTO
  * takes ROW_GROUP4 where it was measured faster on MI355X: rows of 4 or 8
- * heads, chunks of >= 256 tokens and >= 2^22 rows in all (planes x chunks x
- * layers x tokens x heads).  Fewer rows, shorter chunks and other head
- * counts keep PER_HEAD.  A ROW_GROUP or ROW_GROUP4 request that is not
- * possible falls back to PER_HEAD. */
+ * heads, chunks of >= 256 tokens and >= 2^19 rows in all (planes x chunks x
+ * layers x tokens x heads), except dense outputs at rank <= 32 with 2^21 to
+ * 2^23 rows.  Those, fewer rows, shorter chunks and other head counts keep
+ * PER_HEAD.  A ROW_GROUP or ROW_GROUP4 request that is not possible falls
+ * back to PER_HEAD. */
 typedef enum {
   KAMERA_KERNEL_AUTO = 0,
   KAMERA_KERNEL_PER_HEAD = 1,
@@ -239,6 +240,11 @@ typedef struct {
   uint32_t* status;            /* optional device word, bits OR-ed in          */
   const int32_t* delta;        /* optional: relocation of rotated keys         */
   int32_t kernel;              /* kamera_kernel_choice (0: AUTO)               */
+  int32_t max_workgroups;      /* row-group kernel: 0 = one resident wave of
+                                  workgroups on the whole device, > 0 = at most
+                                  this many (leaves CUs to concurrent work);
+                                  same results.  The per-head kernel launches
+                                  one workgroup per task and ignores it.      */
 } kamera_rehydrate_args;
 
 /* kamera_shift -- K' = R(delta_c) K in place on the rope band of every token

@@ -99,7 +99,7 @@ class CRehydrateArgs(ctypes.Structure):
                 ("explicit_chunk_stride", _i64), ("n_planes", _i32), ("plane", CPlane * 2),
                 ("paged", _i32), ("row_base", _vp), ("page_table", _vp), ("pt_stride", _i32),
                 ("page_size", _i32), ("n_pool_pages", _i32), ("status", _vp), ("delta", _vp),
-                ("kernel", _i32)]
+                ("kernel", _i32), ("max_workgroups", _i32)]
 
 
 class CShiftArgs(ctypes.Structure):
@@ -337,7 +337,7 @@ def prepare_rehydrate(k_in, k_out, *, rope: RopeSpec, chunk_pos=None, v_in=None,
                       page_size: int = 16, n_pool_pages: int = 0,
                       patch_frame: int = PATCH_PRE_ROPE, status=None, delta=None,
                       u_pe=None, w_pe=None, k_layer_rank=None, v_layer_rank=None,
-                      pe_layer_rank=None, kernel: int = KERNEL_AUTO) -> Prepared:
+                      pe_layer_rank=None, kernel: int = KERNEL_AUTO, max_workgroups: int = 0) -> Prepared:
     """Rebuild cached chunks at their target positions (``kamera_rehydrate``).
 
     k_in, v_in: [C, L, n, H, D] bf16 (any strides, last dim contiguous).
@@ -353,6 +353,7 @@ def prepare_rehydrate(k_in, k_out, *, rope: RopeSpec, chunk_pos=None, v_in=None,
     band patched by u_pe/w_pe ([C, L, H, n, m_pe], [C, L, H, m_pe, rope_dim]).
     *_layer_rank: int32 [L] device tensors lowering the rank per layer.
     kernel: KERNEL_AUTO, KERNEL_PER_HEAD, KERNEL_ROW_GROUP or KERNEL_ROW_GROUP4 (same results).
+    max_workgroups: 0 = one resident wave on the whole device, else a cap (same results).
     """
     L = lib()
     _bf16(k_in, "k_in"), _bf16(k_out, "k_out"), _bf16(v_in, "v_in"), _bf16(v_out, "v_out")
@@ -401,6 +402,7 @@ def prepare_rehydrate(k_in, k_out, *, rope: RopeSpec, chunk_pos=None, v_in=None,
     _i32_dev(delta, "delta")
     a.delta = _ptr(delta)
     a.kernel = int(kernel)
+    a.max_workgroups = int(max_workgroups)
     keep = (k_in, k_out, v_in, v_out, u_k, w_k, u_v, w_v, chunk_pos, explicit_pos, chunk_tokens,
             row_base, page_table, status, delta, u_pe, w_pe, k_layer_rank, v_layer_rank, pe_layer_rank)
     return Prepared(L.kamera_rehydrate, a, keep)

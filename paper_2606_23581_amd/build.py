@@ -67,7 +67,22 @@ def build(verbose: bool = False, save_temps: bool = False) -> str:
     tmp = LIB + ".tmp"
     _run([hipcc, "-shared", f"--offload-arch={ARCH}", "-fPIC", *objs, "-o", tmp], verbose)
     os.replace(tmp, LIB)
+    build_ceiling(verbose)
     return LIB
+
+
+CEILING_LIB = os.path.join(PKG, "libkamera_ceiling.so")
+
+
+def build_ceiling(verbose: bool = False) -> str:
+    """libkamera_ceiling.so: the benchmark's same-traffic copy kernel (a
+    measurement of the device, not part of the operator's library)."""
+    hipcc = _hipcc()
+    tmp = CEILING_LIB + ".tmp"
+    _run([hipcc, "-shared", "-O3", f"--offload-arch={ARCH}", *NO_PACKED_FP32, "-std=c++17", "-fPIC",
+          "-Wno-unused-command-line-argument", os.path.join(CSRC, "kamera_ceiling.hip"), "-o", tmp], verbose)
+    os.replace(tmp, CEILING_LIB)
+    return CEILING_LIB
 
 
 if __name__ == "__main__":

@@ -212,6 +212,8 @@ static int build_rehydrate(const kamera_rehydrate_args* a, kamera::RehydratePara
     return fail(KAMERA_ERR_SHAPE, "%s: n_planes must be 1 or 2 (got %d)", who, a->n_planes);
   if (a->kernel < KAMERA_KERNEL_AUTO || a->kernel > KAMERA_KERNEL_ROW_GROUP4)
     return fail(KAMERA_ERR_SHAPE, "%s: unknown kernel choice %d", who, a->kernel);
+  if (a->max_workgroups < 0)
+    return fail(KAMERA_ERR_SHAPE, "%s: max_workgroups must be >= 0 (got %d)", who, a->max_workgroups);
   if (a->patch_frame != KAMERA_PATCH_PRE_ROPE && a->patch_frame != KAMERA_PATCH_POST_ROPE)
     return fail(KAMERA_ERR_SHAPE, "%s: unknown patch_frame %d", who, a->patch_frame);
   bool any_rot = false;
@@ -342,6 +344,7 @@ static int build_rehydrate(const kamera_rehydrate_args* a, kamera::RehydratePara
   P.n_chunks = a->n_chunks;
   P.n_layers = a->n_layers;
   P.n_heads = a->n_heads;
+  P.max_wgs = a->max_workgroups;
 
   int64_t units = 0;
   for (int p = 0; p < a->n_planes; ++p) {
@@ -398,13 +401,16 @@ static int build_rehydrate(const kamera_rehydrate_args* a, kamera::RehydratePara
   // take the row-group kernel: a workgroup takes hw = 4 or 8 heads of a token
   // row, so it writes them as one contiguous run (a whole pool page at 8
   // heads).  AUTO follows where it measured faster than the per-head kernel,
-  // averaged over several placements of the buffers in HBM: rows of 4 or 8
-  // heads, chunks of >= 256 tokens and >= 2^22 rows in all (planes x chunks x
-  // layers x tokens x heads) take groups of 4 heads (two workgroups per CU);
-  // 8-head groups never led them by more than the spread of placements and
-  // trail them when relocating (they run out of registers).  Fewer rows, where
-  // a task's set-up is paid over too few tiles, shorter chunks and other head
-  // counts keep the per-head kernel.
+  // over three placements of the buffers in HBM each: rows of 4 or 8 heads
+  // and chunks of >= 256 tokens take groups of 4 heads (two workgroups per CU)
+  // from 2^19 rows in all (planes x chunks x layers x tokens x heads) on --
+  // the row-group kernel's equal shares of tiles and its two tiles in flight
+  // beat the per-head kernel's small tasks there -- except dense outputs at
+  // rank <= 32 with 2^21 .. 2^23 rows, where the per-head kernel's token
+  // blocks are long enough and its four workgroups per CU keep more bytes in
+  // flight.  8-head groups never led 4-head ones by more than the spread of
+  // placements and trail them when relocating (they run out of registers).
+  // Tiny calls, shorter chunks and other head counts keep the per-head kernel.
   const double n_rows = (double)a->n_planes * a->n_chunks * a->n_layers * a->n_tokens * a->n_heads;
   int hw = 0;
   if (a->kernel == KAMERA_KERNEL_ROW_GROUP) {
@@ -412,7 +418,10 @@ static int build_rehydrate(const kamera_rehydrate_args* a, kamera::RehydratePara
   } else if (a->kernel == KAMERA_KERNEL_ROW_GROUP4) {
     hw = 4;
   } else if (a->kernel == KAMERA_KERNEL_AUTO) {
-    hw = (a->n_heads == 4 || a->n_heads == 8) && a->n_tokens >= 256 && n_rows >= 4194304.0 ? 4 : 0;
+    int max_rank = 0;
+    for (int p = 0; p < a->n_planes; ++p) max_rank = std::max(max_rank, (int)a->plane[p].m);
+    const bool dense_window = !a->paged && max_rank <= 32 && n_rows >= 2097152.0 && n_rows < 8388608.0;
+    hw = (a->n_heads == 4 || a->n_heads == 8) && a->n_tokens >= 256 && n_rows >= 524288.0 && !dense_window ? 4 : 0;
   }
   bool rows = hw > 0 && a->n_heads <= kamera::kRgMaxHeads && a->head_dim == 128 &&
               (!any_rot || a->pos_mode != KAMERA_POS_EXPLICIT);
@@ -438,23 +447,14 @@ static int build_rehydrate(const kamera_rehydrate_args* a, kamera::RehydratePara
     o.out_rec = (int32_t)out_rec;
   }
   if (rows) {
-    // a workgroup takes 4 heads (two workgroups per CU) or 8 (one per CU)
-    const int64_t groups = (int64_t)a->n_planes * ceil_div(a->n_heads, hw) * a->n_chunks * a->n_layers;
-    const int64_t want = 2048 * (8 / hw);
-    int tb = 1024;
-    while (tb > 64 && groups * ceil_div(a->n_tokens, tb) < want) tb /= 2;
-    tb = (int)std::min<int64_t>(tb, ceil_div(a->n_tokens, 64) * 64);
+    // a workgroup takes 4 heads (two workgroups per CU) or 8 (one per CU);
+    // the launch holds one resident wave of workgroups, each with an equal
+    // share of the 16-token tiles of its (plane, head group) lane
     P.row_group = hw;
     P.n_hgroups = (int32_t)ceil_div(a->n_heads, hw);
-    P.token_block = tb;
-    P.n_tblk = (int32_t)ceil_div(a->n_tokens, tb);
+    P.unit_tiles = (int32_t)ceil_div(a->n_tokens, kamera::kTileTokens);
     P.blocks_per_group = a->n_planes;
-    const int64_t n_tasks = groups * P.n_tblk;
-    if (n_tasks >= (int64_t)1 << 31)
-      return fail(KAMERA_ERR_RANGE, "%s: %lld tasks exceed one launch", who, (long long)n_tasks);
-    P.n_tasks = n_tasks;
-    rc = pick_grid(P.n_tasks, P.per_xcd, who);
-    if (rc) return rc;
+    P.n_tasks = (int64_t)a->n_planes * P.n_hgroups * a->n_chunks * a->n_layers * P.unit_tiles;
     launch = true;
     return KAMERA_OK;
   }

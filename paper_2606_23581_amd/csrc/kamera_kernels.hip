@@ -242,9 +242,13 @@ __device__ __forceinline__ void tile_load(const TileCtx& T, int i0, TileRegs<NQ,
   }
 }
 
-template <int NQ, int MS, int ROT, bool RELOC>
-__device__ __forceinline__ void tile_compute(const RehydrateParams& P, const TileCtx& T, int i0,
-                                             const TileRegs<NQ, MS>& R, const uint16_t* __restrict__ Wt,
+// One 16-token tile at i0.  R holds its loads.  With EARLY the loads of the
+// wave's next tile (next_i0 >= 0) go into R as soon as the tile has been
+// copied into LDS (row-staged blocks with staged or no U); the return value
+// says whether they did (else the caller issues them).
+template <int NQ, int MS, int ROT, bool RELOC, bool EARLY>
+__device__ __forceinline__ bool tile_compute(const RehydrateParams& P, const TileCtx& T, int i0, int next_i0,
+                                             TileRegs<NQ, MS>& R, const uint16_t* __restrict__ Wt,
                                              uint8_t* tile_lds, const double* s_freq,
                                              const int* s_coord, const float* s_dcs) {
   // relocation up to rank 64 as R(delta) K + R(p) U W (one set of per-token
@@ -286,6 +290,8 @@ __device__ __forceinline__ void tile_compute(const RehydrateParams& P, const Til
       }
     }
   }
+  const bool early = EARLY && Staged<NQ>::value && (MS == 0 || !T.patched || u_staged);
+  if (early && next_i0 >= 0) tile_load<NQ, MS>(T, next_i0, R);
 
   f32x4 acc[2 * NQ];
   if constexpr (kOneAngle) {
@@ -400,6 +406,7 @@ __device__ __forceinline__ void tile_compute(const RehydrateParams& P, const Til
       for (int q = 0; q < NQ; ++q) st16(Q.out + dst + 8 * (g + 4 * q), o[q]);
     }
   }
+  return early;
 }
 
 // Stage W^T of one column block into LDS: Wt[col][k], col in [0, 32*NQ),
@@ -457,12 +464,16 @@ __device__ __forceinline__ void rehydrate_block(const RehydrateParams& P, const 
   uint8_t* tile_lds = lds + 128 * (32 * MS + 8) * 2 + wave * tile_lds_bytes();
   constexpr int kWaves = kThreads / 64;
   const int n_tiles = (t_end - t_begin + kTileTokens - 1) / kTileTokens;
-  // Up to rank 32 the wave's first tile is in flight while W^T is staged: one
-  // memory round trip before the first MFMA instead of two (at higher ranks
-  // the tile's registers next to the staging would spill).
-  constexpr bool kEarly = MS <= 1;
+  // Up to rank 32 the wave's first tile is in flight while W^T is staged (one
+  // memory round trip before the first MFMA instead of two), and each next
+  // tile's loads are issued during the current tile -- as soon as it is in LDS
+  // where the registers allow (no relocation), else after its stores.  At
+  // higher ranks the registers of a tile in flight beside the MFMA operands
+  // would spill: a tile's loads are issued when it starts.
+  constexpr bool kAhead = MS <= 1;
+  constexpr bool kEarly = MS == 0 || (MS == 1 && !RELOC);
   TileRegs<NQ, MS> R;
-  if (kEarly && wave < n_tiles) tile_load<NQ, MS>(T, t_begin + wave * kTileTokens, R);
+  if (kAhead && wave < n_tiles) tile_load<NQ, MS>(T, t_begin + wave * kTileTokens, R);
   if constexpr (MS > 0) {
     if (T.patched) stage_w<NQ>(T, Wt);
   }
@@ -482,9 +493,11 @@ __device__ __forceinline__ void rehydrate_block(const RehydrateParams& P, const 
   }
   __syncthreads();
   for (int tile = wave; tile < n_tiles; tile += kWaves) {
-    if (!kEarly) tile_load<NQ, MS>(T, t_begin + tile * kTileTokens, R);
-    tile_compute<NQ, MS, ROT, RELOC>(P, T, t_begin + tile * kTileTokens, R, Wt, tile_lds, s_freq, s_coord, s_dcs);
-    if (kEarly && tile + kWaves < n_tiles) tile_load<NQ, MS>(T, t_begin + (tile + kWaves) * kTileTokens, R);
+    if (!kAhead) tile_load<NQ, MS>(T, t_begin + tile * kTileTokens, R);
+    const int next_i0 = kAhead && tile + kWaves < n_tiles ? t_begin + (tile + kWaves) * kTileTokens : -1;
+    const bool issued = tile_compute<NQ, MS, ROT, RELOC, kEarly>(P, T, t_begin + tile * kTileTokens, next_i0, R, Wt,
+                                                                 tile_lds, s_freq, s_coord, s_dcs);
+    if (!issued && next_i0 >= 0) tile_load<NQ, MS>(T, next_i0, R);
   }
 }
 

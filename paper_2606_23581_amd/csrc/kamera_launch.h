@@ -90,7 +90,10 @@ struct RehydrateParams {
   int32_t blocks_per_group;          // column blocks of all planes for one (chunk, layer, head, token block)
   int32_t row_group;                 // 0: per-head kernel; 4 or 8: heads per row-group workgroup
   int32_t n_hgroups;                 // row-group: head groups per row
-  int32_t pad3_;
+  int32_t unit_tiles;                // row-group: 16-token tiles per (chunk, layer) unit (n_tokens / 16, rounded up)
+  int32_t lane_wgs;                  // row-group: workgroups per (plane, head group) lane, set at launch
+  int32_t max_wgs;                   // caller's cap on the workgroups of a launch (0: none)
+  int32_t pad4_;
   int64_t n_tasks;
 };
 

@@ -36,21 +36,30 @@ __host__ __device__ constexpr int rg_u_row(int ms) { return 64 * ms + kRowPad; }
 __host__ __device__ constexpr int rg_buf_bytes(int ms, int hw) {
   return hw * kTileTokens * (kRgKRow + rg_u_row(ms));
 }
-constexpr int kRgWtRow = 64 * 2 + kRowPad;                 // W^T staging row: 64 ranks + pad
-constexpr int kRgMaxBlock = 1024;                          // tokens per row-group task
+// W^T staging row of one column: 32 * ms ranks + pad (a round stages 4 heads)
+__host__ __device__ constexpr int rg_wt_row(int ms) { return 64 * ms + kRowPad; }
+__host__ __device__ constexpr int rg_wt_bytes(int ms) { return ms > 0 ? 4 * 128 * rg_wt_row(ms) : 0; }
+constexpr int kRgMaxBlock = 1024;                          // tokens per row-group segment
 __host__ __device__ constexpr int rg_lds_bytes(int ms, int hw) {
-  return (2 * rg_buf_bytes(ms, hw) > 4 * 128 * kRgWtRow ? 2 * rg_buf_bytes(ms, hw) : 4 * 128 * kRgWtRow) +
+  return (2 * rg_buf_bytes(ms, hw) > rg_wt_bytes(ms) ? 2 * rg_buf_bytes(ms, hw) : rg_wt_bytes(ms)) +
          kRgMaxBlock * 4;
 }
+// waves per SIMD the launch bounds ask for: three 4-head workgroups per CU
+// without a patch (40 KiB of LDS each), else two (one with 8 heads); at rank
+// 32 three would spill registers
+__host__ __device__ constexpr int rg_min_waves(int ms, int hw) { return hw == 4 && ms == 0 ? 3 : 8 / hw; }
 
 // per thread and tile: HW * 16 tokens * 16 K chunks over 64 * HW threads,
 // and HW * 16 tokens * (up to 8) U chunks
 constexpr int kRgKVec = 4;
-constexpr int kRgUVec = 2;
+// U vectors per thread and tile at MS rank steps (HW * 16 tokens * 4 MS
+// chunks over 64 * HW threads)
+__host__ __device__ constexpr int rg_u_vec(int ms) { return ms > 0 ? ms : 1; }
 
+template <int MS>
 struct RgRegs {              // one tile's global loads, in flight until the LDS write
   u32x4 k[kRgKVec];
-  u32x4 u[kRgUVec];
+  u32x4 u[rg_u_vec(MS)];
 };
 
 constexpr uint32_t kRgOob = 0x7ffffff0u;                    // byte offset past every buffer extent
@@ -90,9 +99,8 @@ __device__ __forceinline__ void rg_vec(int v, int H, bool head_major, int& h, in
 }
 
 template <int MS, int HW>
-__device__ __forceinline__ void rg_load(const RgTask& T, int i0, RgRegs& R) {
+__device__ __forceinline__ void rg_load(const RgTask& T, int tid, int i0, RgRegs<MS>& R) {
   constexpr int NT = 64 * HW;
-  const int tid = threadIdx.x;
   const int nv = T.H * kTileTokens * 16;
 #pragma unroll
   for (int k = 0; k < kRgKVec; ++k) {
@@ -106,7 +114,7 @@ __device__ __forceinline__ void rg_load(const RgTask& T, int i0, RgRegs& R) {
   if constexpr (MS > 0) {
     const int cpr = 4 * (T.m_steps > 0 ? T.m_steps : 1);   // 16-byte chunks per U row (rank padded to 32)
 #pragma unroll
-    for (int k = 0; k < kRgUVec; ++k) {
+    for (int k = 0; k < rg_u_vec(MS); ++k) {
       const int v = tid + NT * k;
       const int h = v / (kTileTokens * cpr), t = (v / cpr) % kTileTokens, c = v % cpr;
       const int i = i0 + t;
@@ -118,9 +126,8 @@ __device__ __forceinline__ void rg_load(const RgTask& T, int i0, RgRegs& R) {
 }
 
 template <int MS, int HW>
-__device__ __forceinline__ void rg_to_lds(const RgTask& T, const RgRegs& R, uint8_t* buf) {
+__device__ __forceinline__ void rg_to_lds(const RgTask& T, int tid, const RgRegs<MS>& R, uint8_t* buf) {
   constexpr int NT = 64 * HW;
-  const int tid = threadIdx.x;
   const int nv = T.H * kTileTokens * 16;
 #pragma unroll
   for (int k = 0; k < kRgKVec; ++k) {
@@ -133,7 +140,7 @@ __device__ __forceinline__ void rg_to_lds(const RgTask& T, const RgRegs& R, uint
     if (T.m_steps > 0) {
       const int cpr = 4 * T.m_steps;
 #pragma unroll
-      for (int k = 0; k < kRgUVec; ++k) {
+      for (int k = 0; k < rg_u_vec(MS); ++k) {
         const int v = tid + NT * k;
         const int h = v / (kTileTokens * cpr), t = (v / cpr) % kTileTokens, c = v % cpr;
         // a layer rank that is not a multiple of 8 ends inside a chunk: the
@@ -250,10 +257,10 @@ __device__ __forceinline__ void rg_add_turned(f32x4 (&acc)[8], int g, const uint
 
 // one wave: head h of the tile in LDS, result written back in place
 template <int MS, int ROT, int HW, bool RELOC>
-__device__ __forceinline__ void rg_compute(const RehydrateParams& P, const RgTask& T, int i0, int h,
+__device__ __forceinline__ void rg_compute(const RehydrateParams& P, const RgTask& T, int tid, int i0, int h,
                                            const u32x4 (&wa)[8][MS > 0 ? MS : 1], uint8_t* buf,
                                            const double* s_freq, const int* s_coord, const float* s_dcs) {
-  const int lane = threadIdx.x & 63;
+  const int lane = tid & 63;
   const int g = lane >> 4, t = lane & 15;
   uint8_t* krow = buf + (h * kTileTokens + t) * kRgKRow;
   f32x4 acc[8];
@@ -330,10 +337,9 @@ __device__ __forceinline__ void rg_compute(const RehydrateParams& P, const RgTas
 // store phase: every thread writes four 16-byte pieces of the tile's rows;
 // s_page holds the pool page of every token of the block (-1: not written)
 template <int HW>
-__device__ __forceinline__ void rg_store(const RehydrateParams& P, const RgTask& T, int t_begin, int i0,
+__device__ __forceinline__ void rg_store(const RehydrateParams& P, const RgTask& T, int tid, int t_begin, int i0,
                                          const uint8_t* buf, const int* s_page) {
   constexpr int NT = 64 * HW;
-  const int tid = threadIdx.x;
   const int nv = T.H * kTileTokens * 16;
 #pragma unroll
   for (int k = 0; k < kRgKVec; ++k) {
@@ -379,8 +385,9 @@ __device__ __forceinline__ void rg_load_w(const RgTask& T, int h, int k0, int co
 }
 
 // transpose of one staging item into the W^T area: [head % 4][column][rank]
+template <int MS>
 __device__ __forceinline__ void rg_put_w(int hq, int k0, int colb, const uint32_t (&w)[4][4], uint8_t* lds) {
-  uint8_t* base = lds + hq * 128 * kRgWtRow;
+  uint8_t* base = lds + hq * 128 * rg_wt_row(MS);
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
     const int sh = (e & 1) ? 16 : 0;
@@ -389,16 +396,15 @@ __device__ __forceinline__ void rg_put_w(int hq, int k0, int colb, const uint32_
     uint2 v;
     v.x = r0 | (r1 << 16);
     v.y = r2 | (r3 << 16);
-    *reinterpret_cast<uint2*>(base + (colb + e) * kRgWtRow + 2 * k0) = v;
+    *reinterpret_cast<uint2*>(base + (colb + e) * rg_wt_row(MS) + 2 * k0) = v;
   }
 }
 
 template <int MS, int ROT, int HW, bool RELOC>
-__device__ __forceinline__ void rg_run(const RehydrateParams& P, const RgTask& T, int t_begin, int t_end,
+__device__ __forceinline__ void rg_run(const RehydrateParams& P, const RgTask& T, int tid, int t_begin, int t_end,
                                        uint8_t* lds, const double* s_freq, const int* s_coord, const float* s_dcs) {
   constexpr int NT = 64 * HW;
   constexpr int kIpt = 1024 / NT;               // W staging items per thread and round of 4 heads
-  const int tid = threadIdx.x;
   const int h = tid >> 6;                       // wave = head
   const int lane = tid & 63;
   const bool active = h < T.H;
@@ -420,10 +426,10 @@ __device__ __forceinline__ void rg_run(const RehydrateParams& P, const RgTask& T
       }
     }
   }
-  RgRegs R[kRgDepth];
+  RgRegs<MS> R[kRgDepth];
 #pragma unroll
   for (int d = 0; d < kRgDepth; ++d)
-    if (d < n_tiles) rg_load<MS, HW>(T, t_begin + d * kTileTokens, R[d]);
+    if (d < n_tiles) rg_load<MS, HW>(T, tid, t_begin + d * kTileTokens, R[d]);
   // staging item = (head of the round, rank quad, column chunk); the thread's
   // items are tid + NT * j, i.e. heads (tid >> 8) + j * NT / 256 of the round
   const int k0 = 4 * ((tid >> 4) & 15), colb = 8 * (tid & 15), hr = tid >> 8;
@@ -451,17 +457,17 @@ __device__ __forceinline__ void rg_run(const RehydrateParams& P, const RgTask& T
       }
       if (w_item) {
 #pragma unroll
-        for (int j = 0; j < kIpt; ++j) rg_put_w(hr + j * (NT / 256), k0, colb, w[j], lds);
+        for (int j = 0; j < kIpt; ++j) rg_put_w<MS>(hr + j * (NT / 256), k0, colb, w[j], lds);
       }
       __syncthreads();
       if ((h >> 2) == round) {
-        const uint8_t* hb = lds + (h & 3) * 128 * kRgWtRow;
+        const uint8_t* hb = lds + (h & 3) * 128 * rg_wt_row(MS);
 #pragma unroll
         for (int mt = 0; mt < 8; ++mt) {
           const int col = 8 * (t >> 2) + (t & 3) + 32 * (mt >> 1) + 4 * (mt & 1);
 #pragma unroll
           for (int k = 0; k < MS; ++k)
-            wa[mt][k] = (k < T.m_steps) ? *reinterpret_cast<const u32x4*>(hb + col * kRgWtRow + 64 * k + 16 * g)
+            wa[mt][k] = (k < T.m_steps) ? *reinterpret_cast<const u32x4*>(hb + col * rg_wt_row(MS) + 64 * k + 16 * g)
                                         : u32x4{0, 0, 0, 0};
         }
       }
@@ -471,15 +477,15 @@ __device__ __forceinline__ void rg_run(const RehydrateParams& P, const RgTask& T
 
   // kRgDepth register sets (tiles in flight) and two LDS buffers: tile tt
   // uses set tt % kRgDepth and buffer tt % 2; two barriers per tile
-  auto step = [&](int tt, RgRegs& R) {
+  auto step = [&](int tt, RgRegs<MS>& R) {
     const int i0 = t_begin + tt * kTileTokens;
     uint8_t* buf = lds + (tt & 1) * rg_buf_bytes(MS, HW);
-    rg_to_lds<MS, HW>(T, R, buf);
-    if (tt + kRgDepth < n_tiles) rg_load<MS, HW>(T, i0 + kRgDepth * kTileTokens, R);
+    rg_to_lds<MS, HW>(T, tid, R, buf);
+    if (tt + kRgDepth < n_tiles) rg_load<MS, HW>(T, tid, i0 + kRgDepth * kTileTokens, R);
     __syncthreads();
-    if (active) rg_compute<MS, ROT, HW, RELOC>(P, T, i0, h, wa, buf, s_freq, s_coord, s_dcs);
+    if (active) rg_compute<MS, ROT, HW, RELOC>(P, T, tid, i0, h, wa, buf, s_freq, s_coord, s_dcs);
     __syncthreads();
-    rg_store<HW>(P, T, t_begin, i0, buf, s_page);
+    rg_store<HW>(P, T, tid, t_begin, i0, buf, s_page);
   };
   for (int tile = 0; tile < n_tiles; tile += kRgDepth) {
 #pragma unroll
@@ -488,108 +494,222 @@ __device__ __forceinline__ void rg_run(const RehydrateParams& P, const RgTask& T
   }
 }
 
-// RELOC: the keys are already rotated and move by the chunk's delta
+// Start, in a lane's (chunk, layer, 16-token tile) space, of the r-th of g
+// pieces of equal weight.  Without a per-layer rank every tile weighs the
+// same; with one, a tile of layer l weighs the bytes it moves per token and
+// head, scaled by the tokens n of a unit: (512 + 2 r_l) n + 256 r_l -- the row
+// in and out, its U row and its share of the unit's W (r_l the layer's rank).
+// One wave's lanes take contiguous blocks of layers; a scan over the wave and
+// a ballot find the layer that holds the cut.
+__device__ __forceinline__ int64_t rg_cut(const RehydrateParams& P, const PlaneParams& Q, int64_t r, int tid) {
+  const int64_t T = P.unit_tiles;
+  const int L = P.n_layers;
+  if (Q.layer_rank == nullptr) return r * ((int64_t)P.n_chunks * L * T) / P.lane_wgs;
+  const int64_t n = T * kTileTokens;
+  auto weight = [&](int l) -> int64_t {
+    const int rk = min(max(Q.layer_rank[l], 0), Q.m);
+    return (512 + 2 * (int64_t)rk) * n + 256 * (int64_t)rk;
+  };
+  const int lane = tid & 63;
+  const int per = (L + 63) / 64;
+  const int lb = min(L, lane * per), le = min(L, lb + per);
+  int64_t own = 0;
+  for (int l = lb; l < le; ++l) own += weight(l);
+  int64_t incl = own;
+  for (int d = 1; d < 64; d <<= 1) {
+    const int64_t y = __shfl_up(incl, d);
+    if (lane >= d) incl += y;
+  }
+  const int64_t chunk_w = __shfl(incl, 63) * T;
+  const int64_t target = r * ((int64_t)P.n_chunks * chunk_w) / P.lane_wgs;
+  const int64_t c = target / chunk_w;
+  int64_t rem = target - c * chunk_w;
+  const uint64_t holds = __ballot(incl * T > rem);
+  const int owner = holds ? __builtin_ctzll(holds) : 63;
+  rem -= __shfl(incl - own, owner) * T;
+  int l = __shfl(lb, owner);
+  const int l_end = __shfl(le, owner);
+  while (l < l_end - 1 && rem >= weight(l) * T) {
+    rem -= weight(l) * T;
+    ++l;
+  }
+  const int64_t tile = min(rem / weight(l), T);
+  return (c * L + l) * T + tile;
+}
+
+// Persistent form.  Workgroup w serves lane w % lanes -- one (plane, group of
+// HW heads) -- and the (w / lanes)-th of lane_wgs equal, contiguous ranges of
+// that lane's (chunk, layer, 16-token tile) space, walked in segments of at
+// most one unit's tiles (and kRgMaxBlock tokens).  Every workgroup moves the
+// same bytes, so they all finish together, and a unit's set-up (W^T, page
+// numbers) is paid once per segment.  The workgroups of one range index are
+// adjacent in the grid and walk the same tiles at the same pace, so the planes
+// and head groups of a pool page are written together.
+// RELOC: the keys are already rotated and move by the chunk's delta.
 template <int MS, int HW, bool RELOC>
-__global__ __launch_bounds__(64 * HW, 8 / HW) void rehydrate_rows_kernel(const RehydrateParams /*by value, read in place*/) {
+__global__ __launch_bounds__(64 * HW, rg_min_waves(MS, HW)) void rehydrate_rows_kernel(const RehydrateParams /*by value, read in place*/) {
   const RehydrateParams& P = kernel_params<RehydrateParams>();
   extern __shared__ __align__(16) uint8_t lds_dyn[];
   __shared__ double s_freq[kMaxPairs];
   __shared__ int s_coord[kMaxPairs];
   __shared__ float s_dcs[2 * kMaxPairs];        // relocation: cos, sin of delta per pair
 
-  // Consecutive workgroups go to consecutive XCDs, and here consecutive tasks
-  // too: no two tasks share data that an XCD's L2 could keep, so the eight
-  // XCDs work side by side on neighbouring rows instead of on eight distant
-  // ranges (0.5-5% faster on the paged recalls than XCD-contiguous ranges).
-  const int64_t task = blockIdx.x;
-  if (task >= P.n_tasks) return;
-  // the planes (K, V) and head groups of one (chunk, layer, token block) are
-  // adjacent tasks
-  const int pl = (int)(task % P.n_planes);
-  int64_t rem = task / P.n_planes;
-  const int hg = (int)(rem % P.n_hgroups);
-  rem /= P.n_hgroups;
-  const int tb = (int)(rem % P.n_tblk);
-  rem /= P.n_tblk;
-  RgTask T;
-  T.Q = &P.plane[pl];
-  const PlaneParams& Q = *T.Q;
-  T.l = (int)(rem % P.n_layers);
-  T.c = (int)(rem / P.n_layers);
-  T.h0 = hg * HW;
-  T.H = min(HW, P.n_heads - T.h0);
-  T.n_c = chunk_len(P.place, T.c);
-  const int t_begin = tb * P.token_block;
-  if (t_begin >= T.n_c) return;                 // uniform: the whole workgroup leaves
-  const int t_end = min(t_begin + P.token_block, T.n_c);
-  T.t_end = t_end;
-  T.m = Q.m;
-  if (Q.layer_rank != nullptr) {
-    const int r = Q.layer_rank[T.l];
-    T.m = r < 0 ? 0 : (r < Q.m ? r : Q.m);
+  const int half = P.rope.rope_dim / 2;          // 0 when no plane rotates
+  for (int j = threadIdx.x; j < half; j += 64 * HW) {
+    s_freq[j] = P.rope.rev_freq[j];
+    s_coord[j] = P.rope.coord[j];
   }
-  T.m_steps = (T.m + 31) / 32;
-  T.in_head_major = Q.in_s[3] > Q.in_s[2];
-  T.out_head_major = Q.out_s[3] > Q.out_s[2];
-  T.s_in2 = (int)Q.in_s[2];
-  T.s_in3 = (int)Q.in_s[3];
-  T.s_u2 = (int)Q.u_s[2];
-  T.s_u3 = (int)Q.u_s[3];
-  T.s_o2 = (int)Q.out_s[2];
-  T.s_o3 = (int)Q.out_s[3];
-  // the slabs start at the workgroup's first head
-  T.rin = rg_rsrc(Q.in + (int64_t)T.c * Q.in_s[0] + (int64_t)T.l * Q.in_s[1] + (int64_t)T.h0 * Q.in_s[3],
-                  Q.in_rec - 2 * (int64_t)T.h0 * Q.in_s[3]);
-  T.ru = rg_rsrc(Q.U != nullptr ? Q.U + (int64_t)T.c * Q.u_s[0] + (int64_t)T.l * Q.u_s[1] + (int64_t)T.h0 * Q.u_s[2]
-                                : Q.in,
-                 Q.U != nullptr ? Q.u_rec - 2 * (int64_t)T.h0 * Q.u_s[2] : 0);
-  // paged: the layer's pool; dense: the chunk's rows from its row base on
-  const int64_t out_base = P.place.paged ? 0
-                           : (int64_t)T.c * Q.out_s[0] +
-                                 (int64_t)(P.place.row_base ? P.place.row_base[T.c] : 0) * Q.out_s[2];
-  T.rout = rg_rsrc(Q.out + out_base + (int64_t)T.l * Q.out_s[1] + (int64_t)T.h0 * Q.out_s[3],
-                   Q.out_rec - 2 * (int64_t)T.h0 * Q.out_s[3]);
-  T.cp0 = T.cp1 = T.cp2 = 0.0;
-  T.dt = T.dh = T.dw = 0.0;
-  if (RELOC) {
-    T.dt = (double)P.delta[3 * T.c];
-    T.dh = (double)P.delta[3 * T.c + 1];
-    T.dw = (double)P.delta[3 * T.c + 2];
+  // The segment cursor and the chunk s_dcs holds live in VGPRs across a
+  // segment (whose tile loop needs every scalar register); the uniform state
+  // of a segment is derived again from them and the launch parameters.
+  int32_t cur_lo, cur_hi, end_lo, end_hi, dcs_chunk_v = -1;
+  {
+    const int lanes = P.n_planes * P.n_hgroups;
+    const int64_t r = blockIdx.x / (uint32_t)lanes;
+    const PlaneParams& Q = P.plane[(blockIdx.x % (uint32_t)lanes) % P.n_planes];
+    const int64_t f0 = rg_cut(P, Q, r, threadIdx.x), f1 = rg_cut(P, Q, r + 1, threadIdx.x);
+    cur_lo = (int32_t)(uint32_t)f0;
+    cur_hi = (int32_t)(f0 >> 32);
+    end_lo = (int32_t)(uint32_t)f1;
+    end_hi = (int32_t)(f1 >> 32);
   }
-  if (P.chunk_pos != nullptr) {
-    T.cp0 = (double)P.chunk_pos[3 * T.c];
-    T.cp1 = (double)P.chunk_pos[3 * T.c + 1];
-    T.cp2 = (double)P.chunk_pos[3 * T.c + 2];
-  }
-  const int rot = (Q.blk[0].flags & kBlkRotate) ? (P.rope.pairing == 0 ? 1 : 2) : 0;
-  if (rot != 0) {
-    const int half = P.rope.rope_dim / 2;
-    for (int j = threadIdx.x; j < half; j += 64 * HW) {
-      s_freq[j] = P.rope.rev_freq[j];
-      s_coord[j] = P.rope.coord[j];
-      if constexpr (RELOC) {
-        const int sc = P.rope.coord[j];
-        float sn, cs;
-        sincos_rev(sc == 0 ? T.dt : (sc == 1 ? T.dh : T.dw), P.rope.rev_freq[j], sn, cs);
-        s_dcs[2 * j] = cs;
-        s_dcs[2 * j + 1] = sn;
+  for (;;) {
+    asm volatile("" : "+v"(cur_lo), "+v"(cur_hi), "+v"(end_lo), "+v"(end_hi), "+v"(dcs_chunk_v));
+    const int64_t f = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane(cur_hi) << 32) |
+                                (uint32_t)__builtin_amdgcn_readfirstlane(cur_lo));
+    const int64_t f_end = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane(end_hi) << 32) |
+                                    (uint32_t)__builtin_amdgcn_readfirstlane(end_lo));
+    const int dcs_chunk = __builtin_amdgcn_readfirstlane(dcs_chunk_v);
+    if (f >= f_end) break;
+    const int lanes = P.n_planes * P.n_hgroups;
+    const int lane = (int)(blockIdx.x % (uint32_t)lanes);
+    const int pl = lane % P.n_planes;
+    const int hg = lane / P.n_planes;
+    const PlaneParams& Q = P.plane[pl];
+    const int rot = (Q.blk[0].flags & kBlkRotate) ? (P.rope.pairing == 0 ? 1 : 2) : 0;
+    const int64_t cl = f / P.unit_tiles;
+    const int tile0 = (int)(f - cl * P.unit_tiles);
+    int64_t tile1 = min((int64_t)P.unit_tiles, (int64_t)tile0 + (f_end - f));
+    tile1 = min(tile1, (int64_t)tile0 + kRgMaxBlock / kTileTokens);
+    {
+      const int64_t next = f + (tile1 - tile0);
+      cur_lo = (int32_t)(uint32_t)next;
+      cur_hi = (int32_t)(next >> 32);
+    }
+    RgTask T;
+    T.Q = &Q;
+    T.l = (int)(cl % P.n_layers);
+    T.c = (int)(cl / P.n_layers);
+    T.h0 = hg * HW;
+    T.H = min(HW, P.n_heads - T.h0);
+    T.n_c = chunk_len(P.place, T.c);
+    const int t_begin = tile0 * kTileTokens;
+    if (t_begin >= T.n_c) continue;             // uniform: the whole workgroup skips
+    // the thread index as a value the compiler cannot see through: what is
+    // derived from it is derived again per segment instead of held in
+    // registers across the segment loop
+    int tid = threadIdx.x;
+    asm volatile("" : "+v"(tid));
+    const int t_end = min((int)tile1 * kTileTokens, T.n_c);
+    T.t_end = t_end;
+    T.m = Q.m;
+    if (Q.layer_rank != nullptr) {
+      const int lr = Q.layer_rank[T.l];
+      T.m = lr < 0 ? 0 : (lr < Q.m ? lr : Q.m);
+    }
+    T.m_steps = (T.m + 31) / 32;
+    T.in_head_major = Q.in_s[3] > Q.in_s[2];
+    T.out_head_major = Q.out_s[3] > Q.out_s[2];
+    T.s_in2 = (int)Q.in_s[2];
+    T.s_in3 = (int)Q.in_s[3];
+    T.s_u2 = (int)Q.u_s[2];
+    T.s_u3 = (int)Q.u_s[3];
+    T.s_o2 = (int)Q.out_s[2];
+    T.s_o3 = (int)Q.out_s[3];
+    // the slabs start at the workgroup's first head
+    T.rin = rg_rsrc(Q.in + (int64_t)T.c * Q.in_s[0] + (int64_t)T.l * Q.in_s[1] + (int64_t)T.h0 * Q.in_s[3],
+                    Q.in_rec - 2 * (int64_t)T.h0 * Q.in_s[3]);
+    T.ru = rg_rsrc(Q.U != nullptr ? Q.U + (int64_t)T.c * Q.u_s[0] + (int64_t)T.l * Q.u_s[1] +
+                                        (int64_t)T.h0 * Q.u_s[2]
+                                  : Q.in,
+                   Q.U != nullptr ? Q.u_rec - 2 * (int64_t)T.h0 * Q.u_s[2] : 0);
+    // paged: the layer's pool; dense: the chunk's rows from its row base on
+    const int64_t out_base = P.place.paged ? 0
+                             : (int64_t)T.c * Q.out_s[0] +
+                                   (int64_t)(P.place.row_base ? P.place.row_base[T.c] : 0) * Q.out_s[2];
+    T.rout = rg_rsrc(Q.out + out_base + (int64_t)T.l * Q.out_s[1] + (int64_t)T.h0 * Q.out_s[3],
+                     Q.out_rec - 2 * (int64_t)T.h0 * Q.out_s[3]);
+    T.cp0 = T.cp1 = T.cp2 = 0.0;
+    T.dt = T.dh = T.dw = 0.0;
+    if (RELOC) {
+      T.dt = (double)P.delta[3 * T.c];
+      T.dh = (double)P.delta[3 * T.c + 1];
+      T.dw = (double)P.delta[3 * T.c + 2];
+      if (rot != 0 && T.c != dcs_chunk) {
+        // read only after the next barrier; the previous segment's reads
+        // ended before the barrier that closed it
+        for (int j = threadIdx.x; j < half; j += 64 * HW) {
+          const int sc = P.rope.coord[j];
+          float sn, cs;
+          sincos_rev(sc == 0 ? T.dt : (sc == 1 ? T.dh : T.dw), P.rope.rev_freq[j], sn, cs);
+          s_dcs[2 * j] = cs;
+          s_dcs[2 * j + 1] = sn;
+        }
+        dcs_chunk_v = T.c;
       }
     }
+    if (P.chunk_pos != nullptr) {
+      T.cp0 = (double)P.chunk_pos[3 * T.c];
+      T.cp1 = (double)P.chunk_pos[3 * T.c + 1];
+      T.cp2 = (double)P.chunk_pos[3 * T.c + 2];
+    }
+    switch (rot) {
+      case 0: rg_run<MS, 0, HW, RELOC>(P, T, tid, t_begin, t_end, lds_dyn, s_freq, s_coord, s_dcs); break;
+      case 1: rg_run<MS, 1, HW, RELOC>(P, T, tid, t_begin, t_end, lds_dyn, s_freq, s_coord, s_dcs); break;
+      default: rg_run<MS, 2, HW, RELOC>(P, T, tid, t_begin, t_end, lds_dyn, s_freq, s_coord, s_dcs); break;
+    }
+    __syncthreads();                            // LDS (tiles, W^T, pages, s_dcs) free for the next segment
   }
-  switch (rot) {
-    case 0: rg_run<MS, 0, HW, RELOC>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord, s_dcs); break;
-    case 1: rg_run<MS, 1, HW, RELOC>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord, s_dcs); break;
-    default: rg_run<MS, 2, HW, RELOC>(P, T, t_begin, t_end, lds_dyn, s_freq, s_coord, s_dcs); break;
-  }
+}
+
+// Workgroups of one instantiation that the device holds at once (all CUs),
+// asked once per device.
+template <int MS, int HW, bool RELOC>
+hipError_t rows_resident(int dev, int& resident) {
+  static std::atomic<int> cache[kMaxDevices];
+  const bool cached = dev >= 0 && dev < kMaxDevices;
+  if (cached && (resident = cache[dev].load(std::memory_order_acquire)) > 0) return hipSuccess;
+  int per_cu = 0, cus = 0;
+  hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, rehydrate_rows_kernel<MS, HW, RELOC>, 64 * HW,
+                                                              rg_lds_bytes(MS, HW));
+  if (e != hipSuccess) return e;
+  e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return e;
+  resident = per_cu * cus > 0 ? per_cu * cus : 1;
+  if (cached) cache[dev].store(resident, std::memory_order_release);
+  return hipSuccess;
 }
 
 template <int MS, int HW, bool RELOC>
 hipError_t launch_rows(const RehydrateParams& p, hipStream_t s) {
   static std::atomic<bool> lds_set[kMaxDevices];
-  const hipError_t e = ensure_lds_limit((const void*)rehydrate_rows_kernel<MS, HW, RELOC>, rg_lds_bytes(MS, HW), lds_set);
+  hipError_t e = ensure_lds_limit((const void*)rehydrate_rows_kernel<MS, HW, RELOC>, rg_lds_bytes(MS, HW), lds_set);
   if (e != hipSuccess) return e;
-  const dim3 grid((uint32_t)((int64_t)p.per_xcd * 8)), block(64 * HW);
-  hipLaunchKernelGGL((rehydrate_rows_kernel<MS, HW, RELOC>), grid, block, rg_lds_bytes(MS, HW), s, p);
+  int dev = 0, resident = 0;
+  e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  e = rows_resident<MS, HW, RELOC>(dev, resident);
+  if (e != hipSuccess) return e;
+  // one resident wave of workgroups (or the caller's cap), at least one tile each
+  if (p.max_wgs > 0 && p.max_wgs < resident) resident = p.max_wgs;
+  const int lanes = p.n_planes * p.n_hgroups;
+  const int64_t per_lane = (int64_t)p.n_chunks * p.n_layers * p.unit_tiles;
+  int64_t g = resident / lanes > 0 ? resident / lanes : 1;
+  g = g < per_lane ? g : per_lane;
+  RehydrateParams q = p;
+  q.lane_wgs = (int32_t)g;
+  const dim3 grid((uint32_t)(lanes * g)), block(64 * HW);
+  hipLaunchKernelGGL((rehydrate_rows_kernel<MS, HW, RELOC>), grid, block, rg_lds_bytes(MS, HW), s, q);
   return hipGetLastError();
 }
 

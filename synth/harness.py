@@ -141,11 +141,12 @@ def _u_rows(shape, std, gen, arena: _Arena, token_major: bool):
 
 def prepare(name: str, device="cuda", seed: Optional[int] = None, unit_major: bool = True,
             pool_head_major: bool = False, u_token_major: bool = False,
-            separate_pools: bool = False, arena: bool = True) -> Prepared:
+            separate_pools: bool = False, arena: bool = True, kernel: int = 0) -> Prepared:
     """Device tensors and the prepared call of one workload.  The paged pool
     and the relocation window hold K and V interleaved by rows (one tensor
     [.., slot or token, K|V, H, D]) unless ``separate_pools``; the inputs,
-    factors and outputs are carved from one allocation unless not ``arena``."""
+    factors and outputs are carved from one allocation unless not ``arena``.
+    ``kernel`` is the rehydrate kernel requested (0: the library's choice)."""
     import torch
 
     import paper_2606_23581_amd as km
@@ -263,7 +264,7 @@ def prepare(name: str, device="cuda", seed: Optional[int] = None, unit_major: bo
     if w.has_v:
         kw.update(v_in=T["v_in"], v_out=v_out, u_v=T.get("u_v"), w_v=T.get("w_v"),
                   v_patch=(w.patch_offset, w.patch_dim))
-    call = km.prepare_rehydrate(T["k_in"], k_out, **kw)
+    call = km.prepare_rehydrate(T["k_in"], k_out, kernel=kernel, **kw)
 
     def step():
         call.launch()

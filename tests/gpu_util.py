@@ -101,6 +101,7 @@ class RehydrateCase:
     kv_interleaved: bool = False       # K and V outputs in one tensor [L, rows, K|V, H, D]
     kernel: int = 0                    # kamera_kernel_choice requested (0: AUTO)
     plan: Optional[int] = None         # kernel kamera_rehydrate_plan must report for the case
+    max_workgroups: int = 0            # cap on the launch's workgroups (long segments per workgroup)
     seed: int = 0
 
 
@@ -204,7 +205,8 @@ def run_rehydrate(case: RehydrateCase, device):
               pos_mode={"linear": km.POS_LINEAR, "grid3": km.POS_GRID3, "explicit": km.POS_EXPLICIT}[case.pos_mode],
               grid_w=case.grid_w, chunk_pos=dev_i32(pos, device),
               explicit_pos=dev_i32(explicit, device) if explicit is not None else None,
-              chunk_tokens=dev_i32(n_c, device) if case.ragged else None, kernel=case.kernel)
+              chunk_tokens=dev_i32(n_c, device) if case.ragged else None, kernel=case.kernel,
+              max_workgroups=case.max_workgroups)
     status = dev_i32(np.zeros(1), device)
     kw["status"] = status
     if case.reloc:

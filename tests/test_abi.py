@@ -67,7 +67,7 @@ def test_plain_c_consumer(tmp_path):
 
 def test_version_and_struct_layout():
     L = km.lib()
-    assert L.kamera_abi_version() == 2
+    assert L.kamera_abi_version() == 3
     assert L.kamera_struct_size(0) == ctypes.sizeof(km.CRehydrateArgs)
     assert L.kamera_struct_size(1) == ctypes.sizeof(km.CShiftArgs)
     assert L.kamera_struct_size(2) == ctypes.sizeof(km.CScatterArgs)
@@ -144,11 +144,13 @@ def _plan_case(case):
         if case == "auto_recall_relocation":
             a.delta = FAKE + 0x300000000
         C, Ln, H, n = {"auto_recall": (64, 80, 8, 1024), "auto_recall_relocation": (64, 80, 8, 1024),
-                       "auto_recall_128_token_chunks": (64, 80, 8, 128), "auto_2_22_rows": (16, 32, 4, 1024),
-                       "auto_below_2_22_rows": (16, 32, 4, 1023),
+                       "auto_recall_128_token_chunks": (64, 80, 8, 128), "auto_dense_window": (16, 32, 4, 1024),
+                       "auto_dense_window_rank_64": (16, 32, 4, 1024),
+                       "auto_dense_window_low_end": (8, 32, 4, 1024), "auto_below_dense_window": (8, 32, 4, 1023),
                        "row_group_8_heads": (2, 3, 8, 64), "auto_recall_4_heads": (64, 80, 4, 1024),
                        "auto_recall_short_chunks": (64, 80, 8, 256), "auto_mid_8_heads": (16, 32, 8, 1024),
-                       "auto_mid_4_heads": (16, 32, 4, 1024), "auto_small_8_heads": (8, 28, 8, 1024),
+                       "auto_reorder_shape": (8, 28, 4, 1024), "auto_small_8_heads": (8, 28, 8, 1024),
+                       "auto_2_19_rows": (4, 16, 4, 1024), "auto_below_2_19_rows": (4, 16, 4, 1023),
                        "auto_6_heads": (64, 80, 6, 1024)}[case]
         a.n_chunks, a.n_layers, a.n_heads, a.n_tokens = C, Ln, H, n
         for p in range(2):
@@ -158,6 +160,13 @@ def _plan_case(case):
             for k in range(4):
                 a.plane[p].in_stride[k] = a.plane[p].out_stride[k] = strides[k]
                 a.plane[p].u_stride[k], a.plane[p].w_stride[k] = us[k], ws[k]
+        if case == "auto_dense_window_rank_64":
+            for p in range(2):
+                a.plane[p].m = 64
+                a.plane[p].u_stride[0], a.plane[p].u_stride[1] = Ln * H * n * 64, H * n * 64
+                a.plane[p].u_stride[2], a.plane[p].u_stride[3] = n * 64, 64
+                a.plane[p].w_stride[0], a.plane[p].w_stride[1] = Ln * H * 64 * 128, H * 64 * 128
+                a.plane[p].w_stride[2] = 64 * 128
     elif case == "heads_9":
         a.n_heads = 9
     elif case == "rank_72":
@@ -199,12 +208,16 @@ def _plan_case(case):
     ("auto_recall_4_heads", km.PLAN_ROW_GROUP4),
     ("auto_recall_short_chunks", km.PLAN_ROW_GROUP4),
     ("auto_recall_128_token_chunks", km.PLAN_PER_HEAD),
-    ("auto_2_22_rows", km.PLAN_ROW_GROUP4),
-    ("auto_below_2_22_rows", km.PLAN_PER_HEAD),
+    ("auto_dense_window", km.PLAN_PER_HEAD),
+    ("auto_dense_window_rank_64", km.PLAN_ROW_GROUP4),
+    ("auto_dense_window_low_end", km.PLAN_PER_HEAD),
+    ("auto_below_dense_window", km.PLAN_ROW_GROUP4),
     ("auto_recall_relocation", km.PLAN_ROW_GROUP4),
     ("auto_mid_8_heads", km.PLAN_ROW_GROUP4),
-    ("auto_mid_4_heads", km.PLAN_ROW_GROUP4),
+    ("auto_reorder_shape", km.PLAN_ROW_GROUP4),
     ("auto_small_8_heads", km.PLAN_PER_HEAD),
+    ("auto_2_19_rows", km.PLAN_ROW_GROUP4),
+    ("auto_below_2_19_rows", km.PLAN_PER_HEAD),
     ("auto_6_heads", km.PLAN_PER_HEAD),
     ("heads_9", km.PLAN_PER_HEAD),
     ("rank_72", km.PLAN_PER_HEAD),
@@ -225,7 +238,8 @@ def test_rehydrate_plan_picks_the_kernel(case, plan):
     explicit positions, and every byte offset below 2^31, with 8 heads per
     workgroup for wider rows and 4 for rows of <= 4 heads; AUTO takes it, with
     4 heads per workgroup, for rows of 4 or 8 heads, chunks of >= 256 tokens
-    and >= 2^22 rows (planes x chunks x layers x tokens x heads)."""
+    and >= 2^19 rows (planes x chunks x layers x tokens x heads), except dense
+    outputs at rank <= 32 with 2^21 to 2^23 rows."""
     a = _plan_case(case)
     assert km.lib().kamera_rehydrate_plan(ctypes.byref(a)) == plan
     assert km.lib().kamera_validate(0, ctypes.byref(a)) == min(plan, 0)

@@ -142,15 +142,37 @@ REHYDRATE_CASES = {
     "per_head_9_heads_paged": RehydrateCase(H=9, paged=True, kernel=2, plan=1, seed=63),
     # relocation above rank 64 on the per-head kernel: the two-rotation form
     # R(p)(R(delta - p) K + U W) (rank steps of 4 x 32), both frames
-    "relocate_rank_72_per_head": RehydrateCase(reloc=True, m_k=72, m_v=8, n=70, kernel=1, plan=1, seed=66),
+    # few workgroups: each walks many tiles, crossing (chunk, layer) units,
+    # ragged chunk ends and the 1024-token segment limit
+    "rows4_few_workgroups_paged": RehydrateCase(H=8, C=3, L=3, n=300, ragged=True, paged=True, m_k=64, m_v=32,
+                                                sections=(16, 24, 24), pos_mode="grid3", grid_w=20, kernel=3,
+                                                plan=3, max_workgroups=6, seed=84),
+    "rows8_two_workgroups_long_chunk": RehydrateCase(H=8, C=2, L=2, n=1500, unit_major=True, m_k=16, m_v=16,
+                                                     kernel=2, plan=2, max_workgroups=2, seed=85),
+    "rows4_reloc_few_workgroups": RehydrateCase(H=4, C=3, L=2, n=200, reloc=True, m_k=64, m_v=64, kernel=3,
+                                                plan=3, max_workgroups=3, seed=86),
+    "rows4_one_workgroup_per_lane": RehydrateCase(H=8, C=2, L=3, n=130, m_k=32, m_v=0, paged=True, kernel=3,
+                                                  plan=3, max_workgroups=4, seed=87),
+    "per_head_few_workgroups_mla_band": RehydrateCase(D=576, H=1, C=2, L=3, n=300, rope_dim=64, rope_offset=512,
+                                                      pairing="interleaved", theta=1e4, patch=(0, 512), m_k=32,
+                                                      m_pe=8, has_v=False, kernel=1, plan=1, max_workgroups=3,
+                                                      seed=88),
+    "per_head_few_workgroups_layer_rank": RehydrateCase(H=3, L=4, layer_rank=(0, 64, 5, 33), m_k=64, m_v=40,
+                                                        ragged=True, C=3, n=150, paged=True, kernel=1, plan=1,
+                                                        max_workgroups=5, seed=89),
+    "per_head_one_workgroup": RehydrateCase(H=2, C=2, L=2, n=90, sections=(16, 24, 24), pos_mode="grid3", grid_w=9,
+                                            kernel=1, plan=1, max_workgroups=1, seed=90),
+    "per_head_reloc_two_workgroups": RehydrateCase(H=5, C=2, L=2, n=120, reloc=True, m_k=16, m_v=24, kernel=1,
+                                                   plan=1, max_workgroups=2, seed=91),
+    "relocate_rank_72_per_head": RehydrateCase(reloc=True, m_k=72, m_v=8, n=70, kernel=1, plan=1, seed=80),
     "relocate_rank_72_post_frame_paged": RehydrateCase(reloc=True, m_k=72, m_v=72, post_rope=True, paged=True,
                                                        pairing="interleaved", theta=1e4, n=50, kernel=1, plan=1,
-                                                       seed=67),
+                                                       seed=81),
     "relocate_rank_128_per_head": RehydrateCase(reloc=True, m_k=128, m_v=128, n=48, C=1, L=1, H=2, kernel=1, plan=1,
-                                                seed=68),
+                                                seed=82),
     "relocate_rank_128_post_frame_mrope": RehydrateCase(reloc=True, m_k=128, m_v=100, post_rope=True,
                                                         sections=(16, 24, 24), pos_mode="grid3", grid_w=8, n=40,
-                                                        C=2, L=1, H=2, kernel=1, plan=1, seed=69),
+                                                        C=2, L=1, H=2, kernel=1, plan=1, seed=83),
 }
 
 

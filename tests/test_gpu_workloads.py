@@ -101,11 +101,12 @@ def test_workload_rehydrate(device, name):
     print(f"[case] workload {name}", flush=True)
     p = harness.prepare(name, device)
     # the kernel AUTO picks: row groups of 4 heads (two per 8-head row) for the
-    # recalls and the window survivors, per head elsewhere
+    # recalls, the reorder and the window survivors, per head elsewhere
     plan = {"gqa80l_64x1024_m64_mrope_paged": km.PLAN_ROW_GROUP4,
             "gqa80l_64x1024_m64_mrope_paged_deephalf": km.PLAN_ROW_GROUP4,
             "gqa32l_16x1024_m32_mrope_paged": km.PLAN_ROW_GROUP4,
-            "gqa36l_15x1024_survivor_m64": km.PLAN_ROW_GROUP4}
+            "gqa36l_15x1024_survivor_m64": km.PLAN_ROW_GROUP4,
+            "gqa28l_8x1024_m16_reorder": km.PLAN_ROW_GROUP4}
     assert km.rehydrate_plan(p.extra["call"]) == plan.get(name, km.PLAN_PER_HEAD)
     units = harness.sample_units(p.workload, 12 if p.workload.units() > 12 else p.workload.units(), seed=1)
     if p.workload.n_heads == 8:
