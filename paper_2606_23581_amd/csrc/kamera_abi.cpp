@@ -8,6 +8,8 @@
 #include <string.h>
 
 #include <algorithm>
+#include <cstdint>
+#include <initializer_list>
 #include <vector>
 
 #include "kamera.h"
@@ -48,8 +50,8 @@ int check_rope(const kamera_rope& r, int32_t head_dim, const char* who) {
   if (r.rope_dim > KAMERA_MAX_ROPE_DIM)
     return fail(KAMERA_ERR_RANGE, "%s: rope.rope_dim %d exceeds %d", who, r.rope_dim, KAMERA_MAX_ROPE_DIM);
   if (r.rope_offset < 0 || (int64_t)r.rope_offset + r.rope_dim > head_dim)
-    return fail(KAMERA_ERR_SHAPE, "%s: rope band [%d, %d) lies outside the %d-column row", who,
-                r.rope_offset, r.rope_offset + r.rope_dim, head_dim);
+    return fail(KAMERA_ERR_SHAPE, "%s: rope band [%d, %lld) lies outside the %d-column row", who,
+                r.rope_offset, (long long)r.rope_offset + r.rope_dim, head_dim);
   if (r.pairing != KAMERA_PAIR_NEOX && r.pairing != KAMERA_PAIR_INTERLEAVED)
     return fail(KAMERA_ERR_SHAPE, "%s: unknown rope.pairing %d", who, r.pairing);
   if (r.n_sections != 1 && r.n_sections != 3)
@@ -130,31 +132,44 @@ bool strides_ok(const int64_t* s, int n) {
   return true;
 }
 
-// byte range [lo, hi) spanned by a 4-D strided bf16 view with the given extents
-void extent(const void* base, const int64_t* s, const int64_t* ext, int64_t row_elems, uintptr_t& lo,
-            uintptr_t& hi) {
-  int64_t a = 0, b = 0;
-  for (int k = 0; k < 4; ++k) {
-    if (ext[k] <= 0) continue;
-    const int64_t d = (ext[k] - 1) * s[k];
-    if (d < 0) a += d; else b += d;
+// Largest work a call may describe (elements, rows or tasks): far beyond any
+// device, and small enough that the host arithmetic on it cannot overflow.
+constexpr int64_t kMaxWork = (int64_t)1 << 50;
+
+// product of non-negative factors, or -1 once it exceeds kMaxWork
+int64_t bounded_product(std::initializer_list<int64_t> factors) {
+  __int128 p = 1;
+  for (const int64_t f : factors) {
+    if (f < 0) return -1;
+    p *= f;
+    if (p > kMaxWork) return -1;
   }
-  lo = reinterpret_cast<uintptr_t>(base) + a * 2;
-  hi = reinterpret_cast<uintptr_t>(base) + (b + row_elems) * 2;
+  return (int64_t)p;
 }
 
-// byte range [lo, hi) of an n-D strided view (element strides, elem_bytes each)
-// whose innermost rows are row_elems contiguous elements
-void span(const void* base, const int64_t* s, const int64_t* ext, int nd, int64_t row_elems, int elem_bytes,
+// byte range [lo, hi) of an n-D strided view (element strides, elem_bytes
+// each) whose innermost rows are row_elems contiguous elements; false when
+// the range does not fit in the address space (the arithmetic is 128-bit)
+bool span(const void* base, const int64_t* s, const int64_t* ext, int nd, int64_t row_elems, int elem_bytes,
           uintptr_t& lo, uintptr_t& hi) {
-  int64_t a = 0, b = 0;
+  __int128 a = 0, b = 0;
   for (int k = 0; k < nd; ++k) {
     if (ext[k] <= 0) continue;
-    const int64_t d = (ext[k] - 1) * s[k];
+    const __int128 d = (__int128)(ext[k] - 1) * s[k];
     if (d < 0) a += d; else b += d;
   }
-  lo = reinterpret_cast<uintptr_t>(base) + a * elem_bytes;
-  hi = reinterpret_cast<uintptr_t>(base) + (b + row_elems) * elem_bytes;
+  const __int128 p = (__int128)reinterpret_cast<uintptr_t>(base);
+  const __int128 l = p + a * elem_bytes, h = p + (b + row_elems) * elem_bytes;
+  if (l < 0 || h > (__int128)UINTPTR_MAX) return false;
+  lo = (uintptr_t)l;
+  hi = (uintptr_t)h;
+  return true;
+}
+
+// the same for a 4-D bf16 view
+bool extent(const void* base, const int64_t* s, const int64_t* ext, int64_t row_elems, uintptr_t& lo,
+            uintptr_t& hi) {
+  return span(base, s, ext, 4, row_elems, 2, lo, hi);
 }
 
 bool overlap(uintptr_t a0, uintptr_t a1, uintptr_t b0, uintptr_t b1) { return a0 < b1 && b0 < a1; }
@@ -188,12 +203,12 @@ static bool interleaved_rows(const kamera_rehydrate_args* a, const void* b0, con
     if (s0[k] < 0) return false;
   const int64_t r = s0[2];
   if (r <= 0 || s0[1] % r != 0 || (chunk_stride_used && s0[0] % r != 0)) return false;
-  const int64_t span = (int64_t)(a->n_heads - 1) * s0[3] + a->head_dim;
+  const __int128 row_span = (__int128)(a->n_heads - 1) * s0[3] + a->head_dim;
   const uintptr_t p0 = (uintptr_t)b0, p1 = (uintptr_t)b1;
   const uintptr_t gap = p0 > p1 ? p0 - p1 : p1 - p0;
   if (gap % 2 != 0) return false;
-  const int64_t d = (int64_t)(gap / 2);
-  return span <= d && d + span <= r;
+  const __int128 d = (__int128)(gap / 2);
+  return row_span <= d && d + row_span <= r;
 }
 
 // Validation and kernel parameters of a rehydrate call; *launch is false for
@@ -252,8 +267,8 @@ static int build_rehydrate(const kamera_rehydrate_args* a, kamera::RehydratePara
     if (q.rotate != 0 && q.rotate != 1) return fail(KAMERA_ERR_SHAPE, "%s: plane %d rotate must be 0 or 1", who, p);
     if (q.m > 0) {
       if (q.patch_offset < 0 || q.patch_dim <= 0 || (int64_t)q.patch_offset + q.patch_dim > a->head_dim)
-        return fail(KAMERA_ERR_SHAPE, "%s: plane %d patch columns [%d, %d) outside the %d-column row", who, p,
-                    q.patch_offset, q.patch_offset + q.patch_dim, a->head_dim);
+        return fail(KAMERA_ERR_SHAPE, "%s: plane %d patch columns [%d, %lld) outside the %d-column row", who, p,
+                    q.patch_offset, (long long)q.patch_offset + q.patch_dim, a->head_dim);
       if (q.patch_offset % 8 != 0 || q.patch_dim % 8 != 0)
         return fail(KAMERA_ERR_UNSUPPORTED, "%s: plane %d patch columns must start/end on multiples of 8", who, p);
     }
@@ -261,7 +276,8 @@ static int build_rehydrate(const kamera_rehydrate_args* a, kamera::RehydratePara
   int rc = check_paging(a->paged, a->page_table, a->pt_stride, a->page_size, a->n_pool_pages, a->n_tokens, who);
   if (rc) return rc;
 
-  const int64_t work = (int64_t)a->n_chunks * a->n_layers * a->n_heads * a->n_tokens;
+  const int64_t work = bounded_product({a->n_chunks, a->n_layers, a->n_heads, a->n_tokens});
+  if (work < 0) return fail(KAMERA_ERR_RANGE, "%s: chunks x layers x heads x tokens exceeds 2^50", who);
   if (work == 0) return KAMERA_OK;  // empty call: nothing to read or write
 
   if (any_rot && a->pos_mode != KAMERA_POS_EXPLICIT && a->chunk_pos == nullptr)
@@ -282,16 +298,14 @@ static int build_rehydrate(const kamera_rehydrate_args* a, kamera::RehydratePara
     const kamera_plane& q = a->plane[p];
     const int64_t ein[4] = {a->n_chunks, a->n_layers, a->n_tokens, a->n_heads};
     uintptr_t ilo, ihi;
-    extent(q.in, q.in_stride, ein, a->head_dim, ilo, ihi);
+    if (!extent(q.in, q.in_stride, ein, a->head_dim, ilo, ihi))
+      return fail(KAMERA_ERR_RANGE, "%s: plane %d input strides span more than the address space", who, p);
     for (int o = 0; o < a->n_planes; ++o) {
       const kamera_plane& r = a->plane[o];
       uintptr_t olo, ohi;
-      if (a->paged) {
-        const int64_t eo[4] = {1, a->n_layers, (int64_t)a->n_pool_pages * a->page_size, a->n_heads};
-        extent(r.out, r.out_stride, eo, a->head_dim, olo, ohi);
-      } else {
-        extent(r.out, r.out_stride, ein, a->head_dim, olo, ohi);
-      }
+      const int64_t eo[4] = {1, a->n_layers, (int64_t)a->n_pool_pages * a->page_size, a->n_heads};
+      if (!extent(r.out, r.out_stride, a->paged ? eo : ein, a->head_dim, olo, ohi))
+        return fail(KAMERA_ERR_RANGE, "%s: plane %d output strides span more than the address space", who, o);
       // Exact in place is allowed: same base and strides, dense rows, no row
       // base -- every element is then read and written by the workgroup that
       // owns it, provided two different planes cover disjoint columns.
@@ -316,9 +330,10 @@ static int build_rehydrate(const kamera_rehydrate_args* a, kamera::RehydratePara
     const kamera_plane& q1 = a->plane[1];
     const int64_t e_dense[4] = {a->n_chunks, a->n_layers, a->n_tokens, a->n_heads};
     const int64_t e_pool[4] = {1, a->n_layers, (int64_t)a->n_pool_pages * a->page_size, a->n_heads};
-    uintptr_t lo0, hi0, lo1, hi1;
-    extent(q0.out, q0.out_stride, a->paged ? e_pool : e_dense, a->head_dim, lo0, hi0);
-    extent(q1.out, q1.out_stride, a->paged ? e_pool : e_dense, a->head_dim, lo1, hi1);
+    uintptr_t lo0 = 0, hi0 = 0, lo1 = 0, hi1 = 0;
+    if (!extent(q0.out, q0.out_stride, a->paged ? e_pool : e_dense, a->head_dim, lo0, hi0) ||
+        !extent(q1.out, q1.out_stride, a->paged ? e_pool : e_dense, a->head_dim, lo1, hi1))
+      return fail(KAMERA_ERR_RANGE, "%s: output strides span more than the address space", who);
     if (overlap(lo0, hi0, lo1, hi1)) {
       const bool same_map = q0.out == q1.out && memcmp(q0.out_stride, q1.out_stride, sizeof(q0.out_stride)) == 0;
       const int b0 = q0.col_begin, e0 = (q0.col_begin == 0 && q0.col_end == 0) ? a->head_dim : q0.col_end;
@@ -435,12 +450,12 @@ static int build_rehydrate(const kamera_rehydrate_args* a, kamera::RehydratePara
     // the buffer instructions of that kernel take 32-bit byte offsets within
     // one (chunk, layer) slab (dense output: from the chunk's row base on), or
     // within one layer of the pool
-    const int64_t n1 = a->n_tokens - 1, h1 = a->n_heads - 1;
-    const int64_t in_rec = (n1 * o.in_s[2] + h1 * o.in_s[3] + 128) * 2;
-    const int64_t u_rec = o.m > 0 ? (h1 * o.u_s[2] + n1 * o.u_s[3] + o.m) * 2 : 0;
-    const int64_t rows_out = a->paged ? (int64_t)a->n_pool_pages * a->page_size - 1 : n1;
-    const int64_t out_rec = (rows_out * o.out_s[2] + h1 * o.out_s[3] + 128) * 2;
-    const int64_t lim = 0x7ffffff0;
+    const __int128 n1 = a->n_tokens - 1, h1 = a->n_heads - 1;
+    const __int128 in_rec = (n1 * o.in_s[2] + h1 * o.in_s[3] + 128) * 2;
+    const __int128 u_rec = o.m > 0 ? (h1 * o.u_s[2] + n1 * o.u_s[3] + o.m) * 2 : 0;
+    const __int128 rows_out = a->paged ? (__int128)a->n_pool_pages * a->page_size - 1 : n1;
+    const __int128 out_rec = (rows_out * o.out_s[2] + h1 * o.out_s[3] + 128) * 2;
+    const __int128 lim = 0x7ffffff0;
     rows = in_rec <= lim && u_rec <= lim && out_rec <= lim;
     o.in_rec = (int32_t)in_rec;
     o.u_rec = (int32_t)u_rec;
@@ -519,7 +534,8 @@ static int build_shift(const kamera_shift_args* a, kamera::ShiftParams& P, bool&
     return fail(KAMERA_ERR_UNSUPPORTED, "%s: interleaved pairing needs rope_dim %% 8 == 0", who);
   rc = check_paging(a->paged, a->page_table, a->pt_stride, a->page_size, a->n_pool_pages, a->n_tokens, who);
   if (rc) return rc;
-  const int64_t work = (int64_t)a->n_chunks * a->n_layers * a->n_heads * a->n_tokens;
+  const int64_t work = bounded_product({a->n_chunks, a->n_layers, a->n_heads, a->n_tokens});
+  if (work < 0) return fail(KAMERA_ERR_RANGE, "%s: chunks x layers x heads x tokens exceeds 2^50", who);
   if (work == 0) return KAMERA_OK;
   if (a->k == nullptr) return fail(KAMERA_ERR_NULL, "%s: k is NULL", who);
   if (a->delta == nullptr) return fail(KAMERA_ERR_NULL, "%s: delta is NULL", who);
@@ -576,7 +592,8 @@ static int build_scatter(const kamera_scatter_args* a, kamera::ScatterParams& P,
     return fail(KAMERA_ERR_ALIGN, "%s: row_bytes must be a positive multiple of 16", who);
   int rc = check_paging(1, a->page_table, a->pt_stride, a->page_size, a->n_pool_pages, a->n_tokens, who);
   if (rc) return rc;
-  const int64_t work = (int64_t)a->n_chunks * a->n_layers * a->n_tokens;
+  const int64_t work = bounded_product({a->n_chunks, a->n_layers, a->n_tokens, a->row_bytes / 16});
+  if (work < 0) return fail(KAMERA_ERR_RANGE, "%s: chunks x layers x tokens x row vectors exceeds 2^50", who);
   if (work == 0) return KAMERA_OK;
   if (a->rows == nullptr || a->pool == nullptr) return fail(KAMERA_ERR_NULL, "%s: rows or pool is NULL", who);
   for (int k = 0; k < 3; ++k)
@@ -585,21 +602,13 @@ static int build_scatter(const kamera_scatter_args* a, kamera::ScatterParams& P,
     if (a->pool_stride_bytes[k] % 16 != 0) return fail(KAMERA_ERR_ALIGN, "%s: pool strides must be multiples of 16", who);
   if (!aligned16(a->rows) || !aligned16(a->pool)) return fail(KAMERA_ERR_ALIGN, "%s: rows/pool must be 16-byte aligned", who);
   {
-    // the dense rows and the pool must be different memory
-    int64_t a0 = 0, b0 = 0;
+    // the dense rows and the pool must be different memory (byte strides)
     const int64_t ext[3] = {a->n_chunks, a->n_layers, a->n_tokens};
-    for (int k = 0; k < 3; ++k) {
-      const int64_t d = (ext[k] - 1) * a->rows_stride_bytes[k];
-      if (d < 0) a0 += d; else b0 += d;
-    }
-    const uintptr_t slo = reinterpret_cast<uintptr_t>(a->rows) + a0, shi = reinterpret_cast<uintptr_t>(a->rows) + b0 + a->row_bytes;
-    int64_t a1 = 0, b1 = 0;
     const int64_t pext[2] = {a->n_layers, (int64_t)a->n_pool_pages * a->page_size};
-    for (int k = 0; k < 2; ++k) {
-      const int64_t d = (pext[k] - 1) * a->pool_stride_bytes[k];
-      if (d < 0) a1 += d; else b1 += d;
-    }
-    const uintptr_t plo = reinterpret_cast<uintptr_t>(a->pool) + a1, phi = reinterpret_cast<uintptr_t>(a->pool) + b1 + a->row_bytes;
+    uintptr_t slo, shi, plo, phi;
+    if (!span(a->rows, a->rows_stride_bytes, ext, 3, a->row_bytes, 1, slo, shi) ||
+        !span(a->pool, a->pool_stride_bytes, pext, 2, a->row_bytes, 1, plo, phi))
+      return fail(KAMERA_ERR_RANGE, "%s: strides span more than the address space", who);
     if (overlap(slo, shi, plo, phi)) return fail(KAMERA_ERR_ALIAS, "%s: the dense rows overlap the pool", who);
   }
 
@@ -666,9 +675,9 @@ static int build_form(const kamera_form_args* a, kamera::FormParams& P, bool& la
   if (a->m < 1 || a->m > a->dim) return fail(KAMERA_ERR_RANGE, "%s: m = %d outside [1, dim]", who, a->m);
   if (a->sweeps < 0) return fail(KAMERA_ERR_SHAPE, "%s: sweeps must be >= 0", who);
   if (a->n_orbit < 0) return fail(KAMERA_ERR_SHAPE, "%s: n_orbit must be >= 0", who);
-  const int64_t units = (int64_t)a->n_chunks * a->n_layers * a->n_heads;
+  const int64_t units = bounded_product({a->n_chunks, a->n_layers, a->n_heads});
+  if (units < 0 || units > 0x7fffffff) return fail(KAMERA_ERR_RANGE, "%s: too many units", who);
   if (units == 0 || a->n_tokens == 0) return KAMERA_OK;
-  if (units > 0x7fffffff) return fail(KAMERA_ERR_RANGE, "%s: too many units", who);
   if (a->delta == nullptr || a->U == nullptr || a->W == nullptr)
     return fail(KAMERA_ERR_NULL, "%s: delta, U and W are required", who);
   if (!aligned16(a->delta))
@@ -685,18 +694,19 @@ static int build_form(const kamera_form_args* a, kamera::FormParams& P, bool& la
     const int64_t s_d[5] = {a->delta_stride[0], a->delta_stride[1], a->delta_stride[2], a->delta_stride[3],
                             n_orbit > 1 ? a->orbit_stride : 0};
     uintptr_t d0, d1;
-    span(a->delta, s_d, ext_d, 5, a->dim, 4, d0, d1);
     const int64_t ext_u[4] = {a->n_chunks, a->n_layers, a->n_heads, a->n_tokens};
     const int64_t ext_w[4] = {a->n_chunks, a->n_layers, a->n_heads, a->m};
     uintptr_t u0, u1, w0, w1;
-    span(a->U, a->u_stride, ext_u, 4, a->m, 2, u0, u1);
-    span(a->W, a->w_stride, ext_w, 4, a->dim, 2, w0, w1);
+    if (!span(a->delta, s_d, ext_d, 5, a->dim, 4, d0, d1) || !span(a->U, a->u_stride, ext_u, 4, a->m, 2, u0, u1) ||
+        !span(a->W, a->w_stride, ext_w, 4, a->dim, 2, w0, w1))
+      return fail(KAMERA_ERR_RANGE, "%s: strides span more than the address space", who);
     if (overlap(u0, u1, d0, d1) || overlap(w0, w1, d0, d1))
       return fail(KAMERA_ERR_ALIAS, "%s: U and W must not overlap the deficits", who);
     if (a->sigma != nullptr) {
       const int64_t ext_s[3] = {a->n_chunks, a->n_layers, a->n_heads};
       uintptr_t s0, s1;
-      span(a->sigma, a->sigma_stride, ext_s, 3, a->m, 4, s0, s1);
+      if (!span(a->sigma, a->sigma_stride, ext_s, 3, a->m, 4, s0, s1))
+        return fail(KAMERA_ERR_RANGE, "%s: sigma strides span more than the address space", who);
       if (overlap(s0, s1, d0, d1)) return fail(KAMERA_ERR_ALIAS, "%s: sigma must not overlap the deficits", who);
     }
     if (a->sweeps_done != nullptr) {
