@@ -54,7 +54,7 @@
 extern "C" {
 #endif
 
-#define KAMERA_ABI_VERSION 3
+#define KAMERA_ABI_VERSION 4
 
 /* Largest patch rank m accepted (>= the 128-wide head, so a full-rank patch
  * that reproduces any Delta K exactly can be applied). */
@@ -119,6 +119,23 @@ typedef enum {
   KAMERA_KERNEL_ROW_GROUP = 2,   /* 8 heads per workgroup (4 for rows of <= 4) */
   KAMERA_KERNEL_ROW_GROUP4 = 3   /* 4 heads per workgroup, also for wider rows */
 } kamera_kernel_choice;
+
+/* How the row-group kernel spreads its work over the device (same bits
+ * either way).  PERSISTENT: one resident wave of workgroups, each walking an
+ * equal share (in bytes moved) of its (plane, head group)'s 16-token tiles,
+ * so that a unit's set-up (W^T, page numbers) is paid once per long range
+ * and every workgroup finishes together.  BLOCKS: one workgroup per token
+ * block of one (plane, chunk, layer, head group), blocks of up to 1024 tokens
+ * shrunk (to >= 64) until the launch has 4096 of them (2048 with 8-head
+ * groups), handed out by the hardware as workgroups finish.  AUTO takes
+ * BLOCKS where those blocks stay >= 512 tokens (long launches, where it
+ * measured faster) and PERSISTENT otherwise, or whenever max_workgroups > 0.
+ * The per-head kernel ignores the field. */
+typedef enum {
+  KAMERA_SCHEDULE_AUTO = 0,
+  KAMERA_SCHEDULE_PERSISTENT = 1,
+  KAMERA_SCHEDULE_BLOCKS = 2
+} kamera_row_schedule;
 
 typedef enum {
   KAMERA_PATCH_PRE_ROPE = 0,  /* K' = R(pos)(K + U W): the patch lives in the
@@ -240,11 +257,15 @@ typedef struct {
   uint32_t* status;            /* optional device word, bits OR-ed in          */
   const int32_t* delta;        /* optional: relocation of rotated keys         */
   int32_t kernel;              /* kamera_kernel_choice (0: AUTO)               */
-  int32_t max_workgroups;      /* row-group kernel: 0 = one resident wave of
-                                  workgroups on the whole device, > 0 = at most
-                                  this many (leaves CUs to concurrent work);
-                                  same results.  The per-head kernel launches
-                                  one workgroup per task and ignores it.      */
+  int32_t max_workgroups;      /* row-group kernel, persistent schedule: 0 =
+                                  one resident wave of workgroups on the whole
+                                  device, > 0 = at most this many (leaves CUs
+                                  to concurrent work); same results.  Not
+                                  allowed with KAMERA_SCHEDULE_BLOCKS
+                                  (KAMERA_ERR_SHAPE).  The per-head kernel
+                                  launches one workgroup per task and ignores
+                                  it.                                         */
+  int32_t schedule;            /* kamera_row_schedule (0: AUTO)                */
 } kamera_rehydrate_args;
 
 /* kamera_shift -- K' = R(delta_c) K in place on the rope band of every token
@@ -391,6 +412,13 @@ int kamera_validate(int32_t which, const void* args);
 #define KAMERA_PLAN_ROW_GROUP 2
 #define KAMERA_PLAN_ROW_GROUP4 3
 int kamera_rehydrate_plan(const kamera_rehydrate_args* args);
+
+/* How the row-group kernel would spread a kamera_rehydrate call for `args`
+ * (see kamera_row_schedule), after exactly its host-side checks:
+ * KAMERA_SCHEDULE_PERSISTENT or KAMERA_SCHEDULE_BLOCKS; 0 when the call runs
+ * the per-head kernel or has nothing to do; else the negative error code the
+ * call would return.  Touches no device memory. */
+int kamera_rehydrate_schedule(const kamera_rehydrate_args* args);
 
 /* Text of the last error on the calling thread ("" after a successful call);
  * valid until the next call on that thread. */

@@ -57,6 +57,9 @@ PLAN_NONE = 0
 PLAN_PER_HEAD = 1
 PLAN_ROW_GROUP = 2
 PLAN_ROW_GROUP4 = 3
+SCHEDULE_AUTO = 0
+SCHEDULE_PERSISTENT = 1
+SCHEDULE_BLOCKS = 2
 
 
 class KameraUnavailable(RuntimeError):
@@ -99,7 +102,7 @@ class CRehydrateArgs(ctypes.Structure):
                 ("explicit_chunk_stride", _i64), ("n_planes", _i32), ("plane", CPlane * 2),
                 ("paged", _i32), ("row_base", _vp), ("page_table", _vp), ("pt_stride", _i32),
                 ("page_size", _i32), ("n_pool_pages", _i32), ("status", _vp), ("delta", _vp),
-                ("kernel", _i32), ("max_workgroups", _i32)]
+                ("kernel", _i32), ("max_workgroups", _i32), ("schedule", _i32)]
 
 
 class CShiftArgs(ctypes.Structure):
@@ -128,7 +131,8 @@ class CFormArgs(ctypes.Structure):
 EXPORTS = ("kamera_rehydrate", "kamera_shift", "kamera_scatter_paged", "kamera_gather_paged",
            "kamera_form_patch",
            "kamera_check_page_table",
-           "kamera_validate", "kamera_rehydrate_plan", "kamera_last_error", "kamera_abi_version",
+           "kamera_validate", "kamera_rehydrate_plan", "kamera_rehydrate_schedule", "kamera_last_error",
+           "kamera_abi_version",
            "kamera_struct_size")
 
 _LIB = None
@@ -179,6 +183,8 @@ def lib() -> ctypes.CDLL:
     L.kamera_validate.restype = _i32
     L.kamera_rehydrate_plan.argtypes = [ctypes.POINTER(CRehydrateArgs)]
     L.kamera_rehydrate_plan.restype = _i32
+    L.kamera_rehydrate_schedule.argtypes = [ctypes.POINTER(CRehydrateArgs)]
+    L.kamera_rehydrate_schedule.restype = _i32
     L.kamera_struct_size.argtypes = [_i32]
     L.kamera_struct_size.restype = _i64
     sizes = {0: CRehydrateArgs, 1: CShiftArgs, 2: CScatterArgs, 3: CPlane, 4: CRope, 5: CFormArgs}
@@ -330,6 +336,15 @@ def rehydrate_plan(prepared: "Prepared") -> int:
     return rc
 
 
+def rehydrate_schedule(prepared: "Prepared") -> int:
+    """``kamera_rehydrate_schedule`` of a prepared rehydrate call:
+    SCHEDULE_PERSISTENT or SCHEDULE_BLOCKS for the row-group kernel, 0 for the
+    per-head kernel or nothing to do, or an error."""
+    rc = lib().kamera_rehydrate_schedule(ctypes.byref(prepared.args))
+    _check(min(rc, 0))
+    return rc
+
+
 def prepare_rehydrate(k_in, k_out, *, rope: RopeSpec, chunk_pos=None, v_in=None, v_out=None,
                       u_k=None, w_k=None, u_v=None, w_v=None, k_patch: Tuple[int, int] = None,
                       v_patch: Tuple[int, int] = None, pos_mode: int = POS_LINEAR, grid_w: int = 0,
@@ -337,7 +352,8 @@ def prepare_rehydrate(k_in, k_out, *, rope: RopeSpec, chunk_pos=None, v_in=None,
                       page_size: int = 16, n_pool_pages: int = 0,
                       patch_frame: int = PATCH_PRE_ROPE, status=None, delta=None,
                       u_pe=None, w_pe=None, k_layer_rank=None, v_layer_rank=None,
-                      pe_layer_rank=None, kernel: int = KERNEL_AUTO, max_workgroups: int = 0) -> Prepared:
+                      pe_layer_rank=None, kernel: int = KERNEL_AUTO, max_workgroups: int = 0,
+                      schedule: int = SCHEDULE_AUTO) -> Prepared:
     """Rebuild cached chunks at their target positions (``kamera_rehydrate``).
 
     k_in, v_in: [C, L, n, H, D] bf16 (any strides, last dim contiguous).
@@ -354,6 +370,8 @@ def prepare_rehydrate(k_in, k_out, *, rope: RopeSpec, chunk_pos=None, v_in=None,
     *_layer_rank: int32 [L] device tensors lowering the rank per layer.
     kernel: KERNEL_AUTO, KERNEL_PER_HEAD, KERNEL_ROW_GROUP or KERNEL_ROW_GROUP4 (same results).
     max_workgroups: 0 = one resident wave on the whole device, else a cap (same results).
+    schedule: SCHEDULE_AUTO, SCHEDULE_PERSISTENT or SCHEDULE_BLOCKS for the row-group kernel
+    (same results).
     """
     L = lib()
     _bf16(k_in, "k_in"), _bf16(k_out, "k_out"), _bf16(v_in, "v_in"), _bf16(v_out, "v_out")
@@ -403,6 +421,7 @@ def prepare_rehydrate(k_in, k_out, *, rope: RopeSpec, chunk_pos=None, v_in=None,
     a.delta = _ptr(delta)
     a.kernel = int(kernel)
     a.max_workgroups = int(max_workgroups)
+    a.schedule = int(schedule)
     keep = (k_in, k_out, v_in, v_out, u_k, w_k, u_v, w_v, chunk_pos, explicit_pos, chunk_tokens,
             row_base, page_table, status, delta, u_pe, w_pe, k_layer_rank, v_layer_rank, pe_layer_rank)
     return Prepared(L.kamera_rehydrate, a, keep)

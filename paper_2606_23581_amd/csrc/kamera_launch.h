@@ -93,7 +93,8 @@ struct RehydrateParams {
   int32_t unit_tiles;                // row-group: 16-token tiles per (chunk, layer) unit (n_tokens / 16, rounded up)
   int32_t lane_wgs;                  // row-group: workgroups per (plane, head group) lane, set at launch
   int32_t max_wgs;                   // caller's cap on the workgroups of a launch (0: none)
-  int32_t pad4_;
+  int32_t block_tiles;               // row-group: > 0 = one workgroup per token block of this many
+                                     // tiles (hardware dispatch); 0 = persistent, equal ranges
   int64_t n_tasks;
 };
 

@@ -1,8 +1,9 @@
 // gfx950 row-group rehydrate kernel of the Kamera operator:
 // K' = R(pos)(K + U W), V' = V + U_v W_v  (Eq. eq:operator, Sec. 3; serve
-// step of App. A) for rows of <= 8 heads, one workgroup per (plane, chunk,
-// layer, token block, group of heads) writing its heads of a token row
-// together.
+// step of App. A) for rows of <= 8 heads: workgroups each owning one (plane,
+// group of heads) and a contiguous range of its (chunk, layer, 16-token tile)
+// space (long ranges on persistent workgroups, or one token block each),
+// writing their heads of a token row together.
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -14,8 +15,9 @@ namespace kamera {
 // ---------------------------------------------------------------------------
 // Rows of <= 8 heads of 128 columns with one 128-column block per head (the
 // rope band, if any, is the whole head), rank <= 64, positions linear or on a
-// grid, with or without the relocation of already-rotated keys.  A workgroup of HW = 4 or 8 waves owns (plane, chunk,
-// layer, token block, group of HW heads); wave h computes head h of the group
+// grid, with or without the relocation of already-rotated keys.  A workgroup
+// of HW = 4 or 8 waves walks segments of one (plane, chunk, layer) unit's
+// tiles for its group of HW heads; wave h computes head h of the group
 // in the register layout of the per-head kernel (kamera_kernels.hip: lane
 // (g, t) holds chunks g, g+4, g+8, g+12 of token t).  Per 16-token tile the
 // group's heads move
@@ -23,7 +25,7 @@ namespace kamera {
 // and the store phase writes every token's row of the group's heads: with 8
 // heads a pool page of 16 tokens is one contiguous 32 KiB run instead of one
 // 256-byte piece per head.  W^T of every head sits in registers for the whole
-// token block, and the block's page numbers in LDS.  Tile loads and stores are
+// segment, and the segment's page numbers in LDS.  Tile loads and stores are
 // buffer instructions whose out-of-range lanes (ragged tails, missing heads,
 // pages outside the pool) read zeros or write nothing, so the tile loop issues
 // the same memory instructions on every path.
@@ -537,16 +539,103 @@ __device__ __forceinline__ int64_t rg_cut(const RehydrateParams& P, const PlaneP
   return (c * L + l) * T + tile;
 }
 
-// Persistent form.  Workgroup w serves lane w % lanes -- one (plane, group of
-// HW heads) -- and the (w / lanes)-th of lane_wgs equal, contiguous ranges of
-// that lane's (chunk, layer, 16-token tile) space, walked in segments of at
-// most one unit's tiles (and kRgMaxBlock tokens).  Every workgroup moves the
-// same bytes, so they all finish together, and a unit's set-up (W^T, page
-// numbers) is paid once per segment.  The workgroups of one range index are
-// adjacent in the grid and walk the same tiles at the same pace, so the planes
-// and head groups of a pool page are written together.
-// RELOC: the keys are already rotated and move by the chunk's delta.
+// One segment: 16-token tiles [tile0, tile1) (at most kRgMaxBlock tokens) of
+// unit cl = chunk * n_layers + layer, for lane (plane, head group) `lane`.
+// dcs_chunk names the chunk whose (cos, sin) of delta s_dcs holds (-1: none);
+// a relocating segment of another chunk refills it.  Returns the chunk s_dcs
+// holds afterwards.
 template <int MS, int HW, bool RELOC>
+__device__ __forceinline__ int rg_segment(const RehydrateParams& P, int lane, int64_t cl, int tile0, int tile1,
+                                          int tid, int dcs_chunk, uint8_t* lds, double* s_freq, int* s_coord,
+                                          float* s_dcs) {
+  const int pl = lane % P.n_planes;
+  const int hg = lane / P.n_planes;
+  const PlaneParams& Q = P.plane[pl];
+  const int rot = (Q.blk[0].flags & kBlkRotate) ? (P.rope.pairing == 0 ? 1 : 2) : 0;
+  RgTask T;
+  T.Q = &Q;
+  T.l = (int)(cl % P.n_layers);
+  T.c = (int)(cl / P.n_layers);
+  T.h0 = hg * HW;
+  T.H = min(HW, P.n_heads - T.h0);
+  T.n_c = chunk_len(P.place, T.c);
+  const int t_begin = tile0 * kTileTokens;
+  if (t_begin >= T.n_c) return dcs_chunk;       // uniform: the whole workgroup skips
+  const int t_end = min(tile1 * kTileTokens, T.n_c);
+  T.t_end = t_end;
+  T.m = Q.m;
+  if (Q.layer_rank != nullptr) {
+    const int lr = Q.layer_rank[T.l];
+    T.m = lr < 0 ? 0 : (lr < Q.m ? lr : Q.m);
+  }
+  T.m_steps = (T.m + 31) / 32;
+  T.in_head_major = Q.in_s[3] > Q.in_s[2];
+  T.out_head_major = Q.out_s[3] > Q.out_s[2];
+  T.s_in2 = (int)Q.in_s[2];
+  T.s_in3 = (int)Q.in_s[3];
+  T.s_u2 = (int)Q.u_s[2];
+  T.s_u3 = (int)Q.u_s[3];
+  T.s_o2 = (int)Q.out_s[2];
+  T.s_o3 = (int)Q.out_s[3];
+  // the slabs start at the workgroup's first head
+  T.rin = rg_rsrc(Q.in + (int64_t)T.c * Q.in_s[0] + (int64_t)T.l * Q.in_s[1] + (int64_t)T.h0 * Q.in_s[3],
+                  Q.in_rec - 2 * (int64_t)T.h0 * Q.in_s[3]);
+  T.ru = rg_rsrc(Q.U != nullptr ? Q.U + (int64_t)T.c * Q.u_s[0] + (int64_t)T.l * Q.u_s[1] + (int64_t)T.h0 * Q.u_s[2]
+                                : Q.in,
+                 Q.U != nullptr ? Q.u_rec - 2 * (int64_t)T.h0 * Q.u_s[2] : 0);
+  // paged: the layer's pool; dense: the chunk's rows from its row base on
+  const int64_t out_base = P.place.paged ? 0
+                           : (int64_t)T.c * Q.out_s[0] +
+                                 (int64_t)(P.place.row_base ? P.place.row_base[T.c] : 0) * Q.out_s[2];
+  T.rout = rg_rsrc(Q.out + out_base + (int64_t)T.l * Q.out_s[1] + (int64_t)T.h0 * Q.out_s[3],
+                   Q.out_rec - 2 * (int64_t)T.h0 * Q.out_s[3]);
+  T.cp0 = T.cp1 = T.cp2 = 0.0;
+  T.dt = T.dh = T.dw = 0.0;
+  if (RELOC) {
+    T.dt = (double)P.delta[3 * T.c];
+    T.dh = (double)P.delta[3 * T.c + 1];
+    T.dw = (double)P.delta[3 * T.c + 2];
+    if (rot != 0 && T.c != dcs_chunk) {
+      // read only after the next barrier; an earlier segment's reads ended
+      // before the barrier that closed it
+      const int half = P.rope.rope_dim / 2;
+      for (int j = threadIdx.x; j < half; j += 64 * HW) {
+        const int sc = P.rope.coord[j];
+        float sn, cs;
+        sincos_rev(sc == 0 ? T.dt : (sc == 1 ? T.dh : T.dw), P.rope.rev_freq[j], sn, cs);
+        s_dcs[2 * j] = cs;
+        s_dcs[2 * j + 1] = sn;
+      }
+      dcs_chunk = T.c;
+    }
+  }
+  if (P.chunk_pos != nullptr) {
+    T.cp0 = (double)P.chunk_pos[3 * T.c];
+    T.cp1 = (double)P.chunk_pos[3 * T.c + 1];
+    T.cp2 = (double)P.chunk_pos[3 * T.c + 2];
+  }
+  switch (rot) {
+    case 0: rg_run<MS, 0, HW, RELOC>(P, T, tid, t_begin, t_end, lds, s_freq, s_coord, s_dcs); break;
+    case 1: rg_run<MS, 1, HW, RELOC>(P, T, tid, t_begin, t_end, lds, s_freq, s_coord, s_dcs); break;
+    default: rg_run<MS, 2, HW, RELOC>(P, T, tid, t_begin, t_end, lds, s_freq, s_coord, s_dcs); break;
+  }
+  return dcs_chunk;
+}
+
+// Workgroup w serves lane w % lanes -- one (plane, group of HW heads) -- and
+// range w / lanes of that lane's (chunk, layer, 16-token tile) space.  The
+// workgroups of one range index are adjacent in the grid and walk the same
+// tiles at the same pace, so the planes and head groups of a pool page are
+// written together.
+//  * PERSIST = false (block schedule): range r is token block r % nb of unit
+//    r / nb (nb blocks of block_tiles per unit), one segment; there are more
+//    workgroups than fit at once and the hardware hands them out.
+//  * PERSIST = true: one resident wave of workgroups, lane_wgs ranges of equal
+//    weight per lane (so that all finish together), each walked in segments
+//    of at most one unit's tiles (and kRgMaxBlock tokens); a unit's set-up
+//    (W^T, page numbers) is paid once per segment.
+// RELOC: the keys are already rotated and move by the chunk's delta.
+template <int MS, int HW, bool RELOC, bool PERSIST>
 __global__ __launch_bounds__(64 * HW, rg_min_waves(MS, HW)) void rehydrate_rows_kernel(const RehydrateParams /*by value, read in place*/) {
   const RehydrateParams& P = kernel_params<RehydrateParams>();
   extern __shared__ __align__(16) uint8_t lds_dyn[];
@@ -559,129 +648,69 @@ __global__ __launch_bounds__(64 * HW, rg_min_waves(MS, HW)) void rehydrate_rows_
     s_freq[j] = P.rope.rev_freq[j];
     s_coord[j] = P.rope.coord[j];
   }
-  // The segment cursor and the chunk s_dcs holds live in VGPRs across a
-  // segment (whose tile loop needs every scalar register); the uniform state
-  // of a segment is derived again from them and the launch parameters.
-  int32_t cur_lo, cur_hi, end_lo, end_hi, dcs_chunk_v = -1;
-  {
-    const int lanes = P.n_planes * P.n_hgroups;
+  const int lanes = P.n_planes * P.n_hgroups;
+  if constexpr (!PERSIST) {
     const int64_t r = blockIdx.x / (uint32_t)lanes;
-    const PlaneParams& Q = P.plane[(blockIdx.x % (uint32_t)lanes) % P.n_planes];
-    const int64_t f0 = rg_cut(P, Q, r, threadIdx.x), f1 = rg_cut(P, Q, r + 1, threadIdx.x);
-    cur_lo = (int32_t)(uint32_t)f0;
-    cur_hi = (int32_t)(f0 >> 32);
-    end_lo = (int32_t)(uint32_t)f1;
-    end_hi = (int32_t)(f1 >> 32);
-  }
-  for (;;) {
-    asm volatile("" : "+v"(cur_lo), "+v"(cur_hi), "+v"(end_lo), "+v"(end_hi), "+v"(dcs_chunk_v));
-    const int64_t f = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane(cur_hi) << 32) |
-                                (uint32_t)__builtin_amdgcn_readfirstlane(cur_lo));
-    const int64_t f_end = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane(end_hi) << 32) |
-                                    (uint32_t)__builtin_amdgcn_readfirstlane(end_lo));
-    const int dcs_chunk = __builtin_amdgcn_readfirstlane(dcs_chunk_v);
-    if (f >= f_end) break;
-    const int lanes = P.n_planes * P.n_hgroups;
-    const int lane = (int)(blockIdx.x % (uint32_t)lanes);
-    const int pl = lane % P.n_planes;
-    const int hg = lane / P.n_planes;
-    const PlaneParams& Q = P.plane[pl];
-    const int rot = (Q.blk[0].flags & kBlkRotate) ? (P.rope.pairing == 0 ? 1 : 2) : 0;
-    const int64_t cl = f / P.unit_tiles;
-    const int tile0 = (int)(f - cl * P.unit_tiles);
-    int64_t tile1 = min((int64_t)P.unit_tiles, (int64_t)tile0 + (f_end - f));
-    tile1 = min(tile1, (int64_t)tile0 + kRgMaxBlock / kTileTokens);
+    const int nb = (P.unit_tiles + P.block_tiles - 1) / P.block_tiles;
+    const int64_t u = r / nb;
+    const int tile0 = (int)(r - u * nb) * P.block_tiles;
+    const int tile1 = min(tile0 + P.block_tiles, P.unit_tiles);
+    rg_segment<MS, HW, RELOC>(P, (int)(blockIdx.x % (uint32_t)lanes), u, tile0, tile1, threadIdx.x, -1, lds_dyn,
+                              s_freq, s_coord, s_dcs);
+  } else {
+    // The segment cursor and the chunk s_dcs holds live in VGPRs across a
+    // segment (whose tile loop needs every scalar register); the uniform
+    // state of a segment is derived again from them and the launch
+    // parameters.
+    int32_t cur_lo, cur_hi, end_lo, end_hi, dcs_chunk_v = -1;
     {
-      const int64_t next = f + (tile1 - tile0);
-      cur_lo = (int32_t)(uint32_t)next;
-      cur_hi = (int32_t)(next >> 32);
+      const int64_t r = blockIdx.x / (uint32_t)lanes;
+      const PlaneParams& Q = P.plane[(blockIdx.x % (uint32_t)lanes) % P.n_planes];
+      const int64_t f0 = rg_cut(P, Q, r, threadIdx.x), f1 = rg_cut(P, Q, r + 1, threadIdx.x);
+      cur_lo = (int32_t)(uint32_t)f0;
+      cur_hi = (int32_t)(f0 >> 32);
+      end_lo = (int32_t)(uint32_t)f1;
+      end_hi = (int32_t)(f1 >> 32);
     }
-    RgTask T;
-    T.Q = &Q;
-    T.l = (int)(cl % P.n_layers);
-    T.c = (int)(cl / P.n_layers);
-    T.h0 = hg * HW;
-    T.H = min(HW, P.n_heads - T.h0);
-    T.n_c = chunk_len(P.place, T.c);
-    const int t_begin = tile0 * kTileTokens;
-    if (t_begin >= T.n_c) continue;             // uniform: the whole workgroup skips
-    // the thread index as a value the compiler cannot see through: what is
-    // derived from it is derived again per segment instead of held in
-    // registers across the segment loop
-    int tid = threadIdx.x;
-    asm volatile("" : "+v"(tid));
-    const int t_end = min((int)tile1 * kTileTokens, T.n_c);
-    T.t_end = t_end;
-    T.m = Q.m;
-    if (Q.layer_rank != nullptr) {
-      const int lr = Q.layer_rank[T.l];
-      T.m = lr < 0 ? 0 : (lr < Q.m ? lr : Q.m);
-    }
-    T.m_steps = (T.m + 31) / 32;
-    T.in_head_major = Q.in_s[3] > Q.in_s[2];
-    T.out_head_major = Q.out_s[3] > Q.out_s[2];
-    T.s_in2 = (int)Q.in_s[2];
-    T.s_in3 = (int)Q.in_s[3];
-    T.s_u2 = (int)Q.u_s[2];
-    T.s_u3 = (int)Q.u_s[3];
-    T.s_o2 = (int)Q.out_s[2];
-    T.s_o3 = (int)Q.out_s[3];
-    // the slabs start at the workgroup's first head
-    T.rin = rg_rsrc(Q.in + (int64_t)T.c * Q.in_s[0] + (int64_t)T.l * Q.in_s[1] + (int64_t)T.h0 * Q.in_s[3],
-                    Q.in_rec - 2 * (int64_t)T.h0 * Q.in_s[3]);
-    T.ru = rg_rsrc(Q.U != nullptr ? Q.U + (int64_t)T.c * Q.u_s[0] + (int64_t)T.l * Q.u_s[1] +
-                                        (int64_t)T.h0 * Q.u_s[2]
-                                  : Q.in,
-                   Q.U != nullptr ? Q.u_rec - 2 * (int64_t)T.h0 * Q.u_s[2] : 0);
-    // paged: the layer's pool; dense: the chunk's rows from its row base on
-    const int64_t out_base = P.place.paged ? 0
-                             : (int64_t)T.c * Q.out_s[0] +
-                                   (int64_t)(P.place.row_base ? P.place.row_base[T.c] : 0) * Q.out_s[2];
-    T.rout = rg_rsrc(Q.out + out_base + (int64_t)T.l * Q.out_s[1] + (int64_t)T.h0 * Q.out_s[3],
-                     Q.out_rec - 2 * (int64_t)T.h0 * Q.out_s[3]);
-    T.cp0 = T.cp1 = T.cp2 = 0.0;
-    T.dt = T.dh = T.dw = 0.0;
-    if (RELOC) {
-      T.dt = (double)P.delta[3 * T.c];
-      T.dh = (double)P.delta[3 * T.c + 1];
-      T.dw = (double)P.delta[3 * T.c + 2];
-      if (rot != 0 && T.c != dcs_chunk) {
-        // read only after the next barrier; the previous segment's reads
-        // ended before the barrier that closed it
-        for (int j = threadIdx.x; j < half; j += 64 * HW) {
-          const int sc = P.rope.coord[j];
-          float sn, cs;
-          sincos_rev(sc == 0 ? T.dt : (sc == 1 ? T.dh : T.dw), P.rope.rev_freq[j], sn, cs);
-          s_dcs[2 * j] = cs;
-          s_dcs[2 * j + 1] = sn;
-        }
-        dcs_chunk_v = T.c;
+    for (;;) {
+      asm volatile("" : "+v"(cur_lo), "+v"(cur_hi), "+v"(end_lo), "+v"(end_hi), "+v"(dcs_chunk_v));
+      const int64_t f = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane(cur_hi) << 32) |
+                                  (uint32_t)__builtin_amdgcn_readfirstlane(cur_lo));
+      const int64_t f_end = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane(end_hi) << 32) |
+                                      (uint32_t)__builtin_amdgcn_readfirstlane(end_lo));
+      const int dcs_chunk = __builtin_amdgcn_readfirstlane(dcs_chunk_v);
+      if (f >= f_end) break;
+      const int64_t cl = f / P.unit_tiles;
+      const int tile0 = (int)(f - cl * P.unit_tiles);
+      int64_t tile1 = min((int64_t)P.unit_tiles, (int64_t)tile0 + (f_end - f));
+      tile1 = min(tile1, (int64_t)tile0 + kRgMaxBlock / kTileTokens);
+      {
+        const int64_t next = f + (tile1 - tile0);
+        cur_lo = (int32_t)(uint32_t)next;
+        cur_hi = (int32_t)(next >> 32);
       }
+      // the thread index as a value the compiler cannot see through: what is
+      // derived from it is derived again per segment instead of held in
+      // registers across the segment loop
+      int tid = threadIdx.x;
+      asm volatile("" : "+v"(tid));
+      dcs_chunk_v = rg_segment<MS, HW, RELOC>(P, (int)(blockIdx.x % (uint32_t)lanes), cl, tile0, (int)tile1, tid,
+                                              dcs_chunk, lds_dyn, s_freq, s_coord, s_dcs);
+      __syncthreads();                          // LDS (tiles, W^T, pages, s_dcs) free for the next segment
     }
-    if (P.chunk_pos != nullptr) {
-      T.cp0 = (double)P.chunk_pos[3 * T.c];
-      T.cp1 = (double)P.chunk_pos[3 * T.c + 1];
-      T.cp2 = (double)P.chunk_pos[3 * T.c + 2];
-    }
-    switch (rot) {
-      case 0: rg_run<MS, 0, HW, RELOC>(P, T, tid, t_begin, t_end, lds_dyn, s_freq, s_coord, s_dcs); break;
-      case 1: rg_run<MS, 1, HW, RELOC>(P, T, tid, t_begin, t_end, lds_dyn, s_freq, s_coord, s_dcs); break;
-      default: rg_run<MS, 2, HW, RELOC>(P, T, tid, t_begin, t_end, lds_dyn, s_freq, s_coord, s_dcs); break;
-    }
-    __syncthreads();                            // LDS (tiles, W^T, pages, s_dcs) free for the next segment
   }
 }
 
-// Workgroups of one instantiation that the device holds at once (all CUs),
-// asked once per device.
+// Workgroups of the persistent instantiation that the device holds at once
+// (all CUs), asked once per device.
 template <int MS, int HW, bool RELOC>
 hipError_t rows_resident(int dev, int& resident) {
   static std::atomic<int> cache[kMaxDevices];
   const bool cached = dev >= 0 && dev < kMaxDevices;
   if (cached && (resident = cache[dev].load(std::memory_order_acquire)) > 0) return hipSuccess;
   int per_cu = 0, cus = 0;
-  hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, rehydrate_rows_kernel<MS, HW, RELOC>, 64 * HW,
-                                                              rg_lds_bytes(MS, HW));
+  hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, rehydrate_rows_kernel<MS, HW, RELOC, true>,
+                                                              64 * HW, rg_lds_bytes(MS, HW));
   if (e != hipSuccess) return e;
   e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
   if (e != hipSuccess) return e;
@@ -692,8 +721,23 @@ hipError_t rows_resident(int dev, int& resident) {
 
 template <int MS, int HW, bool RELOC>
 hipError_t launch_rows(const RehydrateParams& p, hipStream_t s) {
+  const int lanes = p.n_planes * p.n_hgroups;
+  RehydrateParams q = p;
+  if (p.block_tiles > 0) {
+    // block schedule: one workgroup per token block; the hardware hands them out
+    static std::atomic<bool> lds_set[kMaxDevices];
+    hipError_t e = ensure_lds_limit((const void*)rehydrate_rows_kernel<MS, HW, RELOC, false>, rg_lds_bytes(MS, HW),
+                                    lds_set);
+    if (e != hipSuccess) return e;
+    const int64_t g = (int64_t)p.n_chunks * p.n_layers * ((p.unit_tiles + p.block_tiles - 1) / p.block_tiles);
+    q.lane_wgs = (int32_t)g;
+    const dim3 grid((uint32_t)(lanes * g)), block(64 * HW);
+    hipLaunchKernelGGL((rehydrate_rows_kernel<MS, HW, RELOC, false>), grid, block, rg_lds_bytes(MS, HW), s, q);
+    return hipGetLastError();
+  }
   static std::atomic<bool> lds_set[kMaxDevices];
-  hipError_t e = ensure_lds_limit((const void*)rehydrate_rows_kernel<MS, HW, RELOC>, rg_lds_bytes(MS, HW), lds_set);
+  hipError_t e = ensure_lds_limit((const void*)rehydrate_rows_kernel<MS, HW, RELOC, true>, rg_lds_bytes(MS, HW),
+                                  lds_set);
   if (e != hipSuccess) return e;
   int dev = 0, resident = 0;
   e = hipGetDevice(&dev);
@@ -702,14 +746,12 @@ hipError_t launch_rows(const RehydrateParams& p, hipStream_t s) {
   if (e != hipSuccess) return e;
   // one resident wave of workgroups (or the caller's cap), at least one tile each
   if (p.max_wgs > 0 && p.max_wgs < resident) resident = p.max_wgs;
-  const int lanes = p.n_planes * p.n_hgroups;
   const int64_t per_lane = (int64_t)p.n_chunks * p.n_layers * p.unit_tiles;
   int64_t g = resident / lanes > 0 ? resident / lanes : 1;
   g = g < per_lane ? g : per_lane;
-  RehydrateParams q = p;
   q.lane_wgs = (int32_t)g;
   const dim3 grid((uint32_t)(lanes * g)), block(64 * HW);
-  hipLaunchKernelGGL((rehydrate_rows_kernel<MS, HW, RELOC>), grid, block, rg_lds_bytes(MS, HW), s, q);
+  hipLaunchKernelGGL((rehydrate_rows_kernel<MS, HW, RELOC, true>), grid, block, rg_lds_bytes(MS, HW), s, q);
   return hipGetLastError();
 }
 

@@ -102,6 +102,21 @@ int main(void) {
   fill_rehydrate(&a);
   a.n_tokens = 0;
   CHECK(kamera_rehydrate_plan(&a) == KAMERA_PLAN_NONE);
+  CHECK(kamera_rehydrate_schedule(&a) == 0);
+
+  /* row-group schedule: none for the per-head kernel; a small grid runs
+   * persistent under AUTO; blocks on request, but not with a cap */
+  fill_rehydrate(&a);
+  CHECK(kamera_rehydrate_schedule(&a) == 0);
+  a.kernel = KAMERA_KERNEL_ROW_GROUP4;
+  CHECK(kamera_rehydrate_schedule(&a) == KAMERA_SCHEDULE_PERSISTENT);
+  a.schedule = KAMERA_SCHEDULE_BLOCKS;
+  CHECK(kamera_rehydrate_schedule(&a) == KAMERA_SCHEDULE_BLOCKS);
+  a.max_workgroups = 4;
+  CHECK(kamera_rehydrate_schedule(&a) == KAMERA_ERR_SHAPE);
+  a.schedule = 5;
+  a.max_workgroups = 0;
+  CHECK(kamera_rehydrate_schedule(&a) == KAMERA_ERR_SHAPE);
 
   /* page-table check on a host copy: 2 chunks x 3 pages of 16 tokens */
   int32_t pt[6] = {5, 1, 2, 0, 4, 3};

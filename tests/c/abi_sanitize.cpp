@@ -164,6 +164,9 @@ void check_one(int which, const void* a) {
   if (which == 0 && rc == KAMERA_OK) {
     const int plan = kamera_rehydrate_plan(static_cast<const kamera_rehydrate_args*>(a));
     CHECK(plan >= KAMERA_PLAN_NONE && plan <= KAMERA_PLAN_ROW_GROUP4);
+    const int sched = kamera_rehydrate_schedule(static_cast<const kamera_rehydrate_args*>(a));
+    CHECK((sched == 0) == (plan == KAMERA_PLAN_NONE || plan == KAMERA_PLAN_PER_HEAD));
+    CHECK(sched >= 0 && sched <= KAMERA_SCHEDULE_BLOCKS);
   }
 }
 
@@ -201,6 +204,16 @@ int main() {
     CHECK(kamera_form_patch(&f, nullptr) == KAMERA_OK);
     CHECK(stub_launches() - before == 5);
     CHECK(stub_last_rehydrate_tasks() > 0);
+    // the row-group kernel's two schedules reach the launch: token blocks of
+    // 64 tokens (this grid is small), or persistent ranges
+    kamera_rehydrate_args rb = r;
+    rb.kernel = KAMERA_KERNEL_ROW_GROUP4;
+    rb.schedule = KAMERA_SCHEDULE_BLOCKS;
+    CHECK(kamera_rehydrate(&rb, nullptr) == KAMERA_OK);
+    CHECK(stub_last_rehydrate_row_group() == 4 && stub_last_rehydrate_block_tiles() == 4);
+    rb.schedule = KAMERA_SCHEDULE_AUTO;
+    CHECK(kamera_rehydrate(&rb, nullptr) == KAMERA_OK);
+    CHECK(stub_last_rehydrate_row_group() == 4 && stub_last_rehydrate_block_tiles() == 0);
     // a launch the runtime refuses
     stub_set_launch_error(98);
     CHECK(kamera_rehydrate(&r, nullptr) == KAMERA_ERR_HIP);

@@ -19,6 +19,7 @@ extern "C" void stub_set_launch_error(int e) { g_fail.store(e); }
 extern "C" long stub_launches(void) { return g_launches.load(); }
 extern "C" int stub_last_rehydrate_row_group(void) { return t_last_rehydrate.row_group; }
 extern "C" long long stub_last_rehydrate_tasks(void) { return (long long)t_last_rehydrate.n_tasks; }
+extern "C" int stub_last_rehydrate_block_tiles(void) { return t_last_rehydrate.block_tiles; }
 
 extern "C" const char* hipGetErrorString(hipError_t e) { return e == hipSuccess ? "no error" : "stub launch error"; }
 

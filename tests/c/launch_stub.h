@@ -8,6 +8,7 @@ void stub_set_launch_error(int hip_error);   /* 0: launches succeed */
 long stub_launches(void);                    /* launches so far, all threads */
 int stub_last_rehydrate_row_group(void);     /* this thread's last rehydrate */
 long long stub_last_rehydrate_tasks(void);
+int stub_last_rehydrate_block_tiles(void);   /* 0: persistent schedule */
 #ifdef __cplusplus
 }
 #endif

@@ -102,6 +102,8 @@ class RehydrateCase:
     kernel: int = 0                    # kamera_kernel_choice requested (0: AUTO)
     plan: Optional[int] = None         # kernel kamera_rehydrate_plan must report for the case
     max_workgroups: int = 0            # cap on the launch's workgroups (long segments per workgroup)
+    schedule: int = 0                  # kamera_row_schedule requested (0: AUTO)
+    sched: Optional[int] = None        # schedule kamera_rehydrate_schedule must report for the case
     seed: int = 0
 
 
@@ -206,7 +208,7 @@ def run_rehydrate(case: RehydrateCase, device):
               grid_w=case.grid_w, chunk_pos=dev_i32(pos, device),
               explicit_pos=dev_i32(explicit, device) if explicit is not None else None,
               chunk_tokens=dev_i32(n_c, device) if case.ragged else None, kernel=case.kernel,
-              max_workgroups=case.max_workgroups)
+              max_workgroups=case.max_workgroups, schedule=case.schedule)
     status = dev_i32(np.zeros(1), device)
     kw["status"] = status
     if case.reloc:
@@ -232,6 +234,8 @@ def run_rehydrate(case: RehydrateCase, device):
         prep = km.prepare_rehydrate(ko if case.in_place else dev_in(K), ko, v_out=vo, **kw)
     if case.plan is not None:
         assert km.rehydrate_plan(prep) == case.plan
+    if case.sched is not None:
+        assert km.rehydrate_schedule(prep) == case.sched
     prep.launch()
     import torch
 

@@ -67,7 +67,7 @@ def test_plain_c_consumer(tmp_path):
 
 def test_version_and_struct_layout():
     L = km.lib()
-    assert L.kamera_abi_version() == 3
+    assert L.kamera_abi_version() == 4
     assert L.kamera_struct_size(0) == ctypes.sizeof(km.CRehydrateArgs)
     assert L.kamera_struct_size(1) == ctypes.sizeof(km.CShiftArgs)
     assert L.kamera_struct_size(2) == ctypes.sizeof(km.CScatterArgs)
@@ -243,6 +243,44 @@ def test_rehydrate_plan_picks_the_kernel(case, plan):
     a = _plan_case(case)
     assert km.lib().kamera_rehydrate_plan(ctypes.byref(a)) == plan
     assert km.lib().kamera_validate(0, ctypes.byref(a)) == min(plan, 0)
+
+
+@pytest.mark.parametrize("case,schedule,cap,want", [
+    # 64 x 80 units x 2 planes x 2 head groups: 20480 blocks of 1024 tokens
+    ("auto_recall", km.SCHEDULE_AUTO, 0, km.SCHEDULE_BLOCKS),
+    ("auto_recall_relocation", km.SCHEDULE_AUTO, 0, km.SCHEDULE_BLOCKS),
+    ("auto_recall_short_chunks", km.SCHEDULE_AUTO, 0, km.SCHEDULE_BLOCKS),
+    # 2048 unit lanes: blocks of 512 tokens reach 4096
+    ("auto_mid_8_heads", km.SCHEDULE_AUTO, 0, km.SCHEDULE_BLOCKS),
+    # 448 unit lanes: blocks would shrink to 64 tokens
+    ("auto_reorder_shape", km.SCHEDULE_AUTO, 0, km.SCHEDULE_PERSISTENT),
+    ("auto_2_19_rows", km.SCHEDULE_AUTO, 0, km.SCHEDULE_PERSISTENT),
+    ("default", km.SCHEDULE_AUTO, 0, km.SCHEDULE_PERSISTENT),
+    # a cap on the workgroups asks for the persistent schedule
+    ("auto_recall", km.SCHEDULE_AUTO, 64, km.SCHEDULE_PERSISTENT),
+    ("auto_recall", km.SCHEDULE_PERSISTENT, 0, km.SCHEDULE_PERSISTENT),
+    ("auto_reorder_shape", km.SCHEDULE_BLOCKS, 0, km.SCHEDULE_BLOCKS),
+    ("default", km.SCHEDULE_BLOCKS, 0, km.SCHEDULE_BLOCKS),
+    ("auto_recall", km.SCHEDULE_BLOCKS, 8, km.ERR_SHAPE),
+    ("auto_recall", 3, 0, km.ERR_SHAPE),
+    ("auto_recall", -1, 0, km.ERR_SHAPE),
+    # the per-head kernel, or nothing to do: no schedule
+    ("auto_small_8_heads", km.SCHEDULE_AUTO, 0, 0),
+    ("per_head_requested", km.SCHEDULE_BLOCKS, 0, 0),
+    ("empty", km.SCHEDULE_AUTO, 0, 0),
+])
+def test_rehydrate_schedule_of_the_row_group_kernel(case, schedule, cap, want):
+    """kamera_rehydrate_schedule names how the row-group kernel spreads a
+    call: AUTO takes one workgroup per token block where the blocks (up to
+    1024 tokens, shrunk to >= 64 until the launch has 4096 of them) stay
+    >= 512 tokens, else the persistent schedule, which a cap on the
+    workgroups also selects; a request for blocks with a cap, or an unknown
+    schedule, is rejected by the call's own checks."""
+    a = _plan_case(case)
+    a.schedule = schedule
+    a.max_workgroups = cap
+    assert km.lib().kamera_rehydrate_schedule(ctypes.byref(a)) == want
+    assert km.lib().kamera_validate(0, ctypes.byref(a)) == min(want, 0)
 
 
 def _interleaved_case(case):

@@ -140,19 +140,41 @@ REHYDRATE_CASES = {
     "per_head_explicit_paged": RehydrateCase(H=8, pos_mode="explicit", paged=True, kernel=2, plan=1, seed=61),
     "per_head_rank_72_paged": RehydrateCase(H=8, m_k=72, m_v=8, paged=True, kernel=2, plan=1, seed=62),
     "per_head_9_heads_paged": RehydrateCase(H=9, paged=True, kernel=2, plan=1, seed=63),
-    # relocation above rank 64 on the per-head kernel: the two-rotation form
-    # R(p)(R(delta - p) K + U W) (rank steps of 4 x 32), both frames
     # few workgroups: each walks many tiles, crossing (chunk, layer) units,
     # ragged chunk ends and the 1024-token segment limit
     "rows4_few_workgroups_paged": RehydrateCase(H=8, C=3, L=3, n=300, ragged=True, paged=True, m_k=64, m_v=32,
                                                 sections=(16, 24, 24), pos_mode="grid3", grid_w=20, kernel=3,
-                                                plan=3, max_workgroups=6, seed=84),
+                                                plan=3, max_workgroups=6, sched=1, seed=84),
     "rows8_two_workgroups_long_chunk": RehydrateCase(H=8, C=2, L=2, n=1500, unit_major=True, m_k=16, m_v=16,
-                                                     kernel=2, plan=2, max_workgroups=2, seed=85),
+                                                     kernel=2, plan=2, max_workgroups=2, sched=1, seed=85),
     "rows4_reloc_few_workgroups": RehydrateCase(H=4, C=3, L=2, n=200, reloc=True, m_k=64, m_v=64, kernel=3,
-                                                plan=3, max_workgroups=3, seed=86),
+                                                plan=3, max_workgroups=3, sched=1, seed=86),
     "rows4_one_workgroup_per_lane": RehydrateCase(H=8, C=2, L=3, n=130, m_k=32, m_v=0, paged=True, kernel=3,
-                                                  plan=3, max_workgroups=4, seed=87),
+                                                  plan=3, max_workgroups=4, sched=1, seed=87),
+    # the block schedule (one workgroup per token block, handed out by the
+    # hardware) on small shapes: blocks shrink to 64 tokens here, so units
+    # split into several blocks, the last one short, and ragged chunks end
+    # inside a block
+    "rows4_blocks_paged_ragged_grid": RehydrateCase(H=8, C=3, L=3, n=300, ragged=True, paged=True, m_k=64, m_v=32,
+                                                    sections=(16, 24, 24), pos_mode="grid3", grid_w=20, kernel=3,
+                                                    plan=3, schedule=2, sched=2, seed=92),
+    "rows8_blocks_long_chunk": RehydrateCase(H=8, C=2, L=2, n=1500, unit_major=True, m_k=16, m_v=16, kernel=2,
+                                             plan=2, schedule=2, sched=2, seed=93),
+    "rows4_blocks_reloc_kv_in_place": RehydrateCase(H=8, reloc=True, row_base=False, in_place=True, m_k=64, m_v=64,
+                                                    n=200, sections=(24, 20, 20), section_order="interleaved",
+                                                    pos_mode="grid3", kernel=3, plan=3, schedule=2, sched=2,
+                                                    seed=94, kv_interleaved=True),
+    "rows4_blocks_layer_rank_row_base": RehydrateCase(H=8, L=3, layer_rank=(0, 64, 20), m_k=64, m_v=64, n=130,
+                                                      ragged=True, C=3, kernel=3, plan=3, schedule=2, sched=2,
+                                                      seed=95),
+    "rows4_blocks_reloc_post_frame_paged": RehydrateCase(H=4, reloc=True, post_rope=True, paged=True, m_k=32,
+                                                         m_v=0, n=90, pairing="interleaved", theta=1e4, kernel=3,
+                                                         plan=3, schedule=2, sched=2, seed=96),
+    "rows4_blocks_kv_interleaved_pool_rank_0": RehydrateCase(H=8, paged=True, m_k=0, m_v=0, n=100, kernel=3,
+                                                             plan=3, schedule=2, sched=2, seed=97,
+                                                             kv_interleaved=True),
+    "rows4_auto_small_is_persistent": RehydrateCase(H=8, paged=True, m_k=16, m_v=16, n=100, kernel=3, plan=3,
+                                                    sched=1, seed=98),
     "per_head_few_workgroups_mla_band": RehydrateCase(D=576, H=1, C=2, L=3, n=300, rope_dim=64, rope_offset=512,
                                                       pairing="interleaved", theta=1e4, patch=(0, 512), m_k=32,
                                                       m_pe=8, has_v=False, kernel=1, plan=1, max_workgroups=3,
@@ -164,6 +186,8 @@ REHYDRATE_CASES = {
                                             kernel=1, plan=1, max_workgroups=1, seed=90),
     "per_head_reloc_two_workgroups": RehydrateCase(H=5, C=2, L=2, n=120, reloc=True, m_k=16, m_v=24, kernel=1,
                                                    plan=1, max_workgroups=2, seed=91),
+    # relocation above rank 64 on the per-head kernel: the two-rotation form
+    # R(p)(R(delta - p) K + U W) (rank steps of 4 x 32), both frames
     "relocate_rank_72_per_head": RehydrateCase(reloc=True, m_k=72, m_v=8, n=70, kernel=1, plan=1, seed=80),
     "relocate_rank_72_post_frame_paged": RehydrateCase(reloc=True, m_k=72, m_v=72, post_rope=True, paged=True,
                                                        pairing="interleaved", theta=1e4, n=50, kernel=1, plan=1,
