@@ -405,8 +405,9 @@ def mix_ceiling(p, steps: int):
     """The same-traffic copy on the workload's own buffers: a kernel that reads
     every K/V row, U row and W basis of the call and writes the rows' bits
     into the pool slots of the same page table, split over the device as the
-    row-group rehydrate kernel splits its work, with no arithmetic; 2 or 4
-    tiles in flight, 2 or 4 workgroups per CU.  Returns (GB/s of the
+    row-group rehydrate kernel splits its work (persistent ranges, or one
+    workgroup per token block), with no arithmetic; 2 or 4 tiles in flight,
+    2 or 4 workgroups per CU.  Returns (GB/s of the
     workload's algorithmic bytes at the best variant's mean event time, its
     mean ms, {variant: GB/s}), or None where the workload is not a paged K|V
     recall it covers."""
@@ -428,7 +429,7 @@ def mix_ceiling(p, steps: int):
     fn.argtypes = ([ctypes.c_void_p, ctypes.c_void_p, i64p] * 3)[:9] + [ctypes.c_int32, ctypes.c_void_p,
                                                                        ctypes.c_void_p, i64p, ctypes.c_void_p,
                                                                        ctypes.c_int32, ctypes.c_int32] + \
-        [ctypes.c_int32] * 6 + [ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p]
+        [ctypes.c_int32] * 7 + [ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p]
 
     def strides(t, n):
         return (ctypes.c_int64 * n)(*[int(x) for x in t.stride()[:n]])
@@ -440,11 +441,12 @@ def mix_ceiling(p, steps: int):
     sink = torch.zeros(1 << 16, dtype=torch.int32, device=k_in.device)
     stream = torch.cuda.current_stream()
     best, variants = None, {}
-    for depth, per_cu in ((2, 2), (4, 2), (2, 4), (4, 4)):
+    for depth, per_cu, blocks in ((2, 2, 0), (4, 2, 0), (2, 4, 0), (4, 4, 0), (2, 2, 1), (4, 2, 1), (2, 4, 1),
+                                  (4, 4, 1)):
         args = (k_in.data_ptr(), v_in.data_ptr(), strides(k_in, 4), uk.data_ptr(), uv.data_ptr(), strides(uk, 4),
                 wk.data_ptr(), wv.data_ptr(), strides(wk, 4), w.m_k, kp.data_ptr(), vp.data_ptr(), strides(kp, 3),
                 pt.data_ptr(), int(pt.stride(0)), w.page_size, w.n_chunks, w.n_layers, w.n_heads, w.n_tokens,
-                depth, per_cu, sink.data_ptr(), sink.numel(), ctypes.c_void_p(stream.cuda_stream))
+                depth, per_cu, blocks, sink.data_ptr(), sink.numel(), ctypes.c_void_p(stream.cuda_stream))
         if fn(*args) <= 0:
             return None
         torch.cuda.synchronize()
@@ -457,7 +459,7 @@ def mix_ceiling(p, steps: int):
         torch.cuda.synchronize()
         ms = sum(a.elapsed_time(b) for a, b in zip(starts, ends)) / steps
         gbps = p.bytes_per_step / (ms * 1e-3) / 1e9
-        variants[f"depth{depth}_wg{per_cu}"] = round(gbps, 1)
+        variants[f"{'blocks' if blocks else 'persistent'}_depth{depth}_wg{per_cu}"] = round(gbps, 1)
         if best is None or ms < best[1]:
             best = (gbps, ms)
     return best[0], best[1], variants

@@ -2,11 +2,12 @@
 // of a paged rehydrate and none of its arithmetic.  It reads every input row
 // (K and V), every U row and every W basis of the call and writes the input
 // rows' bits into the pool slots of the same page table, with the work split
-// the row-group rehydrate kernel uses (workgroups of 4 heads x one plane,
-// equal contiguous ranges of 16-token tiles), with 2 or 4 tiles of loads in
-// flight and 2 or 4 workgroups per CU.  Run on the same buffers, the best of
-// those variants is the practical ceiling of that read:write mix and page
-// pattern on the device.  U and W are folded into one
+// the row-group rehydrate kernel uses (workgroups of 4 heads x one plane, and
+// either equal contiguous ranges of 16-token tiles on one resident wave of
+// workgroups, or one workgroup per token block handed out by the hardware),
+// with 2 or 4 tiles of loads in flight and 2 or 4 workgroups per CU.  Run on
+// the same buffers, the best of those variants is the practical ceiling of
+// that read:write mix and page pattern on the device.  U and W are folded into one
 // XOR word per workgroup so that their loads are not removed.
 
 #include <hip/hip_runtime.h>
@@ -38,6 +39,7 @@ struct CeilParams {
   int32_t pt_stride, page_size;
   int32_t n_chunks, n_layers, n_heads, n_tokens, m;
   int32_t unit_tiles, lane_wgs, n_planes, n_hgroups;
+  int32_t block_tiles;                    // > 0: one workgroup per token block of this many tiles
 };
 
 struct Regs {
@@ -55,13 +57,20 @@ __global__ __launch_bounds__(kThreads, 2) void ceiling_paged_copy_kernel(const C
   const int lane = (int)(blockIdx.x % (uint32_t)lanes);
   const int64_t r = blockIdx.x / (uint32_t)lanes;
   const int64_t per_lane = (int64_t)P.n_chunks * P.n_layers * P.unit_tiles;
-  const int64_t f_end = (r + 1) * per_lane / P.lane_wgs;
+  int64_t f_begin = r * per_lane / P.lane_wgs, f_end = (r + 1) * per_lane / P.lane_wgs;
+  if (P.block_tiles > 0) {
+    const int nb = (P.unit_tiles + P.block_tiles - 1) / P.block_tiles;
+    const int64_t u = r / nb;
+    const int b = (int)(r - u * nb);
+    f_begin = u * P.unit_tiles + (int64_t)b * P.block_tiles;
+    f_end = u * P.unit_tiles + min((b + 1) * P.block_tiles, P.unit_tiles);
+  }
   const int pl = lane % P.n_planes, h0 = (lane / P.n_planes) * kHeads;
   const int H = min(kHeads, P.n_heads - h0);
   const int tid = threadIdx.x;
   const int cpr = P.m / 8;                // U 16-byte chunks per token row
   uint32_t acc = 0;
-  for (int64_t f = r * per_lane / P.lane_wgs; f < f_end;) {
+  for (int64_t f = f_begin; f < f_end;) {
     const int64_t cl = f / P.unit_tiles;
     const int tile0 = (int)(f - cl * P.unit_tiles);
     const int tile1 = (int)min((int64_t)P.unit_tiles, tile0 + (f_end - f));
@@ -134,19 +143,22 @@ __global__ __launch_bounds__(kThreads, 2) void ceiling_paged_copy_kernel(const C
 // Copies the K and V rows of a paged rehydrate call (128-column heads, rank m
 // a multiple of 8 up to 64, inputs [c][l][token][head][dim] by strides) into
 // their pool slots, reading U and W as the rehydrate does, with `depth` (2
-// or 4) tiles in flight and `wgs_per_cu` (2 or 4) workgroups per CU.  sink:
-// device uint32 [grid] (see the return value; at most wgs_per_cu * #CU).  Returns the
-// number of workgroups launched, or a negative value on a bad argument or a
-// HIP error.
+// or 4) tiles in flight and at most `wgs_per_cu` (2 or 4) workgroups per CU
+// (an LDS reservation caps them).  blocks = 0: one resident wave of
+// workgroups with equal ranges; 1: one workgroup per token block (up to 1024
+// tokens, shrunk to >= 64 until there are 4096 blocks).  sink: device uint32
+// [grid] (see the return value).  Returns the number of workgroups launched,
+// or a negative value on a bad argument or a HIP error.
 extern "C" int kamera_ceiling_paged_copy(const void* k_in, const void* v_in, const int64_t* in_stride,
                                          const void* u_k, const void* u_v, const int64_t* u_stride,
                                          const void* w_k, const void* w_v, const int64_t* w_stride, int32_t m,
                                          void* k_pool, void* v_pool, const int64_t* pool_stride,
                                          const int32_t* page_table, int32_t pt_stride, int32_t page_size,
                                          int32_t n_chunks, int32_t n_layers, int32_t n_heads, int32_t n_tokens,
-                                         int32_t depth, int32_t wgs_per_cu, uint32_t* sink, int32_t sink_len,
-                                         void* stream) {
-  if ((depth != 2 && depth != 4) || (wgs_per_cu != 2 && wgs_per_cu != 4) || m <= 0 || m > 64 || m % 8 != 0 || n_heads <= 0 || n_tokens <= 0 || n_chunks <= 0 || n_layers <= 0 ||
+                                         int32_t depth, int32_t wgs_per_cu, int32_t blocks, uint32_t* sink,
+                                         int32_t sink_len, void* stream) {
+  if ((depth != 2 && depth != 4) || (wgs_per_cu != 2 && wgs_per_cu != 4) || (blocks != 0 && blocks != 1) || m <= 0 ||
+      m > 64 || m % 8 != 0 || n_heads <= 0 || n_tokens <= 0 || n_chunks <= 0 || n_layers <= 0 ||
       page_size <= 0 || k_in == nullptr || k_pool == nullptr || u_k == nullptr || w_k == nullptr ||
       page_table == nullptr || sink == nullptr ||
       (v_in != nullptr && (u_v == nullptr || w_v == nullptr || v_pool == nullptr)))
@@ -186,14 +198,27 @@ extern "C" int kamera_ceiling_paged_copy(const void* k_in, const void* v_in, con
   const int resident = (per_cu < wgs_per_cu ? per_cu : wgs_per_cu) * cus;
   const int lanes = P.n_planes * P.n_hgroups;
   const int64_t per_lane = (int64_t)n_chunks * n_layers * P.unit_tiles;
-  int64_t g = resident / lanes > 0 ? resident / lanes : 1;
-  g = g < per_lane ? g : per_lane;
+  int64_t g;
+  if (blocks) {
+    const int64_t units = (int64_t)lanes * n_chunks * n_layers;
+    int bt = 1024 / kTile;
+    while (bt > 4 && units * ((P.unit_tiles + bt - 1) / bt) < 4096) bt /= 2;
+    P.block_tiles = bt;
+    g = (int64_t)n_chunks * n_layers * ((P.unit_tiles + bt - 1) / bt);
+  } else {
+    g = resident / lanes > 0 ? resident / lanes : 1;
+    g = g < per_lane ? g : per_lane;
+  }
   P.lane_wgs = (int32_t)g;
+  if ((int64_t)lanes * g > sink_len) return -1;
   const int grid = (int)(lanes * g);
-  if (grid > sink_len) return -1;
+  // at most wgs_per_cu workgroups per CU: each reserves 1/wgs_per_cu of the
+  // 160 KiB of LDS (less a little)
+  const int lds = (160 * 1024) / wgs_per_cu - 1024;
+  if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds) != hipSuccess) return -2;
   if (depth == 2)
-    hipLaunchKernelGGL(ceiling_paged_copy_kernel<2>, dim3(grid), dim3(kThreads), 0, static_cast<hipStream_t>(stream), P);
+    hipLaunchKernelGGL(ceiling_paged_copy_kernel<2>, dim3(grid), dim3(kThreads), lds, static_cast<hipStream_t>(stream), P);
   else
-    hipLaunchKernelGGL(ceiling_paged_copy_kernel<4>, dim3(grid), dim3(kThreads), 0, static_cast<hipStream_t>(stream), P);
+    hipLaunchKernelGGL(ceiling_paged_copy_kernel<4>, dim3(grid), dim3(kThreads), lds, static_cast<hipStream_t>(stream), P);
   return hipGetLastError() == hipSuccess ? grid : -2;
 }
