@@ -465,6 +465,58 @@ def mix_ceiling(p, steps: int):
     return best[0], best[1], variants
 
 
+def size_matched_copy(p, steps: int, cold: bool):
+    """A plain streaming copy of the workload's size on fresh buffers: the
+    library's scatter kernel with an identity page table moving half the
+    call's algorithmic bytes from one dense row tensor to another (rows as
+    wide as the workload's token rows), one launch per step, timed as the
+    workload is (a 1 GiB write between steps when ``cold``), and the
+    runtime's device-to-device copy of the same bytes.  The faster bounds what
+    a launch of this size reaches as a pure copy.  Returns (its GB/s of the
+    copy's own bytes, its mean ms, {copy: GB/s}) or None."""
+    import torch
+
+    import paper_2606_23581_amd as km
+
+    w = p.workload
+    row_elems = w.head_dim * w.n_heads
+    page = 16
+    rows = -(-p.bytes_per_step // 2 // (2 * row_elems))
+    rows = -(-rows // page) * page
+    dev = torch.device("cuda:0")
+    try:
+        src = torch.zeros((1, 1, rows, row_elems), dtype=torch.bfloat16, device=dev)
+        dst = torch.empty((1, rows, row_elems), dtype=torch.bfloat16, device=dev)
+        ident = torch.arange(rows // page, dtype=torch.int32, device=dev).reshape(1, rows // page)
+        flush = torch.empty((1 << 30) // 4, dtype=torch.float32, device=dev) if cold else None
+    except RuntimeError:
+        return None
+    call = km.prepare_scatter_paged(src, dst, ident, page_size=page, n_pool_pages=rows // page)
+    stream = torch.cuda.current_stream()
+    flat_src, flat_dst = src.reshape(-1), dst.reshape(-1)
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+        for k, (a, b) in enumerate(ev):
+            if flush is not None:
+                flush.fill_(float(k))
+            a.record(stream)
+            fn()
+            b.record(stream)
+        torch.cuda.synchronize()
+        return sum(a.elapsed_time(b) for a, b in ev) / steps
+
+    # the library's streaming copy, and the runtime's own device copy
+    ms = {"scatter_identity": timed(call.launch), "device_copy": timed(lambda: flat_dst.copy_(flat_src))}
+    nbytes = 2 * src.numel() * 2
+    del src, dst, ident, flush, flat_src, flat_dst
+    torch.cuda.empty_cache()
+    best = min(ms.values())
+    return nbytes / (best * 1e-3) / 1e9, best, {k: round(nbytes / (v * 1e-3) / 1e9, 1) for k, v in ms.items()}
+
+
 def measured_traffic(name: str, kernel: str):
     """HBM traffic per launch from the committed rocprofv3 counter summary, if it
     was taken on this kernel as its sources stand (else null)."""
@@ -565,6 +617,8 @@ def main():
 
     # the same traffic without the arithmetic, on the same buffers (placement)
     ceiling = mix_ceiling(p, args.steps)
+    # a plain copy of the same size and row width, timed the same way
+    matched = size_matched_copy(p, args.steps, p.bytes_per_step < (4 << 30))
 
     # further placements of the same workload in this process: the first
     # figures above stay the headline; these show the spread of placements
@@ -689,6 +743,10 @@ def main():
         "mix_ceiling_ms": None if ceiling is None else round(ceiling[1], 4),
         "frac_of_mix_ceiling": None if ceiling is None else round(achieved / ceiling[0], 4),
         "mix_ceiling_variants_GBps": None if ceiling is None else ceiling[2],
+        "size_matched_copy_GBps": None if matched is None else round(matched[0], 1),
+        "size_matched_copy_ms": None if matched is None else round(matched[1], 4),
+        "size_matched_copy_variants_GBps": None if matched is None else matched[2],
+        "frac_of_size_matched_copy": None if matched is None else round(achieved / matched[0], 4),
         "placements": placements,
         "cpu_baseline": cpu,
         "context": "paper Sec. 1: ~230 ms to encode vs ~5 ms to replay a 1024-token segment (paper's "
