@@ -276,11 +276,15 @@ def run_rehydrate(case: RehydrateCase, device):
                 poff = case.patch[0]
                 if case.m_pe:
                     # two patches on disjoint columns == one patch with a block basis
+                    # (the latent's rank may be 0)
                     up, wp = fac(Upe, Wpe, 0)
-                    W_full = np.zeros((u.shape[1] + up.shape[1], D))
-                    W_full[:u.shape[1], case.patch[0]:case.patch[0] + w.shape[1]] = w
-                    W_full[u.shape[1]:, case.rope_offset:case.rope_offset + case.rope_dim] = wp
-                    u, w, poff = np.concatenate([u, up], axis=1), W_full, 0
+                    ku = 0 if u is None else u.shape[1]
+                    W_full = np.zeros((ku + up.shape[1], D))
+                    if u is not None:
+                        W_full[:ku, case.patch[0]:case.patch[0] + w.shape[1]] = w
+                    W_full[ku:, case.rope_offset:case.rope_offset + case.rope_dim] = wp
+                    u = up if u is None else np.concatenate([u, up], axis=1)
+                    w, poff = W_full, 0
                 if case.reloc:
                     want = ref.relocate_k(Kin, u, w, orope, p3, delta[c], poff, case.post_rope)
                 else:
