@@ -153,30 +153,56 @@ def _oracle_form(job):
     return 1
 
 
-def form_flops(n: int, d: int, m: int, sweeps: int, orbit: int = 1) -> int:
-    """Flops of the patch-forming kernel on one unit (padded sizes, every group
-    and tile counted, including those the kernel skips once a group is already
-    diagonal, so an upper bound on the executed work): the Gram matrix on the
-    upper-triangle 16x16 tiles, `sweeps` block-Jacobi sweeps of dp/8 - 1 steps
-    each (one 15-step cyclic sweep of 24 flops per 2x2 block and 6 per rotated
-    Q pair in each of the dp/16 groups -- which also yields the diagonal tiles
-    of the rotated G -- then the 16x16 tile products Q_a^T G_ab Q_b on the
-    strict upper triangle and V_tile Q_b, plus the convergence sum), and
-    U = Delta V_m."""
+def jacobi_flops(d: int, sweeps: int) -> int:
+    """Block-Jacobi flops on one unit (padded sizes, every group and tile
+    counted, including those the kernel skips once a group is already
+    diagonal, so an upper bound on the executed work): `sweeps` sweeps of
+    dp/8 - 1 steps each (one 15-step cyclic sweep of 24 flops per 2x2 block
+    and 6 per rotated Q pair in each of the dp/16 groups -- which also yields
+    the diagonal tiles of the rotated G -- then the 16x16 tile products
+    Q_a^T G_ab Q_b on the strict upper triangle and V_tile Q_b, plus the
+    convergence sum)."""
     dp = (d + 15) // 16 * 16
-    mp = (m + 15) // 16 * 16
     nt, ng = dp // 16, dp // 16
-    gram = n * 512 * nt * (nt + 1) // 2
     inner = ng * 15 * (64 * 24 + 128 * 6)
     outer = (ng * (ng - 1) // 2) * 2 * (2 * 16 ** 3) + nt * ng * (2 * 16 ** 3)
-    per_sweep = (dp // 8 - 1) * (inner + outer) + 2 * d * d
+    return sweeps * ((dp // 8 - 1) * (inner + outer) + 2 * d * d)
+
+
+def tridiagonal_flops(d: int, m: int) -> int:
+    """Tridiagonal-solver flops on one unit, as the kernel executes them:
+    Householder steps on the full trailing block of order L = d-1-j (the
+    product A v, 2 L^2, and the rank-2 update, 4 L^2, plus 3 L for the
+    reflector and w), 10 multisection rounds of 8 Sturm sequences per
+    eigenvalue (4 flops per pivot), the twisted factorisation's four passes
+    (D-, D+ beside the twist search, D+ above the twist, the vector and its
+    norm: ~4 flops per element each), and the back-transformation (a dot
+    product and an update of 2 L flops each per reflector and vector)."""
+    house = sum(6 * L * L + 3 * L for L in range(2, d))
+    bisect = 10 * 8 * 4 * d * m
+    vectors = 4 * 4 * d * m
+    back = sum(4 * L * m for L in range(2, d))
+    return house + bisect + vectors + back
+
+
+def form_flops(n: int, d: int, m: int, sweeps: int, orbit: int = 1) -> int:
+    """Flops of the patch-forming kernel on one unit: the Gram matrix on the
+    upper-triangle 16x16 tiles (padded), the eigensolver -- the tridiagonal
+    one when `sweeps` is 0, else `sweeps` block-Jacobi sweeps -- and
+    U = Delta V_m (padded)."""
+    dp = (d + 15) // 16 * 16
+    mp = (m + 15) // 16 * 16
+    nt = dp // 16
+    gram = n * 512 * nt * (nt + 1) // 2
+    eig = tridiagonal_flops(d, m) if sweeps == 0 else jacobi_flops(d, sweeps)
     mean = 0 if orbit <= 1 else 2 * orbit * n * d          # orbit mean, formed in both passes over Delta
-    return gram + sweeps * per_sweep + 2 * n * dp * mp + mean
+    return gram + eig + 2 * n * dp * mp + mean
 
 
 def bench_form(args, pool, n_workers):
     """One step = forming the K and the V patches of every (chunk, layer, head)
-    unit of the workload from fp32 deficits (one launch per plane)."""
+    unit of the workload from fp32 deficits (one launch per plane), with the
+    tridiagonal eigensolver (--sweeps 0, the default) or block Jacobi."""
     import numpy as np
     import torch
 
@@ -209,7 +235,7 @@ def bench_form(args, pool, n_workers):
         U = torch.empty((C, L, H, n, m), dtype=torch.bfloat16, device=dev)
         W = torch.empty((C, L, H, m, d), dtype=torch.bfloat16, device=dev)
         done = torch.zeros((C, L, H), dtype=torch.int32, device=dev)
-        tensors[name] = (D, U, W, done, km.prepare_form_patch(D, U, W, sweeps_done=done))
+        tensors[name] = (D, U, W, done, km.prepare_form_patch(D, U, W, sweeps=args.sweeps, sweeps_done=done))
     stream = torch.cuda.current_stream()
 
     def step():
@@ -276,6 +302,7 @@ def bench_form(args, pool, n_workers):
                    "orbit": K, "n_chunks": C, "n_layers": L, "kv_heads": H,
                    "tokens_per_chunk": n, "dim": d, "planes": [p for p, _ in planes],
                    "rank": {p: m for p, m in planes}},
+        "eigensolver": "tridiagonal" if args.sweeps == 0 else f"block Jacobi, at most {args.sweeps} sweeps",
         "sweeps_run": {"min": int(sw.min()), "mean": round(float(sw.mean()), 2), "max": int(sw.max())},
         "roofline": {"bound": "mfma", "achieved": round(achieved, 3), "peak": FP32_MATRIX_PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / FP32_MATRIX_PEAK_TFLOPS, 4), "traffic": None,
@@ -553,6 +580,8 @@ def main():
                          "spacer allocation (other physical placements in HBM), with their own copy ceilings")
     ap.add_argument("--orbit", type=int, default=1,
                     help="form_patch: deficits averaged per unit (orbit patch of K orderings, K plane only)")
+    ap.add_argument("--sweeps", type=int, default=0,
+                    help="form_patch: 0 = tridiagonal eigensolver, > 0 = block Jacobi with this sweep limit")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print(json.dumps({"error": "this operator benchmark runs on exactly one GPU; the work shards by "

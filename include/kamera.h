@@ -347,9 +347,16 @@ typedef struct {
  * l*delta_stride[1] + h*delta_stride[2] + i*delta_stride[3] + j (fp32,
  * 16-byte aligned rows); U and W as in kamera_plane (bf16); sigma (optional,
  * fp32) receives S[:m] at sigma + c*sigma_stride[0] + l*sigma_stride[1] +
- * h*sigma_stride[2] + k.  Method: Gram matrix Delta^T Delta and cyclic Jacobi
- * in fp32 (up to `sweeps` sweeps, 0 = 12), so singular vectors are accurate
- * to ~1e-6 relative where the spectrum has a gap at m.
+ * h*sigma_stride[2] + k.  Method: the Gram matrix Delta^T Delta in fp32,
+ * then its m largest eigenpairs, by one of two fp32 solvers:
+ *   sweeps = 0 (default): Householder reduction to tridiagonal form,
+ *     multisection on Sturm counts for the eigenvalues, twisted
+ *     factorisation for their eigenvectors (close eigenvalues, within 1e-3 of
+ *     the spectral norm, reorthogonalised), back-transformation;
+ *   sweeps > 0: block cyclic Jacobi, at most `sweeps` sweeps, stopping once
+ *     the off-diagonal mass is negligible (12 reach the fp32 floor here).
+ * Either way singular vectors are accurate to ~1e-5 relative where the
+ * spectrum has a gap at m.
  * Orbit patch (Sec. 5, reorder): with n_orbit = K >= 2 the deficits of K
  * orderings of the same chunk set, at delta + o*orbit_stride (o < K), are
  * averaged (fp32) and the mean is truncated as above: the one rank-m patch
@@ -364,7 +371,7 @@ typedef struct {
   int32_t n_tokens;            /* rows n of each Delta                          */
   int32_t dim;                 /* columns: multiple of 4, <= KAMERA_FORM_MAX_DIM */
   int32_t m;                   /* rank kept: 1 .. dim                           */
-  int32_t sweeps;              /* Jacobi sweep limit (0 = 12)                   */
+  int32_t sweeps;              /* 0 = tridiagonal solver, > 0 = Jacobi limit   */
   int32_t n_orbit;             /* deficits averaged per unit (0 or 1 = one)     */
   const float* delta;
   int64_t delta_stride[4];
@@ -375,7 +382,8 @@ typedef struct {
   float* sigma;
   int64_t sigma_stride[3];
   int64_t orbit_stride;        /* elements between orbit members of delta       */
-  int32_t* sweeps_done;        /* optional: Jacobi sweeps each unit ran, dense
+  int32_t* sweeps_done;        /* optional: Jacobi sweeps each unit ran (0 with
+                                  the tridiagonal solver), dense
                                   [n_chunks][n_layers][n_heads] int32          */
 } kamera_form_args;
 

@@ -531,8 +531,10 @@ def prepare_form_patch(delta, U, W, *, sigma=None, sweeps: int = 0, sweeps_done=
     (Sec. 5, reorder: the K orderings' deficits are averaged first);
     U: bf16 [C, L, H, n, m] (receives U S); W: bf16 [C, L, H, m, d]
     (receives Vt[:m]); sigma: optional fp32 [C, L, H, m] (receives S[:m]).
-    m is U's last dimension.  sweeps_done: optional int32 [C, L, H]
-    (contiguous), receives the Jacobi sweeps each unit ran.
+    m is U's last dimension.  sweeps: 0 (default) takes the tridiagonal
+    eigensolver, > 0 block Jacobi with that sweep limit.  sweeps_done:
+    optional int32 [C, L, H] (contiguous), receives the Jacobi sweeps each
+    unit ran (0 with the tridiagonal solver).
     """
     import torch
 

@@ -751,7 +751,7 @@ static int build_form(const kamera_form_args* a, kamera::FormParams& P, bool& la
   P.n_tokens = a->n_tokens;
   P.dim = a->dim;
   P.m = a->m;
-  P.sweeps = a->sweeps == 0 ? 12 : a->sweeps;
+  P.sweeps = a->sweeps;                        // 0: tridiagonal solver
   P.n_units = (int32_t)units;
   P.n_orbit = n_orbit;
   P.orbit_s = n_orbit > 1 ? a->orbit_stride : 0;

@@ -6,14 +6,20 @@
 // (d is padded to dp, a multiple of 16, with zero rows and columns):
 //   1. Gram matrix G = Delta^T Delta on fp32 MFMA (16x16x4), Delta streamed in
 //      32-row tiles with the next tile's loads in flight during the products;
-//   2. block Jacobi on G: the indices form dp/8 blocks of 8; each step pairs
+//   2. the m largest eigenpairs of G, by default (sweeps == 0) from its
+//      tridiagonal form: Householder reduction, multisection on Sturm counts,
+//      twisted-factorisation vectors, back-transformation (tridiag_solve
+//      below).  A unit whose vectors fail that solver's checks (exactly
+//      multiple eigenvalues) forms G again and takes the other method:
+//   2b. block Jacobi on G: the indices form dp/8 blocks of 8; each step pairs
 //      the blocks round-robin (circle method) into dp/16 groups of 16
 //      indices; one wave per group runs one cyclic Jacobi sweep on the
 //      group's 16x16 principal submatrix, accumulating its rotation Q; then
 //      G <- J^T G J and V <- V J with J = diag(Q_group) as 16x16 tile
 //      products on fp32 MFMA.  Sweeps stop once the off-diagonal mass is
 //      negligible against the diagonal;
-//   3. rank the eigenvalues (diag G) of the real indices, keep the m largest;
+//   3. (after Jacobi) rank the eigenvalues (diag G) of the real indices,
+//      keep the m largest;
 //   4. W[k] = V[:, order[k]]^T and U = Delta V_m, rounded to bf16.
 // With an orbit (Sec. 5, reorder) Delta is the mean of the members' deficits,
 // formed on the fly wherever a Delta tile is staged.
@@ -42,6 +48,7 @@ constexpr int kStageVecs = kFormTile * (kFormMaxDim / 4) / kFormThreads;   // 4-
 constexpr int kBlk = 8;                // block-Jacobi block width
 constexpr int kGrp = 2 * kBlk;         // indices of one rotated group (two blocks)
 constexpr int kLdQ = kGrp + 1;         // padded row stride of a group's 16x16 scratch
+constexpr int kFormFallbackSweeps = 12; // Jacobi limit after a failed tridiagonal solve
 
 __host__ __device__ inline int pad16(int d) { return (d + 15) & ~15; }
 // staged Delta tile row stride: == 16 (mod 32), so the four rows one MFMA
@@ -279,6 +286,387 @@ __device__ __forceinline__ void mfma_steps(const float* pa, int sa, const int (&
   }
 }
 
+// ---------------------------------------------------------------------------
+// Tridiagonal eigensolver for the m largest eigenpairs of G (d x d block at
+// row stride ld), the default method:
+//   A. Householder reduction T = Q^T G Q, Q = H_0 ... H_{d-3}, H_j = I - beta_j
+//      v_j v_j^T.  Step j takes column j below the diagonal, x = A[j+1.., j]:
+//      alpha = -sign(x_0) |x|, v = x - alpha e_0, beta = 2 / v^T v; then the
+//      trailing block A[j+1.., j+1..] becomes A - v w^T - w v^T with
+//      p = beta A v, w = p - (beta / 2)(p^T v) v.  alpha is T's subdiagonal
+//      b_j and A[j][j] its diagonal a_j; v is kept in G's column j below the
+//      diagonal for D.
+//   B. The m largest eigenvalues of T by multisection on Sturm counts (the
+//      number of eigenvalues below s is the number of negative pivots of
+//      T - s I), four points per round on four lanes.
+//   C. Their eigenvectors z by twisted factorisation: forward pivots D+ and
+//      backward pivots D- of T - lambda I, twist r where |D+_r + D-_r -
+//      (a_r - lambda)| is least, z_r = 1, z_i = -(b_i / D+_i) z_{i+1} for
+//      i < r and z_i = -(b_{i-1} / D-_i) z_{i-1} for i > r; eigenvalues within
+//      1e-3 |T| of the previous one form a cluster, whose t-th member takes
+//      the t-th least twist and is orthogonalised against the members before
+//      it.
+//   D. V_m = Q Z: the reflectors applied to Z from H_{d-3} down to H_0.
+// In A the matrix stays in registers: thread (rb, cb) holds the 4 x 4 block
+// at rows 4 rb, columns 4 cb (cb = 2 wave + half-wave, rb = lane % 32), so a
+// step moves only the vectors v and p through LDS; the half-wave holding
+// column j+1 forms the next reflector as soon as its own update is done, so a
+// step takes two barriers.  Pivots in B and C divide with the hardware
+// reciprocal (1 ulp), an error of the order of the rounding already in T.
+// Lanes own the columns they write in C and D, so those phases need no
+// workgroup barrier.
+// Exactly multiple eigenvalues (a deficit of lower rank than m, repeated
+// columns, equal singular values) can give twisted vectors that coincide;
+// before D every vector is checked (finite, its residual on T, and for a
+// cluster member what is left after the orthogonalisation), and the solver
+// returns false when one fails, leaving G destroyed.
+// sv: LDS workspace of 7 dp + 24 floats.  Output (on true): eigenvalues at
+// sv + 4 dp in descending order, eigenvectors as the columns of Z [d][ldz].
+// ---------------------------------------------------------------------------
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xf, 0xf, false));
+}
+// sum over each aligned group of 8 lanes: quad_perm [1,0,3,2], [2,3,0,1],
+// then row_half_mirror (lane i <-> 7 - i: the other quad)
+__device__ __forceinline__ float sum8(float v) {
+  v += dpp_f<0xB1>(v);
+  v += dpp_f<0x4E>(v);
+  return v + dpp_f<0x141>(v);
+}
+
+__device__ bool tridiag_solve(float* G, int ld, float* Z, int ldz, int d, int dp, int m, float* sv, int* s_cs,
+                              int* s_fail) {
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  float* const s_a = sv;                       // T's diagonal
+  float* const s_b = sv + dp;                  // T's subdiagonal
+  float* const s_beta = sv + 2 * dp;           // reflector scales
+  float* const s_p = sv + 3 * dp;              // p of the current step; b^2 from B on
+  float* const s_lam = sv + 4 * dp;            // eigenvalues, descending
+  float* const s_v = sv + 5 * dp;              // [2][dp] v of alternate steps
+  float* const s_misc = sv + 7 * dp;           // Gershgorin lo, hi, pivot floor
+  float* const s_kred = sv + 7 * dp + 8;       // [16] per-wave p^T v partials
+  if (tid == 0) *s_fail = 0;
+
+  // ---- A. Householder reduction, the matrix in registers ----
+  {
+    const int half = lane >> 5, rb = lane & 31, cb = 2 * wave + half;
+    const int hbase = lane & 32;               // first lane of this half-wave
+    const bool rin = 4 * rb < dp, cin = 4 * cb < dp;
+    float A[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const int r = 4 * rb + i, cc = 4 * cb + c;
+        A[i][c] = (r < d && cc < d) ? G[r * ld + cc] : 0.f;
+      }
+    // the reflector of column j, by the half-wave holding it (cb == j / 4):
+    // writes v into s_v[j & 1] and G's column j, a_j, b_j and beta_j
+    auto reflect = [&](int j) {
+      const int jj = j & 3, j1 = (j + 1) & 3;
+      float colv[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) colv[i] = jj == 0 ? A[i][0] : jj == 1 ? A[i][1] : jj == 2 ? A[i][2] : A[i][3];
+      float sq = 0.f;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int r = 4 * rb + i;
+        if (r > j + 1 && r < d) sq += colv[i] * colv[i];
+      }
+      sq = sum8(sq);
+      sq += dpp_f<0x140>(sq);                  // row_mirror: the other 8 lanes of the row
+      sq += __shfl_xor(sq, 16, 64);
+      const float x0 = __shfl(j1 == 0 ? colv[0] : j1 == 1 ? colv[1] : j1 == 2 ? colv[2] : colv[3],
+                              hbase + ((j + 1) >> 2), 64);
+      const float aj = __shfl(jj == 0 ? colv[0] : jj == 1 ? colv[1] : jj == 2 ? colv[2] : colv[3],
+                              hbase + (j >> 2), 64);
+      float beta = 0.f, alpha = x0, v0 = 0.f;
+      if (sq != 0.f) {                         // else already reduced: H_j = I
+        const float nrm = sqrtf(x0 * x0 + sq);
+        alpha = x0 >= 0.f ? -nrm : nrm;
+        v0 = x0 - alpha;
+        beta = 2.f / (v0 * v0 + sq);
+      }
+      f32x4v vv;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int r = 4 * rb + i;
+        vv[i] = (beta == 0.f || r <= j || r >= d) ? 0.f : (r == j + 1 ? v0 : colv[i]);
+        if (r > j && r < d) G[r * ld + j] = vv[i];
+      }
+      if (rin) *reinterpret_cast<f32x4v*>(s_v + (j & 1) * dp + 4 * rb) = vv;
+      if (rb == 0) {
+        s_a[j] = aj;
+        s_b[j] = alpha;
+        s_beta[j] = beta;
+      }
+    };
+    if (d >= 3 && cb == 0) reflect(0);
+    for (int j = 0; j < d - 2; ++j) {
+      __syncthreads();
+      const float beta = s_beta[j];
+      const float* vb = s_v + (j & 1) * dp;
+      // columns of this wave: 8 wave .. 8 wave + 7; none left in the trailing block?
+      const bool active = 8 * wave + 7 > j && 8 * wave < d;
+      // p = beta A v over this thread's block, summed over the half-wave's 32
+      // row blocks: the 4 column sums are halved twice by exchanges (lanes
+      // 16 and 8 apart keep two, then one of them) and the last one summed
+      // over its 8 lanes, so that lane group (b4, b3) ends with column
+      // 4 cb + 2 b4 + b3
+      float keep = 0.f;
+      if (active) {
+        const f32x4v vr = rin ? *reinterpret_cast<const f32x4v*>(vb + 4 * rb) : (f32x4v){0.f, 0.f, 0.f, 0.f};
+        float part[4];
+#pragma unroll
+        for (int c = 0; c < 4; ++c) part[c] = A[0][c] * vr[0] + A[1][c] * vr[1] + A[2][c] * vr[2] + A[3][c] * vr[3];
+        const bool b4 = lane & 16, b3 = lane & 8;
+        float s0 = b4 ? part[2] : part[0], s1 = b4 ? part[3] : part[1];
+        s0 += __shfl_xor(b4 ? part[0] : part[2], 16, 64);
+        s1 += __shfl_xor(b4 ? part[1] : part[3], 16, 64);
+        keep = b3 ? s1 : s0;
+        keep += __shfl_xor(b3 ? s0 : s1, 8, 64);
+        keep = sum8(keep) * beta;
+      }
+      const int col = 4 * cb + ((lane >> 3) & 3);   // the column this lane's group ended with
+      const bool trail = col > j && col < d;
+      float pv = (active && trail) ? keep * vb[col] : 0.f;
+      pv += __shfl_xor(pv, 8, 64);
+      pv += __shfl_xor(pv, 16, 64);
+      pv += __shfl_xor(pv, 32, 64);
+      if ((lane & 7) == 0 && cin) s_p[col] = (active && trail) ? keep : 0.f;
+      if (lane == 0) s_kred[wave] = active ? pv : 0.f;
+      __syncthreads();
+      if (active) {
+        // A -= v w^T + w v^T, w = p - K v, K = (beta / 2) p^T v; p and v are
+        // zero outside the trailing block, so the update is too
+        float kd = 0.f;
+#pragma unroll
+        for (int w4 = 0; w4 < kWaves / 4; ++w4) {
+          const f32x4v k4 = *reinterpret_cast<const f32x4v*>(s_kred + 4 * w4);
+          kd += (k4[0] + k4[1]) + (k4[2] + k4[3]);
+        }
+        const float K = 0.5f * beta * kd;
+        const f32x4v z4 = {0.f, 0.f, 0.f, 0.f};
+        const f32x4v vr = rin ? *reinterpret_cast<const f32x4v*>(vb + 4 * rb) : z4;
+        const f32x4v pr = rin ? *reinterpret_cast<const f32x4v*>(s_p + 4 * rb) : z4;
+        const f32x4v vc = cin ? *reinterpret_cast<const f32x4v*>(vb + 4 * cb) : z4;
+        const f32x4v pc = cin ? *reinterpret_cast<const f32x4v*>(s_p + 4 * cb) : z4;
+        const f32x4v wr = pr - K * vr, wc = pc - K * vc;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int c = 0; c < 4; ++c) A[i][c] -= vr[i] * wc[c] + wr[i] * vc[c];
+      }
+      if (j + 1 < d - 2 && cb == ((j + 1) >> 2)) reflect(j + 1);
+    }
+    // the last 2 x 2 block of T (the whole of T when d <= 2)
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const int r = 4 * rb + i, cc = 4 * cb + c;
+        if (d >= 2 && cc == d - 2 && r == d - 2) s_a[d - 2] = A[i][c];
+        if (d >= 2 && cc == d - 2 && r == d - 1) s_b[d - 2] = A[i][c];
+        if (cc == d - 1 && r == d - 1) s_a[d - 1] = A[i][c];
+      }
+  }
+  __syncthreads();
+
+  // ---- B. the m largest eigenvalues: 4 lanes per eigenvalue ----
+  float* const s_b2 = s_p;
+  if (wave == 0) {                             // Gershgorin interval, b^2, pivot floor
+    float lo = 3.4e38f, hi = -3.4e38f, b2max = 0.f;
+    for (int i = lane; i < d; i += 64) {
+      const float bl = i > 0 ? s_b[i - 1] : 0.f, br = i < d - 1 ? s_b[i] : 0.f;
+      const float r = fabsf(bl) + fabsf(br);
+      lo = fminf(lo, s_a[i] - r);
+      hi = fmaxf(hi, s_a[i] + r);
+      s_b2[i] = br * br;
+      b2max = fmaxf(b2max, br * br);
+    }
+    for (int o = 32; o > 0; o >>= 1) {
+      lo = fminf(lo, __shfl_xor(lo, o, 64));
+      hi = fmaxf(hi, __shfl_xor(hi, o, 64));
+      b2max = fmaxf(b2max, __shfl_xor(b2max, o, 64));
+    }
+    if (lane == 0) {
+      s_misc[0] = lo;
+      s_misc[1] = hi;
+      s_misc[2] = 1.17549435e-38f * fmaxf(1.f, b2max);
+    }
+  }
+  __syncthreads();
+  const float tnorm = fmaxf(fabsf(s_misc[0]), fabsf(s_misc[1]));   // |T| bound
+  if (wave < (4 * m + 63) / 64) {
+    const int k = tid >> 2, t = tid & 3;
+    const int q = d - 1 - k;                   // ascending index of the k-th largest
+    const float pivmin = s_misc[2];
+    float lo = s_misc[0], hi = s_misc[1];
+    for (int it = 0; it < 11; ++it) {          // width / 5^11: below fp32 rounding of |T|
+      const float w = hi - lo;
+      const float x = lo + w * (float)(t + 1) * 0.2f;
+      int cnt = 0;
+      float qv = s_a[0] - x;
+      if (fabsf(qv) < pivmin) qv = -pivmin;
+      cnt += qv < 0.f;
+#pragma unroll 8
+      for (int i = 1; i < d; ++i) {
+        qv = (s_a[i] - x) - s_b2[i - 1] * __builtin_amdgcn_rcpf(qv);
+        if (fabsf(qv) < pivmin) qv = -pivmin;
+        cnt += qv < 0.f;
+      }
+      // the points at or below the eigenvalue: a prefix of the group's lanes
+      const uint64_t bal = __ballot(k < m && cnt <= q);
+      const int nb = __popcll((bal >> (lane & ~3)) & 0xfull);
+      const float nlo = nb > 0 ? lo + w * (float)nb * 0.2f : lo;
+      const float nhi = nb < 4 ? lo + w * (float)(nb + 1) * 0.2f : hi;
+      lo = nlo;
+      hi = fmaxf(nhi, nlo);
+    }
+    if (k < m && t == 0) s_lam[k] = 0.5f * (lo + hi);
+  }
+  __syncthreads();
+  // clusters: runs of eigenvalues within 1e-3 |T| of their predecessor
+  // (equal ones always, also when T = 0)
+  if (tid == 0) {
+    s_cs[0] = 0;
+    for (int j = 1; j < m; ++j) s_cs[j] = (s_lam[j - 1] - s_lam[j] <= 1e-3f * tnorm) ? s_cs[j - 1] : j;
+  }
+  __syncthreads();
+
+  // ---- C. eigenvectors of T: one lane per eigenvalue, in its column of Z ----
+  // D- is kept in the column while D+ is recomputed where it is needed: the
+  // twist search runs D+ forward beside it, then D+ overwrites D- above the
+  // twist (where D- is no longer read) for the upward recurrence.  A zero
+  // pivot is replaced by 1e-30.
+  if (tid < m) {
+    const int k = tid;
+    const float lam = s_lam[k];
+    const float tiny = 1e-30f;
+    float* z = Z + k;
+    float dmv = s_a[d - 1] - lam;              // backward pivots D-
+    z[(d - 1) * ldz] = dmv;
+#pragma unroll 8
+    for (int i = d - 2; i >= 0; --i) {
+      dmv = (s_a[i] - lam) - s_b2[i] * __builtin_amdgcn_rcpf(dmv != 0.f ? dmv : tiny);
+      z[i * ldz] = dmv;
+    }
+    // twist: the (k - cluster start)-th least |gamma_i| (ties: lower index)
+    const int rank = k - s_cs[k] < d - 1 ? k - s_cs[k] : d - 1;
+    int r = 0;
+    float prev = -1.f;
+    int prev_i = -1;
+    for (int s2 = 0; s2 <= rank; ++s2) {
+      float best = 3.4e38f, dpv = s_a[0] - lam;
+      int bi = 0;
+#pragma unroll 8
+      for (int i = 0; i < d; ++i) {
+        if (i > 0) dpv = (s_a[i] - lam) - s_b2[i - 1] * __builtin_amdgcn_rcpf(dpv != 0.f ? dpv : tiny);
+        const float g = fabsf(dpv + z[i * ldz] - (s_a[i] - lam));
+        const bool after = g > prev || (g == prev && i > prev_i);
+        if (after && g < best) {
+          best = g;
+          bi = i;
+        }
+      }
+      prev = best;
+      prev_i = bi;
+      r = bi;
+    }
+    float dpv = s_a[0] - lam;                  // D+ above the twist
+#pragma unroll 8
+    for (int i = 0; i < r; ++i) {
+      if (i > 0) dpv = (s_a[i] - lam) - s_b2[i - 1] * __builtin_amdgcn_rcpf(dpv != 0.f ? dpv : tiny);
+      z[i * ldz] = dpv;
+    }
+    float nrm2 = 1.f, x = 1.f;
+#pragma unroll 8
+    for (int i = r - 1; i >= 0; --i) {
+      const float qd = z[i * ldz];
+      x = -s_b[i] * __builtin_amdgcn_rcpf(qd != 0.f ? qd : tiny) * x;
+      z[i * ldz] = x;
+      nrm2 += x * x;
+    }
+    z[r * ldz] = 1.f;
+    x = 1.f;
+#pragma unroll 8
+    for (int i = r + 1; i < d; ++i) {
+      const float qd = z[i * ldz];
+      x = -s_b[i - 1] * __builtin_amdgcn_rcpf(qd != 0.f ? qd : tiny) * x;
+      z[i * ldz] = x;
+      nrm2 += x * x;
+    }
+    const float inv = 1.f / sqrtf(nrm2);
+#pragma unroll 8
+    for (int i = 0; i < d; ++i) z[i * ldz] *= inv;
+  }
+  __syncthreads();
+  // cluster members orthogonalised against the members before them (wave 0)
+  if (wave == 0) {
+    for (int k = 1; k < m; ++k) {
+      const int c0 = s_cs[k];
+      if (c0 == k) continue;
+      for (int i = c0; i < k; ++i) {
+        float dt = 0.f;
+        for (int r = lane; r < d; r += 64) dt += Z[r * ldz + i] * Z[r * ldz + k];
+        for (int o = 32; o > 0; o >>= 1) dt += __shfl_xor(dt, o, 64);
+        for (int r = lane; r < d; r += 64) Z[r * ldz + k] -= dt * Z[r * ldz + i];
+      }
+      float n2 = 0.f;
+      for (int r = lane; r < d; r += 64) n2 += Z[r * ldz + k] * Z[r * ldz + k];
+      for (int o = 32; o > 0; o >>= 1) n2 += __shfl_xor(n2, o, 64);
+      // a member that was mostly inside the span of the ones before it is
+      // not trusted (twisted vectors of an exactly multiple eigenvalue)
+      if (lane == 0 && !(n2 >= 0.25f)) *s_fail = 1;
+      const float inv = n2 > 0.f ? 1.f / sqrtf(n2) : 0.f;
+      for (int r = lane; r < d; r += 64) Z[r * ldz + k] *= inv;
+    }
+  }
+  __syncthreads();
+  // every vector must satisfy |T z - lambda z| <= 2^-16 |T| (good ones reach
+  // ~d u |T|); a larger or non-finite residual sends the unit to Jacobi
+  if (tid < m) {
+    const float lam = s_lam[tid], inv_tn = tnorm > 0.f ? 1.f / tnorm : 0.f;
+    float r2 = 0.f;
+#pragma unroll 8
+    for (int i = 0; i < d; ++i) {
+      float t = (s_a[i] - lam) * Z[i * ldz + tid];
+      if (i > 0) t += s_b[i - 1] * Z[(i - 1) * ldz + tid];
+      if (i < d - 1) t += s_b[i] * Z[(i + 1) * ldz + tid];
+      t *= inv_tn;
+      r2 += t * t;
+    }
+    if (!(r2 <= 0x1p-32f)) *s_fail = 1;
+  }
+  __syncthreads();
+  if (*s_fail) return false;
+
+  // ---- D. V_m = Q Z: 16 lanes per column, the reflectors from the last ----
+  for (int k0 = 0; k0 < m; k0 += 4 * kWaves) {
+    const int k = k0 + 4 * wave + (lane >> 4), sl = lane & 15;
+    const bool own = k < m;
+    for (int j = d - 3; j >= 0; --j) {
+      const float beta = s_beta[j];
+      if (beta == 0.f) continue;
+      const int L = d - j - 1;
+      const int ov = (j + 1) * ld + j;
+      float y = 0.f;
+      if (own)
+        for (int i = sl; i < L; i += 16) y += G[ov + i * ld] * Z[(j + 1 + i) * ldz + k];
+      y += __shfl_xor(y, 1, 64);
+      y += __shfl_xor(y, 2, 64);
+      y += __shfl_xor(y, 4, 64);
+      y += __shfl_xor(y, 8, 64);
+      y *= beta;
+      if (own)
+        for (int i = sl; i < L; i += 16) Z[(j + 1 + i) * ldz + k] -= y * G[ov + i * ld];
+    }
+  }
+  __syncthreads();
+  return true;
+}
+
 __global__ __launch_bounds__(kFormThreads) void form_patch_kernel(const FormParams /*by value, read in place*/) {
   const FormParams& P = *static_cast<const FormParams*>((const void*)__builtin_amdgcn_kernarg_segment_ptr());
   float* const lds_f = form_lds;
@@ -307,8 +695,13 @@ __global__ __launch_bounds__(kFormThreads) void form_patch_kernel(const FormPara
   const int wave = tid >> 6, lane = tid & 63;
   const int lj = lane >> 4, lr = lane & 15;  // MFMA operand slot (k within a step) and row/column
 
+  // With the tridiagonal solver (sweeps == 0) a unit whose vectors fail its
+  // checks forms G again and runs block Jacobi instead.
+  int sweeps = P.sweeps;
+  bool tri_ok = false;
+  __shared__ int s_fail;
   // ---- 1. G = Delta^T Delta on MFMA: wave owns up to 3 tiles (I <= J) ----
-  {
+  auto form_gram = [&]() {
     const int nt = dp / 16;
     const int ntiles = nt * (nt + 1) / 2;
     const int ldt = tile_ld(dp);
@@ -378,6 +771,24 @@ __global__ __launch_bounds__(kFormThreads) void form_patch_kernel(const FormPara
     // V = I (the staged tile is no longer needed)
     for (int e = tid; e < dp * dp; e += kFormThreads) V[(e / dp) * ld + e % dp] = (e / dp == e % dp) ? 1.f : 0.f;
     __syncthreads();
+  };
+  form_gram();
+  if (sweeps == 0) {
+    // ---- 2'. tridiagonal eigensolver: eigenpairs in order, eigenvalues onto
+    // G's diagonal and vectors into V's first m columns ----
+    float* sv = Ss;                            // 7 dp + 24 floats of the 51 dp here
+    tri_ok = tridiag_solve(G, ld, V, ld, d, dp, m, sv, s_order, &s_fail);
+    if (tri_ok) {
+      if (tid < m) {
+        G[tid * ld + tid] = sv[4 * dp + tid];
+        s_order[tid] = tid;
+      }
+      if (P.sweeps_done != nullptr && tid == 0) P.sweeps_done[unit] = 0;
+      __syncthreads();
+    } else {
+      sweeps = kFormFallbackSweeps;
+      form_gram();
+    }
   }
 
   // ---- 2. block Jacobi ----
@@ -387,7 +798,7 @@ __global__ __launch_bounds__(kFormThreads) void form_patch_kernel(const FormPara
   int sweeps_run = 0;
   int cur = 0;                                 // buffer of the step being formed
   bool pending = false;                        // V still owes the previous step's rotation
-  for (int sweep = 0; sweep < P.sweeps; ++sweep) {
+  for (int sweep = 0; sweep < (tri_ok ? 0 : sweeps); ++sweep) {
     // stop once the off-diagonal mass is negligible against the diagonal
     float off = 0.f, dia = 0.f;
     for (int e = tid; e < d * d; e += kFormThreads) {
@@ -514,10 +925,10 @@ __global__ __launch_bounds__(kFormThreads) void form_patch_kernel(const FormPara
             kWaves, wave, lj, lr);
     __syncthreads();
   }
-  if (P.sweeps_done != nullptr && tid == 0) P.sweeps_done[unit] = sweeps_run;
+  if (P.sweeps_done != nullptr && tid == 0 && !tri_ok) P.sweeps_done[unit] = sweeps_run;
 
-  // ---- 3. the m largest eigenvalues (ties by index) ----
-  if (tid < d) {
+  // ---- 3. the m largest eigenvalues (ties by index), after Jacobi ----
+  if (!tri_ok && tid < d) {
     const float li = G[tid * ld + tid];
     int rank = 0;
     for (int j = 0; j < d; ++j) {

@@ -563,19 +563,35 @@ def test_scatter_bad_page_is_flagged(device):
 # compile-side patch forming
 # ---------------------------------------------------------------------------
 
+def _check_patch(delta, Ub, Wb, sg, m, tag):
+    """One unit's patch against the fp64 truncated SVD: product, singular
+    values, W's orthonormal rows and the Eckart-Young residual.  U and W are
+    stored in bf16 (unit roundoff 2^-8 each), so the product's relative
+    Frobenius error is bounded by ~2 * 2^-8 plus the fp32 subspace error; the
+    bound used is 2^-6."""
+    Dl = delta.astype(np.float64)
+    Ur, Wr, S = ref.form_patch(Dl, m)
+    Ug, Wg = ref.bf16_to_f64(Ub), ref.bf16_to_f64(Wb)
+    prod_ref = Ur @ Wr
+    rel = np.linalg.norm(Ug @ Wg - prod_ref) / np.linalg.norm(prod_ref)
+    assert rel <= 2.0 ** -6, (tag, rel)
+    assert np.max(np.abs(sg - S[:m]) / S[:m]) <= 1e-4, (tag, sg[:4], S[:4])
+    assert np.max(np.abs(Wg @ Wg.T - np.eye(m))) <= 2.0 ** -6, tag
+    opt = np.linalg.norm(Dl - prod_ref)
+    got = np.linalg.norm(Dl - Ug @ Wg)
+    assert got <= opt + 2.0 ** -6 * np.linalg.norm(prod_ref), (tag, got, opt)
+
+
 @pytest.mark.parametrize("n,d,m", [(100, 128, 16), (1024, 128, 64), (37, 64, 8), (50, 36, 1), (64, 32, 32),
                                    (7, 4, 2), (130, 16, 16), (2000, 128, 128), (300, 100, 40)])
 def test_form_patch_matches_svd(device, n, d, m):
-    """Planted deficits with a spectral gap at m (rank-m signal + small noise):
-    U W must match the fp64 truncated SVD's product, the singular values the
-    fp64 ones, W's rows must be orthonormal and the residual Eckart-Young's.
-    U and W are stored in bf16 (unit roundoff 2^-8 each), so the product's
-    relative Frobenius error is bounded by ~2 * 2^-8 plus the fp32 subspace
-    error; the bound used is 2^-6."""
+    """Planted deficits with a spectral gap at m (rank-m signal + small noise),
+    through both eigensolvers (the tridiagonal default and block Jacobi): U W
+    must match the fp64 truncated SVD's product, the singular values the fp64
+    ones, W's rows must be orthonormal and the residual Eckart-Young's."""
     import paper_2606_23581_amd as km
     import torch
 
-    print(f"[case] form_patch n{n} d{d} m{m}", flush=True)
     rng = np.random.default_rng(n * 1000 + d + m)
     C, L, H = 2, 2, 2
     delta = np.empty((C, L, H, n, d), np.float32)
@@ -585,31 +601,83 @@ def test_form_patch_matches_svd(device, n, d, m):
         sig = np.linspace(10.0, 2.0, m)
         delta[idx] = (A * sig) @ B.T + 0.01 * rng.standard_normal((n, d))
     dt = torch.from_numpy(delta).to(device)
-    U = torch.zeros((C, L, H, n, m), dtype=torch.bfloat16, device=device)
-    W = torch.zeros((C, L, H, m, d), dtype=torch.bfloat16, device=device)
-    sigma = torch.zeros((C, L, H, m), dtype=torch.float32, device=device)
-    done = torch.full((C, L, H), -1, dtype=torch.int32, device=device)
-    km.form_patch(dt, U, W, sigma=sigma, sweeps_done=done)
-    torch.cuda.synchronize()
-    # converged within the default limit of 12 sweeps, after at least one
-    assert ((done >= 1) & (done < 12)).all(), done.cpu().numpy()
-    capped = torch.full_like(done, -1)
-    km.form_patch(dt, torch.empty_like(U), torch.empty_like(W), sweeps=1, sweeps_done=capped)
+    for sweeps in (0, 12):
+        print(f"[case] form_patch n{n} d{d} m{m} sweeps {sweeps}", flush=True)
+        U = torch.zeros((C, L, H, n, m), dtype=torch.bfloat16, device=device)
+        W = torch.zeros((C, L, H, m, d), dtype=torch.bfloat16, device=device)
+        sigma = torch.zeros((C, L, H, m), dtype=torch.float32, device=device)
+        done = torch.full((C, L, H), -1, dtype=torch.int32, device=device)
+        km.form_patch(dt, U, W, sigma=sigma, sweeps=sweeps, sweeps_done=done)
+        torch.cuda.synchronize()
+        if sweeps == 0:
+            assert (done == 0).all(), done.cpu().numpy()        # no Jacobi sweep with the tridiagonal solver
+        else:
+            # Jacobi converged within 12 sweeps, after at least one
+            assert ((done >= 1) & (done < 12)).all(), done.cpu().numpy()
+        Ub, Wb, sg = bits(U), bits(W), sigma.cpu().numpy()
+        for idx in np.ndindex(C, L, H):
+            _check_patch(delta[idx], Ub[idx], Wb[idx], sg[idx], m, (sweeps,) + idx)
+    capped = torch.full((C, L, H), -1, dtype=torch.int32, device=device)
+    km.form_patch(dt, torch.empty((C, L, H, n, m), dtype=torch.bfloat16, device=device),
+                  torch.empty((C, L, H, m, d), dtype=torch.bfloat16, device=device), sweeps=1, sweeps_done=capped)
     torch.cuda.synchronize()
     assert (capped == 1).all()
-    Ub, Wb, sg = bits(U), bits(W), sigma.cpu().numpy()
-    for idx in np.ndindex(C, L, H):
-        Dl = delta[idx].astype(np.float64)
-        Ur, Wr, S = ref.form_patch(Dl, m)
-        Ug, Wg = ref.bf16_to_f64(Ub[idx]), ref.bf16_to_f64(Wb[idx])
-        prod_ref = Ur @ Wr
-        rel = np.linalg.norm(Ug @ Wg - prod_ref) / np.linalg.norm(prod_ref)
-        assert rel <= 2.0 ** -6, (idx, rel)
-        assert np.max(np.abs(sg[idx] - S[:m]) / S[:m]) <= 1e-4, (idx, sg[idx][:4], S[:4])
-        assert np.max(np.abs(Wg @ Wg.T - np.eye(m))) <= 2.0 ** -6
-        opt = np.linalg.norm(Dl - prod_ref)
-        got = np.linalg.norm(Dl - Ug @ Wg)
-        assert got <= opt + 2.0 ** -6 * np.linalg.norm(prod_ref), (idx, got, opt)
+
+
+@pytest.mark.parametrize("sweeps", [0, 12])
+def test_form_patch_degenerate_spectra(device, sweeps):
+    """Spectra where the eigensolvers meet multiple or zero eigenvalues:
+    the patch is still the truncation wherever that is unique, and W's rows
+    stay orthonormal.
+      * zero deficit: U = 0, sigma = 0;
+      * m equal singular values over noise-free rank m: U W = Delta;
+      * identical columns (rank 1, a (d-1)-fold zero eigenvalue): U W = Delta;
+      * a decaying spectrum without a gap at m, s_k = (1 + k)^(-1/4), the
+        shape of the benchmark's deficits: the Eckart-Young residual."""
+    import paper_2606_23581_amd as km
+    import torch
+
+    print(f"[case] form_patch degenerate spectra sweeps {sweeps}", flush=True)
+    rng = np.random.default_rng(4242)
+    cases = []
+    cases.append(("zero", np.zeros((64, 32)), 8))
+    Aq = np.linalg.qr(rng.standard_normal((100, 8)))[0]
+    Bq = np.linalg.qr(rng.standard_normal((32, 8)))[0]
+    cases.append(("equal", (Aq * 5.0) @ Bq.T, 8))
+    X = rng.standard_normal((50, 1))
+    cases.append(("identical_columns", np.repeat(X, 16, axis=1), 4))
+    A = rng.standard_normal((1024, 128))
+    Q = np.linalg.qr(rng.standard_normal((128, 128)))[0]
+    cases.append(("decaying", (A * (1.0 + np.arange(128)) ** -0.25) @ Q, 64))
+    for name, D, m in cases:
+        n, d = D.shape
+        D32 = D.astype(np.float32)
+        dt = torch.from_numpy(D32.reshape(1, 1, 1, n, d)).to(device)
+        U = torch.zeros((1, 1, 1, n, m), dtype=torch.bfloat16, device=device)
+        W = torch.zeros((1, 1, 1, m, d), dtype=torch.bfloat16, device=device)
+        sigma = torch.full((1, 1, 1, m), -1.0, dtype=torch.float32, device=device)
+        km.form_patch(dt, U, W, sigma=sigma, sweeps=sweeps)
+        torch.cuda.synchronize()
+        Ug, Wg, sg = ref.bf16_to_f64(bits(U)[0, 0, 0]), ref.bf16_to_f64(bits(W)[0, 0, 0]), sigma.cpu().numpy()[0, 0, 0]
+        assert np.all(np.isfinite(Ug)) and np.all(np.isfinite(Wg)) and np.all(np.isfinite(sg)), name
+        assert np.max(np.abs(Wg @ Wg.T - np.eye(m))) <= 2.0 ** -6, name
+        Dl = D32.astype(np.float64)
+        if name == "zero":
+            assert np.all(Ug == 0) and np.all(sg == 0), name
+        elif name in ("equal", "identical_columns"):
+            rel = np.linalg.norm(Ug @ Wg - Dl) / np.linalg.norm(Dl)
+            assert rel <= 2.0 ** -6, (name, rel)
+            # the square root of an fp32 eigenvalue of G near zero carries an
+            # absolute error ~ sqrt(d u) sigma_1 (u = 2^-24): 2^-9 sigma_1 at d <= 32
+            S = np.linalg.svd(Dl, compute_uv=False)[:m]
+            assert np.max(np.abs(sg - S)) <= 2.0 ** -9 * S[0], (name, sg, S)
+        else:
+            Ur, Wr, S = ref.form_patch(Dl, m)
+            prod_ref = Ur @ Wr
+            opt = np.linalg.norm(Dl - prod_ref)
+            got = np.linalg.norm(Dl - Ug @ Wg)
+            assert got <= opt + 2.0 ** -6 * np.linalg.norm(prod_ref), (name, got, opt)
+            assert np.max(np.abs(sg - S[:m]) / S[:m]) <= 1e-4, (name, sg[:4], S[:4])
 
 
 @pytest.mark.parametrize("K,n,d,m", [(3, 200, 128, 16), (6, 64, 64, 8), (1, 90, 128, 32)])
