@@ -294,8 +294,7 @@ __device__ __forceinline__ void mfma_steps(const float* pa, int sa, const int (&
 //      alpha = -sign(x_0) |x|, v = x - alpha e_0, beta = 2 / v^T v; then the
 //      trailing block A[j+1.., j+1..] becomes A - v w^T - w v^T with
 //      p = beta A v, w = p - (beta / 2)(p^T v) v.  alpha is T's subdiagonal
-//      b_j and A[j][j] its diagonal a_j; v is kept in G's column j below the
-//      diagonal for D.
+//      b_j and A[j][j] its diagonal a_j; v is kept in G's row j for D.
 //   B. The m largest eigenvalues of T by multisection on Sturm counts (the
 //      number of eigenvalues below s is the number of negative pivots of
 //      T - s I), four points per round on four lanes.
@@ -307,11 +306,12 @@ __device__ __forceinline__ void mfma_steps(const float* pa, int sa, const int (&
 //      the t-th least twist and is orthogonalised against the members before
 //      it.
 //   D. V_m = Q Z: the reflectors applied to Z from H_{d-3} down to H_0.
-// In A the matrix stays in registers: thread (rb, cb) holds the 4 x 4 block
-// at rows 4 rb, columns 4 cb (cb = 2 wave + half-wave, rb = lane % 32), so a
-// step moves only the vectors v and p through LDS; the half-wave holding
-// column j+1 forms the next reflector as soon as its own update is done, so a
-// step takes two barriers.  Pivots in B and C divide with the hardware
+// In A the matrix stays in registers: thread (rb, cb) holds the 8 x 2 block
+// at rows 8 rb, columns 2 cb (cb = 4 wave + lane / 16, rb = lane % 16), so
+// that a column block's 16 row blocks form one DPP row and every reduction
+// is DPP adds and lane reads; a step moves only the vectors v and p through
+// LDS, and the row holding column j+1 forms the next reflector as soon as
+// its own update is done, so a step takes two barriers.  Pivots in B and C divide with the hardware
 // reciprocal (1 ulp), an error of the order of the rounding already in T.
 // Lanes own the columns they write in C and D, so those phases need no
 // workgroup barrier.
@@ -320,7 +320,7 @@ __device__ __forceinline__ void mfma_steps(const float* pa, int sa, const int (&
 // before D every vector is checked (finite, its residual on T, and for a
 // cluster member what is left after the orthogonalisation), and the solver
 // returns false when one fails, leaving G destroyed.
-// sv: LDS workspace of 7 dp + 24 floats.  Output (on true): eigenvalues at
+// sv: LDS workspace of 9 dp floats (16-byte aligned).  Output (on true): eigenvalues at
 // sv + 4 dp in descending order, eigenvectors as the columns of Z [d][ldz].
 // ---------------------------------------------------------------------------
 template <int CTRL>
@@ -335,137 +335,379 @@ __device__ __forceinline__ float sum8(float v) {
   return v + dpp_f<0x141>(v);
 }
 
+// A compile-time integer as a function argument.
+template <int V>
+struct IntC {
+  static constexpr int value = V;
+};
+
+// 16-byte LDS load of four consecutive floats.
+__device__ __forceinline__ f32x4v ld4(const float* p) { return *reinterpret_cast<const f32x4v*>(p); }
+
+// One eigenvector of T (diagonal a, subdiagonal b, b2[i] = b_i^2 and
+// b2s[i] = b_{i-1}^2, both floored at FLT_MIN, 0 where b does not exist) for
+// the eigenvalue lam by twisted factorisation, into z[i * ldz].  D- is kept
+// in the column while D+ is recomputed where it is needed: the twist search
+// runs D+ forward beside it, then D+ overwrites D- above the twist (where D-
+// is no longer read) for the upward recurrence.  The pivot recurrences run in
+// IEEE arithmetic as the Sturm counts do, from an infinite pivot beyond the
+// first row; in the vector's recurrences a zero pivot is replaced by 1e-30.
+// The twist is the rank-th least |gamma_i| (ties: lower index).  Every loop
+// runs over aligned groups of four rows (d is a multiple of 4) with the
+// shared operands read as 16-byte vectors, the next group loaded ahead.
+__device__ __forceinline__ void twisted_vector(const float* __restrict__ a, const float* __restrict__ b,
+                                               const float* __restrict__ b2, const float* __restrict__ b2s,
+                                               float* __restrict__ z, int ldz, int d, float lam, int rank) {
+  const float tiny = 1e-30f;
+  const int ng = d >> 2;
+  {                                            // backward pivots D-, bottom up
+    float dmv = __builtin_inff();
+    f32x4v an = ld4(a + d - 4), bn = ld4(b2 + d - 4);
+    for (int g = ng - 1; g >= 0; --g) {
+      const f32x4v ac = an, bc = bn;
+      if (g > 0) {
+        an = ld4(a + 4 * g - 4);
+        bn = ld4(b2 + 4 * g - 4);
+      }
+#pragma unroll
+      for (int u = 3; u >= 0; --u) {
+        dmv = (ac[u] - lam) - bc[u] * __builtin_amdgcn_rcpf(dmv);
+        z[(4 * g + u) * ldz] = dmv;
+      }
+    }
+  }
+  int r = 0;
+  float prev = -1.f;
+  int prev_i = -1;
+  for (int s2 = 0; s2 <= rank; ++s2) {         // twist search, D+ top down beside D-
+    float best = 3.4e38f, dpv = __builtin_inff();
+    int bi = 0;
+    f32x4v an = ld4(a), bn = ld4(b2s);
+    float zn[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) zn[u] = z[u * ldz];
+    for (int g = 0; g < ng; ++g) {
+      const f32x4v ac = an, bc = bn;
+      float zc[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) zc[u] = zn[u];
+      if (g + 1 < ng) {
+        an = ld4(a + 4 * g + 4);
+        bn = ld4(b2s + 4 * g + 4);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) zn[u] = z[(4 * g + 4 + u) * ldz];
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int i = 4 * g + u;
+        const float al = ac[u] - lam;
+        dpv = al - bc[u] * __builtin_amdgcn_rcpf(dpv);
+        const float gm = fabsf(dpv + zc[u] - al);
+        const bool after = gm > prev || (gm == prev && i > prev_i);
+        if (after && gm < best) {
+          best = gm;
+          bi = i;
+        }
+      }
+    }
+    prev = best;
+    prev_i = bi;
+    r = bi;
+  }
+  {                                            // D+ above the twist
+    float dpv = __builtin_inff();
+    for (int g = 0; 4 * g < r; ++g) {
+      const f32x4v ac = ld4(a + 4 * g), bc = ld4(b2s + 4 * g);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        dpv = (ac[u] - lam) - bc[u] * __builtin_amdgcn_rcpf(dpv);
+        if (4 * g + u < r) z[(4 * g + u) * ldz] = dpv;
+      }
+    }
+  }
+  // the vector from the twist outwards; the pivots of a group are read
+  // before any of its rows is overwritten
+  float nrm2 = 1.f, x = 1.f;
+  for (int g = (r - 1) >> 2; g >= 0 && r > 0; --g) {
+    const f32x4v bc = ld4(b + 4 * g);
+    float q[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) q[u] = z[(4 * g + u) * ldz];
+#pragma unroll
+    for (int u = 3; u >= 0; --u) {
+      const int i = 4 * g + u;
+      if (i < r) {
+        x = -bc[u] * __builtin_amdgcn_rcpf(q[u] != 0.f ? q[u] : tiny) * x;
+        z[i * ldz] = x;
+        nrm2 += x * x;
+      }
+    }
+  }
+  z[r * ldz] = 1.f;
+  x = 1.f;
+  for (int g = (r + 1) >> 2; 4 * g < d; ++g) {
+    float q[4], bb[4];                         // pivots D- and b_{i-1} of the group
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = 4 * g + u;
+      q[u] = z[i * ldz];
+      bb[u] = i > 0 ? b[i - 1] : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = 4 * g + u;
+      if (i > r) {
+        x = -bb[u] * __builtin_amdgcn_rcpf(q[u] != 0.f ? q[u] : tiny) * x;
+        z[i * ldz] = x;
+        nrm2 += x * x;
+      }
+    }
+  }
+  const float inv = 1.f / sqrtf(nrm2);
+  for (int g = 0; g < ng; ++g) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) z[(4 * g + u) * ldz] *= inv;
+  }
+}
+
+// V_m = Q Z for the m columns of Z: the reflectors (v_j in G's row j, zero
+// outside rows j+1 .. d-1; scale beta_j) applied from H_{d-3} down to H_0
+// with Z in registers: 16 lanes (one DPP row) per column, lane rb holding
+// rows 8 rb .. 8 rb + 7, the next reflector loaded while this one is applied.
+__device__ __forceinline__ void back_transform(const float* __restrict__ G, int ld, float* __restrict__ Z, int ldz,
+                                               const float* __restrict__ beta, int d, int dp, int m) {
+  typedef float f32x2v __attribute__((ext_vector_type(2)));
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int rb = lane & 15;
+  const bool rin = 8 * rb < dp;
+  // lanes past the padded rows read the (finite) first entries of the row
+  // instead; their z stays zero, so they add nothing and write nothing back
+  const int ro = rin ? 8 * rb : 0;
+  auto load_v = [&](int j, float* v) {
+#pragma unroll
+    for (int h = 0; h < 4; ++h) {
+      const f32x2v t = *reinterpret_cast<const f32x2v*>(G + j * ld + ro + 2 * h);
+      v[2 * h] = t[0];
+      v[2 * h + 1] = t[1];
+    }
+  };
+  for (int k0 = 0; k0 < m; k0 += 4 * kWaves) {
+    const int k = k0 + 4 * wave + (lane >> 4);
+    const bool own = k < m && rin;
+    float z[8], vn[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) z[i] = own ? Z[(8 * rb + i) * ldz + k] : 0.f;
+    float bn = 0.f;
+    if (d >= 3) {
+      load_v(d - 3, vn);
+      bn = beta[d - 3];
+    }
+    for (int j = d - 3; j >= 0; --j) {
+      float v[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) v[i] = vn[i];
+      const float bj = bn;
+      if (j > 0) {
+        load_v(j - 1, vn);
+        bn = beta[j - 1];
+      }
+      float y = 0.f, y2 = 0.f;
+#pragma unroll
+      for (int i = 0; i < 8; i += 2) {
+        y += v[i] * z[i];
+        y2 += v[i + 1] * z[i + 1];
+      }
+      y = sum8(y + y2);
+      y = (y + dpp_f<0x140>(y)) * bj;          // row_mirror: the other 8 lanes of the row
+      y = rin ? y : 0.f;                       // lanes past the padded rows keep z = 0
+#pragma unroll
+      for (int i = 0; i < 8; ++i) z[i] -= y * v[i];
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+      if (own && 8 * rb + i < d) Z[(8 * rb + i) * ldz + k] = z[i];
+  }
+}
+
 __device__ bool tridiag_solve(float* G, int ld, float* Z, int ldz, int d, int dp, int m, float* sv, int* s_cs,
                               int* s_fail) {
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   float* const s_a = sv;                       // T's diagonal
   float* const s_b = sv + dp;                  // T's subdiagonal
   float* const s_beta = sv + 2 * dp;           // reflector scales
-  float* const s_p = sv + 3 * dp;              // p of the current step; b^2 from B on
+  float* const s_p = sv + 3 * dp;              // p of the current step; b_i^2 from B on
   float* const s_lam = sv + 4 * dp;            // eigenvalues, descending
   float* const s_v = sv + 5 * dp;              // [2][dp] v of alternate steps
-  float* const s_misc = sv + 7 * dp;           // Gershgorin lo, hi, pivot floor
+  float* const s_misc = sv + 7 * dp;           // Gershgorin lo, hi
   float* const s_kred = sv + 7 * dp + 8;       // [16] per-wave p^T v partials
+  float* const s_b2s = sv + 8 * dp;            // b_{i-1}^2 (0 at i = 0), from B on
   if (tid == 0) *s_fail = 0;
 
   // ---- A. Householder reduction, the matrix in registers ----
   {
-    const int half = lane >> 5, rb = lane & 31, cb = 2 * wave + half;
-    const int hbase = lane & 32;               // first lane of this half-wave
-    const bool rin = 4 * rb < dp, cin = 4 * cb < dp;
-    float A[4][4];
+    typedef float f32x2v __attribute__((ext_vector_type(2)));
+    const int row16 = lane >> 4, rb = lane & 15, cb = 4 * wave + row16;
+    const bool rin = 8 * rb < dp, cin = 2 * cb < dp;
+    const bool b3 = lane & 8;                  // which of the block's two columns this lane ends with
+    float A[8][2];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 8; ++i)
 #pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        const int r = 4 * rb + i, cc = 4 * cb + c;
+      for (int c = 0; c < 2; ++c) {
+        const int r = 8 * rb + i, cc = 2 * cb + c;
         A[i][c] = (r < d && cc < d) ? G[r * ld + cc] : 0.f;
       }
-    // the reflector of column j, by the half-wave holding it (cb == j / 4):
-    // writes v into s_v[j & 1] and G's column j, a_j, b_j and beta_j
-    auto reflect = [&](int j) {
-      const int jj = j & 3, j1 = (j + 1) & 3;
-      float colv[4];
+    auto rl = [](float x, int l) { return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), l)); };
+    // the reflector of column j, by the DPP row holding it (cb == j / 2):
+    // writes v (zero outside rows j+1 .. d-1) into s_v[j & 1] and G's row j,
+    // a_j, b_j and beta_j
+    // (JJ = j % 2 as a compile-time constant: the column is picked without
+    // selects, and never by a run-time index, which would move A out of
+    // registers)
+    auto reflect = [&](int j, auto jjc) {
+      constexpr int JJ = decltype(jjc)::value;
+      const int rbase = lane & 48;
+      float colv[8];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) colv[i] = jj == 0 ? A[i][0] : jj == 1 ? A[i][1] : jj == 2 ? A[i][2] : A[i][3];
+      for (int i = 0; i < 8; ++i) colv[i] = A[i][JJ];
       float sq = 0.f;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int r = 4 * rb + i;
+      for (int i = 0; i < 8; ++i) {
+        const int r = 8 * rb + i;
         if (r > j + 1 && r < d) sq += colv[i] * colv[i];
       }
       sq = sum8(sq);
       sq += dpp_f<0x140>(sq);                  // row_mirror: the other 8 lanes of the row
-      sq += __shfl_xor(sq, 16, 64);
-      const float x0 = __shfl(j1 == 0 ? colv[0] : j1 == 1 ? colv[1] : j1 == 2 ? colv[2] : colv[3],
-                              hbase + ((j + 1) >> 2), 64);
-      const float aj = __shfl(jj == 0 ? colv[0] : jj == 1 ? colv[1] : jj == 2 ? colv[2] : colv[3],
-                              hbase + (j >> 2), 64);
+      const int i1 = (j + 1) & 7, i0 = j & 7;
+      float x1 = colv[0], x0v = colv[0];
+#pragma unroll
+      for (int i = 1; i < 8; ++i) {
+        x1 = i == i1 ? colv[i] : x1;
+        x0v = i == i0 ? colv[i] : x0v;
+      }
+      const float x0 = rl(x1, rbase + ((j + 1) >> 3));
+      const float aj = rl(x0v, rbase + (j >> 3));
       float beta = 0.f, alpha = x0, v0 = 0.f;
       if (sq != 0.f) {                         // else already reduced: H_j = I
         const float nrm = sqrtf(x0 * x0 + sq);
         alpha = x0 >= 0.f ? -nrm : nrm;
         v0 = x0 - alpha;
-        beta = 2.f / (v0 * v0 + sq);
+        beta = 2.f * __builtin_amdgcn_rcpf(v0 * v0 + sq);
       }
-      f32x4v vv;
+      float vv[8];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int r = 4 * rb + i;
+      for (int i = 0; i < 8; ++i) {
+        const int r = 8 * rb + i;
         vv[i] = (beta == 0.f || r <= j || r >= d) ? 0.f : (r == j + 1 ? v0 : colv[i]);
-        if (r > j && r < d) G[r * ld + j] = vv[i];
       }
-      if (rin) *reinterpret_cast<f32x4v*>(s_v + (j & 1) * dp + 4 * rb) = vv;
+      if (rin) {
+        f32x4v* sv4 = reinterpret_cast<f32x4v*>(s_v + (j & 1) * dp + 8 * rb);
+        sv4[0] = (f32x4v){vv[0], vv[1], vv[2], vv[3]};
+        sv4[1] = (f32x4v){vv[4], vv[5], vv[6], vv[7]};
+        f32x2v* grow = reinterpret_cast<f32x2v*>(G + j * ld + 8 * rb);   // row j, for the back-transformation
+#pragma unroll
+        for (int h = 0; h < 4; ++h) grow[h] = (f32x2v){vv[2 * h], vv[2 * h + 1]};
+      }
       if (rb == 0) {
         s_a[j] = aj;
         s_b[j] = alpha;
         s_beta[j] = beta;
       }
     };
-    if (d >= 3 && cb == 0) reflect(0);
+    __syncthreads();                           // G is read into registers before rows of it are overwritten
+    if (d >= 3 && cb == 0) reflect(0, IntC<0>{});
     for (int j = 0; j < d - 2; ++j) {
       __syncthreads();
       const float beta = s_beta[j];
       const float* vb = s_v + (j & 1) * dp;
       // columns of this wave: 8 wave .. 8 wave + 7; none left in the trailing block?
       const bool active = 8 * wave + 7 > j && 8 * wave < d;
-      // p = beta A v over this thread's block, summed over the half-wave's 32
-      // row blocks: the 4 column sums are halved twice by exchanges (lanes
-      // 16 and 8 apart keep two, then one of them) and the last one summed
-      // over its 8 lanes, so that lane group (b4, b3) ends with column
-      // 4 cb + 2 b4 + b3
-      float keep = 0.f;
+      float vr[8], vc[2];
       if (active) {
-        const f32x4v vr = rin ? *reinterpret_cast<const f32x4v*>(vb + 4 * rb) : (f32x4v){0.f, 0.f, 0.f, 0.f};
-        float part[4];
+        const f32x4v z4 = {0.f, 0.f, 0.f, 0.f};
+        const f32x4v v0 = rin ? ld4(vb + 8 * rb) : z4, v1 = rin ? ld4(vb + 8 * rb + 4) : z4;
+        const f32x2v c2 = cin ? *reinterpret_cast<const f32x2v*>(vb + 2 * cb) : (f32x2v){0.f, 0.f};
 #pragma unroll
-        for (int c = 0; c < 4; ++c) part[c] = A[0][c] * vr[0] + A[1][c] * vr[1] + A[2][c] * vr[2] + A[3][c] * vr[3];
-        const bool b4 = lane & 16, b3 = lane & 8;
-        float s0 = b4 ? part[2] : part[0], s1 = b4 ? part[3] : part[1];
-        s0 += __shfl_xor(b4 ? part[0] : part[2], 16, 64);
-        s1 += __shfl_xor(b4 ? part[1] : part[3], 16, 64);
-        keep = b3 ? s1 : s0;
-        keep += __shfl_xor(b3 ? s0 : s1, 8, 64);
+        for (int i = 0; i < 4; ++i) {
+          vr[i] = v0[i];
+          vr[4 + i] = v1[i];
+        }
+        vc[0] = c2[0];
+        vc[1] = c2[1];
+        // p = beta A v over this thread's block, summed over the row's 16
+        // row blocks: the two column sums are halved by an exchange across
+        // the row's halves (row_mirror), the kept one summed over its 8 lanes
+        float part[2];
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+          float s0 = 0.f, s1 = 0.f;
+#pragma unroll
+          for (int i = 0; i < 8; i += 2) {
+            s0 += A[i][c] * vr[i];
+            s1 += A[i + 1][c] * vr[i + 1];
+          }
+          part[c] = s0 + s1;
+        }
+        float keep = (b3 ? part[1] : part[0]) + dpp_f<0x140>(b3 ? part[0] : part[1]);
         keep = sum8(keep) * beta;
+        const int col = 2 * cb + (b3 ? 1 : 0);
+        const bool trail = col > j && col < d;
+        if ((lane & 7) == 0 && cin) s_p[col] = trail ? keep : 0.f;
+        // p^T v over the wave's 8 columns: each row's two column values met
+        // by row_mirror, then the four rows read out
+        // (the lane reads stay outside the lane-0 branch: inside it the other
+        // lanes are inactive and their values undefined)
+        float pv = trail ? keep * (b3 ? vc[1] : vc[0]) : 0.f;
+        pv += dpp_f<0x140>(pv);
+        const float pvw = (rl(pv, 0) + rl(pv, 16)) + (rl(pv, 32) + rl(pv, 48));
+        if (lane == 0) s_kred[wave] = pvw;
+      } else {
+        if ((lane & 7) == 0 && cin) s_p[2 * cb + (b3 ? 1 : 0)] = 0.f;
+        if (lane == 0) s_kred[wave] = 0.f;
       }
-      const int col = 4 * cb + ((lane >> 3) & 3);   // the column this lane's group ended with
-      const bool trail = col > j && col < d;
-      float pv = (active && trail) ? keep * vb[col] : 0.f;
-      pv += __shfl_xor(pv, 8, 64);
-      pv += __shfl_xor(pv, 16, 64);
-      pv += __shfl_xor(pv, 32, 64);
-      if ((lane & 7) == 0 && cin) s_p[col] = (active && trail) ? keep : 0.f;
-      if (lane == 0) s_kred[wave] = active ? pv : 0.f;
       __syncthreads();
+      // the wave that forms the next reflector goes first on its SIMD, so
+      // that the reflector is ready when the other waves finish their updates
+      const bool owner = wave == ((j + 1) >> 3) && j + 1 < d - 2;
+      if (owner) __builtin_amdgcn_s_setprio(2);
       if (active) {
         // A -= v w^T + w v^T, w = p - K v, K = (beta / 2) p^T v; p and v are
         // zero outside the trailing block, so the update is too
         float kd = 0.f;
 #pragma unroll
         for (int w4 = 0; w4 < kWaves / 4; ++w4) {
-          const f32x4v k4 = *reinterpret_cast<const f32x4v*>(s_kred + 4 * w4);
+          const f32x4v k4 = ld4(s_kred + 4 * w4);
           kd += (k4[0] + k4[1]) + (k4[2] + k4[3]);
         }
         const float K = 0.5f * beta * kd;
         const f32x4v z4 = {0.f, 0.f, 0.f, 0.f};
-        const f32x4v vr = rin ? *reinterpret_cast<const f32x4v*>(vb + 4 * rb) : z4;
-        const f32x4v pr = rin ? *reinterpret_cast<const f32x4v*>(s_p + 4 * rb) : z4;
-        const f32x4v vc = cin ? *reinterpret_cast<const f32x4v*>(vb + 4 * cb) : z4;
-        const f32x4v pc = cin ? *reinterpret_cast<const f32x4v*>(s_p + 4 * cb) : z4;
-        const f32x4v wr = pr - K * vr, wc = pc - K * vc;
+        const f32x4v p0 = rin ? ld4(s_p + 8 * rb) : z4, p1 = rin ? ld4(s_p + 8 * rb + 4) : z4;
+        const f32x2v pc2 = cin ? *reinterpret_cast<const f32x2v*>(s_p + 2 * cb) : (f32x2v){0.f, 0.f};
+        float wr[8];
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < 4; ++i) {
+          wr[i] = p0[i] - K * vr[i];
+          wr[4 + i] = p1[i] - K * vr[4 + i];
+        }
+        const float wc0 = pc2[0] - K * vc[0], wc1 = pc2[1] - K * vc[1];
 #pragma unroll
-          for (int c = 0; c < 4; ++c) A[i][c] -= vr[i] * wc[c] + wr[i] * vc[c];
+        for (int i = 0; i < 8; ++i) {
+          A[i][0] = fmaf(-vr[i], wc0, fmaf(-wr[i], vc[0], A[i][0]));
+          A[i][1] = fmaf(-vr[i], wc1, fmaf(-wr[i], vc[1], A[i][1]));
+        }
       }
-      if (j + 1 < d - 2 && cb == ((j + 1) >> 2)) reflect(j + 1);
+      if (j + 1 < d - 2 && cb == ((j + 1) >> 1)) {
+        if ((j + 1) & 1) reflect(j + 1, IntC<1>{});
+        else reflect(j + 1, IntC<0>{});
+      }
+      if (owner) __builtin_amdgcn_s_setprio(0);
     }
     // the last 2 x 2 block of T (the whole of T when d <= 2)
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 8; ++i)
 #pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        const int r = 4 * rb + i, cc = 4 * cb + c;
+      for (int c = 0; c < 2; ++c) {
+        const int r = 8 * rb + i, cc = 2 * cb + c;
         if (d >= 2 && cc == d - 2 && r == d - 2) s_a[d - 2] = A[i][c];
         if (d >= 2 && cc == d - 2 && r == d - 1) s_b[d - 2] = A[i][c];
         if (cc == d - 1 && r == d - 1) s_a[d - 1] = A[i][c];
@@ -474,26 +716,31 @@ __device__ bool tridiag_solve(float* G, int ld, float* Z, int ldz, int d, int dp
   __syncthreads();
 
   // ---- B. the m largest eigenvalues: 4 lanes per eigenvalue ----
+  // Sturm counts in IEEE arithmetic: a zero pivot gives an infinite next one,
+  // whose reciprocal is zero, so the sequence runs on without a test; b^2 is
+  // floored at FLT_MIN so that no 0 * inf occurs, and a pivot counts as
+  // negative by its sign bit (-0 included), which keeps the count the one of
+  // a nearby perturbed matrix.  The recurrence starts from an infinite pivot
+  // before row 0 (b_{-1}^2 = 0) and takes a and b^2 four rows at a time, the
+  // next four loaded ahead.
   float* const s_b2 = s_p;
-  if (wave == 0) {                             // Gershgorin interval, b^2, pivot floor
-    float lo = 3.4e38f, hi = -3.4e38f, b2max = 0.f;
+  if (wave == 0) {                             // Gershgorin interval and b^2
+    float lo = 3.4e38f, hi = -3.4e38f;
     for (int i = lane; i < d; i += 64) {
       const float bl = i > 0 ? s_b[i - 1] : 0.f, br = i < d - 1 ? s_b[i] : 0.f;
       const float r = fabsf(bl) + fabsf(br);
       lo = fminf(lo, s_a[i] - r);
       hi = fmaxf(hi, s_a[i] + r);
-      s_b2[i] = br * br;
-      b2max = fmaxf(b2max, br * br);
+      s_b2[i] = i < d - 1 ? fmaxf(br * br, 1.17549435e-38f) : 0.f;
+      s_b2s[i] = i > 0 ? fmaxf(bl * bl, 1.17549435e-38f) : 0.f;
     }
     for (int o = 32; o > 0; o >>= 1) {
       lo = fminf(lo, __shfl_xor(lo, o, 64));
       hi = fmaxf(hi, __shfl_xor(hi, o, 64));
-      b2max = fmaxf(b2max, __shfl_xor(b2max, o, 64));
     }
     if (lane == 0) {
       s_misc[0] = lo;
       s_misc[1] = hi;
-      s_misc[2] = 1.17549435e-38f * fmaxf(1.f, b2max);
     }
   }
   __syncthreads();
@@ -501,23 +748,27 @@ __device__ bool tridiag_solve(float* G, int ld, float* Z, int ldz, int d, int dp
   if (wave < (4 * m + 63) / 64) {
     const int k = tid >> 2, t = tid & 3;
     const int q = d - 1 - k;                   // ascending index of the k-th largest
-    const float pivmin = s_misc[2];
     float lo = s_misc[0], hi = s_misc[1];
     for (int it = 0; it < 11; ++it) {          // width / 5^11: below fp32 rounding of |T|
       const float w = hi - lo;
       const float x = lo + w * (float)(t + 1) * 0.2f;
-      int cnt = 0;
-      float qv = s_a[0] - x;
-      if (fabsf(qv) < pivmin) qv = -pivmin;
-      cnt += qv < 0.f;
-#pragma unroll 8
-      for (int i = 1; i < d; ++i) {
-        qv = (s_a[i] - x) - s_b2[i - 1] * __builtin_amdgcn_rcpf(qv);
-        if (fabsf(qv) < pivmin) qv = -pivmin;
-        cnt += qv < 0.f;
+      float qv = __builtin_inff();
+      uint32_t cnt = 0;
+      f32x4v an = ld4(s_a), bn = ld4(s_b2s);
+      for (int i = 0; i < d; i += 4) {
+        const f32x4v ac = an, bc = bn;
+        if (i + 4 < d) {
+          an = ld4(s_a + i + 4);
+          bn = ld4(s_b2s + i + 4);
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          qv = (ac[u] - x) - bc[u] * __builtin_amdgcn_rcpf(qv);
+          cnt += __float_as_uint(qv) >> 31;
+        }
       }
       // the points at or below the eigenvalue: a prefix of the group's lanes
-      const uint64_t bal = __ballot(k < m && cnt <= q);
+      const uint64_t bal = __ballot(k < m && (int)cnt <= q);
       const int nb = __popcll((bal >> (lane & ~3)) & 0xfull);
       const float nlo = nb > 0 ? lo + w * (float)nb * 0.2f : lo;
       const float nhi = nb < 4 ? lo + w * (float)(nb + 1) * 0.2f : hi;
@@ -536,70 +787,14 @@ __device__ bool tridiag_solve(float* G, int ld, float* Z, int ldz, int d, int dp
   __syncthreads();
 
   // ---- C. eigenvectors of T: one lane per eigenvalue, in its column of Z ----
-  // D- is kept in the column while D+ is recomputed where it is needed: the
-  // twist search runs D+ forward beside it, then D+ overwrites D- above the
-  // twist (where D- is no longer read) for the upward recurrence.  A zero
-  // pivot is replaced by 1e-30.
+  // The twist rank of an eigenvalue is its place in its run of numerically
+  // equal ones (within 2^-20 |T|), so that the members of an exactly
+  // multiple eigenvalue take different twists; every other one takes its
+  // best twist, which gives the accurate vector.
   if (tid < m) {
-    const int k = tid;
-    const float lam = s_lam[k];
-    const float tiny = 1e-30f;
-    float* z = Z + k;
-    float dmv = s_a[d - 1] - lam;              // backward pivots D-
-    z[(d - 1) * ldz] = dmv;
-#pragma unroll 8
-    for (int i = d - 2; i >= 0; --i) {
-      dmv = (s_a[i] - lam) - s_b2[i] * __builtin_amdgcn_rcpf(dmv != 0.f ? dmv : tiny);
-      z[i * ldz] = dmv;
-    }
-    // twist: the (k - cluster start)-th least |gamma_i| (ties: lower index)
-    const int rank = k - s_cs[k] < d - 1 ? k - s_cs[k] : d - 1;
-    int r = 0;
-    float prev = -1.f;
-    int prev_i = -1;
-    for (int s2 = 0; s2 <= rank; ++s2) {
-      float best = 3.4e38f, dpv = s_a[0] - lam;
-      int bi = 0;
-#pragma unroll 8
-      for (int i = 0; i < d; ++i) {
-        if (i > 0) dpv = (s_a[i] - lam) - s_b2[i - 1] * __builtin_amdgcn_rcpf(dpv != 0.f ? dpv : tiny);
-        const float g = fabsf(dpv + z[i * ldz] - (s_a[i] - lam));
-        const bool after = g > prev || (g == prev && i > prev_i);
-        if (after && g < best) {
-          best = g;
-          bi = i;
-        }
-      }
-      prev = best;
-      prev_i = bi;
-      r = bi;
-    }
-    float dpv = s_a[0] - lam;                  // D+ above the twist
-#pragma unroll 8
-    for (int i = 0; i < r; ++i) {
-      if (i > 0) dpv = (s_a[i] - lam) - s_b2[i - 1] * __builtin_amdgcn_rcpf(dpv != 0.f ? dpv : tiny);
-      z[i * ldz] = dpv;
-    }
-    float nrm2 = 1.f, x = 1.f;
-#pragma unroll 8
-    for (int i = r - 1; i >= 0; --i) {
-      const float qd = z[i * ldz];
-      x = -s_b[i] * __builtin_amdgcn_rcpf(qd != 0.f ? qd : tiny) * x;
-      z[i * ldz] = x;
-      nrm2 += x * x;
-    }
-    z[r * ldz] = 1.f;
-    x = 1.f;
-#pragma unroll 8
-    for (int i = r + 1; i < d; ++i) {
-      const float qd = z[i * ldz];
-      x = -s_b[i - 1] * __builtin_amdgcn_rcpf(qd != 0.f ? qd : tiny) * x;
-      z[i * ldz] = x;
-      nrm2 += x * x;
-    }
-    const float inv = 1.f / sqrtf(nrm2);
-#pragma unroll 8
-    for (int i = 0; i < d; ++i) z[i * ldz] *= inv;
+    int rank = 0;
+    while (rank < tid && rank < d - 1 && s_lam[tid - rank - 1] - s_lam[tid - rank] <= 0x1p-20f * tnorm) ++rank;
+    twisted_vector(s_a, s_b, s_b2, s_b2s, Z + tid, ldz, d, s_lam[tid], rank);
   }
   __syncthreads();
   // cluster members orthogonalised against the members before them (wave 0)
@@ -642,27 +837,8 @@ __device__ bool tridiag_solve(float* G, int ld, float* Z, int ldz, int d, int dp
   __syncthreads();
   if (*s_fail) return false;
 
-  // ---- D. V_m = Q Z: 16 lanes per column, the reflectors from the last ----
-  for (int k0 = 0; k0 < m; k0 += 4 * kWaves) {
-    const int k = k0 + 4 * wave + (lane >> 4), sl = lane & 15;
-    const bool own = k < m;
-    for (int j = d - 3; j >= 0; --j) {
-      const float beta = s_beta[j];
-      if (beta == 0.f) continue;
-      const int L = d - j - 1;
-      const int ov = (j + 1) * ld + j;
-      float y = 0.f;
-      if (own)
-        for (int i = sl; i < L; i += 16) y += G[ov + i * ld] * Z[(j + 1 + i) * ldz + k];
-      y += __shfl_xor(y, 1, 64);
-      y += __shfl_xor(y, 2, 64);
-      y += __shfl_xor(y, 4, 64);
-      y += __shfl_xor(y, 8, 64);
-      y *= beta;
-      if (own)
-        for (int i = sl; i < L; i += 16) Z[(j + 1 + i) * ldz + k] -= y * G[ov + i * ld];
-    }
-  }
+  // ---- D. V_m = Q Z ----
+  back_transform(G, ld, Z, ldz, s_beta, d, dp, m);
   __syncthreads();
   return true;
 }
