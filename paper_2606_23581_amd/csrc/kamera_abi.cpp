@@ -511,6 +511,10 @@ static int build_rehydrate(const kamera_rehydrate_args* a, kamera::RehydratePara
   if (n_tasks >= (int64_t)1 << 31)
     return fail(KAMERA_ERR_RANGE, "%s: %lld tasks exceed one launch", who, (long long)n_tasks);
   P.n_tasks = n_tasks;
+  P.fd_bpg = kamera::make_fast_div((uint32_t)std::max(1, nb_all));
+  P.fd_tblk = kamera::make_fast_div((uint32_t)std::max(1, P.n_tblk));
+  P.fd_heads = kamera::make_fast_div((uint32_t)std::max(1, a->n_heads));
+  P.fd_layers = kamera::make_fast_div((uint32_t)std::max(1, a->n_layers));
   rc = pick_grid(P.n_tasks, P.per_xcd, who);
   if (rc) return rc;
   launch = true;
@@ -580,6 +584,8 @@ static int build_shift(const kamera_shift_args* a, kamera::ShiftParams& P, bool&
   P.token_block = tb;
   P.n_tblk = (int32_t)ceil_div(a->n_tokens, tb);
   P.n_tasks = (int64_t)a->n_chunks * a->n_layers * P.n_tblk;
+  P.fd_tblk = kamera::make_fast_div((uint32_t)std::max(1, P.n_tblk));
+  P.fd_layers = kamera::make_fast_div((uint32_t)std::max(1, a->n_layers));
   rc = pick_grid(P.n_tasks, P.per_xcd, who);
   if (rc) return rc;
   launch = true;
@@ -650,6 +656,8 @@ static int build_scatter(const kamera_scatter_args* a, kamera::ScatterParams& P,
   P.token_block = tb;
   P.n_tblk = (int32_t)ceil_div(a->n_tokens, tb);
   P.n_tasks = (int64_t)a->n_chunks * a->n_layers * P.n_tblk;
+  P.fd_tblk = kamera::make_fast_div((uint32_t)std::max(1, P.n_tblk));
+  P.fd_layers = kamera::make_fast_div((uint32_t)std::max(1, a->n_layers));
   rc = pick_grid(P.n_tasks, P.per_xcd, who);
   if (rc) return rc;
   launch = true;

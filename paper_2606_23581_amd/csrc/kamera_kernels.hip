@@ -513,20 +513,25 @@ __global__ __launch_bounds__(kThreads, MS == 4 || RELOC ? 3 : 4) void rehydrate_
   const int64_t task = xcd_task(P.per_xcd);
   if (task >= P.n_tasks) return;
   // tasks of one (chunk, layer, head, token block) are adjacent: the key
-  // blocks (rotation, VALU-heavier) run next to the value blocks (pure streams)
-  int64_t rem = task / P.blocks_per_group;
-  const int r = (int)(task % P.blocks_per_group);
+  // blocks (rotation, VALU-heavier) run next to the value blocks (pure streams);
+  // task < 2^31, so the coordinates come from 32-bit invariant divisions
+  const uint32_t tk = (uint32_t)task;
+  uint32_t rem = fast_div(tk, P.fd_bpg);
+  const int r = (int)(tk - rem * (uint32_t)P.blocks_per_group);
   const int pl = (P.n_planes == 2 && r >= P.plane[1].block_base) ? 1 : 0;
   const PlaneParams& Q = P.plane[pl];
   const int b = r - Q.block_base;
-  const int tb = (int)(rem % P.n_tblk);
-  rem /= P.n_tblk;
+  uint32_t q = fast_div(rem, P.fd_tblk);
+  const int tb = (int)(rem - q * (uint32_t)P.n_tblk);
+  rem = q;
   TileCtx T;
   T.Q = &Q;
-  T.h = (int)(rem % P.n_heads);
-  rem /= P.n_heads;
-  T.l = (int)(rem % P.n_layers);
-  T.c = (int)(rem / P.n_layers);
+  q = fast_div(rem, P.fd_heads);
+  T.h = (int)(rem - q * (uint32_t)P.n_heads);
+  rem = q;
+  q = fast_div(rem, P.fd_layers);
+  T.l = (int)(rem - q * (uint32_t)P.n_layers);
+  T.c = (int)q;
   T.n_c = chunk_len(P.place, T.c);
   const int t_begin = tb * P.token_block;
   if (t_begin >= T.n_c) return;                 // uniform: the whole workgroup leaves
@@ -596,9 +601,10 @@ __global__ __launch_bounds__(kThreads) void shift_kernel(const ShiftParams /*by 
   const ShiftParams& P = kernel_params<ShiftParams>();
   const int64_t task = xcd_task(P.per_xcd);
   if (task >= P.n_tasks) return;
-  const int tb = (int)(task % P.n_tblk);
-  const int l = (int)((task / P.n_tblk) % P.n_layers);
-  const int c = (int)(task / ((int64_t)P.n_tblk * P.n_layers));
+  const uint32_t tk = (uint32_t)task, q = fast_div(tk, P.fd_tblk), c32 = fast_div(q, P.fd_layers);
+  const int tb = (int)(tk - q * (uint32_t)P.n_tblk);
+  const int l = (int)(q - c32 * (uint32_t)P.n_layers);
+  const int c = (int)c32;
   const int n_c = chunk_len(P.place, c);
   const int t_begin = tb * P.token_block;
   if (t_begin >= n_c) return;
@@ -706,9 +712,10 @@ __global__ __launch_bounds__(kThreads) void scatter_kernel(const ScatterParams /
   const ScatterParams& P = kernel_params<ScatterParams>();
   const int64_t task = xcd_task(P.per_xcd);
   if (task >= P.n_tasks) return;
-  const int tb = (int)(task % P.n_tblk);
-  const int l = (int)((task / P.n_tblk) % P.n_layers);
-  const int c = (int)(task / ((int64_t)P.n_tblk * P.n_layers));
+  const uint32_t tk = (uint32_t)task, q = fast_div(tk, P.fd_tblk), c32 = fast_div(q, P.fd_layers);
+  const int tb = (int)(tk - q * (uint32_t)P.n_tblk);
+  const int l = (int)(q - c32 * (uint32_t)P.n_layers);
+  const int c = (int)c32;
   const int n_c = chunk_len(P.place, c);
   const int t_begin = tb * P.token_block;
   if (t_begin >= n_c) return;

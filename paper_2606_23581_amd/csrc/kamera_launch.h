@@ -18,6 +18,36 @@ constexpr int kRgMaxHeads = 8;       // heads of a row taken by one row-group wo
 
 enum BlockFlags : int { kBlkPatch = 1, kBlkRotate = 2 };
 
+// Division of n < 2^32 by an invariant divisor d >= 1 as a multiply-high, a
+// subtraction, an add and two shifts (Granlund and Montgomery, "Division by
+// invariant integers using multiplication", 1994, the unsigned method): with
+// l = ceil(log2 d) and m = floor(2^32 (2^l - d) / d) + 1 (< 2^32),
+// floor(n / d) = (t + ((n - t) >> min(l, 1))) >> max(l - 1, 0), t = mulhi(m, n).
+// The kernels take their task coordinates this way: the divisors are set on
+// the host, and a run-time division costs a long instruction sequence.
+struct FastDiv {
+  uint32_t m;
+  uint32_t s1, s2;
+  uint32_t pad_;
+};
+
+inline FastDiv make_fast_div(uint32_t d) {       // d >= 1
+  uint32_t l = 0;
+  while (l < 32 && (uint64_t(1) << l) < d) ++l;
+  FastDiv f;
+  f.m = (uint32_t)((((uint64_t(1) << l) - d) << 32) / d + 1);
+  f.s1 = l > 0 ? 1u : 0u;
+  f.s2 = l > 0 ? l - 1 : 0u;
+  f.pad_ = 0;
+  return f;
+}
+
+// (constexpr: callable from device code too)
+constexpr uint32_t fast_div(uint32_t n, const FastDiv& f) {
+  const uint32_t t = (uint32_t)(((uint64_t)n * f.m) >> 32);
+  return (t + ((n - t) >> f.s1)) >> f.s2;
+}
+
 // One rotated band: per-pair frequency in revolutions per position unit,
 // theta^(-2j/rope_dim) / (2 pi), in fp64, and the coordinate (t, h, w) it uses.
 struct RopeParams {
@@ -96,6 +126,8 @@ struct RehydrateParams {
   int32_t block_tiles;               // row-group: > 0 = one workgroup per token block of this many
                                      // tiles (hardware dispatch); 0 = persistent, equal ranges
   int64_t n_tasks;
+  // per-head task decode: blocks_per_group, n_tblk, n_heads, n_layers
+  FastDiv fd_bpg, fd_tblk, fd_heads, fd_layers;
 };
 
 struct ShiftParams {
@@ -111,6 +143,7 @@ struct ShiftParams {
   int32_t per_xcd;
   int32_t pad_;
   int64_t n_tasks;
+  FastDiv fd_tblk, fd_layers;        // task decode
 };
 
 struct ScatterParams {
@@ -126,6 +159,7 @@ struct ScatterParams {
   int32_t per_xcd;
   int32_t gather;                    // 1: pool -> dense rows
   int64_t n_tasks;
+  FastDiv fd_tblk, fd_layers;        // task decode
 };
 
 constexpr int kFormMaxDim = 128;     // patch forming: columns of Delta

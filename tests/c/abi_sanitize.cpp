@@ -20,6 +20,7 @@
 #include <vector>
 
 #include "kamera.h"
+#include "kamera_launch.h"
 #include "launch_stub.h"
 
 namespace {
@@ -190,6 +191,25 @@ void fuzz(uint64_t seed, int iters) {
 }  // namespace
 
 int main() {
+  // the kernels' invariant-divisor division: exact for every dividend below
+  // 2^32 (edge values around multiples of d, the extremes, random ones)
+  {
+    std::mt19937_64 rng(7);
+    auto check_d = [&](uint32_t d) {
+      const kamera::FastDiv f = kamera::make_fast_div(d);
+      const uint32_t edges[] = {0u, 1u, d - 1, d, d + 1, 2 * d - 1, 2 * d, 0x00FFFFFFu, 0x7FFFFFFFu, 0xFFFFFFFEu,
+                                0xFFFFFFFFu, (0xFFFFFFFFu / d) * d, (0xFFFFFFFFu / d) * d - 1};
+      for (uint32_t n : edges) CHECK(kamera::fast_div(n, f) == n / d);
+      for (int k = 0; k < 64; ++k) {
+        const uint32_t n = (uint32_t)rng();
+        CHECK(kamera::fast_div(n, f) == n / d);
+      }
+    };
+    for (uint32_t d = 1; d <= 4096; ++d) check_d(d);
+    for (int k = 0; k < 4096; ++k) check_d(1u + (uint32_t)(rng() % 0x7FFFFFFFu));
+    check_d(0x80000000u);
+    check_d(0xFFFFFFFFu);
+  }
   // the valid calls pass and launch once each
   {
     const kamera_rehydrate_args r = valid_rehydrate();
