@@ -217,21 +217,14 @@ def bench_form(args, pool, n_workers):
     C, L, H, n, d = w.n_chunks, w.n_layers, w.n_heads, w.n_tokens, w.head_dim
     planes = [("k", w.m_k)] + ([("v", w.m_v)] if w.has_v and w.m_v and args.orbit == 1 else [])
     K = max(1, args.orbit)
-    gen = torch.Generator(device=dev)
-    gen.manual_seed(w.seed + 7)
-    # deficits: Gaussian token coefficients on a decaying spectrum
-    # sigma_k = (1 + k)^(-1/4) in a random orthonormal basis, so that about
-    # 90% of the energy sits in the top ~80% of the components
-    sig = (1.0 + torch.arange(d, device=dev, dtype=torch.float32)) ** -0.25
+    from synth.harness import form_deficits
+
+    # deficits: Gaussian token coefficients on a decaying spectrum (1 + k)^(-1/4)
+    # in a random orthonormal basis per plane (synth.harness.form_deficits)
+    deficits = form_deficits(w, dev, [name for name, _ in planes], orbit=K)
     tensors = {}
     for name, m in planes:
-        q, _ = torch.linalg.qr(torch.randn((d, d), generator=gen, device=dev, dtype=torch.float32))
-        D = torch.empty((K, C, L, H, n, d) if K > 1 else (C, L, H, n, d), dtype=torch.float32, device=dev)
-        Dv = D.view(K * C, L, H, n, d)
-        for c in range(K * C):
-            a = torch.randn((L, H, n, d), generator=gen, device=dev, dtype=torch.float32)
-            torch.matmul(a * sig, q.contiguous(), out=Dv[c])
-            del a
+        D = deficits[name]
         U = torch.empty((C, L, H, n, m), dtype=torch.bfloat16, device=dev)
         W = torch.empty((C, L, H, m, d), dtype=torch.bfloat16, device=dev)
         done = torch.zeros((C, L, H), dtype=torch.int32, device=dev)

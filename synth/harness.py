@@ -288,3 +288,33 @@ def sample_units(w: Workload, k: int, seed: int = 0) -> List[tuple]:
         l, h = divmod(rem, w.n_heads)
         out.append((c, l, h))
     return out
+
+
+def form_deficits(w: Workload, device, planes, orbit: int = 1, chunks: Optional[int] = None):
+    """Synthetic fp32 deficits for patch forming on workload w: for each plane
+    name, a tensor [C, L, H, n, d] (or [K, C, L, H, n, d] for an orbit of K
+    orderings) of N(0, 1) token coefficients on the decaying spectrum
+    sigma_k = (1 + k)^(-1/4) in one random orthonormal basis per plane, so that
+    about 90% of the energy sits in the top ~80% of the components and the
+    spectrum has no gap at the rank.  chunks: generate only the first few
+    chunks (the rest of the tensor is left uninitialised)."""
+    import torch
+
+    dev = torch.device(device)
+    C, L, H, n, d = w.n_chunks, w.n_layers, w.n_heads, w.n_tokens, w.head_dim
+    K = max(1, orbit)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(w.seed + 7)
+    sig = (1.0 + torch.arange(d, device=dev, dtype=torch.float32)) ** -0.25
+    out = {}
+    for name in planes:
+        q, _ = torch.linalg.qr(torch.randn((d, d), generator=gen, device=dev, dtype=torch.float32))
+        D = torch.empty((K, C, L, H, n, d) if K > 1 else (C, L, H, n, d), dtype=torch.float32, device=dev)
+        Dv = D.view(K * C, L, H, n, d)
+        for c in range(K * C if chunks is None else min(K * C, chunks)):
+            a = torch.randn((L, H, n, d), generator=gen, device=dev, dtype=torch.float32)
+            torch.matmul(a * sig, q.contiguous(), out=Dv[c])
+            del a
+        out[name] = D
+    return out
+

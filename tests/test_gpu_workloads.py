@@ -215,3 +215,52 @@ def test_workload_window_slides(device):
     assert drift <= w.slides * 2.0 ** -7
     del p
     _free()
+
+
+def test_form_patch_benchmark_workload(device):
+    """Patch forming at the benchmark's size and launch configuration: the K
+    and the V deficits of every (chunk, layer, head) unit of the 80-layer
+    recall (64 x 80 x 8 units of 1024 x 128, rank 64, on a spectrum with no
+    gap at the rank), one launch per plane with the default tridiagonal
+    solver.  Sampled units are checked against the fp64 SVD: the singular
+    values within 1e-4 relative, W's rows orthonormal to 2^-6 and the
+    residual of U W within 2^-6 |U_ref W_ref| of the Eckart-Young optimum
+    (without a gap the truncation's subspace is not unique, its residual is);
+    at most one unit in a thousand may fall back to Jacobi."""
+    import torch
+
+    import paper_2606_23581_amd as km
+
+    w = synth.WORKLOADS["gqa80l_64x1024_m64_mrope_paged"]
+    C, L, H, n, d = w.n_chunks, w.n_layers, w.n_heads, w.n_tokens, w.head_dim
+    planes = [("k", w.m_k), ("v", w.m_v)]
+    deficits = harness.form_deficits(w, device, [name for name, _ in planes])
+    units = harness.sample_units(w, 24, seed=5)
+    for name, m in planes:
+        print(f"[case] form_patch full size, plane {name}", flush=True)
+        D = deficits[name]
+        U = torch.empty((C, L, H, n, m), dtype=torch.bfloat16, device=device)
+        W = torch.empty((C, L, H, m, d), dtype=torch.bfloat16, device=device)
+        sigma = torch.empty((C, L, H, m), dtype=torch.float32, device=device)
+        done = torch.full((C, L, H), -1, dtype=torch.int32, device=device)
+        km.form_patch(D, U, W, sigma=sigma, sweeps_done=done)
+        torch.cuda.synchronize()
+        dn = done.cpu().numpy()
+        assert (dn >= 0).all()
+        assert int((dn > 0).sum()) <= max(1, dn.size // 1000), int((dn > 0).sum())
+        for (c, l, h) in units:
+            Dl = D[c, l, h].double().cpu().numpy()
+            Ug = ref.bf16_to_f64(bits(U[c, l, h]))
+            Wg = ref.bf16_to_f64(bits(W[c, l, h]))
+            sg = sigma[c, l, h].cpu().numpy().astype(np.float64)
+            Ur, Wr, S = ref.form_patch(Dl, m)
+            assert np.max(np.abs(sg - S[:m]) / S[:m]) <= 1e-4, (name, c, l, h)
+            assert np.max(np.abs(Wg @ Wg.T - np.eye(m))) <= 2.0 ** -6, (name, c, l, h)
+            prod_ref = Ur @ Wr
+            opt = np.linalg.norm(Dl - prod_ref)
+            got = np.linalg.norm(Dl - Ug @ Wg)
+            assert got <= opt + 2.0 ** -6 * np.linalg.norm(prod_ref), (name, c, l, h, got, opt)
+        del U, W, sigma, done
+        deficits[name] = None
+        del D
+        _free()
