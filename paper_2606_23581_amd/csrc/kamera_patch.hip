@@ -566,40 +566,44 @@ __device__ bool tridiag_solve(float* G, int ld, float* Z, int ldz, int d, int dp
     // registers)
     auto reflect = [&](int j, auto jjc) {
       constexpr int JJ = decltype(jjc)::value;
-      const int rbase = lane & 48;
       float colv[8];
 #pragma unroll
       for (int i = 0; i < 8; ++i) colv[i] = A[i][JJ];
-      float sq = 0.f;
+      // x below its first entry (rows j+2 .. d-1): v there, and its squares
+      // summed as a tree
+      float vv[8], q[8];
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
         const int r = 8 * rb + i;
-        if (r > j + 1 && r < d) sq += colv[i] * colv[i];
+        vv[i] = (r > j + 1 && r < d) ? colv[i] : 0.f;
+        q[i] = vv[i] * vv[i];
       }
+      float sq = ((q[0] + q[1]) + (q[2] + q[3])) + ((q[4] + q[5]) + (q[6] + q[7]));
       sq = sum8(sq);
       sq += dpp_f<0x140>(sq);                  // row_mirror: the other 8 lanes of the row
-      const int i1 = (j + 1) & 7, i0 = j & 7;
-      float x1 = colv[0], x0v = colv[0];
-#pragma unroll
-      for (int i = 1; i < 8; ++i) {
-        x1 = i == i1 ? colv[i] : x1;
-        x0v = i == i0 ? colv[i] : x0v;
-      }
-      const float x0 = rl(x1, rbase + ((j + 1) >> 3));
-      const float aj = rl(x0v, rbase + (j >> 3));
+      // x_0 (row j+1) and a_j (row j): entry i % 8 of every lane, picked by a
+      // three-level select tree, then read from the lane holding that row
+      auto pick = [&](int i) {
+        const float p01 = (i & 1) ? colv[1] : colv[0], p23 = (i & 1) ? colv[3] : colv[2];
+        const float p45 = (i & 1) ? colv[5] : colv[4], p67 = (i & 1) ? colv[7] : colv[6];
+        const float p03 = (i & 2) ? p23 : p01, p47 = (i & 2) ? p67 : p45;
+        return (i & 4) ? p47 : p03;
+      };
+      const int rrow = 16 * ((j >> 1) & 3);    // first lane of this DPP row, as a scalar
+      const float x0 = rl(pick((j + 1) & 7), rrow + ((j + 1) >> 3));
+      const float aj = rl(pick(j & 7), rrow + (j >> 3));
+      // (hardware square root and reciprocal, 1 ulp each: beta is formed from
+      // the v that is stored, so H stays orthogonal to rounding)
       float beta = 0.f, alpha = x0, v0 = 0.f;
-      if (sq != 0.f) {                         // else already reduced: H_j = I
-        const float nrm = sqrtf(x0 * x0 + sq);
+      if (sq != 0.f) {                         // else already reduced: H_j = I (and v = 0 below x_0)
+        const float nrm = __builtin_amdgcn_sqrtf(x0 * x0 + sq);
         alpha = x0 >= 0.f ? -nrm : nrm;
         v0 = x0 - alpha;
         beta = 2.f * __builtin_amdgcn_rcpf(v0 * v0 + sq);
       }
-      float vv[8];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const int r = 8 * rb + i;
-        vv[i] = (beta == 0.f || r <= j || r >= d) ? 0.f : (r == j + 1 ? v0 : colv[i]);
-      }
+      for (int i = 0; i < 8; ++i)
+        if (8 * rb + i == j + 1) vv[i] = v0;
       if (rin) {
         f32x4v* sv4 = reinterpret_cast<f32x4v*>(s_v + (j & 1) * dp + 8 * rb);
         sv4[0] = (f32x4v){vv[0], vv[1], vv[2], vv[3]};
