@@ -299,7 +299,7 @@ def bench_form(args, pool, n_workers):
         "sweeps_run": {"min": int(sw.min()), "mean": round(float(sw.mean()), 2), "max": int(sw.max())},
         "roofline": {"bound": "mfma", "achieved": round(achieved, 3), "peak": FP32_MATRIX_PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / FP32_MATRIX_PEAK_TFLOPS, 4), "traffic": None,
-                     "kernel": "form_patch_kernel", "kernel_ms": round(gpu_ms / len(planes), 4),
+                     "kernel": "form_patch_kernel + form_u_kernel", "kernel_ms": round(gpu_ms / len(planes), 4),
                      "flops_per_step": int(flops)},
         "cpu_baseline": cpu,
     }

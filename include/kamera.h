@@ -356,13 +356,17 @@ typedef struct {
  *   sweeps > 0: block cyclic Jacobi, at most `sweeps` sweeps, stopping once
  *     the off-diagonal mass is negligible (12 reach the fp32 floor here).
  * Either way singular vectors are accurate to ~1e-5 relative where the
- * spectrum has a gap at m.
+ * spectrum has a gap at m.  W = V_m^T (bf16) is written first; U = Delta W^T
+ * is then formed from that stored W in a second launch on the same stream
+ * (Delta enters as a two-part bf16 split, ~2^-16 relative), so that U W is
+ * the projection onto exactly the kept W.
  * Orbit patch (Sec. 5, reorder): with n_orbit = K >= 2 the deficits of K
  * orderings of the same chunk set, at delta + o*orbit_stride (o < K), are
  * averaged (fp32) and the mean is truncated as above: the one rank-m patch
  * with the least total squared error over those orderings.  A held-out
  * ordering is simply not passed.  n_orbit 0 or 1 = a single deficit.
- * U, W and sigma must not overlap the deficits (KAMERA_ERR_ALIAS). */
+ * U, W and sigma must not overlap the deficits, nor U overlap W
+ * (KAMERA_ERR_ALIAS). */
 #define KAMERA_FORM_MAX_DIM 128
 typedef struct {
   int32_t n_chunks;

@@ -730,6 +730,7 @@ static int build_form(const kamera_form_args* a, kamera::FormParams& P, bool& la
       return fail(KAMERA_ERR_RANGE, "%s: strides span more than the address space", who);
     if (overlap(u0, u1, d0, d1) || overlap(w0, w1, d0, d1))
       return fail(KAMERA_ERR_ALIAS, "%s: U and W must not overlap the deficits", who);
+    if (overlap(u0, u1, w0, w1)) return fail(KAMERA_ERR_ALIAS, "%s: U must not overlap W (U is formed from W)", who);
     if (a->sigma != nullptr) {
       const int64_t ext_s[3] = {a->n_chunks, a->n_layers, a->n_heads};
       uintptr_t s0, s1;
@@ -764,6 +765,15 @@ static int build_form(const kamera_form_args* a, kamera::FormParams& P, bool& la
   P.n_orbit = n_orbit;
   P.orbit_s = n_orbit > 1 ? a->orbit_stride : 0;
   P.inv_orbit = 1.0f / (float)n_orbit;
+  {
+    bool wv = reinterpret_cast<uintptr_t>(a->W) % 16 == 0, up = reinterpret_cast<uintptr_t>(a->U) % 4 == 0;
+    for (int k = 0; k < 4; ++k) {
+      wv = wv && a->w_stride[k] % 8 == 0;
+      up = up && a->u_stride[k] % 2 == 0;
+    }
+    P.w_vec = wv ? 1 : 0;
+    P.u_pair = up ? 1 : 0;
+  }
   launch = true;
   return KAMERA_OK;
 }

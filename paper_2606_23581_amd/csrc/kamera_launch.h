@@ -183,6 +183,8 @@ struct FormParams {
   int32_t n_units;
   int32_t n_orbit;                  // >= 1 deficits averaged per unit
   float inv_orbit;                  // 1 / n_orbit
+  int32_t w_vec;                    // W rows 16-byte aligned: 8 entries per load
+  int32_t u_pair;                   // U rows 4-byte aligned: 2 ranks per store
 };
 
 size_t form_lds_bytes(int dim, int m);

@@ -1,11 +1,12 @@
-// gfx950 kernel of the compile-side patch forming (App. A compile step):
+// gfx950 kernels of the compile-side patch forming (App. A compile step):
 // the top-m singular triplets of each deficit Delta (n x d) as the stored
-// patch, U = Delta V_m (the singular values folded in) and W = V_m^T.
+// patch, W = V_m^T and U = Delta V_m (the singular values folded in).
 //
-// One 1024-thread workgroup per (chunk, layer, head) unit, everything in LDS
-// (d is padded to dp, a multiple of 16, with zero rows and columns):
+// form_patch_kernel: one 1024-thread workgroup per (chunk, layer, head) unit,
+// everything in LDS (d is padded to dp, a multiple of 16, with zero rows and
+// columns):
 //   1. Gram matrix G = Delta^T Delta on fp32 MFMA (16x16x4), Delta streamed in
-//      32-row tiles with the next tile's loads in flight during the products;
+//      128-row tiles with the next tile's loads in flight during the products;
 //   2. the m largest eigenpairs of G, by default (sweeps == 0) from its
 //      tridiagonal form: Householder reduction, multisection on Sturm counts,
 //      twisted-factorisation vectors, back-transformation (tridiag_solve
@@ -20,9 +21,10 @@
 //      negligible against the diagonal;
 //   3. (after Jacobi) rank the eigenvalues (diag G) of the real indices,
 //      keep the m largest;
-//   4. W[k] = V[:, order[k]]^T and U = Delta V_m, rounded to bf16.
+//   4. W[k] = V[:, order[k]]^T, rounded to bf16, and sigma.
+// form_u_kernel then forms U = Delta W^T from the stored W (below).
 // With an orbit (Sec. 5, reorder) Delta is the mean of the members' deficits,
-// formed on the fly wherever a Delta tile is staged.
+// formed on the fly wherever Delta is read.
 // The eigenvalues of G are the squared singular values of Delta and its
 // eigenvectors the right singular vectors, so U W is the rank-m truncation.
 // Padded indices keep zero rows and columns: every rotation that touches
@@ -1119,7 +1121,7 @@ __global__ __launch_bounds__(kFormThreads) void form_patch_kernel(const FormPara
   }
   __syncthreads();
 
-  // ---- 4. W = V_m^T, sigma, and U = Delta V_m ----
+  // ---- 4. W = V_m^T and sigma (U = Delta W^T follows in form_u_kernel) ----
   uint16_t* Wout = P.W + (int64_t)c * P.w_s[0] + (int64_t)l * P.w_s[1] + (int64_t)h * P.w_s[2];
   for (int e = tid; e < m * d; e += kFormThreads) {
     const int k = e / d, j = e % d;
@@ -1130,110 +1132,161 @@ __global__ __launch_bounds__(kFormThreads) void form_patch_kernel(const FormPara
     P.sigma[(int64_t)c * P.sigma_s[0] + (int64_t)l * P.sigma_s[1] + (int64_t)h * P.sigma_s[2] + tid] =
         sqrtf(lam > 0.f ? lam : 0.f);
   }
-  // V_m [dp][ldv] (zero beyond d rows and m columns) and a Delta tile
-  // [32][ldu] after it; V_m is gathered into registers first because it
-  // may overlap V, which is still being read
-  const int mp = pad16(m);
-  const int ldv = (mp % 32 == 16) ? mp : mp + 16;        // 4 rows x 16 columns: disjoint banks
-  const int ldu = dp + ((dp % 32 == 0) ? 2 : 18);        // 16 rows x 2 columns: disjoint banks
-  float* Vm = G;
-  float* T = G + dp * ldv;
-  {
-    constexpr int kMaxPer = kFormMaxDim * kFormMaxDim / kFormThreads;
-    float vals[kMaxPer];
+}
+
+// LDS floats: phase 1 G [dp][gv_ld] and the staged tile [kFormTile][tile_ld];
+// phase 2 G and V [dp][gv_ld] each, the groups' S [16][17] and two sets of
+// their Q [16][17] (the tridiagonal solver's vectors live in that last area)
+size_t form_lds_bytes(int dim, int /*m*/) {
+  const size_t dp = (size_t)pad16(dim), ld = (size_t)gv_ld((int)dp), ng = dp / (2 * kBlk);
+  const size_t f1 = dp * ld + kFormTile * (size_t)tile_ld((int)dp);
+  const size_t f2 = 2 * dp * ld + 3 * ng * kGrp * kLdQ;
+  return (f1 > f2 ? f1 : f2) * sizeof(float);
+}
+
+// ---------------------------------------------------------------------------
+// U = Delta W^T, the factor's token side, from the W form_patch_kernel has
+// stored (so U W is formed from exactly the kept W).  A wave takes kURows
+// token rows of one unit, as 16-row tiles, and the ranks 64 at a time; the
+// products are 16x16x32 bf16 MFMAs with fp32 accumulation.  Delta is read in
+// fp32 and split into hi = bf16(Delta) and lo = bf16(Delta - hi), and both
+// parts are multiplied, so Delta enters to ~2^-16 relative.  Lane (kg, t)
+// holds row t of a tile on k-slots 8 kg .. 8 kg + 7 (A operand), rank t on
+// the same slots (B operand), and rows 4 kg .. 4 kg + 3 of rank t of the
+// product.  With an orbit the members' rows are averaged in fp32 first.
+// ---------------------------------------------------------------------------
+constexpr int kURows = 64;            // token rows per wave
+constexpr int kUThreads = 256;
+constexpr int kURowsPerBlock = kURows * (kUThreads / 64);
+
+typedef __bf16 bf16x8v __attribute__((ext_vector_type(8)));
+typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
+
+// eight bf16 (element 2q in the low half of word q) from fp32 values
+__device__ __forceinline__ u32x4v pack_bf16x8(const float (&x)[8]) {
+  u32x4v r;
 #pragma unroll
-    for (int u = 0; u < kMaxPer; ++u) {
-      const int e = tid + u * kFormThreads, j = e / mp, k = e - j * mp;
-      vals[u] = (e < dp * mp && j < d && k < m) ? V[j * ld + s_order[k]] : 0.f;
+  for (int q = 0; q < 4; ++q) r[q] = (uint32_t)to_bf16_rne(x[2 * q]) | ((uint32_t)to_bf16_rne(x[2 * q + 1]) << 16);
+  return r;
+}
+
+__global__ __launch_bounds__(kUThreads) void form_u_kernel(const FormParams /*by value, read in place*/) {
+  const FormParams& P = *static_cast<const FormParams*>((const void*)__builtin_amdgcn_kernarg_segment_ptr());
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int t = lane & 15, kg = lane >> 4;
+  const int n = P.n_tokens, d = P.dim, m = P.m;
+  const uint32_t bpu = (uint32_t)((n + kURowsPerBlock - 1) / kURowsPerBlock);   // blocks per unit
+  const uint32_t unit = blockIdx.x / bpu;
+  if ((int)unit >= P.n_units) return;
+  const int h = (int)(unit % (uint32_t)P.n_heads);
+  const int l = (int)((unit / (uint32_t)P.n_heads) % (uint32_t)P.n_layers);
+  const int c = (int)(unit / ((uint32_t)P.n_heads * (uint32_t)P.n_layers));
+  const int row0 = (int)(blockIdx.x - unit * bpu) * kURowsPerBlock + wave * kURows;
+  if (row0 >= n) return;                       // no barrier in this kernel
+  const float* delta = P.delta + (int64_t)c * P.delta_s[0] + (int64_t)l * P.delta_s[1] + (int64_t)h * P.delta_s[2];
+  const uint16_t* Wu = P.W + (int64_t)c * P.w_s[0] + (int64_t)l * P.w_s[1] + (int64_t)h * P.w_s[2];
+  uint16_t* Uu = P.U + (int64_t)c * P.u_s[0] + (int64_t)l * P.u_s[1] + (int64_t)h * P.u_s[2];
+  const int ks = (d + 31) / 32;                // k-steps of 32 dims (<= 4)
+  // Delta row i, dims [8 kg + 32 s, +8) as fp32 (zero past n or d; d is a multiple of 4)
+  auto load_rows = [&](int i, float (&x)[4][8]) {
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
+#pragma unroll
+      for (int hf = 0; hf < 2; ++hf) {
+        const int j = 32 * s + 8 * kg + 4 * hf;
+        f32x4v v = {0.f, 0.f, 0.f, 0.f};
+        if (s < ks && i < n && j < d) {
+          const float* row = delta + (int64_t)i * P.delta_s[3] + j;
+          v = *reinterpret_cast<const f32x4v*>(row);
+          if (P.n_orbit > 1) {
+            for (int o = 1; o < P.n_orbit; ++o) v += *reinterpret_cast<const f32x4v*>(row + (int64_t)o * P.orbit_s);
+            v *= P.inv_orbit;
+          }
+        }
+#pragma unroll
+        for (int e = 0; e < 4; ++e) x[s][4 * hf + e] = v[e];
+      }
+  };
+  for (int r0 = 0; r0 < m; r0 += 64) {
+    // B operands: W rows r0 + 16 ct + t, dims [8 kg + 32 s, +8)
+    u32x4v wb[4][4];
+#pragma unroll
+    for (int ct = 0; ct < 4; ++ct) {
+      const int r = r0 + 16 * ct + t;
+#pragma unroll
+      for (int s = 0; s < 4; ++s) {
+        u32x4v v = {0u, 0u, 0u, 0u};
+        const int j0 = 32 * s + 8 * kg;
+        if (r < m && s < ks && j0 < d) {
+          const uint16_t* wr = Wu + (int64_t)r * P.w_s[3] + j0;
+          if (P.w_vec && j0 + 8 <= d) {
+            v = *reinterpret_cast<const u32x4v*>(wr);
+          } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+              if (j0 + e < d) v[e >> 1] |= (uint32_t)wr[e] << (16 * (e & 1));
+          }
+        }
+        wb[ct][s] = v;
+      }
     }
-    __syncthreads();
+    for (int rt = 0; rt < kURows / 16; ++rt) {
+      const int i0 = row0 + 16 * rt;
+      if (i0 >= n) break;                      // uniform
+      float x[4][8];
+      load_rows(i0 + t, x);
+      f32x4v acc[4];
 #pragma unroll
-    for (int u = 0; u < kMaxPer; ++u) {
-      const int e = tid + u * kFormThreads, j = e / mp, k = e - j * mp;
-      if (e < dp * mp) Vm[j * ldv + k] = vals[u];
-    }
-  }
-  // U = Delta V_m on MFMA: the 16 x 16 output tiles of a staged tile
-  // (kFormTile / 16 row tiles x mp / 16 rank tiles), up to 4 per wave with
-  // their chains interleaved
-  uint16_t* Uout = P.U + (int64_t)c * P.u_s[0] + (int64_t)l * P.u_s[1] + (int64_t)h * P.u_s[2];
-  {
-    constexpr int kRowTiles = kFormTile / 16;
-    const int nout = kRowTiles * (mp / 16);
-    const int my_out = (nout - wave + kWaves - 1) / kWaves;        // output tiles of this wave (<= 4)
-    int ort[4], oct[4];
+      for (int ct = 0; ct < 4; ++ct) acc[ct] = (f32x4v){0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int ot = wave + u * kWaves;
-      ort[u] = ot < nout ? ot % kRowTiles : 0;
-      oct[u] = ot < nout ? ot / kRowTiles : 0;
-    }
-    const int vec_per_row = dp / 4;
-    f32x4v x[kStageVecs];
-    load_tile(P, delta, 0, n, d, vec_per_row, tid, x);
-    for (int t0 = 0; t0 < n; t0 += kFormTile) {
-      __syncthreads();
+      for (int s = 0; s < 4; ++s) {
+        if (s < ks) {
+          float lo[8];
 #pragma unroll
-      for (int u = 0; u < kStageVecs; ++u) {
-        const int e = tid + u * kFormThreads, r = e / vec_per_row, v4 = e - r * vec_per_row;
-        if (e < kFormTile * vec_per_row) {
-          typedef float f32x2v __attribute__((ext_vector_type(2)));
-          f32x2v* dst = reinterpret_cast<f32x2v*>(T + r * ldu + 4 * v4);
-          dst[0] = (f32x2v){x[u][0], x[u][1]};
-          dst[1] = (f32x2v){x[u][2], x[u][3]};
+          for (int e = 0; e < 8; ++e) lo[e] = x[s][e] - __uint_as_float((uint32_t)to_bf16_rne(x[s][e]) << 16);
+          const bf16x8v ahi = __builtin_bit_cast(bf16x8v, pack_bf16x8(x[s]));
+          const bf16x8v alo = __builtin_bit_cast(bf16x8v, pack_bf16x8(lo));
+#pragma unroll
+          for (int ct = 0; ct < 4; ++ct) {
+            const bf16x8v b = __builtin_bit_cast(bf16x8v, wb[ct][s]);
+            acc[ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi, b, acc[ct], 0, 0, 0);
+            acc[ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(alo, b, acc[ct], 0, 0, 0);
+          }
         }
       }
-      __syncthreads();
-      if (t0 + kFormTile < n) load_tile(P, delta, t0 + kFormTile, n, d, vec_per_row, tid, x);
-      if (wave < nout) {
-        f32x4v acc[4];
+      if (P.u_pair) {
+        // ranks t and t ^ 1 meet by a DPP swap; the even lane stores both
 #pragma unroll
-        for (int u = 0; u < 4; ++u) acc[u] = (f32x4v){0.f, 0.f, 0.f, 0.f};
-        // as in the Gram: a scalar slot count picks a loop without branches
-        const int my = __builtin_amdgcn_readfirstlane(my_out);
-        const float* ta = T + lr * ldu + lj;
-        const float* vb = Vm + lj * ldv + lr;
-        int oa[4], ob[4];
+        for (int ct = 0; ct < 4; ++ct) {
+          const int r = r0 + 16 * ct + t;
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          oa[u] = 16 * ort[u] * ldu;
-          ob[u] = 16 * oct[u];
+          for (int q = 0; q < 4; ++q) {
+            const float nb = dpp_f<0xB1>(acc[ct][q]);
+            const int i = i0 + 4 * kg + q;
+            if ((t & 1) == 0 && r < m && i < n) {
+              uint16_t* dst = Uu + (int64_t)i * P.u_s[3] + r;
+              if (r + 1 < m)
+                *reinterpret_cast<uint32_t*>(dst) = (uint32_t)to_bf16_rne(acc[ct][q]) | ((uint32_t)to_bf16_rne(nb) << 16);
+              else
+                *dst = to_bf16_rne(acc[ct][q]);
+            }
+          }
         }
-        if (my == 4) mfma_steps<4>(ta, 4, oa, vb, 4 * ldv, ob, dp / 4, acc);
-        else if (my == 3) mfma_steps<3>(ta, 4, oa, vb, 4 * ldv, ob, dp / 4, acc);
-        else if (my == 2) mfma_steps<2>(ta, 4, oa, vb, 4 * ldv, ob, dp / 4, acc);
-        else if (my == 1) mfma_steps<1>(ta, 4, oa, vb, 4 * ldv, ob, dp / 4, acc);
-        // lane (lj, lr) holds U[t0 + 16 rt + 4 lj + i][16 ct + lr]
+      } else {
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int col = 16 * oct[u] + lr;
-          if (wave + u * kWaves < nout && col < m) {
+        for (int ct = 0; ct < 4; ++ct) {
+          const int r = r0 + 16 * ct + t;
+          if (r < m) {
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              const int row = t0 + 16 * ort[u] + 4 * lj + i;
-              if (row < n) Uout[(int64_t)row * P.u_s[3] + col] = to_bf16_rne(acc[u][i]);
+            for (int q = 0; q < 4; ++q) {
+              const int i = i0 + 4 * kg + q;
+              if (i < n) Uu[(int64_t)i * P.u_s[3] + r] = to_bf16_rne(acc[ct][q]);
             }
           }
         }
       }
     }
   }
-}
-
-// LDS floats: phase 1 G [dp][gv_ld] and the staged tile [kFormTile][tile_ld];
-// phase 2 G and V [dp][gv_ld] each, the groups' S [16][17] and two sets of
-// their Q [16][17]; phase 4 V_m [dp][ldv] and a tile [kFormTile][ldu]
-size_t form_lds_bytes(int dim, int m) {
-  const size_t dp = (size_t)pad16(dim), ld = (size_t)gv_ld((int)dp), ng = dp / (2 * kBlk);
-  const size_t mp = (size_t)pad16(m);
-  const size_t ldv = (mp % 32 == 16) ? mp : mp + 16;
-  const size_t ldu = dp + ((dp % 32 == 0) ? 2 : 18);
-  const size_t f1 = dp * ld + kFormTile * (size_t)tile_ld((int)dp);
-  const size_t f2 = 2 * dp * ld + 3 * ng * kGrp * kLdQ;
-  const size_t f4 = dp * ldv + kFormTile * ldu;
-  size_t f = f1 > f2 ? f1 : f2;
-  f = f > f4 ? f : f4;
-  return f * sizeof(float);
 }
 
 hipError_t launch_form_patch(const FormParams& p, hipStream_t s) {
@@ -1243,6 +1296,11 @@ hipError_t launch_form_patch(const FormParams& p, hipStream_t s) {
       ensure_lds_limit((const void*)form_patch_kernel, (int)form_lds_bytes(kFormMaxDim, kFormMaxDim), lds_set);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(form_patch_kernel, dim3((uint32_t)p.n_units), dim3(kFormThreads), lds, s, p);
+  const hipError_t e1 = hipGetLastError();
+  if (e1 != hipSuccess) return e1;
+  // U from the stored W, on the same stream: after the W of every unit
+  const int64_t bpu = (p.n_tokens + kURowsPerBlock - 1) / kURowsPerBlock;
+  hipLaunchKernelGGL(form_u_kernel, dim3((uint32_t)(bpu * p.n_units)), dim3(kUThreads), 0, s, p);
   return hipGetLastError();
 }
 

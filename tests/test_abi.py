@@ -683,7 +683,7 @@ def form_args():
     ("sweeps", km.ERR_SHAPE), ("negative", km.ERR_SHAPE), ("orbit_negative", km.ERR_SHAPE),
     ("orbit_stride", km.ERR_ALIGN), ("orbit_ok", km.OK), ("u_over_delta", km.ERR_ALIAS),
     ("w_over_orbit", km.ERR_ALIAS), ("sigma_over_delta", km.ERR_ALIAS), ("sigma_apart", km.OK),
-    ("done_over_delta", km.ERR_ALIAS),
+    ("done_over_delta", km.ERR_ALIAS), ("u_over_w", km.ERR_ALIAS),
 ])
 def test_form_patch_validation(case, code):
     a = form_args()
@@ -723,6 +723,9 @@ def test_form_patch_validation(case, code):
         a.sigma = FAKE + (3 << 36)
     elif case == "done_over_delta":
         a.sweeps_done = FAKE + 4 * 256
+    elif case == "u_over_w":
+        # U is formed from the stored W, so the two may not share memory
+        a.U = a.W + 8
     assert km.lib().kamera_validate(4, ctypes.byref(a)) == code, km.last_error()
     if code != km.OK:
         assert km.lib().kamera_form_patch(ctypes.byref(a), None) == code
