@@ -867,7 +867,6 @@ __global__ __launch_bounds__(kFormThreads) void form_patch_kernel(const FormPara
   const int ld = gv_ld(dp);                  // padded LDS row stride of G and V
   const int nb = dp / kBlk;                  // Jacobi blocks (even)
   const int ng = nb / 2;                     // groups rotated per step
-  const uint32_t ng_magic = (65536u + ng - 1) / ng;   // t / ng == (t * ng_magic) >> 16 for t < 128
   float* G = lds_f;                          // [dp][ld]
   float* V = lds_f + dp * ld;                // [dp][ld]; holds Delta tiles in phase 1
   float* Ss = V + dp * ld;                   // [ng][16][kLdQ] group matrices
