@@ -683,7 +683,8 @@ def form_args():
     ("sweeps", km.ERR_SHAPE), ("negative", km.ERR_SHAPE), ("orbit_negative", km.ERR_SHAPE),
     ("orbit_stride", km.ERR_ALIGN), ("orbit_ok", km.OK), ("u_over_delta", km.ERR_ALIAS),
     ("w_over_orbit", km.ERR_ALIAS), ("sigma_over_delta", km.ERR_ALIAS), ("sigma_apart", km.OK),
-    ("done_over_delta", km.ERR_ALIAS), ("u_over_w", km.ERR_ALIAS),
+    ("done_over_delta", km.ERR_ALIAS), ("u_over_w", km.ERR_ALIAS), ("too_many_units", km.ERR_RANGE),
+    ("too_many_rows", km.ERR_RANGE),
 ])
 def test_form_patch_validation(case, code):
     a = form_args()
@@ -726,6 +727,12 @@ def test_form_patch_validation(case, code):
     elif case == "u_over_w":
         # U is formed from the stored W, so the two may not share memory
         a.U = a.W + 8
+    elif case == "too_many_units":
+        # 2^22 + 1 units of 1024 work-items: more than a dispatch counts
+        a.n_chunks, a.n_layers, a.n_heads = 4097, 32, 32
+    elif case == "too_many_rows":
+        # 2^16 units of 2^16 tokens: 2^32 work-items of the U kernel
+        a.n_chunks, a.n_layers, a.n_heads, a.n_tokens = 64, 32, 32, 1 << 16
     assert km.lib().kamera_validate(4, ctypes.byref(a)) == code, km.last_error()
     if code != km.OK:
         assert km.lib().kamera_form_patch(ctypes.byref(a), None) == code
