@@ -487,7 +487,8 @@ static int build_rehydrate(const kamera_rehydrate_args* a, kamera::RehydratePara
                         (a->schedule == KAMERA_SCHEDULE_AUTO && a->max_workgroups == 0 && bt >= 512 / kamera::kTileTokens);
     P.block_tiles = blocks ? bt : 0;
     P.n_tasks = lanes_units * P.unit_tiles;
-    if (lanes_units * ceil_div(P.unit_tiles, bt) >= (int64_t)1 << 31)
+    // the dispatch packet counts work-items in 32 bits (64 * hw per block)
+    if (lanes_units * ceil_div(P.unit_tiles, bt) * 64 * hw > 0xFFFFFFFFLL)
       return fail(KAMERA_ERR_RANGE, "%s: %lld token blocks exceed one launch", who,
                   (long long)(lanes_units * ceil_div(P.unit_tiles, bt)));
     launch = true;

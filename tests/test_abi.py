@@ -283,6 +283,33 @@ def test_rehydrate_schedule_of_the_row_group_kernel(case, schedule, cap, want):
     assert km.lib().kamera_validate(0, ctypes.byref(a)) == min(want, 0)
 
 
+@pytest.mark.parametrize("layers,code", [(3, km.OK), (4, km.ERR_RANGE)])
+def test_row_group_blocks_fit_one_dispatch(layers, code):
+    """The block schedule launches one workgroup of 256 threads per token
+    block; a dispatch counts its work-items in 32 bits, so 2^21 chunks x 4
+    layers x 2 planes of 256-token blocks (2^32 work-items, blocks far below
+    2^31) are rejected while 3 layers (3 x 2^30) still launch."""
+    a = _plan_case("auto_reorder_shape")
+    a.kernel, a.schedule = km.KERNEL_ROW_GROUP4, km.SCHEDULE_BLOCKS
+    C, Ln, H, n = 1 << 21, layers, 4, 256
+    a.n_chunks, a.n_layers, a.n_heads, a.n_tokens = C, Ln, H, n
+    a.chunk_pos = FAKE + (1 << 41)
+    for p in range(2):
+        strides = [Ln * n * H * 128, n * H * 128, H * 128, 128]
+        us = [Ln * H * n * 16, H * n * 16, n * 16, 16]
+        ws = [Ln * H * 16 * 128, H * 16 * 128, 16 * 128, 128]
+        for k in range(4):
+            a.plane[p].in_stride[k] = a.plane[p].out_stride[k] = strides[k]
+            a.plane[p].u_stride[k], a.plane[p].w_stride[k] = us[k], ws[k]
+        for i, f in enumerate(("in_", "out", "U", "W")):
+            setattr(a.plane[p], f, FAKE + (1 + 4 * p + i) * (1 << 42))
+    assert km.lib().kamera_validate(0, ctypes.byref(a)) == code, km.last_error()
+    if code == km.ERR_RANGE:
+        assert "exceed one launch" in km.last_error()
+    else:
+        assert km.lib().kamera_rehydrate_schedule(ctypes.byref(a)) == km.SCHEDULE_BLOCKS
+
+
 def _interleaved_case(case):
     """Both planes write one tensor [C][L][n][K|V][H][D] (dense) or a pool
     [L][slot][K|V][H][D] (paged): H = 4, D = 128, so a row of one plane spans
