@@ -5,8 +5,10 @@
 // form_patch_kernel: one 1024-thread workgroup per (chunk, layer, head) unit,
 // everything in LDS (d is padded to dp, a multiple of 16, with zero rows and
 // columns):
-//   1. Gram matrix G = Delta^T Delta on fp32 MFMA (16x16x4), Delta streamed in
-//      128-row tiles with the next tile's loads in flight during the products;
+//   1. Gram matrix G = Delta^T Delta at fp32 accuracy on bf16 MFMA (16x16x32):
+//      Delta split exactly into three bf16 parts, six products per tile,
+//      streamed in 64-row tiles with the next tile's loads in flight during
+//      the products;
 //   2. the m largest eigenpairs of G, by default (sweeps == 0) from its
 //      tridiagonal form: Householder reduction, multisection on Sturm counts,
 //      twisted-factorisation vectors, back-transformation (tridiag_solve
@@ -45,17 +47,20 @@ typedef float f32x4v __attribute__((ext_vector_type(4)));
 
 constexpr int kFormThreads = 1024;
 constexpr int kWaves = kFormThreads / 64;
-constexpr int kFormTile = 128;         // Delta rows per staged tile
-constexpr int kStageVecs = kFormTile * (kFormMaxDim / 4) / kFormThreads;   // 4-float vectors per thread
+constexpr int kGramRows = 64;          // Delta rows per staged tile of the Gram product
 constexpr int kBlk = 8;                // block-Jacobi block width
 constexpr int kGrp = 2 * kBlk;         // indices of one rotated group (two blocks)
 constexpr int kLdQ = kGrp + 1;         // padded row stride of a group's 16x16 scratch
 constexpr int kFormFallbackSweeps = 12; // Jacobi limit after a failed tridiagonal solve
 
 __host__ __device__ inline int pad16(int d) { return (d + 15) & ~15; }
-// staged Delta tile row stride: == 16 (mod 32), so the four rows one MFMA
-// operand load touches fall on disjoint banks
-__host__ __device__ inline int tile_ld(int dp) { return (dp % 32 == 16) ? dp : dp + 16; }
+// bf16 offset of rows 8 j .. 8 j + 7 of column c in a staged Gram part:
+// columns of kGramRows rows, their 16-byte pieces permuted by (c >> 1) & 7,
+// so that the 32 lanes of a half wave reading 8-row pieces of 16 consecutive
+// columns (two pieces each), and 16 lanes storing one piece of consecutive
+// columns, touch distinct banks (16-byte reads are served per half wave over
+// 512 bytes of banks, 16-byte stores per quarter wave over 256 bytes)
+__device__ __forceinline__ int gram_slot(int c, int j) { return c * kGramRows + 8 * (j ^ ((c >> 1) & 7)); }
 // row stride of G and V: == 2 (mod 32), so an MFMA operand load of 16 rows
 // x 2 columns (half a wave) and a 16-row tile's row pieces fall on distinct banks
 __host__ __device__ inline int gv_ld(int dp) { return dp + ((2 - dp) % 32 + 32) % 32; }
@@ -85,6 +90,31 @@ __device__ __forceinline__ uint16_t to_bf16_rne(float x) {
   return (uint16_t)(__builtin_bit_cast(uint32_t, r) & 0xffffu);
 }
 
+typedef __bf16 bf16x8v __attribute__((ext_vector_type(8)));
+typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
+
+// eight bf16 (element 2q in the low half of word q) from fp32 values
+__device__ __forceinline__ u32x4v pack_bf16x8(const float (&x)[8]) {
+  u32x4v r;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) r[q] = (uint32_t)to_bf16_rne(x[2 * q]) | ((uint32_t)to_bf16_rne(x[2 * q + 1]) << 16);
+  return r;
+}
+
+// x = hi + mid + lo exactly, each part bf16 (RNE): bf16 keeps 8 significant
+// bits, so x - hi and x - hi - mid are exact in fp32 and the last remainder
+// has at most 8 significant bits left (outside the subnormal range)
+__device__ __forceinline__ void split3_bf16x8(const float (&x)[8], u32x4v& hi, u32x4v& mid, u32x4v& lo) {
+  float r[8], q[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) r[e] = x[e] - __uint_as_float((uint32_t)to_bf16_rne(x[e]) << 16);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) q[e] = r[e] - __uint_as_float((uint32_t)to_bf16_rne(r[e]) << 16);
+  hi = pack_bf16x8(x);
+  mid = pack_bf16x8(r);
+  lo = pack_bf16x8(q);
+}
+
 __device__ __forceinline__ float block_sum(float v, float* red) {
   // wave reduction, then across the 16 waves through LDS
   for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
@@ -96,17 +126,6 @@ __device__ __forceinline__ float block_sum(float v, float* red) {
 #pragma unroll
   for (int w = 0; w < kFormThreads / 64; ++w) s += red[w];
   return s;
-}
-
-// Row i, columns [4 v4, 4 v4 + 4) of the (orbit-mean) deficit.
-__device__ __forceinline__ f32x4v load_delta4(const FormParams& P, const float* delta, int64_t i, int v4) {
-  const float* row = delta + i * P.delta_s[3] + 4 * v4;
-  f32x4v x = *reinterpret_cast<const f32x4v*>(row);
-  if (P.n_orbit > 1) {
-    for (int o = 1; o < P.n_orbit; ++o) x += *reinterpret_cast<const f32x4v*>(row + (int64_t)o * P.orbit_s);
-    x *= P.inv_orbit;
-  }
-  return x;
 }
 
 // The workgroup's dynamic LDS (one unit's working set).
@@ -205,15 +224,35 @@ __device__ __forceinline__ void group_sweep(int so, int qo, int lane, float* G, 
   }
 }
 
-// Rows [t0, t0 + kFormTile) of the (orbit-mean) deficit as 4-float vectors,
-// kStageVecs per thread (zero past n rows and d columns).
-__device__ __forceinline__ void load_tile(const FormParams& P, const float* delta, int t0, int n, int d,
-                                          int vec_per_row, int tid, f32x4v (&x)[kStageVecs]) {
+// Rows i0 .. i0 + 7 of column j of the (orbit-mean) deficit (zero past n
+// rows or d columns); a wave's lanes take consecutive columns, so each row's
+// loads are one contiguous piece.  Orbit members are read two at a time, all
+// their loads issued before the sums, which keep the members' order.
+__device__ __forceinline__ void load_col8(const FormParams& P, const float* delta, int i0, int j, int n, int d,
+                                          float (&x)[8]) {
+  const float* v = delta + (int64_t)i0 * P.delta_s[3] + j;
+  bool ok[8];
 #pragma unroll
-  for (int u = 0; u < kStageVecs; ++u) {
-    const int e = tid + u * kFormThreads, r = e / vec_per_row, v4 = e - r * vec_per_row;
-    x[u] = (f32x4v){0.f, 0.f, 0.f, 0.f};
-    if (e < kFormTile * vec_per_row && t0 + r < n && 4 * v4 < d) x[u] = load_delta4(P, delta, t0 + r, v4);
+  for (int e = 0; e < 8; ++e) {
+    ok[e] = j < d && i0 + e < n;
+    x[e] = ok[e] ? v[(int64_t)e * P.delta_s[3]] : 0.f;
+  }
+  if (P.n_orbit > 1) {
+    for (int o = 1; o < P.n_orbit; o += 2) {
+      const bool two = o + 1 < P.n_orbit;
+      const float* v1 = v + (int64_t)o * P.orbit_s;
+      const float* v2 = v1 + P.orbit_s;
+      float y[8], z[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        y[e] = ok[e] ? v1[(int64_t)e * P.delta_s[3]] : 0.f;
+        z[e] = ok[e] && two ? v2[(int64_t)e * P.delta_s[3]] : 0.f;
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) x[e] = (x[e] + y[e]) + z[e];
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) x[e] *= P.inv_orbit;
   }
 }
 
@@ -268,23 +307,79 @@ __device__ __forceinline__ void apply_v(float* V, int ld, int qo, const int* grp
 
 }  // namespace
 
-// nk k-steps of NS interleaved 16x16x4 MFMA chains: step k of chain u takes
-// its A operand at pa[k * sa + oa[u]] and its B operand at pb[k * sb + ob[u]]
-// (this lane's element).  No branch inside, so the loads of a step run ahead
-// of its MFMAs.
-template <int NS, int N>
-__device__ __forceinline__ void mfma_steps(const float* pa, int sa, const int (&oa)[N], const float* pb, int sb,
-                                           const int (&ob)[N], int nk, f32x4v (&acc)[N]) {
-#pragma unroll 4
-  for (int k = 0; k < nk; ++k) {
-    float a[NS], b[NS];
-#pragma unroll
-    for (int u = 0; u < NS; ++u) {
-      a[u] = pa[k * sa + oa[u]];
-      b[u] = pb[k * sb + ob[u]];
+// The Gram tiles (I, J), I <= J, of nt x nt blocks of 16 go in sets of at
+// most three consecutive tiles of one block row (row I's nt - I tiles split
+// evenly), so a set's products share their A operand.  The sets are dealt
+// largest first, in row order, each to the SIMD (wave mod 4) with the least
+// work so far that still has a wave free.  Returns this wave's tile count
+// (0: none) with its block row I and first block column J0; nt <= 8 makes at
+// most 15 sets.
+__device__ __forceinline__ int gram_set(int nt, int wave, int& I0, int& J0) {
+  int l0 = 0, l1 = 0, l2 = 0, l3 = 0, u0 = 0, u1 = 0, u2 = 0, u3 = 0;
+  for (int sz = 3; sz >= 1; --sz) {
+    for (int I = 0; I < nt; ++I) {
+      const int k = nt - I, ns = (k + 2) / 3, base = k / ns, extra = k - base * ns;
+      int J = I;
+      for (int s = 0; s < ns; ++s) {
+        const int z = base + (s < extra ? 1 : 0);
+        if (z == sz) {
+          int q = -1, bl = 1 << 30;
+          if (u0 < 4 && l0 < bl) { q = 0; bl = l0; }
+          if (u1 < 4 && l1 < bl) { q = 1; bl = l1; }
+          if (u2 < 4 && l2 < bl) { q = 2; bl = l2; }
+          if (u3 < 4 && l3 < bl) { q = 3; bl = l3; }
+          const int used = q == 0 ? u0 : q == 1 ? u1 : q == 2 ? u2 : u3;
+          if (q + 4 * used == wave) {
+            I0 = I;
+            J0 = J;
+            return z;
+          }
+          if (q == 0) { ++u0; l0 += z; }
+          else if (q == 1) { ++u1; l1 += z; }
+          else if (q == 2) { ++u2; l2 += z; }
+          else { ++u3; l3 += z; }
+        }
+        J += z;
+      }
     }
+  }
+  I0 = J0 = 0;
+  return 0;
+}
+
+// The NS tiles (I, J0 + u) of a set on the staged rows: lane (kg, t) reads
+// 8 consecutive rows of one column from each bf16 part (parts at Tb, part
+// stride `part`), and a tile takes the six products of the parts that are
+// not below 2^-27 relative.  A's three parts are loaded first; then B's parts
+// one at a time, each used at once by the products that need it (hi: mid hi,
+// lo hi, hi hi; mid: mid mid, hi mid; lo: hi lo), round the tiles, so
+// consecutive MFMAs update different accumulators and only one B part per
+// tile is held.  A diagonal first tile takes A's parts as its B.
+template <int NS, bool DIAG>
+__device__ __forceinline__ void gram_steps(const uint16_t* Tb, int part, int I, int J0, int kg, int t,
+                                           f32x4v (&acc)[3]) {
 #pragma unroll
-    for (int u = 0; u < NS; ++u) acc[u] = mfma4(a[u], b[u], acc[u]);
+  for (int ks = 0; ks < kGramRows / 32; ++ks) {
+    const int kj = 4 * ks + kg;                // this lane's 8-row piece
+    bf16x8v a[3];
+    const uint16_t* pa = Tb + gram_slot(16 * I + t, kj);
+#pragma unroll
+    for (int q = 0; q < 3; ++q) a[q] = *reinterpret_cast<const bf16x8v*>(pa + q * part);
+#pragma unroll
+    for (int q = 0; q < 3; ++q) {
+      bf16x8v b[NS];
+#pragma unroll
+      for (int u = 0; u < NS; ++u)
+        b[u] = (DIAG && u == 0) ? a[q]
+                                : *reinterpret_cast<const bf16x8v*>(Tb + gram_slot(16 * (J0 + u) + t, kj) + q * part);
+      constexpr int kCount[3] = {3, 2, 1};   // A parts 1, 2, 0 | 1, 0 | 0
+#pragma unroll
+      for (int r = 0; r < kCount[q]; ++r) {
+        const int ia = q == 0 ? (r == 0 ? 1 : r == 1 ? 2 : 0) : q == 1 ? (r == 0 ? 1 : 0) : 0;
+#pragma unroll
+        for (int u = 0; u < NS; ++u) acc[u] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[ia], b[u], acc[u], 0, 0, 0);
+      }
+    }
   }
 }
 
@@ -881,67 +976,61 @@ __global__ __launch_bounds__(kFormThreads) void form_patch_kernel(const FormPara
   int sweeps = P.sweeps;
   bool tri_ok = false;
   __shared__ int s_fail;
-  // ---- 1. G = Delta^T Delta on MFMA: wave owns up to 3 tiles (I <= J) ----
+  // ---- 1. G = Delta^T Delta on MFMA: a wave owns up to 3 tiles of one block row ----
   auto form_gram = [&]() {
     const int nt = dp / 16;
-    const int ntiles = nt * (nt + 1) / 2;
-    const int ldt = tile_ld(dp);
-    const int my_tiles = (ntiles - wave + kWaves - 1) / kWaves;   // tiles wave, wave + 16, ... (<= 3)
-    float* T = V;                            // staged tile [kFormTile][ldt]
-    int tI[3], tJ[3];
+    uint16_t* Tb = reinterpret_cast<uint16_t*>(V);   // staged parts hi, mid, lo: [3][dp][kGramRows] bf16
+    const int part = dp * kGramRows;
+    // this wave's tiles (gI, gJ + u), u < my: the same on every lane
+    int gI, gJ;
+    const int my = __builtin_amdgcn_readfirstlane(gram_set(nt, wave, gI, gJ));
+    gI = __builtin_amdgcn_readfirstlane(gI);
+    gJ = __builtin_amdgcn_readfirstlane(gJ);
+    const bool gdiag = gI == gJ;
     f32x4v acc[3];
 #pragma unroll
-    for (int u = 0; u < 3; ++u) {
-      int t = wave + u * kWaves, I = 0;
-      const int t_in = t;
-      if (t < ntiles) {
-        while (t >= nt - I) {                // row I of the upper triangle holds nt - I tiles
-          t -= nt - I;
-          ++I;
-        }
-      }
-      tI[u] = t_in < ntiles ? I : 0;         // (an idle slot reads tile (0, 0) and stores nothing)
-      tJ[u] = t_in < ntiles ? I + t : 0;
-      acc[u] = (f32x4v){0.f, 0.f, 0.f, 0.f};
-    }
-    // the tile (kFormTile rows x dp columns) is staged as 4-float vectors,
-    // kStageVecs per thread; the next tile's loads are in flight during the
-    // products on the current one
-    const int vec_per_row = dp / 4;
-    f32x4v x[kStageVecs];
-    load_tile(P, delta, 0, n, d, vec_per_row, tid, x);
-    for (int t0 = 0; t0 < n; t0 += kFormTile) {
+    for (int u = 0; u < 3; ++u) acc[u] = (f32x4v){0.f, 0.f, 0.f, 0.f};
+    // thread (sg, sc) stages rows 8 sg .. 8 sg + 7 of column sc of each
+    // kGramRows-row tile, split into three bf16 parts, as one 16-byte piece
+    // per part; the next tile's loads are in flight during the products on
+    // the current one
+    const bool stager = tid < (kGramRows / 8) * dp;
+    const int sg = stager ? tid / dp : 0, sc = stager ? tid - sg * dp : 0;
+    float x[8];
+    load_col8(P, delta, 8 * sg, stager ? sc : d, n, d, x);
+    for (int t0 = 0; t0 < n; t0 += kGramRows) {
       __syncthreads();
-#pragma unroll
-      for (int u = 0; u < kStageVecs; ++u) {
-        const int e = tid + u * kFormThreads, r = e / vec_per_row, v4 = e - r * vec_per_row;
-        if (e < kFormTile * vec_per_row) *reinterpret_cast<f32x4v*>(T + r * ldt + 4 * v4) = x[u];
+      if (stager) {
+        u32x4v hi, mid, lo;
+        split3_bf16x8(x, hi, mid, lo);
+        uint16_t* q = Tb + gram_slot(sc, sg);
+        *reinterpret_cast<u32x4v*>(q) = hi;
+        *reinterpret_cast<u32x4v*>(q + part) = mid;
+        *reinterpret_cast<u32x4v*>(q + 2 * part) = lo;
       }
       __syncthreads();
-      if (t0 + kFormTile < n) load_tile(P, delta, t0 + kFormTile, n, d, vec_per_row, tid, x);
-      // the slot count is the same on every lane: one scalar branch picks a
-      // loop without branches, whose loads run ahead of its MFMAs; rows past n
-      // are staged as zeros, so every tile takes all k-steps
-      const int my = __builtin_amdgcn_readfirstlane(my_tiles);
-      const float* trow = T + lj * ldt + lr;
-      int oa[3], ob[3];
-#pragma unroll
-      for (int u = 0; u < 3; ++u) {
-        oa[u] = 16 * tI[u];
-        ob[u] = 16 * tJ[u];
+      if (t0 + kGramRows < n) load_col8(P, delta, t0 + kGramRows + 8 * sg, stager ? sc : d, n, d, x);
+      // the set is the same on every lane: one scalar branch picks a loop
+      // without branches; rows past n are staged as zeros, so every tile
+      // takes all k-steps
+      if (gdiag) {
+        if (my == 3) gram_steps<3, true>(Tb, part, gI, gJ, lj, lr, acc);
+        else if (my == 2) gram_steps<2, true>(Tb, part, gI, gJ, lj, lr, acc);
+        else if (my == 1) gram_steps<1, true>(Tb, part, gI, gJ, lj, lr, acc);
+      } else {
+        if (my == 3) gram_steps<3, false>(Tb, part, gI, gJ, lj, lr, acc);
+        else if (my == 2) gram_steps<2, false>(Tb, part, gI, gJ, lj, lr, acc);
+        else if (my == 1) gram_steps<1, false>(Tb, part, gI, gJ, lj, lr, acc);
       }
-      if (my == 3) mfma_steps<3>(trow, 4 * ldt, oa, trow, 4 * ldt, ob, kFormTile / 4, acc);
-      else if (my == 2) mfma_steps<2>(trow, 4 * ldt, oa, trow, 4 * ldt, ob, kFormTile / 4, acc);
-      else if (my == 1) mfma_steps<1>(trow, 4 * ldt, oa, trow, 4 * ldt, ob, kFormTile / 4, acc);
     }
-    // lane (lj, lr) holds G[16I + 4 lj + i][16J + lr]; store it and its mirror
+    // lane (lj, lr) holds G[16 gI + 4 lj + i][16 (gJ + u) + lr]; store it and its mirror
 #pragma unroll
     for (int u = 0; u < 3; ++u) {
-      if (wave + u * kWaves < ntiles) {
+      if (u < my) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int row = 16 * tI[u] + 4 * lj + i, col = 16 * tJ[u] + lr;
-          if (tI[u] < tJ[u] || row <= col) {
+          const int row = 16 * gI + 4 * lj + i, col = 16 * (gJ + u) + lr;
+          if (gI < gJ + u || row <= col) {
             G[row * ld + col] = acc[u][i];
             G[col * ld + row] = acc[u][i];
           }
@@ -1133,12 +1222,12 @@ __global__ __launch_bounds__(kFormThreads) void form_patch_kernel(const FormPara
   }
 }
 
-// LDS floats: phase 1 G [dp][gv_ld] and the staged tile [kFormTile][tile_ld];
+// LDS floats: phase 1 G [dp][gv_ld] and the staged parts [3][dp][kGramRows] bf16;
 // phase 2 G and V [dp][gv_ld] each, the groups' S [16][17] and two sets of
 // their Q [16][17] (the tridiagonal solver's vectors live in that last area)
 size_t form_lds_bytes(int dim, int /*m*/) {
   const size_t dp = (size_t)pad16(dim), ld = (size_t)gv_ld((int)dp), ng = dp / (2 * kBlk);
-  const size_t f1 = dp * ld + kFormTile * (size_t)tile_ld((int)dp);
+  const size_t f1 = dp * ld + 3 * dp * kGramRows / 2;
   const size_t f2 = 2 * dp * ld + 3 * ng * kGrp * kLdQ;
   return (f1 > f2 ? f1 : f2) * sizeof(float);
 }
@@ -1157,17 +1246,6 @@ size_t form_lds_bytes(int dim, int /*m*/) {
 constexpr int kURows = 64;            // token rows per wave
 constexpr int kUThreads = 256;
 constexpr int kURowsPerBlock = kURows * (kUThreads / 64);
-
-typedef __bf16 bf16x8v __attribute__((ext_vector_type(8)));
-typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
-
-// eight bf16 (element 2q in the low half of word q) from fp32 values
-__device__ __forceinline__ u32x4v pack_bf16x8(const float (&x)[8]) {
-  u32x4v r;
-#pragma unroll
-  for (int q = 0; q < 4; ++q) r[q] = (uint32_t)to_bf16_rne(x[2 * q]) | ((uint32_t)to_bf16_rne(x[2 * q + 1]) << 16);
-  return r;
-}
 
 __global__ __launch_bounds__(kUThreads) void form_u_kernel(const FormParams /*by value, read in place*/) {
   const FormParams& P = *static_cast<const FormParams*>((const void*)__builtin_amdgcn_kernarg_segment_ptr());
