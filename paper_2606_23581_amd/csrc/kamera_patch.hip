@@ -570,30 +570,37 @@ __device__ __forceinline__ void twisted_vector(const float* __restrict__ a, cons
 // V_m = Q Z for the m columns of Z: the reflectors (v_j in G's row j, zero
 // outside rows j+1 .. d-1; scale beta_j) applied from H_{d-3} down to H_0
 // with Z in registers: 16 lanes (one DPP row) per column, lane rb holding
-// rows 8 rb .. 8 rb + 7, the next reflector loaded while this one is applied.
+// rows 32 h + 2 rb + e (h < 4, e < 2), the next reflector loaded while this
+// one is applied.  With that row split each 8-byte read of a reflector
+// covers 128 contiguous bytes and the Z accesses of a wave fall on distinct
+// banks (8 consecutive rows per lane made both conflict: 2-way and 8-way).
 __device__ __forceinline__ void back_transform(const float* __restrict__ G, int ld, float* __restrict__ Z, int ldz,
                                                const float* __restrict__ beta, int d, int dp, int m) {
   typedef float f32x2v __attribute__((ext_vector_type(2)));
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int rb = lane & 15;
-  const bool rin = 8 * rb < dp;
-  // lanes past the padded rows read the (finite) first entries of the row
-  // instead; their z stays zero, so they add nothing and write nothing back
-  const int ro = rin ? 8 * rb : 0;
+  // rows 32 h + 2 rb and + 1 are both inside the padded rows or both past them
+  bool vin[4];
+#pragma unroll
+  for (int h = 0; h < 4; ++h) vin[h] = 32 * h + 2 * rb < dp;
+  // rows past the padded ones take v = 0 (and keep z = 0)
   auto load_v = [&](int j, float* v) {
 #pragma unroll
     for (int h = 0; h < 4; ++h) {
-      const f32x2v t = *reinterpret_cast<const f32x2v*>(G + j * ld + ro + 2 * h);
+      const f32x2v t = vin[h] ? *reinterpret_cast<const f32x2v*>(G + j * ld + 32 * h + 2 * rb) : f32x2v{0.f, 0.f};
       v[2 * h] = t[0];
       v[2 * h + 1] = t[1];
     }
   };
   for (int k0 = 0; k0 < m; k0 += 4 * kWaves) {
     const int k = k0 + 4 * wave + (lane >> 4);
-    const bool own = k < m && rin;
+    const bool own = k < m;
     float z[8], vn[8];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) z[i] = own ? Z[(8 * rb + i) * ldz + k] : 0.f;
+    for (int i = 0; i < 8; ++i) {
+      const int r = 32 * (i >> 1) + 2 * rb + (i & 1);
+      z[i] = own && vin[i >> 1] ? Z[r * ldz + k] : 0.f;
+    }
     float bn = 0.f;
     if (d >= 3) {
       load_v(d - 3, vn);
@@ -616,13 +623,14 @@ __device__ __forceinline__ void back_transform(const float* __restrict__ G, int 
       }
       y = sum8(y + y2);
       y = (y + dpp_f<0x140>(y)) * bj;          // row_mirror: the other 8 lanes of the row
-      y = rin ? y : 0.f;                       // lanes past the padded rows keep z = 0
 #pragma unroll
       for (int i = 0; i < 8; ++i) z[i] -= y * v[i];
     }
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
-      if (own && 8 * rb + i < d) Z[(8 * rb + i) * ldz + k] = z[i];
+    for (int i = 0; i < 8; ++i) {
+      const int r = 32 * (i >> 1) + 2 * rb + (i & 1);
+      if (own && r < d) Z[r * ldz + k] = z[i];
+    }
   }
 }
 
