@@ -173,13 +173,13 @@ def tridiagonal_flops(d: int, m: int) -> int:
     """Tridiagonal-solver flops on one unit, as the kernel executes them:
     Householder steps on the full trailing block of order L = d-1-j (the
     product A v, 2 L^2, and the rank-2 update, 4 L^2, plus 3 L for the
-    reflector and w), 10 multisection rounds of 8 Sturm sequences per
+    reflector and w), 8 multisection rounds of 8 Sturm sequences per
     eigenvalue (4 flops per pivot), the twisted factorisation's four passes
     (D-, D+ beside the twist search, D+ above the twist, the vector and its
     norm: ~4 flops per element each), and the back-transformation (a dot
     product and an update of 2 L flops each per reflector and vector)."""
     house = sum(6 * L * L + 3 * L for L in range(2, d))
-    bisect = 10 * 8 * 4 * d * m
+    bisect = 8 * 8 * 4 * d * m
     vectors = 4 * 4 * d * m
     back = sum(4 * L * m for L in range(2, d))
     return house + bisect + vectors + back

@@ -824,7 +824,7 @@ __device__ bool tridiag_solve(float* G, int ld, float* Z, int ldz, int d, int dp
   }
   __syncthreads();
 
-  // ---- B. the m largest eigenvalues: 4 lanes per eigenvalue ----
+  // ---- B. the m largest eigenvalues: 8 lanes per eigenvalue ----
   // Sturm counts in IEEE arithmetic: a zero pivot gives an infinite next one,
   // whose reciprocal is zero, so the sequence runs on without a test; b^2 is
   // floored at FLT_MIN so that no 0 * inf occurs, and a pivot counts as
@@ -854,13 +854,18 @@ __device__ bool tridiag_solve(float* G, int ld, float* Z, int ldz, int d, int dp
   }
   __syncthreads();
   const float tnorm = fmaxf(fabsf(s_misc[0]), fabsf(s_misc[1]));   // |T| bound
-  if (wave < (4 * m + 63) / 64) {
-    const int k = tid >> 2, t = tid & 3;
+  // 9-section: the group's 8 lanes evaluate the 8 inner points of the
+  // interval, so 8 rounds narrow it to width / 9^8, below fp32 rounding of
+  // |T| (two waves per SIMD at rank 64: the Sturm recurrences are a
+  // dependent chain per lane, and 16 lanes per eigenvalue were slower,
+  // four waves per SIMD contending for the vector ALU)
+  if (tid < 8 * m) {
+    const int k = tid >> 3, t = tid & 7;
     const int q = d - 1 - k;                   // ascending index of the k-th largest
     float lo = s_misc[0], hi = s_misc[1];
-    for (int it = 0; it < 11; ++it) {          // width / 5^11: below fp32 rounding of |T|
+    for (int it = 0; it < 8; ++it) {
       const float w = hi - lo;
-      const float x = lo + w * (float)(t + 1) * 0.2f;
+      const float x = lo + w * (float)(t + 1) * (1.f / 9.f);
       float qv = __builtin_inff();
       uint32_t cnt = 0;
       f32x4v an = ld4(s_a), bn = ld4(s_b2s);
@@ -877,21 +882,32 @@ __device__ bool tridiag_solve(float* G, int ld, float* Z, int ldz, int d, int dp
         }
       }
       // the points at or below the eigenvalue: a prefix of the group's lanes
-      const uint64_t bal = __ballot(k < m && (int)cnt <= q);
-      const int nb = __popcll((bal >> (lane & ~3)) & 0xfull);
-      const float nlo = nb > 0 ? lo + w * (float)nb * 0.2f : lo;
-      const float nhi = nb < 4 ? lo + w * (float)(nb + 1) * 0.2f : hi;
+      const uint64_t bal = __ballot((int)cnt <= q);
+      const int nb = __popcll((bal >> (lane & ~7)) & 0xffull);
+      const float nlo = nb > 0 ? lo + w * (float)nb * (1.f / 9.f) : lo;
+      const float nhi = nb < 8 ? lo + w * (float)(nb + 1) * (1.f / 9.f) : hi;
       lo = nlo;
       hi = fmaxf(nhi, nlo);
     }
-    if (k < m && t == 0) s_lam[k] = 0.5f * (lo + hi);
+    if (t == 0) s_lam[k] = 0.5f * (lo + hi);
   }
   __syncthreads();
   // clusters: runs of eigenvalues within 1e-3 |T| of their predecessor
-  // (equal ones always, also when T = 0)
-  if (tid == 0) {
-    s_cs[0] = 0;
-    for (int j = 1; j < m; ++j) s_cs[j] = (s_lam[j - 1] - s_lam[j] <= 1e-3f * tnorm) ? s_cs[j - 1] : j;
+  // (equal ones always, also when T = 0): s_cs[j] is the last run start at or
+  // before j, a running maximum over the starts (wave 0, 64 entries a pass)
+  if (wave == 0) {
+    int carry = 0;
+    for (int base = 0; base < m; base += 64) {
+      const int j = base + lane;
+      int v = (j < m && (j == 0 || !(s_lam[j - 1] - s_lam[j] <= 1e-3f * tnorm))) ? j : 0;
+      for (int o = 1; o < 64; o <<= 1) {
+        const int u = __shfl_up(v, o, 64);
+        if (lane >= o) v = v > u ? v : u;
+      }
+      v = v > carry ? v : carry;
+      if (j < m) s_cs[j] = v;
+      carry = __shfl(v, 63, 64);
+    }
   }
   __syncthreads();
 
@@ -906,25 +922,35 @@ __device__ bool tridiag_solve(float* G, int ld, float* Z, int ldz, int d, int dp
     twisted_vector(s_a, s_b, s_b2, s_b2s, Z + tid, ldz, d, s_lam[tid], rank);
   }
   __syncthreads();
-  // cluster members orthogonalised against the members before them (wave 0)
+  // cluster members orthogonalised against the members before them (wave 0):
+  // z_k stays in registers (rows lane and lane + 64) through its member's
+  // pass, and a wave sum is three DPP adds per 8 lanes, one row_mirror and
+  // four lane reads (the loop bounds are the same on every lane)
   if (wave == 0) {
+    auto wsum = [](float x) {
+      x = sum8(x);
+      x += dpp_f<0x140>(x);
+      const auto rd = [&](int l) { return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), l)); };
+      return (rd(0) + rd(16)) + (rd(32) + rd(48));
+    };
+    const bool r0 = lane < d, r1 = lane + 64 < d;
     for (int k = 1; k < m; ++k) {
       const int c0 = s_cs[k];
       if (c0 == k) continue;
+      float zk0 = r0 ? Z[lane * ldz + k] : 0.f, zk1 = r1 ? Z[(lane + 64) * ldz + k] : 0.f;
       for (int i = c0; i < k; ++i) {
-        float dt = 0.f;
-        for (int r = lane; r < d; r += 64) dt += Z[r * ldz + i] * Z[r * ldz + k];
-        for (int o = 32; o > 0; o >>= 1) dt += __shfl_xor(dt, o, 64);
-        for (int r = lane; r < d; r += 64) Z[r * ldz + k] -= dt * Z[r * ldz + i];
+        const float zi0 = r0 ? Z[lane * ldz + i] : 0.f, zi1 = r1 ? Z[(lane + 64) * ldz + i] : 0.f;
+        const float dt = wsum(zi0 * zk0 + zi1 * zk1);
+        zk0 -= dt * zi0;
+        zk1 -= dt * zi1;
       }
-      float n2 = 0.f;
-      for (int r = lane; r < d; r += 64) n2 += Z[r * ldz + k] * Z[r * ldz + k];
-      for (int o = 32; o > 0; o >>= 1) n2 += __shfl_xor(n2, o, 64);
+      const float n2 = wsum(zk0 * zk0 + zk1 * zk1);
       // a member that was mostly inside the span of the ones before it is
       // not trusted (twisted vectors of an exactly multiple eigenvalue)
       if (lane == 0 && !(n2 >= 0.25f)) *s_fail = 1;
       const float inv = n2 > 0.f ? 1.f / sqrtf(n2) : 0.f;
-      for (int r = lane; r < d; r += 64) Z[r * ldz + k] *= inv;
+      if (r0) Z[lane * ldz + k] = zk0 * inv;
+      if (r1) Z[(lane + 64) * ldz + k] = zk1 * inv;
     }
   }
   __syncthreads();
