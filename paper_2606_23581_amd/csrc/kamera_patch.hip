@@ -241,7 +241,7 @@ __device__ __forceinline__ void load_col8(const FormParams& P, const float* delt
     for (int o = 1; o < P.n_orbit; o += 2) {
       const bool two = o + 1 < P.n_orbit;
       const float* v1 = v + (int64_t)o * P.orbit_s;
-      const float* v2 = v1 + P.orbit_s;
+      const float* v2 = two ? v1 + P.orbit_s : v1;
       float y[8], z[8];
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
