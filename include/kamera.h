@@ -26,9 +26,10 @@
  *
  * Conventions shared by every entry point
  *   - Every tensor pointer is a DEVICE pointer owned by the caller.  The
- *     library never allocates, frees or synchronises; a call enqueues one
- *     kernel on `stream` (a hipStream_t; NULL = the default stream) and
- *     returns.  Results are visible to later work on that stream.
+ *     library never allocates, frees or synchronises; a call enqueues its
+ *     kernel (kamera_form_patch: two, one after the other) on `stream` (a
+ *     hipStream_t; NULL = the default stream) and returns.  Results are
+ *     visible to later work on that stream.
  *   - KV rows are bf16.  Strides are in ELEMENTS (bf16) unless named _bytes;
  *     the innermost (column) stride is always 1.  Row starts must be 16-byte
  *     aligned: base pointers 16-byte aligned and every stride a multiple of 8.
