@@ -500,11 +500,10 @@ __device__ __forceinline__ void twisted_vector(const float* __restrict__ a, cons
         const float al = ac[u] - lam;
         dpv = al - bc[u] * __builtin_amdgcn_rcpf(dpv);
         const float gm = fabsf(dpv + zc[u] - al);
-        const bool after = gm > prev || (gm == prev && i > prev_i);
-        if (after && gm < best) {
-          best = gm;
-          bi = i;
-        }
+        // (bitwise, so that the selection compiles to selects, not branches)
+        const bool take = ((gm > prev) | ((gm == prev) & (i > prev_i))) & (gm < best);
+        best = take ? gm : best;
+        bi = take ? i : bi;
       }
     }
     prev = best;
@@ -523,40 +522,68 @@ __device__ __forceinline__ void twisted_vector(const float* __restrict__ a, cons
     }
   }
   // the vector from the twist outwards; the pivots of a group are read
-  // before any of its rows is overwritten
+  // before any of its rows is overwritten, the next group's during this one.
+  // Every row of a visited group is stored: rows outside the pass get back
+  // the value just read (D- below the twist, the vector above it), so the
+  // steps are selects and not branches.
   float nrm2 = 1.f, x = 1.f;
-  for (int g = (r - 1) >> 2; g >= 0 && r > 0; --g) {
-    const f32x4v bc = ld4(b + 4 * g);
-    float q[4];
+  if (r > 0) {
+    int g = (r - 1) >> 2;
+    float qn[4];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) q[u] = z[(4 * g + u) * ldz];
+    for (int u = 0; u < 4; ++u) qn[u] = z[(4 * g + u) * ldz];
+    f32x4v bn = ld4(b + 4 * g);
+    for (; g >= 0; --g) {
+      float q[4];
 #pragma unroll
-    for (int u = 3; u >= 0; --u) {
-      const int i = 4 * g + u;
-      if (i < r) {
-        x = -bc[u] * __builtin_amdgcn_rcpf(q[u] != 0.f ? q[u] : tiny) * x;
-        z[i * ldz] = x;
-        nrm2 += x * x;
+      for (int u = 0; u < 4; ++u) q[u] = qn[u];
+      const f32x4v bc = bn;
+      if (g > 0) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) qn[u] = z[(4 * g - 4 + u) * ldz];
+        bn = ld4(b + 4 * g - 4);
+      }
+#pragma unroll
+      for (int u = 3; u >= 0; --u) {
+        const int i = 4 * g + u;
+        const bool in = i < r;
+        const float xn = -bc[u] * __builtin_amdgcn_rcpf(q[u] != 0.f ? q[u] : tiny) * x;
+        x = in ? xn : x;
+        nrm2 += in ? xn * xn : 0.f;
+        z[i * ldz] = in ? xn : q[u];
       }
     }
   }
   z[r * ldz] = 1.f;
   x = 1.f;
-  for (int g = (r + 1) >> 2; 4 * g < d; ++g) {
-    float q[4], bb[4];                         // pivots D- and b_{i-1} of the group
+  {
+    int g = (r + 1) >> 2;
+    float qn[4], bbn[4];
+    auto load_group = [&](int gg) {
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int i = 4 * g + u;
-      q[u] = z[i * ldz];
-      bb[u] = i > 0 ? b[i - 1] : 0.f;
-    }
+      for (int u = 0; u < 4; ++u) {
+        const int i = 4 * gg + u;
+        qn[u] = z[i * ldz];
+        bbn[u] = i > 0 ? b[i - 1] : 0.f;
+      }
+    };
+    if (4 * g < d) load_group(g);
+    for (; 4 * g < d; ++g) {
+      float q[4], bb[4];                       // pivots D- and b_{i-1} of the group
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int i = 4 * g + u;
-      if (i > r) {
-        x = -bb[u] * __builtin_amdgcn_rcpf(q[u] != 0.f ? q[u] : tiny) * x;
-        z[i * ldz] = x;
-        nrm2 += x * x;
+      for (int u = 0; u < 4; ++u) {
+        q[u] = qn[u];
+        bb[u] = bbn[u];
+      }
+      if (4 * g + 4 < d) load_group(g + 1);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int i = 4 * g + u;
+        const bool in = i > r;
+        const float xn = -bb[u] * __builtin_amdgcn_rcpf(q[u] != 0.f ? q[u] : tiny) * x;
+        x = in ? xn : x;
+        nrm2 += in ? xn * xn : 0.f;
+        z[i * ldz] = in ? xn : q[u];
       }
     }
   }
