@@ -594,6 +594,152 @@ __device__ __forceinline__ void twisted_vector(const float* __restrict__ a, cons
   }
 }
 
+// The same vector with two lanes per eigenvalue, on two waves, where Z has a
+// spare column per eigenvalue (2 m <= ldz): the lane pair's pivots D- (into
+// the vector's column zm) and D+ (into the spare column zp) run at once; the
+// twist is then a scan over both stored columns; the vector above the twist
+// (from D+, written into zm) and below it (from D-, in place) again run at
+// once, each pass writing only its own rows.  Same recurrences, same
+// arithmetic as twisted_vector.
+__device__ __forceinline__ void tw_pivots(const float* __restrict__ a, const float* __restrict__ b2,
+                                          const float* __restrict__ b2s, float* __restrict__ z, int ldz, int d,
+                                          float lam, bool backward) {
+  const int ng = d >> 2;
+  float pv = __builtin_inff();
+  if (backward) {                              // D-, bottom up
+    f32x4v an = ld4(a + d - 4), bn = ld4(b2 + d - 4);
+    for (int g = ng - 1; g >= 0; --g) {
+      const f32x4v ac = an, bc = bn;
+      if (g > 0) {
+        an = ld4(a + 4 * g - 4);
+        bn = ld4(b2 + 4 * g - 4);
+      }
+#pragma unroll
+      for (int u = 3; u >= 0; --u) {
+        pv = (ac[u] - lam) - bc[u] * __builtin_amdgcn_rcpf(pv);
+        z[(4 * g + u) * ldz] = pv;
+      }
+    }
+  } else {                                     // D+, top down
+    f32x4v an = ld4(a), bn = ld4(b2s);
+    for (int g = 0; g < ng; ++g) {
+      const f32x4v ac = an, bc = bn;
+      if (g + 1 < ng) {
+        an = ld4(a + 4 * g + 4);
+        bn = ld4(b2s + 4 * g + 4);
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        pv = (ac[u] - lam) - bc[u] * __builtin_amdgcn_rcpf(pv);
+        z[(4 * g + u) * ldz] = pv;
+      }
+    }
+  }
+}
+
+// the twist from the stored pivots: the rank-th least |gamma_i|,
+// gamma_i = D+_i + D-_i - (a_i - lam) (ties: lower index)
+__device__ __forceinline__ int tw_twist(const float* __restrict__ a, const float* __restrict__ zm,
+                                        const float* __restrict__ zp, int ldz, int d, float lam, int rank) {
+  const int ng = d >> 2;
+  float prev = -1.f;
+  int prev_i = -1, r = 0;
+  for (int s2 = 0; s2 <= rank; ++s2) {
+    float best = 3.4e38f;
+    int bi = 0;
+    for (int g = 0; g < ng; ++g) {
+      const f32x4v ac = ld4(a + 4 * g);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int i = 4 * g + u;
+        const float al = ac[u] - lam;
+        const float gm = fabsf(zp[i * ldz] + zm[i * ldz] - al);
+        const bool take = ((gm > prev) | ((gm == prev) & (i > prev_i))) & (gm < best);
+        best = take ? gm : best;
+        bi = take ? i : bi;
+      }
+    }
+    prev = best;
+    prev_i = bi;
+    r = bi;
+  }
+  return r;
+}
+
+// rows r-1 .. 0 of the vector (x_r = 1) from D+ (column zp) into column zm;
+// returns their sum of squares
+__device__ __forceinline__ float tw_up(const float* __restrict__ b, const float* __restrict__ zp,
+                                       float* __restrict__ zm, int ldz, int r) {
+  const float tiny = 1e-30f;
+  float n2 = 0.f, x = 1.f;
+  if (r > 0) {
+    int g = (r - 1) >> 2;
+    float qn[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) qn[u] = zp[(4 * g + u) * ldz];
+    f32x4v bn = ld4(b + 4 * g);
+    for (; g >= 0; --g) {
+      float q[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) q[u] = qn[u];
+      const f32x4v bc = bn;
+      if (g > 0) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) qn[u] = zp[(4 * g - 4 + u) * ldz];
+        bn = ld4(b + 4 * g - 4);
+      }
+#pragma unroll
+      for (int u = 3; u >= 0; --u) {
+        const int i = 4 * g + u;
+        const bool in = i < r;
+        const float xn = -bc[u] * __builtin_amdgcn_rcpf(q[u] != 0.f ? q[u] : tiny) * x;
+        x = in ? xn : x;
+        n2 += in ? xn * xn : 0.f;
+        if (in) zm[i * ldz] = xn;
+      }
+    }
+  }
+  return n2;
+}
+
+// rows r+1 .. d-1 of the vector (x_r = 1) from D- (column zm, in place);
+// returns their sum of squares
+__device__ __forceinline__ float tw_down(const float* __restrict__ b, float* __restrict__ zm, int ldz, int d,
+                                         int r) {
+  const float tiny = 1e-30f;
+  float n2 = 0.f, x = 1.f;
+  int g = (r + 1) >> 2;
+  float qn[4], bbn[4];
+  auto load_group = [&](int gg) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = 4 * gg + u;
+      qn[u] = zm[i * ldz];
+      bbn[u] = i > 0 ? b[i - 1] : 0.f;
+    }
+  };
+  if (4 * g < d) load_group(g);
+  for (; 4 * g < d; ++g) {
+    float q[4], bb[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      q[u] = qn[u];
+      bb[u] = bbn[u];
+    }
+    if (4 * g + 4 < d) load_group(g + 1);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = 4 * g + u;
+      const bool in = i > r;
+      const float xn = -bb[u] * __builtin_amdgcn_rcpf(q[u] != 0.f ? q[u] : tiny) * x;
+      x = in ? xn : x;
+      n2 += in ? xn * xn : 0.f;
+      if (in) zm[i * ldz] = xn;
+    }
+  }
+  return n2;
+}
+
 // V_m = Q Z for the m columns of Z: the reflectors (v_j in G's row j, zero
 // outside rows j+1 .. d-1; scale beta_j) applied from H_{d-3} down to H_0
 // with Z in registers: 16 lanes (one DPP row) per column, lane rb holding
@@ -943,7 +1089,38 @@ __device__ bool tridiag_solve(float* G, int ld, float* Z, int ldz, int d, int dp
   // equal ones (within 2^-20 |T|), so that the members of an exactly
   // multiple eigenvalue take different twists; every other one takes its
   // best twist, which gives the accurate vector.
-  if (tid < m) {
+  if (2 * m <= ldz && m <= 64) {
+    // two lanes per eigenvalue k = lane: wave 0 holds the vector's column k,
+    // wave 1 the spare column m + k (free until the back-transformation)
+    float* const s_n2 = sv + 9 * dp;           // [2][64] partial sums of squares
+    int* const s_tw = reinterpret_cast<int*>(sv + 9 * dp + 128);   // [64] twists
+    const bool pair = wave < 2 && lane < m;
+    if (pair) tw_pivots(s_a, s_b2, s_b2s, Z + lane + wave * m, ldz, d, s_lam[lane], wave == 0);
+    __syncthreads();
+    if (wave == 0 && lane < m) {
+      int rank = 0;
+      while (rank < lane && rank < d - 1 && s_lam[lane - rank - 1] - s_lam[lane - rank] <= 0x1p-20f * tnorm) ++rank;
+      const int r = tw_twist(s_a, Z + lane, Z + m + lane, ldz, d, s_lam[lane], rank);
+      s_tw[lane] = r;
+      Z[r * ldz + lane] = 1.f;                 // (row r of the spare column is not read again)
+    }
+    __syncthreads();
+    if (pair) {
+      const int r = s_tw[lane];
+      s_n2[wave * 64 + lane] = wave == 0 ? tw_up(s_b, Z + m + lane, Z + lane, ldz, r)
+                                         : tw_down(s_b, Z + lane, ldz, d, r);
+    }
+    __syncthreads();
+    if (pair) {                                // rows split between the two waves
+      const float inv = 1.f / sqrtf(1.f + s_n2[lane] + s_n2[64 + lane]);
+      const int h = ((d >> 2) + 1) >> 1;      // groups of the first wave
+      const int g0 = wave == 0 ? 0 : h, g1 = wave == 0 ? h : (d >> 2);
+      for (int g = g0; g < g1; ++g) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) Z[(4 * g + u) * ldz + lane] *= inv;
+      }
+    }
+  } else if (tid < m) {
     int rank = 0;
     while (rank < tid && rank < d - 1 && s_lam[tid - rank - 1] - s_lam[tid - rank] <= 0x1p-20f * tnorm) ++rank;
     twisted_vector(s_a, s_b, s_b2, s_b2s, Z + tid, ldz, d, s_lam[tid], rank);
@@ -1107,7 +1284,7 @@ __global__ __launch_bounds__(kFormThreads) void form_patch_kernel(const FormPara
   if (sweeps == 0) {
     // ---- 2'. tridiagonal eigensolver: eigenpairs in order, eigenvalues onto
     // G's diagonal and vectors into V's first m columns ----
-    float* sv = Ss;                            // 7 dp + 24 floats of the 51 dp here
+    float* sv = Ss;                            // 9 dp + 192 floats of the 51 dp here
     tri_ok = tridiag_solve(G, ld, V, ld, d, dp, m, sv, s_order, &s_fail);
     if (tri_ok) {
       if (tid < m) {
