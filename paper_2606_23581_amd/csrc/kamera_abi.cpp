@@ -709,7 +709,8 @@ static int build_form(const kamera_form_args* a, kamera::FormParams& P, bool& la
   if (units == 0 || a->n_tokens == 0) return KAMERA_OK;
   // the dispatch packets count work-items in 32 bits: 1024 per unit for the
   // eigensolver kernel, 256 per 256 token rows of a unit for the U kernel
-  if (units * 1024 > 0xFFFFFFFFLL || ceil_div(a->n_tokens, 256) * units * 256 > 0xFFFFFFFFLL)
+  // (its grid rounded up to a multiple of 8)
+  if (units * 1024 > 0xFFFFFFFFLL || (ceil_div(ceil_div(a->n_tokens, 256) * units, 8) * 8) * 256 > 0xFFFFFFFFLL)
     return fail(KAMERA_ERR_RANGE, "%s: %lld units of %d tokens exceed one launch", who, (long long)units,
                 a->n_tokens);
   if (a->delta == nullptr || a->U == nullptr || a->W == nullptr)

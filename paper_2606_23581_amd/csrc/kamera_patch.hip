@@ -1491,12 +1491,16 @@ __global__ __launch_bounds__(kUThreads) void form_u_kernel(const FormParams /*by
   const int t = lane & 15, kg = lane >> 4;
   const int n = P.n_tokens, d = P.dim, m = P.m;
   const uint32_t bpu = (uint32_t)((n + kURowsPerBlock - 1) / kURowsPerBlock);   // blocks per unit
-  const uint32_t unit = blockIdx.x / bpu;
+  // workgroups go to the 8 XCDs in turn: block b takes the place
+  // (b mod 8) * (grid / 8) + b / 8, so that the blocks of one unit share an
+  // XCD and read its W from that XCD's L2 (the grid is a multiple of 8)
+  const uint32_t place = (blockIdx.x & 7u) * (gridDim.x >> 3) + (blockIdx.x >> 3);
+  const uint32_t unit = place / bpu;
   if ((int)unit >= P.n_units) return;
   const int h = (int)(unit % (uint32_t)P.n_heads);
   const int l = (int)((unit / (uint32_t)P.n_heads) % (uint32_t)P.n_layers);
   const int c = (int)(unit / ((uint32_t)P.n_heads * (uint32_t)P.n_layers));
-  const int row0 = (int)(blockIdx.x - unit * bpu) * kURowsPerBlock + wave * kURows;
+  const int row0 = (int)(place - unit * bpu) * kURowsPerBlock + wave * kURows;
   if (row0 >= n) return;                       // no barrier in this kernel
   const float* delta = P.delta + (int64_t)c * P.delta_s[0] + (int64_t)l * P.delta_s[1] + (int64_t)h * P.delta_s[2];
   const uint16_t* Wu = P.W + (int64_t)c * P.w_s[0] + (int64_t)l * P.w_s[1] + (int64_t)h * P.w_s[2];
@@ -1615,7 +1619,8 @@ hipError_t launch_form_patch(const FormParams& p, hipStream_t s) {
   if (e1 != hipSuccess) return e1;
   // U from the stored W, on the same stream: after the W of every unit
   const int64_t bpu = (p.n_tokens + kURowsPerBlock - 1) / kURowsPerBlock;
-  hipLaunchKernelGGL(form_u_kernel, dim3((uint32_t)(bpu * p.n_units)), dim3(kUThreads), 0, s, p);
+  const int64_t blocks = (bpu * p.n_units + 7) / 8 * 8;   // the places past the units return at once
+  hipLaunchKernelGGL(form_u_kernel, dim3((uint32_t)blocks), dim3(kUThreads), 0, s, p);
   return hipGetLastError();
 }
 
