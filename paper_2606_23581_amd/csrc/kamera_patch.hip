@@ -1159,19 +1159,35 @@ __device__ bool tridiag_solve(float* G, int ld, float* Z, int ldz, int d, int dp
   }
   __syncthreads();
   // every vector must satisfy |T z - lambda z| <= 2^-16 |T| (good ones reach
-  // ~d u |T|); a larger or non-finite residual sends the unit to Jacobi
-  if (tid < m) {
-    const float lam = s_lam[tid], inv_tn = tnorm > 0.f ? 1.f / tnorm : 0.f;
-    float r2 = 0.f;
+  // ~d u |T|); a larger or non-finite residual sends the unit to Jacobi.
+  // The rows of a vector are split over four waves (two at rank > 64), the
+  // partial sums meeting in LDS (phase C's scratch)
+  {
+    float* const s_r2 = sv + 9 * dp;           // [4][128]
+    const int mc = (m + 63) >> 6, parts = 4 / mc;
+    if (wave < 4) {
+      const int k = lane + 64 * (wave % mc), part = wave / mc;
+      const int i0 = part * (d / parts), i1 = i0 + d / parts;
+      if (k < m) {
+        const float lam = s_lam[k], inv_tn = tnorm > 0.f ? 1.f / tnorm : 0.f;
+        float r2 = 0.f;
 #pragma unroll 8
-    for (int i = 0; i < d; ++i) {
-      float t = (s_a[i] - lam) * Z[i * ldz + tid];
-      if (i > 0) t += s_b[i - 1] * Z[(i - 1) * ldz + tid];
-      if (i < d - 1) t += s_b[i] * Z[(i + 1) * ldz + tid];
-      t *= inv_tn;
-      r2 += t * t;
+        for (int i = i0; i < i1; ++i) {
+          float t = (s_a[i] - lam) * Z[i * ldz + k];
+          if (i > 0) t += s_b[i - 1] * Z[(i - 1) * ldz + k];
+          if (i < d - 1) t += s_b[i] * Z[(i + 1) * ldz + k];
+          t *= inv_tn;
+          r2 += t * t;
+        }
+        s_r2[part * 128 + k] = r2;
+      }
     }
-    if (!(r2 <= 0x1p-32f)) *s_fail = 1;
+    __syncthreads();
+    if (tid < m) {
+      float r2 = 0.f;
+      for (int q = 0; q < parts; ++q) r2 += s_r2[q * 128 + tid];
+      if (!(r2 <= 0x1p-32f)) *s_fail = 1;
+    }
   }
   __syncthreads();
   if (*s_fail) return false;
