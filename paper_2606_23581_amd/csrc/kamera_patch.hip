@@ -1489,7 +1489,8 @@ size_t form_lds_bytes(int dim, int /*m*/) {
 // ---------------------------------------------------------------------------
 // U = Delta W^T, the factor's token side, from the W form_patch_kernel has
 // stored (so U W is formed from exactly the kept W).  A wave takes kURows
-// token rows of one unit, as 16-row tiles, and the ranks 64 at a time; the
+// token rows of one unit, as 16-row tiles, and the ranks 64 at a time (the
+// workgroup's four waves share those 64 W rows, staged once in LDS); the
 // products are 16x16x32 bf16 MFMAs with fp32 accumulation.  Delta is read in
 // fp32 and split into hi = bf16(Delta) and lo = bf16(Delta - hi), and both
 // parts are multiplied, so Delta enters to ~2^-16 relative.  Lane (kg, t)
@@ -1500,6 +1501,8 @@ size_t form_lds_bytes(int dim, int /*m*/) {
 constexpr int kURows = 64;            // token rows per wave
 constexpr int kUThreads = 256;
 constexpr int kURowsPerBlock = kURows * (kUThreads / 64);
+constexpr int kUWLd = 144;            // bf16 per staged W row: 288 bytes, so the B-operand reads
+                                      // of a half wave (16 rows x 2 pieces) fall on distinct banks
 
 __global__ __launch_bounds__(kUThreads) void form_u_kernel(const FormParams /*by value, read in place*/) {
   const FormParams& P = *static_cast<const FormParams*>((const void*)__builtin_amdgcn_kernarg_segment_ptr());
@@ -1517,7 +1520,8 @@ __global__ __launch_bounds__(kUThreads) void form_u_kernel(const FormParams /*by
   const int l = (int)((unit / (uint32_t)P.n_heads) % (uint32_t)P.n_layers);
   const int c = (int)(unit / ((uint32_t)P.n_heads * (uint32_t)P.n_layers));
   const int row0 = (int)(place - unit * bpu) * kURowsPerBlock + wave * kURows;
-  if (row0 >= n) return;                       // no barrier in this kernel
+  // (a wave past the unit's rows still takes part in the W staging)
+  __shared__ __align__(16) uint16_t s_w[64 * kUWLd];
   const float* delta = P.delta + (int64_t)c * P.delta_s[0] + (int64_t)l * P.delta_s[1] + (int64_t)h * P.delta_s[2];
   const uint16_t* Wu = P.W + (int64_t)c * P.w_s[0] + (int64_t)l * P.w_s[1] + (int64_t)h * P.w_s[2];
   uint16_t* Uu = P.U + (int64_t)c * P.u_s[0] + (int64_t)l * P.u_s[1] + (int64_t)h * P.u_s[2];
@@ -1543,31 +1547,34 @@ __global__ __launch_bounds__(kUThreads) void form_u_kernel(const FormParams /*by
       }
   };
   for (int r0 = 0; r0 < m; r0 += 64) {
-    // B operands: W rows r0 + 16 ct + t, dims [8 kg + 32 s, +8)
-    u32x4v wb[4][4];
+    // W rows r0 .. r0 + 63 into LDS, 16-byte pieces (zero past m or d), once
+    // for the workgroup's four waves
+    __syncthreads();                           // the previous ranks' W is consumed
 #pragma unroll
-    for (int ct = 0; ct < 4; ++ct) {
-      const int r = r0 + 16 * ct + t;
+    for (int q = 0; q < 64 * 16 / kUThreads; ++q) {
+      const int e = threadIdx.x + q * kUThreads, rr = e >> 4, j0 = 8 * (e & 15);
+      const int r = r0 + rr;
+      u32x4v v = {0u, 0u, 0u, 0u};
+      if (r < m && j0 < d) {
+        const uint16_t* wr = Wu + (int64_t)r * P.w_s[3] + j0;
+        if (P.w_vec && j0 + 8 <= d) {
+          v = *reinterpret_cast<const u32x4v*>(wr);
+        } else {
 #pragma unroll
-      for (int s = 0; s < 4; ++s) {
-        u32x4v v = {0u, 0u, 0u, 0u};
-        const int j0 = 32 * s + 8 * kg;
-        if (r < m && s < ks && j0 < d) {
-          const uint16_t* wr = Wu + (int64_t)r * P.w_s[3] + j0;
-          if (P.w_vec && j0 + 8 <= d) {
-            v = *reinterpret_cast<const u32x4v*>(wr);
-          } else {
-#pragma unroll
-            for (int e = 0; e < 8; ++e)
-              if (j0 + e < d) v[e >> 1] |= (uint32_t)wr[e] << (16 * (e & 1));
-          }
+          for (int e2 = 0; e2 < 8; ++e2)
+            if (j0 + e2 < d) v[e2 >> 1] |= (uint32_t)wr[e2] << (16 * (e2 & 1));
         }
-        wb[ct][s] = v;
       }
+      *reinterpret_cast<u32x4v*>(s_w + rr * kUWLd + j0) = v;
     }
+    __syncthreads();
+    // B operands: W rows r0 + 16 ct + t, dims [8 kg + 32 s, +8)
+    auto wb = [&](int ct, int s) {
+      return *reinterpret_cast<const u32x4v*>(s_w + (16 * ct + t) * kUWLd + 32 * s + 8 * kg);
+    };
     for (int rt = 0; rt < kURows / 16; ++rt) {
       const int i0 = row0 + 16 * rt;
-      if (i0 >= n) break;                      // uniform
+      if (i0 >= n) break;                      // uniform in the wave (no barrier inside)
       float x[4][8];
       load_rows(i0 + t, x);
       f32x4v acc[4];
@@ -1583,7 +1590,7 @@ __global__ __launch_bounds__(kUThreads) void form_u_kernel(const FormParams /*by
           const bf16x8v alo = __builtin_bit_cast(bf16x8v, pack_bf16x8(lo));
 #pragma unroll
           for (int ct = 0; ct < 4; ++ct) {
-            const bf16x8v b = __builtin_bit_cast(bf16x8v, wb[ct][s]);
+            const bf16x8v b = __builtin_bit_cast(bf16x8v, wb(ct, s));
             acc[ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi, b, acc[ct], 0, 0, 0);
             acc[ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(alo, b, acc[ct], 0, 0, 0);
           }
