@@ -1300,7 +1300,7 @@ __global__ __launch_bounds__(kFormThreads) void form_patch_kernel(const FormPara
   if (sweeps == 0) {
     // ---- 2'. tridiagonal eigensolver: eigenpairs in order, eigenvalues onto
     // G's diagonal and vectors into V's first m columns ----
-    float* sv = Ss;                            // 9 dp + 192 floats of the 51 dp here
+    float* sv = Ss;                            // 9 dp + 512 floats of the 51 dp here
     tri_ok = tridiag_solve(G, ld, V, ld, d, dp, m, sv, s_order, &s_fail);
     if (tri_ok) {
       if (tid < m) {
